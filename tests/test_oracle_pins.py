@@ -1,0 +1,320 @@
+"""Pins of the float64 oracle against what the paper and the mathematics fix.
+
+None of these compare the oracle with itself.  Each pin restates a fact
+independently of the oracle's token-by-token recurrence:
+
+* a hand-derived three-token example (tests/golden/hand_T3_d2.json);
+* the closed-form scan reads of Appendix C (Eq. 16) with retention one,
+  written as dense masked matrix products;
+* textbook special cases: eta = 0, T = 1, identical unit inputs (a plain
+  exclusive prefix sum), orthonormal inputs;
+* central finite differences of L = sum <dY, y> (exact up to rounding here,
+  because L is at most quadratic in every input), including a read-only
+  perturbation that isolates the transpose read gtilde;
+* a complex-step Jacobian-vector product against the reverse sweep (adjoint
+  identity);
+* Theorem 1's statement that the scan equals the serial learner: token-by-token
+  decode steps reproduce the scan and end at W_0 + Delta_T;
+* dW_0 = sum_b dY^T X, a plain matrix product.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import gradlev_oracle as orc
+
+pytestmark = []
+
+PREFIXES = [orc.EXCLUSIVE, orc.INCLUSIVE]
+
+
+def rand_problem(B=2, H=3, T=7, d=4, m=5, seed=0, eta="token"):
+    rng = np.random.default_rng(seed)
+    W0 = rng.standard_normal((H, m, d))
+    X = rng.standard_normal((B, H, T, d))
+    G = rng.standard_normal((B, H, T, m))
+    dY = rng.standard_normal((B, H, T, m))
+    e = rng.uniform(0.05, 0.6, size=(B, H, T)) if eta == "token" else float(eta)
+    return W0, X, G, e, dY
+
+
+def closed_form_fwd(W0, X, G, eta, prefix):
+    """Appendix C, Eq. 16 with alpha = 1, as dense masked products."""
+    B, H, T, d = X.shape
+    e = np.broadcast_to(np.asarray(eta, float), (B, H, T))
+    k = -1 if prefix == orc.EXCLUSIVE else 0
+    mask = np.tril(np.ones((T, T)), k)
+    Y = np.empty(G.shape)
+    for b in range(B):
+        for h in range(H):
+            A = (X[b, h] @ X[b, h].T) * mask           # A[t, s] = x_t . x_s
+            Y[b, h] = X[b, h] @ W0[h].T - A @ (e[b, h][:, None] * G[b, h])
+    return Y
+
+
+def closed_form_gtilde(W0, X, G, eta, dY, prefix):
+    """Second line of Eq. 16 queried by dY_t: W_0^T dY_t + Delta_t^T dY_t."""
+    B, H, T, d = X.shape
+    e = np.broadcast_to(np.asarray(eta, float), (B, H, T))
+    k = -1 if prefix == orc.EXCLUSIVE else 0
+    mask = np.tril(np.ones((T, T)), k)
+    out = np.empty(X.shape)
+    for b in range(B):
+        for h in range(H):
+            E = (dY[b, h] @ G[b, h].T) * mask * e[b, h][None, :]   # E[t, s]
+            out[b, h] = dY[b, h] @ W0[h] - E @ X[b, h]
+    return out
+
+
+def rel_err(a, b):
+    return np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300)
+
+
+# --------------------------------------------------------------------------
+# Hand-derived example
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_hand_example(golden_dir, prefix):
+    with open(os.path.join(golden_dir, "hand_T3_d2.json")) as f:
+        gd = json.load(f)
+    W0 = np.array(gd["W0"], float)[None]
+    X = np.array(gd["X"], float)[None, None]
+    G = np.array(gd["G"], float)[None, None]
+    dY = np.array(gd["dY"], float)[None, None]
+    exp = gd[prefix]
+    Y = orc.scan_fwd(W0, X, G, gd["eta"], prefix)
+    np.testing.assert_array_equal(Y[0, 0], np.array(exp["y"], float))
+    out = orc.scan_bwd(W0, X, G, gd["eta"], dY, prefix)
+    for key in ("gtilde", "dx", "dg", "deta"):
+        np.testing.assert_array_equal(out[key][0, 0], np.array(exp[key], float), err_msg=key)
+    np.testing.assert_array_equal(out["dw0"][0], np.array(exp["dw0"], float))
+
+
+def test_hand_example_decode(golden_dir):
+    with open(os.path.join(golden_dir, "hand_T3_d2.json")) as f:
+        gd = json.load(f)
+    W = np.array(gd["W0"], float)[None, None]
+    for t in range(3):
+        x = np.array(gd["X"][t], float)[None, None]
+        g = np.array(gd["G"][t], float)[None, None]
+        y, W = orc.decode_step(W, x, g, gd["eta"])
+        np.testing.assert_array_equal(y[0, 0], np.array(gd["exclusive"]["y"][t], float))
+    np.testing.assert_array_equal(W[0, 0], np.array(gd["decode_final_W"], float))
+
+
+# --------------------------------------------------------------------------
+# Closed forms (Theorem 1: the scan equals the serial learner)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+@pytest.mark.parametrize("shape", [(2, 3, 7, 4, 5), (1, 2, 33, 6, 3), (1, 1, 1, 3, 3)])
+def test_fwd_equals_closed_form(prefix, shape):
+    B, H, T, d, m = shape
+    W0, X, G, e, _ = rand_problem(B, H, T, d, m, seed=T)
+    Y = orc.scan_fwd(W0, X, G, e, prefix)
+    assert rel_err(Y, closed_form_fwd(W0, X, G, e, prefix)) < 1e-12
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_gtilde_equals_closed_form(prefix):
+    W0, X, G, e, dY = rand_problem(2, 2, 19, 5, 3, seed=4)
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix)
+    assert rel_err(out["gtilde"], closed_form_gtilde(W0, X, G, e, dY, prefix)) < 1e-12
+
+
+def test_scalar_eta_matches_broadcast():
+    W0, X, G, _, dY = rand_problem(1, 2, 9, 4, 4, seed=8)
+    e = np.full((1, 2, 9), 0.3)
+    Y1 = orc.scan_fwd(W0, X, G, 0.3)
+    Y2 = orc.scan_fwd(W0, X, G, e)
+    np.testing.assert_array_equal(Y1, Y2)
+    b1 = orc.scan_bwd(W0, X, G, 0.3, dY)
+    b2 = orc.scan_bwd(W0, X, G, e, dY)
+    for k in b1:
+        np.testing.assert_array_equal(b1[k], b2[k])
+
+
+# --------------------------------------------------------------------------
+# Special cases
+# --------------------------------------------------------------------------
+
+def test_eta_zero_is_static_map():
+    W0, X, G, _, dY = rand_problem(2, 2, 11, 4, 6, seed=1)
+    Y = orc.scan_fwd(W0, X, G, 0.0)
+    for b in range(2):
+        for h in range(2):
+            np.testing.assert_allclose(Y[b, h], X[b, h] @ W0[h].T, rtol=0, atol=1e-14)
+    out = orc.scan_bwd(W0, X, G, 0.0, dY)
+    for b in range(2):
+        for h in range(2):
+            np.testing.assert_allclose(out["gtilde"][b, h], dY[b, h] @ W0[h], rtol=0, atol=1e-14)
+    np.testing.assert_array_equal(out["dg"], 0.0)
+    np.testing.assert_allclose(out["dx"], out["gtilde"], rtol=0, atol=0)
+    # deta does not vanish at eta = 0: d/d eta_t of -eta_t <dY_u, g_t>(x_t.x_u).
+    ref = np.zeros((2, 2, 11))
+    for t in range(11):
+        for u in range(t + 1, 11):
+            ref[:, :, t] -= np.einsum("bhm,bhm->bh", dY[:, :, u], G[:, :, t]) * \
+                np.einsum("bhd,bhd->bh", X[:, :, t], X[:, :, u])
+    assert rel_err(out["deta"], ref) < 1e-12
+
+
+def test_single_token_reads_slow_weights():
+    W0, X, G, e, dY = rand_problem(3, 2, 1, 5, 4, seed=2)
+    Y = orc.scan_fwd(W0, X, G, e)
+    np.testing.assert_allclose(Y[:, :, 0], np.einsum("hmd,bhd->bhm", W0, X[:, :, 0]), atol=1e-14)
+    out = orc.scan_bwd(W0, X, G, e, dY)
+    np.testing.assert_array_equal(out["dg"], 0.0)
+    np.testing.assert_array_equal(out["deta"], 0.0)
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_identical_unit_inputs_give_prefix_sum(prefix):
+    """x_t = e_k for all t: y_t = W0 e_k - (exclusive|inclusive) cumsum of eta g."""
+    rng = np.random.default_rng(5)
+    T, d, m, k = 13, 4, 3, 2
+    W0 = rng.standard_normal((1, m, d))
+    X = np.zeros((1, 1, T, d))
+    X[..., k] = 1.0
+    G = rng.standard_normal((1, 1, T, m))
+    e = rng.uniform(0.1, 0.5, size=(1, 1, T))
+    Y = orc.scan_fwd(W0, X, G, e, prefix)
+    writes = e[0, 0, :, None] * G[0, 0]
+    incl = np.cumsum(writes, axis=0)
+    pre = incl if prefix == orc.INCLUSIVE else np.vstack([np.zeros((1, m)), incl[:-1]])
+    np.testing.assert_allclose(Y[0, 0], W0[0][:, k][None, :] - pre, rtol=0, atol=1e-13)
+
+
+def test_orthonormal_inputs_read_slow_weights():
+    """Exclusive reads of mutually orthogonal inputs never see earlier writes."""
+    rng = np.random.default_rng(6)
+    d, m, T = 8, 5, 8
+    Q, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    X = Q.T[None, None]                      # rows are orthonormal
+    W0 = rng.standard_normal((1, m, d))
+    G = rng.standard_normal((1, 1, T, m))
+    Y = orc.scan_fwd(W0, X, G, 0.7)
+    np.testing.assert_allclose(Y[0, 0], X[0, 0] @ W0[0].T, atol=1e-13)
+    # Inclusive reads see exactly their own write: y_t = W0 x_t - eta g_t |x_t|^2.
+    Yi = orc.scan_fwd(W0, X, G, 0.7, orc.INCLUSIVE)
+    np.testing.assert_allclose(Yi[0, 0], X[0, 0] @ W0[0].T - 0.7 * G[0, 0], atol=1e-13)
+
+
+def test_input_scaling():
+    """Scaling X by c scales the W0 term by c and the Delta term by c^2."""
+    W0, X, G, e, _ = rand_problem(1, 2, 10, 4, 3, seed=9)
+    c = 1.7
+    base = orc.scan_fwd(W0, X, G, 0.0)
+    full = orc.scan_fwd(W0, X, G, e)
+    scaled = orc.scan_fwd(W0, c * X, G, e)
+    np.testing.assert_allclose(scaled, c * base + c * c * (full - base), rtol=1e-12, atol=1e-12)
+
+
+def test_dw0_is_plain_product():
+    W0, X, G, e, dY = rand_problem(3, 2, 9, 4, 5, seed=10)
+    out = orc.scan_bwd(W0, X, G, e, dY)
+    ref = np.einsum("bhtm,bhtd->hmd", dY, X)
+    assert rel_err(out["dw0"], ref) < 1e-13
+
+
+# --------------------------------------------------------------------------
+# Finite differences (exact up to rounding: L is quadratic in X, linear else)
+# --------------------------------------------------------------------------
+
+def _loss(W0, X, G, e, dY, prefix):
+    return float(np.sum(orc.scan_fwd(W0, X, G, e, prefix) * dY))
+
+
+def _fd(f, a, h=1e-3):
+    g = np.zeros_like(a)
+    it = np.nditer(a, flags=["multi_index"])
+    for _ in it:
+        i = it.multi_index
+        ap, am = a.copy(), a.copy()
+        ap[i] += h
+        am[i] -= h
+        g[i] = (f(ap) - f(am)) / (2 * h)
+    return g
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_backward_matches_finite_differences(prefix):
+    W0, X, G, e, dY = rand_problem(2, 1, 5, 3, 4, seed=11)
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix)
+    fd_x = _fd(lambda a: _loss(W0, a, G, e, dY, prefix), X)
+    fd_g = _fd(lambda a: _loss(W0, X, a, e, dY, prefix), G)
+    fd_e = _fd(lambda a: _loss(W0, X, G, a, dY, prefix), e)
+    fd_w = _fd(lambda a: _loss(a, X, G, e, dY, prefix), W0)
+    assert rel_err(out["dx"], fd_x) < 1e-9
+    assert rel_err(out["dg"], fd_g) < 1e-9
+    assert rel_err(out["deta"], fd_e) < 1e-9
+    assert rel_err(out["dw0"], fd_w) < 1e-9
+
+
+def _split_read_write(W0, Xr, Xw, G, e, prefix):
+    """y_t = (W0 - sum_{s<t or s<=t} e_s g_s xw_s^T) xr_t, reads and writes separate."""
+    B, H, T, d = Xr.shape
+    Y = np.zeros(G.shape)
+    for t in range(T):
+        last = t if prefix == orc.EXCLUSIVE else t + 1
+        for s in range(last):
+            Y[:, :, t] -= e[:, :, s, None] * G[:, :, s] * np.einsum(
+                "bhd,bhd->bh", Xw[:, :, s], Xr[:, :, t])[..., None]
+        Y[:, :, t] += np.einsum("hmd,bhd->bhm", W0, Xr[:, :, t])
+    return Y
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_gtilde_is_read_side_gradient(prefix):
+    """gtilde is dL/dx through the read alone (Eq. 4); dx - gtilde is the write side."""
+    W0, X, G, e, dY = rand_problem(1, 2, 6, 3, 4, seed=12)
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix)
+    fd_read = _fd(lambda a: float(np.sum(_split_read_write(W0, a, X, G, e, prefix) * dY)), X)
+    fd_write = _fd(lambda a: float(np.sum(_split_read_write(W0, X, a, G, e, prefix) * dY)), X)
+    assert rel_err(out["gtilde"], fd_read) < 1e-9
+    assert rel_err(out["dx"] - out["gtilde"], fd_write) < 1e-9
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_adjoint_identity_complex_step(prefix):
+    """<dY, J v> (complex-step JVP, exact to rounding) equals <J^T dY, v>."""
+    W0, X, G, e, dY = rand_problem(2, 2, 8, 4, 3, seed=13)
+    rng = np.random.default_rng(14)
+    vW, vX, vG, ve = (rng.standard_normal(a.shape) for a in (W0, X, G, e))
+    h = 1e-30
+    Yc = orc.scan_fwd(W0 + 1j * h * vW, X + 1j * h * vX, G + 1j * h * vG, e + 1j * h * ve, prefix)
+    jvp = float(np.sum(np.imag(Yc) / h * dY))
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix)
+    vjp = float(np.sum(out["dw0"] * vW) + np.sum(out["dx"] * vX) +
+                np.sum(out["dg"] * vG) + np.sum(out["deta"] * ve))
+    assert abs(jvp - vjp) <= 1e-12 * max(1.0, abs(jvp))
+
+
+# --------------------------------------------------------------------------
+# Deployment: decode steps equal the exclusive scan (Theorem 1)
+# --------------------------------------------------------------------------
+
+def test_decode_steps_equal_scan():
+    rng = np.random.default_rng(15)
+    S, H, T, d, m = 3, 2, 12, 5, 4
+    W0 = rng.standard_normal((H, m, d))
+    X = rng.standard_normal((S, H, T, d))
+    G = rng.standard_normal((S, H, T, m))
+    e = rng.uniform(0.1, 0.4, size=(S, H, T))
+    Y = orc.scan_fwd(W0, X, G, e)
+    W = np.broadcast_to(W0, (S, H, m, d)).copy()
+    for t in range(T):
+        y, W = orc.decode_step(W, X[:, :, t], G[:, :, t], e[:, :, t])
+        np.testing.assert_allclose(y, Y[:, :, t], rtol=0, atol=1e-12)
+    final = W0[None] - np.einsum("sht,shtm,shtd->shmd", e, G, X)
+    np.testing.assert_allclose(W, final, rtol=0, atol=1e-12)
+
+
+def test_oracle_rejects_unknown_prefix():
+    W0, X, G, e, dY = rand_problem(1, 1, 2, 2, 2)
+    with pytest.raises(ValueError):
+        orc.scan_fwd(W0, X, G, e, "shifted")
