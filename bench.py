@@ -1,0 +1,364 @@
+#!/usr/bin/env python3
+"""Benchmark of the GradLev scan library on one MI355X.
+
+A step is one pass of the whole hot path over one batch: the forward scan and
+the full backward (gtilde, dX, dG, deta, dW0) of the lm-bf16 workload
+(B=8, H=16, T=2048, d=m=64, bf16 inputs, eta=0.1, chunk 64), inputs already
+resident in HBM.  Two input sets alternate between steps so that the 256 MB
+Infinity Cache cannot carry a step's inputs into the next one.
+
+Prints ONE JSON line with the headline (fwd+bwd tokens/s, tokens = B*T per
+step), the roofline of the dominant kernel measured with HIP events recorded
+around its launches inside the timed region, the float64 oracle timed on the
+host, and secondary measurements of the other workloads (long-context scan,
+24-layer stack, decode).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "scan fwd+bwd tokens/s & MFMA util; decode tokens/s & HBM GB/s (1 MI355X)"
+PEAK_HBM = 8.0e12        # bytes/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15       # dense bf16 MFMA flop/s
+PEAK_FP32_MFMA = 157.3e12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="lm-bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--cpu-sample-batch", type=int, default=2,
+                    help="batch rows of the workload the float64 oracle is timed on")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# Algorithmic work (per token and head; C = the tile each kernel uses)
+# ---------------------------------------------------------------------------
+
+def flops_fwd(d, m, C):
+    return 4 * m * d + (C - 1) * (d + m)
+
+
+def flops_bwd(d, m, C):
+    return 10 * m * d + (C - 1) * (3 * d + 2 * m)
+
+
+def bytes_fwd(d, m, es):
+    # read x, g; write y (fp32)
+    return es * (d + m) + 4 * m
+
+
+def bytes_bwd(d, m, es):
+    # read x, g, dY; write gtilde, dX (fp32, d each), dG (fp32, m), deta (fp32)
+    return es * (d + 2 * m) + 4 * (2 * d + m) + 4
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class ScanRunner:
+    """Preallocated inputs/outputs/workspace for repeated fwd+bwd steps."""
+
+    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0):
+        self.gl, self.torch, self.wl = gl, torch, wl
+        self.sets = [W.device_scan_inputs(wl, layer0 + i, device, torch=torch) for i in range(nsets)]
+        self.shape = gl.make_shape(wl.B, wl.H, wl.T, wl.d, wl.m,
+                                   gl.BF16 if wl.dtype == "bf16" else gl.F32, chunk=wl.chunk)
+        self.plan = gl.plan(self.shape)
+        self.ws = torch.empty(max(self.plan.workspace_bytes, 256), dtype=torch.uint8, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
+        self.Y = torch.empty(B, H, T, m, **f32)
+        self.outs = {"gtilde": torch.empty(B, H, T, d, **f32), "dx": torch.empty(B, H, T, d, **f32),
+                     "dg": torch.empty(B, H, T, m, **f32), "deta": torch.empty(B, H, T, **f32),
+                     "dw0": torch.empty(H, m, d, **f32)}
+
+    def step(self, i):
+        s = self.sets[i % len(self.sets)]
+        self.gl.scan_fwd(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
+                         workspace=self.ws)
+        self.gl.scan_bwd(s["W0"], s["X"], s["G"], s["dY"], s["eta"], chunk=self.wl.chunk,
+                         out=self.outs, workspace=self.ws)
+
+
+def timed(torch, fn, steps, warmup):
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        fn(i)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps  # ms per step
+
+
+def kernel_avgs(gl):
+    return {k: (ms / n * 1e3 if n else None, n) for k, (ms, n) in gl.timing_read().items()}
+
+
+def scan_work(wl, plan):
+    es = 2 if wl.dtype == "bf16" else 4
+    th = wl.B * wl.H * wl.T
+    return {
+        "flops": th * (flops_fwd(wl.d, wl.m, plan.fwd_chunk) + flops_bwd(wl.d, wl.m, plan.bwd_chunk)),
+        "bytes": th * (bytes_fwd(wl.d, wl.m, es) + bytes_bwd(wl.d, wl.m, es)),
+        "bytes_fwd": th * bytes_fwd(wl.d, wl.m, es),
+        "bytes_bwd": th * bytes_bwd(wl.d, wl.m, es),
+    }
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch from committed rocprofv3 --pmc runs, if still current."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec:
+        return None
+    import hashlib
+    h = hashlib.sha256()
+    for rel in rec.get("sources", []):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("source_sha256"):
+        return None  # kernel changed since the counters were taken
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(W, wl, batch):
+    """The float64 oracle, as it stands, on `batch` rows of the workload."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    from oracle import gradlev_oracle as orc
+    inp = W.scan_inputs(wl, B=batch)
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    if ctx:
+        ctx.__enter__()
+    try:
+        t0 = time.perf_counter()
+        orc.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"])
+        t1 = time.perf_counter()
+        orc.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["eta"], inp["dY"])
+        t2 = time.perf_counter()
+    finally:
+        if ctx:
+            ctx.__exit__(None, None, None)
+    tokens = batch * wl.T
+    return {"value": tokens / (t2 - t0), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{wl.name} with B={batch} (H={wl.H}, T={wl.T}, d=m={wl.d}); fwd {t1 - t0:.1f} s + "
+                      f"bwd {t2 - t1:.1f} s of float64 numpy, one thread"}
+
+
+def secondary_scan(gl, torch, W, name, steps, warmup, device):
+    wl = W.SCAN_WORKLOADS[name]
+    if wl.layers == 1:
+        run = ScanRunner(gl, torch, W, wl, 1, device)
+        fn = run.step
+        runs = [run]
+    else:
+        runs = [ScanRunner(gl, torch, W, wl, 1, device, layer0=l) for l in range(wl.layers)]
+        # Layers share output buffers: the write traffic is identical and 24
+        # separate sets would only add allocation.
+        for r in runs[1:]:
+            r.Y, r.outs, r.ws = runs[0].Y, runs[0].outs, runs[0].ws
+
+        def fn(i):
+            for r in runs:
+                r.step(0)
+    gl.timing_reset()
+    gl.timing_enable(True)
+    ms = timed(torch, fn, steps, warmup)
+    k = kernel_avgs(gl)
+    gl.timing_enable(False)
+    work = scan_work(wl, runs[0].plan)
+    L = wl.layers
+    res = {"ms_per_step": ms, "tokens_per_s": wl.B * wl.T / (ms * 1e-3),
+           "tflops_algorithmic": L * work["flops"] / (ms * 1e-3) / 1e12,
+           "frac_bf16_peak": L * work["flops"] / (ms * 1e-3) / PEAK_BF16,
+           "hbm_GBps_algorithmic": L * work["bytes"] / (ms * 1e-3) / 1e9,
+           "frac_hbm_peak": L * work["bytes"] / (ms * 1e-3) / PEAK_HBM,
+           "kernel_avg_us": {n: round(v[0], 2) for n, v in k.items() if v[0] is not None},
+           "plan": {"fwd": [runs[0].plan.fwd_chunk, runs[0].plan.fwd_segment, runs[0].plan.fwd_nseg],
+                    "bwd": [runs[0].plan.bwd_chunk, runs[0].plan.bwd_segment, runs[0].plan.bwd_nseg]}}
+    if L > 1:
+        res["layers"] = L
+        res["model_tokens_per_s"] = res["tokens_per_s"]
+        res["layer_tokens_per_s"] = res["tokens_per_s"] * L
+    del runs
+    torch.cuda.empty_cache()
+    return res
+
+
+def secondary_decode(gl, torch, W, device, graph=True):
+    wl = W.DECODE_WORKLOADS["decode-f32"]
+    S, H, d, m, n = wl.S, wl.H, wl.d, wl.m, wl.steps
+    gen = torch.Generator(device=device)
+    gen.manual_seed(wl.seed)
+    state = (torch.randn(S, H, m, d, device=device, generator=gen) * wl.w_std).contiguous()
+    xs = (torch.randn(n, S, H, d, device=device, generator=gen) * wl.x_std).contiguous()
+    gs = (torch.randn(n, S, H, m, device=device, generator=gen) * wl.g_std).contiguous()
+    ys = torch.empty(n, S, H, m, device=device)
+
+    def run_all(_=0):
+        for t in range(n):
+            gl.decode_step(state, xs[t], gs[t], wl.eta, out=ys[t])
+
+    per_step_bytes = 4 * (2 * S * H * m * d + S * H * (d + m) + S * H * m)
+    run_all()  # warm-up
+    torch.cuda.synchronize()
+    mode = "eager"
+    fn = run_all
+    if graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    run_all()
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+
+            def fn(_=0):
+                g.replay()
+            mode = "hip graph of 512 launches"
+        except Exception as e:  # graph capture unavailable: time eager launches
+            log(f"decode graph capture failed ({e}); timing eager launches")
+            fn = run_all
+    gl.timing_reset()
+    gl.timing_enable(True)
+    ms = timed(torch, fn, 3, 1)
+    k = kernel_avgs(gl)
+    gl.timing_enable(False)
+    step_us = ms * 1e3 / n
+    kern_us = k["decode"][0]
+    res = {"mode": mode, "us_per_step": step_us,
+           "seq_tokens_per_s": S * n / (ms * 1e-3),
+           "hbm_GBps_algorithmic": per_step_bytes / (step_us * 1e-6) / 1e9,
+           "frac_hbm_peak": per_step_bytes / (step_us * 1e-6) / PEAK_HBM,
+           "bytes_per_step": per_step_bytes}
+    if kern_us:
+        res["kernel_avg_us"] = kern_us
+        res["kernel_GBps_algorithmic"] = per_step_bytes / (kern_us * 1e-6) / 1e9
+        res["kernel_frac_hbm_peak"] = per_step_bytes / (kern_us * 1e-6) / PEAK_HBM
+    del state, xs, gs, ys
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the GradLev scan shards over (batch, head) with no "
+              "communication, and this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_34174_amd as gl
+    from paper_2609_34174_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    gl.lib()
+
+    wl = W.SCAN_WORKLOADS[args.workload]
+    log(f"workload {wl.name}: preparing inputs")
+    run = ScanRunner(gl, torch, W, wl, 2, device)
+    plan = run.plan
+    work = scan_work(wl, plan)
+
+    log(f"warmup {args.warmup} + timed {args.steps} steps")
+    gl.timing_reset()
+    for i in range(args.warmup):
+        run.step(i)
+    torch.cuda.synchronize()
+    gl.timing_enable(True)
+    gl.timing_reset()
+    ms = timed(torch, run.step, args.steps, 0)
+    k = kernel_avgs(gl)
+    gl.timing_enable(False)
+    log(f"{ms:.4f} ms/step; kernels (us): " + ", ".join(f"{n}={v[0]:.1f}" for n, v in k.items() if v[0]))
+
+    step_s = ms * 1e-3
+    tokens = wl.B * wl.T
+    es = 2 if wl.dtype == "bf16" else 4
+    th = wl.B * wl.H * wl.T
+    # Dominant kernel: the chunked backward scan.
+    dom = "bwd_main"
+    dom_us = k[dom][0]
+    dom_bytes = th * bytes_bwd(wl.d, wl.m, es)
+    achieved = dom_bytes / (dom_us * 1e-6)
+    traffic = load_traffic(dom)
+    roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM, "traffic": traffic, "kernel": dom,
+                "kernel_avg_us": dom_us, "algorithmic_bytes_per_launch": dom_bytes}
+    result = {
+        "metric": METRIC,
+        "value": tokens / step_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic: seeded device RNG with the workload's shapes and distributions",
+        "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_in": wl.d, "d_out": wl.m,
+                   "chunk": wl.chunk, "eta": wl.eta, "prefix": "exclusive",
+                   "step": "scan_fwd + scan_bwd with gtilde, dX, dG, deta, dW0",
+                   "plan": {"fwd": [plan.fwd_chunk, plan.fwd_segment, plan.fwd_nseg],
+                            "bwd": [plan.bwd_chunk, plan.bwd_segment, plan.bwd_nseg]}},
+        "roofline": roofline,
+        "step_roofline": {"hbm_GBps_algorithmic": work["bytes"] / step_s / 1e9,
+                          "frac_hbm_peak": work["bytes"] / step_s / PEAK_HBM,
+                          "tflops_algorithmic": work["flops"] / step_s / 1e12,
+                          "frac_bf16_mfma_peak": work["flops"] / step_s / PEAK_BF16},
+        "kernel_avg_us": {n: round(v[0], 3) for n, v in k.items() if v[0] is not None},
+    }
+
+    if not args.no_secondary:
+        sec = {}
+        for name in ("long-bf16", "stack-bf16"):
+            log(f"secondary {name}")
+            sec[name] = secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
+        log("secondary decode-f32")
+        sec["decode-f32"] = secondary_decode(gl, torch, W, device)
+        result["secondary"] = sec
+
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on the host")
+        result["cpu_baseline"] = cpu_baseline(W, wl, args.cpu_sample_batch)
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * gradlev.h - C ABI of the GradLev fast-weight scan library for MI355X (gfx950).
+ *
+ * GradLev (arXiv 2609.34174) adapts a linear map y_t = W_t x_t by online
+ * gradient descent with unit retention (Section 3, Eq. 2):
+ *
+ *     W_{t+1} = W_t - eta_t g_t x_t^T,      W_t = W_0 + Delta_t,   Delta_0 = 0.
+ *
+ * Given every token's input x_t and proposed costate g_t up front (Section 3,
+ * step 1), the adapted weights are a prefix sum of rank-1 writes and the whole
+ * sequence is evaluated in parallel (Section 3, steps 2-3; Appendix C, Eq. 16).
+ * This library computes that scan, its backward, and the token-by-token
+ * deployment update on the GPU.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All array arguments are caller-owned DEVICE pointers, row-major and
+ *   contiguous, 16-byte aligned.  The library never allocates device memory,
+ *   never frees caller memory and keeps no pointer after a call returns.
+ * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *   default stream).  Results are valid once the stream has been synchronised.
+ * - Every entry point validates its arguments on the host BEFORE touching the
+ *   HIP runtime, and returns a status code; nothing is thrown across the ABI.
+ *   On any error no work has been enqueued, except GRADLEV_ERR_HIP, which
+ *   reports a failed launch.
+ * - Outputs must not overlap inputs or each other (decode's W is in/out).
+ * - Floating point: X, G and dY are fp32 or bf16 (values as stored, bf16 being
+ *   round-to-nearest-even storage).  W_0, eta, fast states and every output are
+ *   fp32, following the paper's precision contract of 16-bit activations with
+ *   32-bit parameters and fast states (Appendix E, "Numerical implementation").
+ *   Contractions run on the MFMA units with fp32 accumulation; fp32 states are
+ *   split into two bf16 terms when they meet bf16 operands.
+ */
+#ifndef GRADLEV_H
+#define GRADLEV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of X, G and dY. */
+enum { GRADLEV_F32 = 0, GRADLEV_BF16 = 1 };
+
+/* Read convention of the scans.
+ * EXCLUSIVE (the paper's, Section 3 step 2 and Appendix C): token t reads the
+ *   weights before its own write, y_t = (W_0 + Delta_t) x_t.
+ * INCLUSIVE: token t reads after its own write, y_t = (W_0 + Delta_{t+1}) x_t. */
+enum { GRADLEV_EXCLUSIVE = 0, GRADLEV_INCLUSIVE = 1 };
+
+/* Status codes. */
+enum {
+  GRADLEV_OK = 0,
+  GRADLEV_ERR_INVALID = -1,     /* NULL required pointer, non-positive size, bad enum */
+  GRADLEV_ERR_UNSUPPORTED = -2, /* valid but outside the compiled shapes */
+  GRADLEV_ERR_ALIGN = -3,       /* a pointer is not 16-byte aligned */
+  GRADLEV_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required */
+  GRADLEV_ERR_HIP = -5          /* a HIP launch failed */
+};
+
+/* Problem description for the scans.
+ *   B, H      batch and heads; each (b, h) is an independent sequence (>= 1)
+ *   T         tokens per sequence (>= 1, any value; a partial last chunk is masked)
+ *   d_in      input width d of the adapted map  (64 or 128)
+ *   d_out     output width m of the adapted map (64 or 128)
+ *   chunk     intra-chunk tile length hint: 0 (library default), 64 or 128.
+ *             It changes the rounding order only, never the result in exact
+ *             arithmetic; the library may use a smaller tile where a kernel's
+ *             LDS budget requires it.
+ *   segment   tokens per workgroup segment hint: 0 (library default) or a
+ *             positive multiple of 64.  Segments of one sequence run in
+ *             parallel and are joined by an fp32 carry of their aggregated
+ *             writes; like `chunk` it changes the rounding order only.
+ *   in_dtype  GRADLEV_F32 or GRADLEV_BF16
+ *   prefix    GRADLEV_EXCLUSIVE or GRADLEV_INCLUSIVE */
+typedef struct gradlev_shape {
+  int64_t B, H, T, d_in, d_out;
+  int64_t chunk;
+  int64_t segment;
+  int32_t in_dtype;
+  int32_t prefix;
+} gradlev_shape;
+
+/* How a call will be executed (for callers sizing grids or counting work). */
+typedef struct gradlev_plan {
+  int64_t fwd_chunk, fwd_segment, fwd_nseg; /* tile, tokens/segment, segments per sequence */
+  int64_t bwd_chunk, bwd_segment, bwd_nseg;
+  size_t workspace_bytes;                   /* bytes needed by fwd and by bwd */
+} gradlev_plan;
+
+/* Fills *plan for shape *s.  Pure host computation, no HIP call.
+ * Returns GRADLEV_OK, GRADLEV_ERR_INVALID or GRADLEV_ERR_UNSUPPORTED. */
+int gradlev_scan_plan(const gradlev_shape* s, gradlev_plan* plan);
+
+/* Workspace bytes that gradlev_scan_fwd and gradlev_scan_bwd need for *s
+ * (written to *bytes; may be 0).  Pure host computation.
+ * The workspace is scratch: its contents on entry are ignored and on exit are
+ * unspecified.  One workspace must not be shared by calls that may overlap. */
+int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes);
+
+/* Forward scan (Section 3 step 2, Eq. 3; Appendix C, Eq. 16, first line).
+ *
+ *   Y[b,h,t,:] = (W0[h] + Delta_t) X[b,h,t,:],
+ *   Delta_t    = - sum_{s<t} eta[b,h,s] G[b,h,s,:] X[b,h,s,:]^T   (s<=t if INCLUSIVE)
+ *
+ *   W0   [H, m, d]     fp32   slow weights W_0, shared over the batch
+ *   X    [B, H, T, d]  in_dtype  map inputs x_t
+ *   G    [B, H, T, m]  in_dtype  proposed costates g_hat_t
+ *   eta  [B, H, T]     fp32   per-token step sizes, or NULL to use eta_scalar
+ *   Y    [B, H, T, m]  fp32   output (fully overwritten)
+ *   workspace / workspace_bytes: device scratch of at least
+ *        gradlev_scan_workspace_bytes(s) bytes (may be NULL if that is 0). */
+int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X,
+                     const void* G, const float* eta, float eta_scalar, float* Y,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of the forward scan for an upstream gradient dY = dL/dY.
+ *
+ * Read side (Section 3 step 3, Eq. 4; Appendix C, Eq. 16, second line) - the
+ * paper's grounded costate target for the map input:
+ *   gtilde[b,h,t,:] = (W0[h] + Delta_t)^T dY[b,h,t,:]     (Delta_{t+1} if INCLUSIVE)
+ * Reverse-time terms (vector-Jacobian product through the prefix sums, with
+ * suffix R_t = sum_{u>t} dY_u X_u^T, u>=t if INCLUSIVE):
+ *   u_t      = -R_t X_t
+ *   dG[t]    = eta_t u_t                       dL/dG
+ *   deta[t]  = <G_t, u_t>                      dL/deta
+ *   dX[t]    = gtilde_t - eta_t R_t^T G_t      total dL/dX (read + write side)
+ *   dW0[h]   = sum_b sum_t dY_t X_t^T          dL/dW0, summed over the batch
+ * The paper's own training detaches writes (Appendix E, "Initialization and
+ * gradients") and uses gtilde only; pass NULL for outputs you do not need and
+ * their work is skipped.  At least one output must be non-NULL.
+ *
+ *   dY      [B, H, T, m] in_dtype
+ *   gtilde  [B, H, T, d] fp32 or NULL      dX [B, H, T, d] fp32 or NULL
+ *   dG      [B, H, T, m] fp32 or NULL      deta [B, H, T] fp32 or NULL
+ *   dW0     [H, m, d]    fp32 or NULL (overwritten)
+ * Other arguments as in gradlev_scan_fwd.  Reductions are in a fixed order, so
+ * repeated calls are bitwise identical. */
+int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X,
+                     const void* G, const float* eta, float eta_scalar,
+                     const void* dY, float* gtilde, float* dX, float* dG,
+                     float* deta, float* dW0, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
+/* One deployment step for S sequences x H heads (Section 3, "Training
+ * objective", last sentences; Appendix A, last sentence): score with the
+ * current weights, then write the true costate.
+ *
+ *   y[s,h,:]   = W[s,h] x[s,h,:]                       (before the write)
+ *   W[s,h]    <- W[s,h] - eta[s,h] g[s,h,:] x[s,h,:]^T
+ *
+ *   W    [S, H, d_out, d_in] fp32  fast weights, updated in place
+ *   x    [S, H, d_in]  fp32        g [S, H, d_out] fp32
+ *   eta  [S, H] fp32 or NULL (then eta_scalar)
+ *   y    [S, H, d_out] fp32 output
+ * Supported: d_in in {16, 32, 64, 128, 256}; d_out in [1, 1024].
+ * Exclusive only: deployment needs y before the costate g exists. */
+int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
+                        float* W, const float* x, const float* g,
+                        const float* eta, float eta_scalar, float* y,
+                        void* stream);
+
+/* Kernel timing for benchmarks and tracing.  While enabled, every kernel the
+ * library launches is bracketed by HIP events recorded on the caller's stream
+ * (events are created by the library on first use and reused; no device
+ * memory is allocated).  gradlev_timing_read waits for the recorded events and
+ * returns, for one kernel family, the summed duration in milliseconds and the
+ * number of launches since the last reset.  Not thread-safe: use from one host
+ * thread.  At most 65536 launches per family are kept between resets.
+ * Families: */
+enum {
+  GRADLEV_K_FWD_AGG = 0,   /* per-segment write aggregates (forward)      */
+  GRADLEV_K_FWD_CARRY = 1, /* cross-segment prefix (forward)              */
+  GRADLEV_K_FWD_MAIN = 2,  /* chunked forward scan                         */
+  GRADLEV_K_BWD_AGG = 3,   /* per-segment aggregates (backward)           */
+  GRADLEV_K_BWD_CARRY = 4, /* cross-segment prefix/suffix (backward)      */
+  GRADLEV_K_BWD_MAIN = 5,  /* chunked backward scan                        */
+  GRADLEV_K_BWD_DW0 = 6,   /* batch reduction of dW0                       */
+  GRADLEV_K_DECODE = 7,    /* deployment step                              */
+  GRADLEV_K_COUNT = 8
+};
+int gradlev_timing_enable(int on);   /* returns the previous setting */
+int gradlev_timing_reset(void);
+int gradlev_timing_read(int family, double* ms, int64_t* launches);
+
+/* Static, human-readable text for a status code. */
+const char* gradlev_error_string(int code);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int gradlev_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRADLEV_H */

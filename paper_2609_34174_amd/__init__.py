@@ -1,0 +1,289 @@
+"""GradLev fast-weight scans on MI355X (gfx950): thin Python binding.
+
+Every function here only marshals arguments (shapes, dtypes, device
+pointers, the current HIP stream) into the C ABI of ``libgradlev.so``
+(declared in ``include/gradlev.h``).  All arithmetic runs in the library's
+HIP kernels; there is no fallback: if the library is not built, or a tensor
+is not on a ROCm device, a call raises.
+
+    import paper_2609_34174_amd as gl
+    Y = gl.scan_fwd(W0, X, G, eta=0.1)
+    out = gl.scan_bwd(W0, X, G, dY, eta=0.1)     # dict of gradients
+    y = gl.decode_step(W, x, g, eta=0.1)          # updates W in place
+
+Shapes: W0 [H,m,d] fp32; X [B,H,T,d], G/dY [B,H,T,m] (fp32 or bf16, all
+three the same); eta a float or an fp32 [B,H,T] tensor.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "libgradlev.so")
+
+F32, BF16 = 0, 1
+EXCLUSIVE, INCLUSIVE = 0, 1
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4, -5
+
+_PREFIX = {"exclusive": EXCLUSIVE, "inclusive": INCLUSIVE}
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("H", ctypes.c_int64), ("T", ctypes.c_int64),
+                ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64),
+                ("chunk", ctypes.c_int64), ("segment", ctypes.c_int64),
+                ("in_dtype", ctypes.c_int32), ("prefix", ctypes.c_int32)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("fwd_chunk", ctypes.c_int64), ("fwd_segment", ctypes.c_int64),
+                ("fwd_nseg", ctypes.c_int64), ("bwd_chunk", ctypes.c_int64),
+                ("bwd_segment", ctypes.c_int64), ("bwd_nseg", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+class GradLevError(RuntimeError):
+    def __init__(self, code, what):
+        super().__init__(f"{what}: {error_string(code)} (status {code})")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"GradLev HIP library not built ({LIB_PATH}); run "
+                               "`python -m paper_2609_34174_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, f32p = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p
+        L.gradlev_version.restype = ctypes.c_int
+        L.gradlev_error_string.restype = ctypes.c_char_p
+        L.gradlev_error_string.argtypes = [ctypes.c_int]
+        L.gradlev_scan_plan.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(Plan)]
+        L.gradlev_scan_workspace_bytes.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(ctypes.c_size_t)]
+        L.gradlev_scan_fwd.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
+                                       f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_bwd.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
+                                       vp, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_decode_step.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p,
+                                          ctypes.c_float, f32p, vp]
+        L.gradlev_timing_enable.argtypes = [ctypes.c_int]
+        L.gradlev_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_int64)]
+        for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd",
+                     "gradlev_scan_bwd", "gradlev_decode_step", "gradlev_timing_enable",
+                     "gradlev_timing_reset", "gradlev_timing_read"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def error_string(code: int) -> str:
+    return lib().gradlev_error_string(int(code)).decode()
+
+
+def make_shape(B, H, T, d_in, d_out, dtype=BF16, prefix="exclusive", chunk=0, segment=0) -> Shape:
+    return Shape(int(B), int(H), int(T), int(d_in), int(d_out), int(chunk), int(segment),
+                 int(dtype), _PREFIX[prefix] if isinstance(prefix, str) else int(prefix))
+
+
+def plan(shape: Shape) -> Plan:
+    p = Plan()
+    rc = lib().gradlev_scan_plan(ctypes.byref(shape), ctypes.byref(p))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_plan")
+    return p
+
+
+def workspace_bytes(shape: Shape) -> int:
+    n = ctypes.c_size_t(0)
+    rc = lib().gradlev_scan_workspace_bytes(ctypes.byref(shape), ctypes.byref(n))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_workspace_bytes")
+    return int(n.value)
+
+
+# ---------------------------------------------------------------------------
+# torch marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_dev(name, t, dtype=None, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a ROCm GPU (got {t.device}); there is no CPU path")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _scan_shape(W0, X, G, prefix, chunk, segment):
+    torch = _torch()
+    _check_dev("X", X)
+    if X.dim() != 4:
+        raise ValueError("X must be [B, H, T, d]")
+    B, H, T, d = X.shape
+    if X.dtype == torch.bfloat16:
+        dt = BF16
+    elif X.dtype == torch.float32:
+        dt = F32
+    else:
+        raise TypeError("X must be float32 or bfloat16")
+    _check_dev("G", G, X.dtype)
+    if G.dim() != 4 or tuple(G.shape[:3]) != (B, H, T):
+        raise ValueError("G must be [B, H, T, m]")
+    m = G.shape[3]
+    _check_dev("W0", W0, torch.float32, (H, m, d))
+    return make_shape(B, H, T, d, m, dt, prefix, chunk, segment)
+
+
+def _eta_args(eta, B, H, T, X):
+    torch = _torch()
+    if isinstance(eta, torch.Tensor):
+        _check_dev("eta", eta, torch.float32, (B, H, T))
+        if eta.device != X.device:
+            raise ValueError("eta must be on the same device as X")
+        return eta, 0.0
+    return None, float(eta)
+
+
+def _workspace(shape, device, workspace):
+    torch = _torch()
+    need = workspace_bytes(shape)
+    if need == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def scan_fwd(W0, X, G, eta=0.1, *, prefix="exclusive", chunk=0, segment=0, out=None, workspace=None):
+    """Forward scan; returns Y [B,H,T,m] fp32 (see gradlev_scan_fwd)."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, prefix, chunk, segment)
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    if out is None:
+        out = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    _check_dev("out", out, torch.float32, (s.B, s.H, s.T, s.d_out))
+    ws, wsn = _workspace(s, X.device, workspace)
+    rc = lib().gradlev_scan_fwd(ctypes.byref(s), _ptr(W0), _ptr(X), _ptr(G), _ptr(e), es, _ptr(out),
+                                _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_fwd")
+    return out
+
+
+BWD_OUTPUTS = ("gtilde", "dx", "dg", "deta", "dw0")
+
+
+def scan_bwd(W0, X, G, dY, eta=0.1, *, prefix="exclusive", chunk=0, segment=0,
+             outputs=BWD_OUTPUTS, out=None, workspace=None):
+    """Backward of the forward scan; returns a dict with the requested outputs.
+
+    outputs: any of "gtilde" [B,H,T,d], "dx" [B,H,T,d], "dg" [B,H,T,m],
+    "deta" [B,H,T], "dw0" [H,m,d] (all fp32).  ``out`` may pre-supply tensors.
+    """
+    torch = _torch()
+    s = _scan_shape(W0, X, G, prefix, chunk, segment)
+    _check_dev("dY", dY, X.dtype, (s.B, s.H, s.T, s.d_out))
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    shapes = {"gtilde": (s.B, s.H, s.T, s.d_in), "dx": (s.B, s.H, s.T, s.d_in),
+              "dg": (s.B, s.H, s.T, s.d_out), "deta": (s.B, s.H, s.T), "dw0": (s.H, s.d_out, s.d_in)}
+    res = dict(out or {})
+    for k in outputs:
+        if k not in shapes:
+            raise ValueError(f"unknown output {k!r}")
+        if k not in res:
+            res[k] = torch.empty(shapes[k], dtype=torch.float32, device=X.device)
+        _check_dev(k, res[k], torch.float32, shapes[k])
+    ws, wsn = _workspace(s, X.device, workspace)
+    rc = lib().gradlev_scan_bwd(ctypes.byref(s), _ptr(W0), _ptr(X), _ptr(G), _ptr(e), es, _ptr(dY),
+                                _ptr(res.get("gtilde")), _ptr(res.get("dx")), _ptr(res.get("dg")),
+                                _ptr(res.get("deta")), _ptr(res.get("dw0")), _ptr(ws), wsn,
+                                _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_bwd")
+    return res
+
+
+def decode_step(W, x, g, eta=0.1, *, out=None):
+    """One deployment step: returns y = W x and updates W <- W - eta g x^T in place."""
+    torch = _torch()
+    _check_dev("W", W, torch.float32)
+    if W.dim() != 4:
+        raise ValueError("W must be [S, H, m, d]")
+    S, H, m, d = W.shape
+    _check_dev("x", x, torch.float32, (S, H, d))
+    _check_dev("g", g, torch.float32, (S, H, m))
+    if isinstance(eta, torch.Tensor):
+        _check_dev("eta", eta, torch.float32, (S, H))
+        e, es = eta, 0.0
+    else:
+        e, es = None, float(eta)
+    if out is None:
+        out = torch.empty(S, H, m, dtype=torch.float32, device=W.device)
+    _check_dev("out", out, torch.float32, (S, H, m))
+    rc = lib().gradlev_decode_step(S, H, d, m, _ptr(W), _ptr(x), _ptr(g), _ptr(e), es, _ptr(out),
+                                   _stream(W.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_decode_step")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Kernel timing (HIP events recorded by the library around each launch)
+# ---------------------------------------------------------------------------
+
+KERNELS = ("fwd_agg", "fwd_carry", "fwd_main", "bwd_agg", "bwd_carry", "bwd_main", "bwd_dw0", "decode")
+
+
+def timing_enable(on: bool = True) -> bool:
+    """Turn per-launch event timing on or off; returns the previous setting."""
+    return bool(lib().gradlev_timing_enable(1 if on else 0))
+
+
+def timing_reset() -> None:
+    lib().gradlev_timing_reset()
+
+
+def timing_read() -> dict:
+    """{kernel: (total_ms, launches)} since the last reset (waits for the events)."""
+    out = {}
+    for i, name in enumerate(KERNELS):
+        ms, n = ctypes.c_double(0.0), ctypes.c_int64(0)
+        rc = lib().gradlev_timing_read(i, ctypes.byref(ms), ctypes.byref(n))
+        if rc != OK:
+            raise GradLevError(rc, "gradlev_timing_read")
+        out[name] = (ms.value, int(n.value))
+    return out
+
+
+__all__ = ["timing_enable", "timing_reset", "timing_read", "KERNELS", "scan_fwd", "scan_bwd", "decode_step", "plan", "workspace_bytes", "make_shape",
+           "error_string", "lib", "GradLevError", "Shape", "Plan", "F32", "BF16",
+           "EXCLUSIVE", "INCLUSIVE", "BWD_OUTPUTS"]

@@ -1,0 +1,217 @@
+// C ABI of the GradLev scan library: argument validation, work planning,
+// workspace layout and dispatch to the gfx950 kernels.  Every check runs on
+// the host before any HIP runtime call, so invalid calls return a status code
+// without touching a device.
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/gradlev.h"
+#include "internal.hpp"
+
+namespace gradlev {
+namespace {
+
+constexpr int kNumCU = 256;           // MI355X compute units
+constexpr int64_t kMaxElems = int64_t(1) << 40;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Plan {
+  ScanProblem fwd, bwd;
+  size_t ws_fwd, ws_bwd;
+  // Offsets (bytes) inside the workspace.
+  size_t off_aggA, off_aggB, off_rfin;
+};
+
+int64_t pick_nseg(int64_t BH, int64_t T, int C, int wgs_per_cu, int64_t hint) {
+  const int64_t nchunks = (T + C - 1) / C;
+  int64_t seg_chunks;
+  if (hint > 0) {
+    seg_chunks = (hint + C - 1) / C;
+  } else {
+    const int64_t target = (int64_t)kNumCU * wgs_per_cu;
+    int64_t nseg = (target + BH - 1) / BH;
+    if (nseg < 1) nseg = 1;
+    if (nseg > nchunks) nseg = nchunks;
+    seg_chunks = (nchunks + nseg - 1) / nseg;
+  }
+  if (seg_chunks < 1) seg_chunks = 1;
+  return seg_chunks;
+}
+
+int make_plan(const gradlev_shape* s, Plan* out) {
+  if (!s || !out) return GRADLEV_ERR_INVALID;
+  if (s->B < 1 || s->H < 1 || s->T < 1 || s->d_in < 1 || s->d_out < 1) return GRADLEV_ERR_INVALID;
+  if (s->in_dtype != GRADLEV_F32 && s->in_dtype != GRADLEV_BF16) return GRADLEV_ERR_INVALID;
+  if (s->prefix != GRADLEV_EXCLUSIVE && s->prefix != GRADLEV_INCLUSIVE) return GRADLEV_ERR_INVALID;
+  if (s->chunk < 0 || s->segment < 0) return GRADLEV_ERR_INVALID;
+  if ((s->d_in != 64 && s->d_in != 128) || (s->d_out != 64 && s->d_out != 128)) return GRADLEV_ERR_UNSUPPORTED;
+  if (s->chunk != 0 && s->chunk != 64 && s->chunk != 128) return GRADLEV_ERR_UNSUPPORTED;
+  if (s->segment % 64 != 0) return GRADLEV_ERR_UNSUPPORTED;
+  const int64_t BH = s->B * s->H;
+  if (s->B > kMaxElems / s->H || BH > kMaxElems / s->T) return GRADLEV_ERR_UNSUPPORTED;
+  const int64_t wmax = s->d_in > s->d_out ? s->d_in : s->d_out;
+  if (BH * s->T > kMaxElems / wmax) return GRADLEV_ERR_UNSUPPORTED;
+  if (BH > 65535) return GRADLEV_ERR_UNSUPPORTED;  // grid y limit
+
+  const int bf = s->in_dtype == GRADLEV_BF16;
+  const int d = (int)s->d_in, m = (int)s->d_out;
+  const size_t md = (size_t)m * d * sizeof(float);
+
+  ScanProblem base{};
+  base.B = s->B;
+  base.H = s->H;
+  base.T = s->T;
+  base.d = d;
+  base.m = m;
+  base.bf16 = bf;
+  base.inclusive = s->prefix == GRADLEV_INCLUSIVE;
+
+  out->fwd = base;
+  out->fwd.chunk = fwd_chunk_for(bf, d, m, (int)s->chunk);
+  int64_t sc = pick_nseg(BH, s->T, out->fwd.chunk, fwd_wgs_per_cu(bf, d, m, out->fwd.chunk), s->segment);
+  out->fwd.seg_len = sc * out->fwd.chunk;
+  out->fwd.nseg = (s->T + out->fwd.seg_len - 1) / out->fwd.seg_len;
+  if (out->fwd.nseg > 65535) return GRADLEV_ERR_UNSUPPORTED;
+
+  out->bwd = base;
+  out->bwd.chunk = bwd_chunk_for(bf, d, m, (int)s->chunk);
+  sc = pick_nseg(BH, s->T, out->bwd.chunk, bwd_wgs_per_cu(bf, d, m, out->bwd.chunk), s->segment);
+  out->bwd.seg_len = sc * out->bwd.chunk;
+  out->bwd.nseg = (s->T + out->bwd.seg_len - 1) / out->bwd.seg_len;
+  if (out->bwd.nseg > 65535) return GRADLEV_ERR_UNSUPPORTED;
+
+  out->ws_fwd = out->fwd.nseg > 1 ? round_up((size_t)BH * out->fwd.nseg * md, 256) : 0;
+  out->off_aggA = 0;
+  out->off_aggB = round_up((size_t)BH * out->bwd.nseg * md, 256);
+  out->off_rfin = out->off_aggB + (out->bwd.nseg > 1 ? round_up((size_t)BH * out->bwd.nseg * md, 256) : 0);
+  out->ws_bwd = out->off_rfin + round_up((size_t)BH * md, 256);
+  return GRADLEV_OK;
+}
+
+int check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return GRADLEV_OK;
+  if (!ws || have < need) return GRADLEV_ERR_WORKSPACE;
+  if (!aligned16(ws)) return GRADLEV_ERR_ALIGN;
+  return GRADLEV_OK;
+}
+
+}  // namespace
+}  // namespace gradlev
+
+using namespace gradlev;
+
+extern "C" {
+
+int gradlev_version(void) { return 100; }
+
+const char* gradlev_error_string(int code) {
+  switch (code) {
+    case GRADLEV_OK: return "success";
+    case GRADLEV_ERR_INVALID: return "invalid argument (null pointer, non-positive size or unknown enum)";
+    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64)";
+    case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
+    case GRADLEV_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status code";
+  }
+}
+
+int gradlev_scan_plan(const gradlev_shape* s, gradlev_plan* plan) {
+  if (!plan) return GRADLEV_ERR_INVALID;
+  Plan p;
+  const int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  plan->fwd_chunk = p.fwd.chunk;
+  plan->fwd_segment = p.fwd.seg_len;
+  plan->fwd_nseg = p.fwd.nseg;
+  plan->bwd_chunk = p.bwd.chunk;
+  plan->bwd_segment = p.bwd.seg_len;
+  plan->bwd_nseg = p.bwd.nseg;
+  plan->workspace_bytes = p.ws_fwd > p.ws_bwd ? p.ws_fwd : p.ws_bwd;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
+  if (!bytes) return GRADLEV_ERR_INVALID;
+  Plan p;
+  const int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  *bytes = p.ws_fwd > p.ws_bwd ? p.ws_fwd : p.ws_bwd;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                     const float* eta, float eta_scalar, float* Y, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  Plan p;
+  int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
+  if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
+    return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.ws_fwd);
+  if (rc != GRADLEV_OK) return rc;
+  FwdPtrs f{};
+  f.W0 = W0;
+  f.X = X;
+  f.G = G;
+  f.eta = eta;
+  f.eta_scalar = eta_scalar;
+  f.Y = Y;
+  f.agg = static_cast<float*>(workspace);
+  const hipError_t e = launch_scan_fwd(p.fwd, f, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                     const float* eta, float eta_scalar, const void* dY, float* gtilde,
+                     float* dX, float* dG, float* deta, float* dW0, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  Plan p;
+  int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
+  if (!gtilde && !dX && !dG && !deta && !dW0) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dW0};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.ws_bwd);
+  if (rc != GRADLEV_OK) return rc;
+  char* ws = static_cast<char*>(workspace);
+  BwdPtrs b{};
+  b.W0 = W0;
+  b.X = X;
+  b.G = G;
+  b.eta = eta;
+  b.eta_scalar = eta_scalar;
+  b.dY = dY;
+  b.gtilde = gtilde;
+  b.dX = dX;
+  b.dG = dG;
+  b.deta = deta;
+  b.dW0 = dW0;
+  b.aggA = reinterpret_cast<float*>(ws + p.off_aggA);
+  b.aggB = reinterpret_cast<float*>(ws + p.off_aggB);
+  b.rfin = reinterpret_cast<float*>(ws + p.off_rfin);
+  const hipError_t e = launch_scan_bwd(p.bwd, b, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out, float* W, const float* x,
+                        const float* g, const float* eta, float eta_scalar, float* y, void* stream) {
+  if (S < 1 || H < 1 || d_in < 1 || d_out < 1) return GRADLEV_ERR_INVALID;
+  if (!W || !x || !g || !y) return GRADLEV_ERR_INVALID;
+  if (d_in != 16 && d_in != 32 && d_in != 64 && d_in != 128 && d_in != 256) return GRADLEV_ERR_UNSUPPORTED;
+  if (d_out > 1024) return GRADLEV_ERR_UNSUPPORTED;
+  if (S > kMaxElems / H || S * H > 0x7fffffff) return GRADLEV_ERR_UNSUPPORTED;
+  if (!aligned16(W) || !aligned16(x) || !aligned16(g) || !aligned16(y) || (eta && !aligned16(eta)))
+    return GRADLEV_ERR_ALIGN;
+  const hipError_t e = launch_decode(S, H, (int)d_in, (int)d_out, W, x, g, eta, eta_scalar, y,
+                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+}  // extern "C"

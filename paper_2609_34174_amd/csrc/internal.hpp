@@ -1,0 +1,64 @@
+// Host-side interface between the C ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gradlev {
+
+// One forward/backward problem after validation and planning.
+struct ScanProblem {
+  int64_t B, H, T;
+  int d, m;          // d_in, d_out
+  int bf16;          // 1: X, G, dY are bf16; 0: fp32
+  int inclusive;     // 1: inclusive reads
+  int chunk;         // effective tile length of the kernel in use
+  int64_t seg_len;   // tokens per segment (multiple of chunk)
+  int64_t nseg;      // segments per sequence
+};
+
+struct FwdPtrs {
+  const float* W0;
+  const void* X;
+  const void* G;
+  const float* eta;
+  float eta_scalar;
+  float* Y;
+  float* agg;  // [B*H][nseg][m][d] workspace, or nullptr when nseg == 1
+};
+
+struct BwdPtrs {
+  const float* W0;
+  const void* X;
+  const void* G;
+  const float* eta;
+  float eta_scalar;
+  const void* dY;
+  float* gtilde;
+  float* dX;
+  float* dG;
+  float* deta;
+  float* dW0;
+  float* aggA;  // [B*H][nseg][m][d]: segment write aggregates -> inclusive prefix
+  float* aggB;  // [B*H][nseg][m][d]: segment dY x^T aggregates -> exclusive suffix
+  float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
+};
+
+// Tile lengths each kernel family supports for a shape (LDS budget).
+int fwd_chunk_for(int bf16, int d, int m, int requested);
+int bwd_chunk_for(int bf16, int d, int m, int requested);
+// Resident workgroups per CU for the main kernels (LDS bound).
+int fwd_wgs_per_cu(int bf16, int d, int m, int chunk);
+int bwd_wgs_per_cu(int bf16, int d, int m, int chunk);
+
+// Optional event timing around each kernel launch (see gradlev_timing_*).
+void timing_begin(int family, hipStream_t s);
+void timing_end(int family, hipStream_t s);
+
+hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& a, hipStream_t s);
+hipError_t launch_scan_bwd(const ScanProblem& p, const BwdPtrs& a, hipStream_t s);
+hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const float* x,
+                         const float* g, const float* eta, float eta_scalar, float* y,
+                         hipStream_t s);
+
+}  // namespace gradlev

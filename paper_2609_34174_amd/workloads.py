@@ -92,10 +92,13 @@ DECODE_WORKLOADS = {
 def round_bf16(a: np.ndarray) -> np.ndarray:
     """Round to the nearest bfloat16 (ties to even); returns float32 values."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    out = (u.astype(np.uint32) << 16).view(np.float32)
-    # NaN/Inf never occur in these workloads; keep them as they are anyway.
+    u = a.view(np.uint32)
+    # Adding 0x7FFF plus the lowest kept bit and truncating is round-to-nearest-
+    # even on the upper 16 bits.  Finite inputs never wrap in uint32.
+    r = ((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF)
+    r += u
+    r &= np.uint32(0xFFFF0000)
+    out = r.view(np.float32)
     bad = ~np.isfinite(a)
     if bad.any():
         out = np.where(bad, a, out)

@@ -1,0 +1,147 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+The library must load, export every symbol that include/gradlev.h declares,
+and reject invalid calls with the documented status codes before touching
+the HIP runtime.  Pointers passed here are fake but never dereferenced,
+because every call below fails validation.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_34174_amd as gl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gradlev.h")
+
+FAKE = ctypes.c_void_p(1 << 20)        # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p((1 << 20) + 8)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(gl.LIB_PATH):
+        pytest.skip("library not built")
+    return gl.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gradlev_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("gradlev_scan_fwd", "gradlev_scan_bwd", "gradlev_decode_step",
+                     "gradlev_scan_workspace_bytes", "gradlev_scan_plan", "gradlev_error_string"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_error_strings(L):
+    for code in (0, -1, -2, -3, -4, -5, 7):
+        assert isinstance(gl.error_string(code), str) and gl.error_string(code)
+    assert gl.error_string(0) == "success"
+
+
+def shape(**kw):
+    base = dict(B=2, H=4, T=300, d_in=64, d_out=64, dtype=gl.BF16, prefix="exclusive")
+    base.update(kw)
+    return gl.make_shape(**base)
+
+
+def plan_rc(s):
+    p = gl.Plan()
+    return gl.lib().gradlev_scan_plan(ctypes.byref(s), ctypes.byref(p)), p
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(B=0), gl.ERR_INVALID), (dict(H=-1), gl.ERR_INVALID), (dict(T=0), gl.ERR_INVALID),
+    (dict(d_in=0), gl.ERR_INVALID), (dict(dtype=7), gl.ERR_INVALID), (dict(prefix=3), gl.ERR_INVALID),
+    (dict(chunk=-64), gl.ERR_INVALID), (dict(d_in=96), gl.ERR_UNSUPPORTED),
+    (dict(d_out=256), gl.ERR_UNSUPPORTED), (dict(chunk=32), gl.ERR_UNSUPPORTED),
+    (dict(segment=100), gl.ERR_UNSUPPORTED),
+])
+def test_plan_rejects(L, bad, code):
+    rc, _ = plan_rc(shape(**bad))
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(dtype=gl.F32), dict(d_in=128, d_out=128),
+                                dict(d_in=64, d_out=128), dict(d_in=128, d_out=64, dtype=gl.F32),
+                                dict(T=1), dict(T=16384, B=2, H=16, d_in=128, d_out=128, chunk=128),
+                                dict(segment=64), dict(prefix="inclusive")])
+def test_plan_is_consistent(L, kw):
+    s = shape(**kw)
+    rc, p = plan_rc(s)
+    assert rc == gl.OK
+    for C, seg, n in ((p.fwd_chunk, p.fwd_segment, p.fwd_nseg), (p.bwd_chunk, p.bwd_segment, p.bwd_nseg)):
+        assert C in (32, 64, 128)
+        assert seg % C == 0 and seg >= C
+        assert n == -(-s.T // seg) and n >= 1
+    assert gl.workspace_bytes(s) == p.workspace_bytes
+    if kw.get("segment"):
+        assert p.fwd_segment == max(kw["segment"], p.fwd_chunk)
+
+
+def test_workspace_covers_aggregates(L):
+    s = shape(B=8, H=16, T=2048)
+    p = gl.plan(s)
+    md = 64 * 64 * 4
+    assert p.workspace_bytes >= 8 * 16 * max(p.fwd_nseg, 2 * p.bwd_nseg + 1) * md
+
+
+def fwd_call(s, W0=FAKE, X=FAKE, G=FAKE, eta=None, Y=FAKE, ws=FAKE, wsn=1 << 40):
+    return gl.lib().gradlev_scan_fwd(ctypes.byref(s), W0, X, G, eta, 0.1, Y, ws, wsn, None)
+
+
+def bwd_call(s, outs=(FAKE, FAKE, FAKE, FAKE, FAKE), ws=FAKE, wsn=1 << 40, dY=FAKE):
+    return gl.lib().gradlev_scan_bwd(ctypes.byref(s), FAKE, FAKE, FAKE, None, 0.1, dY, *outs, ws, wsn, None)
+
+
+def test_fwd_validation_before_launch(L):
+    s = shape()
+    assert fwd_call(s, W0=None) == gl.ERR_INVALID
+    assert fwd_call(s, Y=None) == gl.ERR_INVALID
+    assert fwd_call(s, X=MISALIGNED) == gl.ERR_ALIGN
+    assert fwd_call(s, eta=MISALIGNED) == gl.ERR_ALIGN
+    assert fwd_call(s, ws=None) == gl.ERR_WORKSPACE
+    assert fwd_call(s, wsn=16) == gl.ERR_WORKSPACE
+    assert fwd_call(s, ws=MISALIGNED) == gl.ERR_ALIGN
+    assert fwd_call(shape(d_in=32)) == gl.ERR_UNSUPPORTED
+    assert gl.lib().gradlev_scan_fwd(None, FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, 1 << 40, None) == gl.ERR_INVALID
+
+
+def test_bwd_validation_before_launch(L):
+    s = shape()
+    assert bwd_call(s, outs=(None,) * 5) == gl.ERR_INVALID
+    assert bwd_call(s, dY=None) == gl.ERR_INVALID
+    assert bwd_call(s, outs=(None, MISALIGNED, None, None, None)) == gl.ERR_ALIGN
+    assert bwd_call(s, ws=None) == gl.ERR_WORKSPACE
+    assert bwd_call(s, wsn=1024) == gl.ERR_WORKSPACE
+
+
+def test_decode_validation_before_launch(L):
+    f = gl.lib().gradlev_decode_step
+    assert f(0, 16, 64, 64, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
+    assert f(4, 16, 64, 64, None, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
+    assert f(4, 16, 48, 64, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_UNSUPPORTED
+    assert f(4, 16, 64, 2048, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_UNSUPPORTED
+    assert f(4, 16, 64, 64, MISALIGNED, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_ALIGN
+
+
+def test_binding_refuses_cpu_tensors(L):
+    torch = pytest.importorskip("torch")
+    X = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    G = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    W0 = torch.zeros(1, 64, 64)
+    with pytest.raises(ValueError, match="ROCm GPU"):
+        gl.scan_fwd(W0, X, G, 0.1)

@@ -1,0 +1,245 @@
+"""GPU parity: the HIP scans and decode step against the float64 oracle.
+
+Every call goes through the C ABI (via the thin ctypes binding).  Inputs are
+seeded and synthetic with the workloads' distributions; the oracle consumes
+the same already-quantised values.  Tolerances (normwise, per output tensor)
+are those of tests/parity_util.py: fp32 max_rel <= 1e-5; bf16 max_rel <= 2e-2
+and mean_rel <= 1e-3.
+
+Small cases span several chunks, several segments (forced with the segment
+hint) and a ragged last chunk; the five workload configurations run at full
+size, with the oracle on sampled sequences where the full oracle would take
+minutes (every (b, h) sequence is an independent problem, so a sampled
+sequence is checked completely).
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import gradlev_oracle as orc
+from paper_2609_34174_amd import workloads as W
+from parity_util import check, log, to_dev, to_host
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2609_34174_amd as gl  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no ROCm GPU visible")
+    gl.lib()  # raises if the HIP library is missing: there is no fallback
+    yield
+    torch.cuda.synchronize()
+
+
+def small_inputs(B, H, T, d, m, dtype, seed, eta_kind):
+    base = W.SCAN_WORKLOADS["lm-bf16"]
+    wl = dataclasses.replace(base, B=B, H=H, T=T, d=d, m=m, dtype=dtype, x_dist="normal",
+                             x_std=d ** -0.5, g_std=0.1, seed=seed)
+    inp = W.scan_inputs(wl)
+    if eta_kind == "token":
+        inp["eta"] = W.eta_tokens(B, H, T, seed + 100)
+    return inp
+
+
+def run_gpu(inp, dtype, prefix, chunk=0, segment=0, outputs=gl.BWD_OUTPUTS, with_bwd=True):
+    W0 = to_dev(inp["W0"], "f32", torch)
+    X = to_dev(inp["X"], dtype, torch)
+    G = to_dev(inp["G"], dtype, torch)
+    eta = inp["eta"]
+    eta_d = to_dev(eta, "f32", torch) if isinstance(eta, np.ndarray) else eta
+    Y = gl.scan_fwd(W0, X, G, eta_d, prefix=prefix, chunk=chunk, segment=segment)
+    res = {"y": Y}
+    if with_bwd:
+        dY = to_dev(inp["dY"], dtype, torch)
+        res.update(gl.scan_bwd(W0, X, G, dY, eta_d, prefix=prefix, chunk=chunk, segment=segment,
+                               outputs=outputs))
+    torch.cuda.synchronize()
+    return {k: to_host(v) for k, v in res.items()}
+
+
+def oracle_all(inp, prefix):
+    ref = {"y": orc.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"], prefix)}
+    ref.update(orc.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["eta"], inp["dY"], prefix))
+    return ref
+
+
+KEYS = ("y", "gtilde", "dx", "dg", "deta", "dw0")
+
+
+# ---------------------------------------------------------------------------
+# Small cases: every dtype / convention / width / eta form, ragged T, forced
+# multi-segment carries.
+# ---------------------------------------------------------------------------
+
+SMALL = []
+for dtype in ("f32", "bf16"):
+    for prefix in ("exclusive", "inclusive"):
+        for (d, m) in ((64, 64), (128, 128), (64, 128), (128, 64)):
+            for T, seg in ((1, 0), (37, 0), (200, 64), (333, 128)):
+                SMALL.append((dtype, prefix, d, m, T, seg))
+
+
+@pytest.mark.parametrize("dtype,prefix,d,m,T,seg", SMALL)
+def test_small_parity(dtype, prefix, d, m, T, seg):
+    eta_kind = "token" if (T + d) % 2 else "scalar"
+    log(f"small dtype={dtype} prefix={prefix} d={d} m={m} T={T} seg={seg} eta={eta_kind}")
+    inp = small_inputs(2, 3, T, d, m, dtype, seed=T * 7 + d + m, eta_kind=eta_kind)
+    out = run_gpu(inp, dtype, prefix, segment=seg)
+    ref = oracle_all(inp, prefix)
+    for k in KEYS:
+        check(k, out[k], ref[k], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_chunk_hint_and_segments_change_rounding_only(dtype):
+    log(f"chunk/segment hints dtype={dtype}")
+    inp = small_inputs(1, 2, 700, 64, 64, dtype, seed=5, eta_kind="token")
+    ref = oracle_all(inp, "exclusive")
+    for chunk, seg in ((0, 0), (128, 0), (64, 64), (128, 256), (0, 640)):
+        out = run_gpu(inp, dtype, "exclusive", chunk=chunk, segment=seg)
+        for k in KEYS:
+            check(f"{k}", out[k], ref[k], dtype)
+
+
+def test_eta_zero_reads_slow_weights():
+    log("eta = 0")
+    inp = small_inputs(2, 2, 150, 64, 64, "bf16", seed=9, eta_kind="scalar")
+    inp["eta"] = 0.0
+    out = run_gpu(inp, "bf16", "exclusive", segment=64)
+    ref = oracle_all(inp, "exclusive")
+    for k in ("y", "gtilde", "dx", "deta", "dw0"):
+        check(k, out[k], ref[k], "bf16")
+    assert np.all(out["dg"] == 0.0)
+
+
+def test_optional_outputs_are_independent():
+    """A NULL output skips work without changing the others (bitwise)."""
+    log("optional outputs")
+    inp = small_inputs(2, 2, 300, 64, 64, "bf16", seed=11, eta_kind="token")
+    full = run_gpu(inp, "bf16", "exclusive", segment=128)
+    for subset in (("gtilde",), ("dx",), ("dg",), ("deta",), ("dw0",), ("gtilde", "deta")):
+        part = run_gpu(inp, "bf16", "exclusive", segment=128, outputs=subset)
+        for k in subset:
+            np.testing.assert_array_equal(part[k], full[k], err_msg=str(subset))
+
+
+def test_backward_is_deterministic():
+    log("determinism")
+    inp = small_inputs(4, 4, 1000, 64, 64, "bf16", seed=12, eta_kind="scalar")
+    a = run_gpu(inp, "bf16", "exclusive")
+    b = run_gpu(inp, "bf16", "exclusive")
+    for k in KEYS:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+# ---------------------------------------------------------------------------
+# Workload configurations at full size
+# ---------------------------------------------------------------------------
+
+def test_small_f32_config():
+    wl = W.SCAN_WORKLOADS["small-f32"]
+    for prefix in ("exclusive", "inclusive"):
+        log(f"config small-f32 prefix={prefix}")
+        inp = W.scan_inputs(wl)
+        out = run_gpu(inp, "f32", prefix, chunk=wl.chunk)
+        ref = oracle_all(inp, prefix)
+        for k in KEYS:
+            check(k, out[k], ref[k], "f32")
+
+
+def _sampled_config(wl, layer, heads):
+    """Full-size GPU run; the oracle checks every output of the sampled heads.
+
+    Inputs are drawn on the device with the workload's seeded generator (the
+    full host draw would take minutes at these sizes); the sampled heads are
+    copied back and handed to the oracle as they are.  Each sampled head is
+    checked over all batch rows, which also covers dW0[h].
+    """
+    log(f"config {wl.name} layer={layer}: drawing inputs on the device")
+    inp = W.device_scan_inputs(wl, layer, "cuda", torch=torch)
+    log(f"config {wl.name} layer={layer}: GPU fwd+bwd (full size)")
+    Y = gl.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"], chunk=wl.chunk)
+    out = gl.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["dY"], inp["eta"], chunk=wl.chunk)
+    out["y"] = Y
+    torch.cuda.synchronize()
+    for h in heads:
+        log(f"  oracle on head h={h} (all {wl.B} batch rows, T={wl.T})")
+        sl = {"W0": to_host(inp["W0"][h:h + 1]), "X": to_host(inp["X"][:, h:h + 1]),
+              "G": to_host(inp["G"][:, h:h + 1]), "dY": to_host(inp["dY"][:, h:h + 1]),
+              "eta": inp["eta"]}
+        ref = oracle_all(sl, "exclusive")
+        for k in ("y", "gtilde", "dx", "dg", "deta"):
+            check(k, to_host(out[k][:, h:h + 1]), ref[k], wl.dtype)
+        check("dw0", to_host(out["dw0"][h:h + 1]), ref["dw0"], wl.dtype)
+
+
+@pytest.mark.timeout(300)
+def test_lm_bf16_config():
+    _sampled_config(W.SCAN_WORKLOADS["lm-bf16"], 0, [0, 9])
+
+
+@pytest.mark.timeout(300)
+def test_long_bf16_config():
+    _sampled_config(W.SCAN_WORKLOADS["long-bf16"], 0, [3])
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("layer", [0, 23])
+def test_stack_bf16_config_layers(layer):
+    _sampled_config(W.SCAN_WORKLOADS["stack-bf16"], layer, [31])
+
+
+# ---------------------------------------------------------------------------
+# Decode
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d,m,eta_kind", [(64, 64, "scalar"), (16, 7, "state"), (32, 300, "scalar"),
+                                          (128, 128, "state"), (256, 64, "scalar"), (64, 1, "state")])
+def test_decode_small(d, m, eta_kind):
+    log(f"decode small d={d} m={m} eta={eta_kind}")
+    rng = np.random.default_rng(d * 1000 + m)
+    S, H, steps = 5, 3, 6
+    Wh = (rng.standard_normal((S, H, m, d)) * d ** -0.5).astype(np.float32)
+    Wd = to_dev(Wh, "f32", torch)
+    Wr = Wh.astype(np.float64)
+    for step in range(steps):
+        x = (rng.standard_normal((S, H, d)) * d ** -0.5).astype(np.float32)
+        g = (rng.standard_normal((S, H, m)) * 0.1).astype(np.float32)
+        eta = rng.uniform(0, 0.2, (S, H)).astype(np.float32) if eta_kind == "state" else 0.1
+        ed = to_dev(eta, "f32", torch) if eta_kind == "state" else eta
+        y = gl.decode_step(Wd, to_dev(x, "f32", torch), to_dev(g, "f32", torch), ed)
+        yr, Wr = orc.decode_step(Wr, x, g, eta if eta_kind == "state" else np.float32(0.1))
+        check("y", to_host(y), yr, "f32")
+    check("W", to_host(Wd), Wr, "f32")
+
+
+@pytest.mark.timeout(300)
+def test_decode_config():
+    wl = W.DECODE_WORKLOADS["decode-f32"]
+    log(f"config {wl.name}: {wl.steps} steps of S={wl.S} H={wl.H}")
+    W0 = W.decode_initial_state(wl)
+    Wd = to_dev(W0, "f32", torch)
+    picks = [(0, 0), (17, 5), (255, 15)]
+    Wr = np.stack([W0[s, h] for s, h in picks]).astype(np.float64)[:, None]
+    worst = 0.0
+    for step in range(wl.steps):
+        x, g = W.decode_step_inputs(wl, step)
+        y = to_host(gl.decode_step(Wd, to_dev(x, "f32", torch), to_dev(g, "f32", torch), wl.eta))
+        xs = np.stack([x[s, h] for s, h in picks])[:, None]
+        gs = np.stack([g[s, h] for s, h in picks])[:, None]
+        yr, Wr = orc.decode_step(Wr, xs, gs, np.float32(wl.eta))
+        ys = np.stack([y[s, h] for s, h in picks])[:, None]
+        mx = np.max(np.abs(ys - yr)) / np.max(np.abs(yr))
+        worst = max(worst, mx)
+        if step % 128 == 0:
+            log(f"  step {step}: y max_rel {mx:.2e}")
+    log(f"  worst y max_rel over {wl.steps} steps: {worst:.2e}")
+    assert worst <= 1e-5
+    Wf = to_host(Wd)
+    check("W", np.stack([Wf[s, h] for s, h in picks])[:, None], Wr, "f32")
