@@ -72,7 +72,9 @@ enum {
  *   segment   tokens per workgroup segment hint: 0 (library default) or a
  *             positive multiple of 64.  Segments of one sequence run in
  *             parallel and are joined by an fp32 carry of their aggregated
- *             writes; like `chunk` it changes the rounding order only.
+ *             writes; like `chunk` it changes the rounding order only.  At
+ *             most 16 segments per sequence: a hint giving more is
+ *             GRADLEV_ERR_UNSUPPORTED (the default never does).
  *   in_dtype  GRADLEV_F32 or GRADLEV_BF16
  *   prefix    GRADLEV_EXCLUSIVE or GRADLEV_INCLUSIVE */
 typedef struct gradlev_shape {

@@ -35,6 +35,7 @@ int64_t pick_nseg(int64_t BH, int64_t T, int C, int wgs_per_cu, int64_t hint) {
     int64_t nseg = (target + BH - 1) / BH;
     if (nseg < 1) nseg = 1;
     if (nseg > nchunks) nseg = nchunks;
+    if (nseg > 16) nseg = 16;  // the carry kernel joins at most 16 segments
     seg_chunks = (nchunks + nseg - 1) / nseg;
   }
   if (seg_chunks < 1) seg_chunks = 1;
@@ -54,7 +55,9 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   if (s->B > kMaxElems / s->H || BH > kMaxElems / s->T) return GRADLEV_ERR_UNSUPPORTED;
   const int64_t wmax = s->d_in > s->d_out ? s->d_in : s->d_out;
   if (BH * s->T > kMaxElems / wmax) return GRADLEV_ERR_UNSUPPORTED;
-  if (BH > 65535) return GRADLEV_ERR_UNSUPPORTED;  // grid y limit
+  // Per-sequence byte offsets are 32-bit (buffer addressing): T * width * 4 < 2^31.
+  if (s->T > (int64_t(1) << 31) / (4 * wmax) - 1) return GRADLEV_ERR_UNSUPPORTED;
+  if (BH > (int64_t(1) << 26)) return GRADLEV_ERR_UNSUPPORTED;  // 1-D grid of 8 * nseg * ceil(BH / 8) blocks
 
   const int bf = s->in_dtype == GRADLEV_BF16;
   const int d = (int)s->d_in, m = (int)s->d_out;
@@ -74,19 +77,20 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   int64_t sc = pick_nseg(BH, s->T, out->fwd.chunk, fwd_wgs_per_cu(bf, d, m, out->fwd.chunk), s->segment);
   out->fwd.seg_len = sc * out->fwd.chunk;
   out->fwd.nseg = (s->T + out->fwd.seg_len - 1) / out->fwd.seg_len;
-  if (out->fwd.nseg > 65535) return GRADLEV_ERR_UNSUPPORTED;
+  if (out->fwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
 
   out->bwd = base;
   out->bwd.chunk = bwd_chunk_for(bf, d, m, (int)s->chunk);
   sc = pick_nseg(BH, s->T, out->bwd.chunk, bwd_wgs_per_cu(bf, d, m, out->bwd.chunk), s->segment);
   out->bwd.seg_len = sc * out->bwd.chunk;
   out->bwd.nseg = (s->T + out->bwd.seg_len - 1) / out->bwd.seg_len;
-  if (out->bwd.nseg > 65535) return GRADLEV_ERR_UNSUPPORTED;
+  if (out->bwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
 
   out->ws_fwd = out->fwd.nseg > 1 ? round_up((size_t)BH * out->fwd.nseg * md, 256) : 0;
+  const size_t agg_b = out->bwd.nseg > 1 ? round_up((size_t)BH * out->bwd.nseg * md, 256) : 0;
   out->off_aggA = 0;
   out->off_aggB = round_up((size_t)BH * out->bwd.nseg * md, 256);
-  out->off_rfin = out->off_aggB + (out->bwd.nseg > 1 ? round_up((size_t)BH * out->bwd.nseg * md, 256) : 0);
+  out->off_rfin = out->off_aggB + agg_b;
   out->ws_bwd = out->off_rfin + round_up((size_t)BH * md, 256);
   return GRADLEV_OK;
 }
@@ -111,7 +115,7 @@ const char* gradlev_error_string(int code) {
   switch (code) {
     case GRADLEV_OK: return "success";
     case GRADLEV_ERR_INVALID: return "invalid argument (null pointer, non-positive size or unknown enum)";
-    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64)";
+    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64 giving at most 16 segments)";
     case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
     case GRADLEV_ERR_HIP: return "HIP launch failed";

@@ -36,6 +36,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
@@ -47,7 +48,29 @@ __device__ __forceinline__ f32x8 cat(f32x4 a, f32x4 b) {
 __device__ __forceinline__ int slot_k(int e, int q) { return 16 * (e >> 2) + 4 * q + (e & 3); }
 
 // ---------------------------------------------------------------------------
-// Operand policies
+// LDS tiles.  Every staged matrix lives in LDS row-major, unpadded, with its
+// 4-element chunks XOR-swizzled by row:
+//     element (r, k) of a [rows][K] tile is stored at
+//     r*K + 4*((k/4) ^ swz(r)) + k%4,     swz(r) = 4*(r%4) + (r/4)%4.
+// With 32 banks of 4 bytes, both fragment reads below touch 16 distinct
+// 8-byte chunks per 16-lane group (no bank conflicts), and a 16-lane group
+// writing one row's 16 chunks is conflict-free as well.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int swz(int r, int K) { return (((r & 3) << 2) | ((r >> 2) & 3)) & ((K >> 2) - 1); }
+__device__ __forceinline__ int lds_off(int r, int k, int K) {
+  return r * K + ((((k >> 2) ^ swz(r, K)) << 2) | (k & 3));
+}
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// ---------------------------------------------------------------------------
+// Operand policies.  load_n reads the fragment of row (row0 + c) of a tile
+// with k along the tile's columns; load_t reads it with k along the tile's
+// rows (the operand row index n0 + c is a tile column) - the hardware
+// transposing read ds_read_b64_tr_b16 for bf16: inside each 16-lane group,
+// lane 4a+b receives element b of the 8-byte rows addressed by lanes a, a+4,
+// a+8, a+12, so lane i points at row k0 + 4q + i/4, columns n0 + 4(i%4).
 // ---------------------------------------------------------------------------
 struct OpBF16 {
   typedef bf16 elem;
@@ -57,25 +80,29 @@ struct OpBF16 {
   __device__ static __forceinline__ f32x4 mma(f32x4 acc, frag a, frag b) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
   }
-  // Fragment of row (row0 + c) of a k-contiguous LDS array, K step at k0.
-  __device__ static __forceinline__ frag load(const elem* base, int ld, int row0, int k0, int lane) {
-    const elem* p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
-    bf16x4 a = *reinterpret_cast<const bf16x4*>(p);
-    bf16x4 b = *reinterpret_cast<const bf16x4*>(p + 16);
+  __device__ static __forceinline__ frag load_n(const elem* base, int K, int row0, int k0, int lane) {
+    const int r = row0 + (lane & 15), k = k0 + 4 * (lane >> 4);
+    const bf16x4 a = *reinterpret_cast<const bf16x4*>(base + lds_off(r, k, K));
+    const bf16x4 b = *reinterpret_cast<const bf16x4*>(base + lds_off(r, k + 16, K));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
   }
-  __device__ static __forceinline__ f32x8 load_f32(const elem* base, int ld, int row0, int k0, int lane) {
-    frag f = load(base, ld, row0, k0, lane);
+  __device__ static __forceinline__ frag load_t(const elem* base, int K, int k0, int n0, int lane) {
+    const int c = lane & 15, r = k0 + 4 * (lane >> 4) + (c >> 2), n = n0 + 4 * (c & 3);
+    const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + lds_off(r, n, K)));
+    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + lds_off(r + 16, n, K)));
+    const i16x8 v = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(frag, v);
+  }
+  __device__ static __forceinline__ f32x8 to_f32(frag f) {
     f32x8 v;
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = (float)f[e];
     return v;
   }
-  __device__ static __forceinline__ frag round(f32x8 v) {
-    frag f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) f[e] = (bf16)v[e];
-    return f;
+  __device__ static __forceinline__ frag neg(frag f) {
+    i16x8 v = __builtin_bit_cast(i16x8, f);
+    v ^= (short)0x8000;
+    return __builtin_bit_cast(frag, v);
   }
   // v ~= hi + lo, both bf16 (about 16 significant bits in total).
   __device__ static __forceinline__ void split(f32x8 v, frag& hi, frag& lo) {
@@ -86,14 +113,23 @@ struct OpBF16 {
       lo[e] = (bf16)(v[e] - (float)h);
     }
   }
-  // Store 4 consecutive elements (8 bytes).
+  // Store 4 consecutive elements (one chunk, 8 bytes).
   __device__ static __forceinline__ void store4(elem* p, f32x4 v) {
     bf16x4 o;
 #pragma unroll
     for (int r = 0; r < 4; ++r) o[r] = (bf16)v[r];
     *reinterpret_cast<bf16x4*>(p) = o;
   }
-  __device__ static __forceinline__ void store1(elem* p, float v) { *p = (bf16)v; }
+  __device__ static __forceinline__ void store4_split(elem* hi, elem* lo, f32x4 v) {
+    bf16x4 h, l;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      h[r] = (bf16)v[r];
+      l[r] = (bf16)(v[r] - (float)h[r]);
+    }
+    *reinterpret_cast<bf16x4*>(hi) = h;
+    *reinterpret_cast<bf16x4*>(lo) = l;
+  }
 };
 
 struct OpF32 {
@@ -106,22 +142,30 @@ struct OpF32 {
     for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], acc, 0, 0, 0);
     return acc;
   }
-  __device__ static __forceinline__ frag load(const elem* base, int ld, int row0, int k0, int lane) {
-    const elem* p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
-    f32x4 a = *reinterpret_cast<const f32x4*>(p);
-    f32x4 b = *reinterpret_cast<const f32x4*>(p + 16);
+  __device__ static __forceinline__ frag load_n(const elem* base, int K, int row0, int k0, int lane) {
+    const int r = row0 + (lane & 15), k = k0 + 4 * (lane >> 4);
+    const f32x4 a = *reinterpret_cast<const f32x4*>(base + lds_off(r, k, K));
+    const f32x4 b = *reinterpret_cast<const f32x4*>(base + lds_off(r, k + 16, K));
     return cat(a, b);
   }
-  __device__ static __forceinline__ f32x8 load_f32(const elem* base, int ld, int row0, int k0, int lane) {
-    return load(base, ld, row0, k0, lane);
+  __device__ static __forceinline__ frag load_t(const elem* base, int K, int k0, int n0, int lane) {
+    const int c = lane & 15, q = lane >> 4;
+    frag v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = base[lds_off(k0 + slot_k(e, q), n0 + c, K)];
+    return v;
   }
-  __device__ static __forceinline__ frag round(f32x8 v) { return v; }
+  __device__ static __forceinline__ f32x8 to_f32(frag f) { return f; }
+  __device__ static __forceinline__ frag neg(frag f) { return -f; }
   __device__ static __forceinline__ void split(f32x8 v, frag& hi, frag& lo) {
     hi = v;
     lo = v;  // unused: kSplit == 1
   }
   __device__ static __forceinline__ void store4(elem* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
-  __device__ static __forceinline__ void store1(elem* p, float v) { *p = v; }
+  __device__ static __forceinline__ void store4_split(elem* hi, elem* lo, f32x4 v) {
+    (void)lo;
+    *reinterpret_cast<f32x4*>(hi) = v;
+  }
 };
 
 // acc += P * Q where P is given as fp32 values (split when the op needs it).
@@ -140,69 +184,38 @@ __device__ __forceinline__ f32x4 mma_split_b(f32x4 acc, const typename OP::frag&
   return acc;
 }
 
-// ---------------------------------------------------------------------------
-// Chunk tile staging: a C x K tile of a row-major [T][K] global matrix, held
-// in registers as 16-byte vectors while the previous chunk computes, then
-// written to LDS row-major (k = column) and/or transposed (k = row).
-// Rows at or beyond `rows` are zero-filled, which masks a partial chunk.
-// ---------------------------------------------------------------------------
-template <class OP, int C, int K, int NT>
-struct TileRegs {
-  typedef typename OP::elem elem;
-  static constexpr int VE = 16 / (int)sizeof(elem);  // elements per vector
-  static constexpr int NV = C * K / VE;               // vectors per tile
-  static constexpr int PER = (NV + NT - 1) / NT;
-  static_assert(K % VE == 0, "row width must hold whole vectors");
-  uint4 v[PER];
-
-  __device__ __forceinline__ void load(const elem* src, int rows, int tid) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int idx = tid + i * NT;
-      const int row = idx * VE / K;
-      uint4 z = {0u, 0u, 0u, 0u};
-      if (idx < NV && row < rows) z = *reinterpret_cast<const uint4*>(src + (int64_t)idx * VE);
-      v[i] = z;
-    }
-  }
-  __device__ __forceinline__ void clear() {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) v[i] = uint4{0u, 0u, 0u, 0u};
-  }
-  // lds[row][col], row stride ld (elements; ld * sizeof(elem) multiple of 8).
-  __device__ __forceinline__ void store_rows(elem* lds, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int idx = tid + i * NT;
-      if (idx >= NV) continue;
-      const int row = idx * VE / K, col = idx * VE % K;
-      elem* p = lds + row * ld + col;
-      const uint2* s = reinterpret_cast<const uint2*>(&v[i]);
-      reinterpret_cast<uint2*>(p)[0] = s[0];
-      reinterpret_cast<uint2*>(p)[1] = s[1];
-    }
-  }
-  // lds[col][row], row stride ld.
-  __device__ __forceinline__ void store_cols(elem* lds, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int idx = tid + i * NT;
-      if (idx >= NV) continue;
-      const int row = idx * VE / K, col = idx * VE % K;
-      const elem* s = reinterpret_cast<const elem*>(&v[i]);
-#pragma unroll
-      for (int e = 0; e < VE; ++e) lds[(col + e) * ld + row] = s[e];
-    }
-  }
-};
-
-__device__ __forceinline__ int tri_row(int idx) {
-  // Row tb of the idx-th lower-triangular tile (tb >= sb), row-major order.
-  int tb = 0;
-  while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
-  return tb;
-}
-
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+// ---------------------------------------------------------------------------
+// Buffer addressing.  Streaming loads and stores of chunk data go through a
+// raw buffer resource spanning one sequence's rows: an access at or past the
+// resource's size reads zero / is dropped by the hardware, which masks the
+// partial last chunk without a branch.  Branch-free memory operations keep
+// the compiler's count of outstanding loads exact, so loads issued for later
+// chunks stay in flight across the current chunk's barriers.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOOB = 0x80000000u;  // an offset past every resource (sizes are < 2^31)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ bf16x4 buf_load4(rsrc_t r, uint32_t off, const bf16*) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ f32x4 buf_load4(rsrc_t r, uint32_t off, const float*) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ float buf_load1(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ void buf_store4(rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void buf_store1(rsrc_t r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, 0);
+}
 
 }  // namespace gradlev

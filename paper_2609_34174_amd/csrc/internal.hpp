@@ -39,8 +39,8 @@ struct BwdPtrs {
   float* dG;
   float* deta;
   float* dW0;
-  float* aggA;  // [B*H][nseg][m][d]: segment write aggregates -> inclusive prefix
-  float* aggB;  // [B*H][nseg][m][d]: segment dY x^T aggregates -> exclusive suffix
+  float* aggA;   // [B*H][nseg][d][m]: segment write aggregates -> segment end states (transposed)
+  float* aggB;   // [B*H][nseg][d][m]: segment dY x^T aggregates -> suffixes (transposed)
   float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
 };
 

@@ -9,19 +9,18 @@
 // (u >= t and Delta_{t+1} for the inclusive convention.)
 //
 // Chunk form, chunk n of C tokens, W_n = W_0 + Delta_{nC}, R_n = suffix after
-// the chunk, V = diag(eta) G, M the causal mask:
-//   gtilde = dY W_n - (M o dY V^T) X
+// the chunk, V = diag(eta) G, M the causal mask, E = M o (dY V^T):
+//   gtilde = dY W_n - E X
 //   U      = -(X R_n^T + (M o X X^T)^T dY)             dG = diag(eta) U
-//   dXw    = -(V R_n + (M o dY V^T)^T X)                dX = gtilde + dXw
+//   dXw    = -(V R_n + E^T X)                           dX = gtilde + dXw
 //   W_n    = W_{n+1} + V^T X     (the state is un-written chunk by chunk)
 //   R_{n-1}= R_n + dY^T X
-// A workgroup walks its segment's chunks from last to first, carrying R
-// forward in reverse time and un-writing W from the state at the segment's
-// end (W_0 minus the inclusive prefix of segment aggregates).  Waves own
-// column blocks of W and R (for the products contracted over m) and row
-// blocks of a second copy of R (for the product contracted over d), so every
-// state operand is read straight from accumulator registers.
-#include "../../include/gradlev.h"
+// A workgroup walks its segment's chunks from last to first, carrying R in
+// reverse time and un-writing W from the state at the segment's end (both
+// provided by the aggregate and carry kernels).  Waves own column blocks of
+// W and R in registers; R is also published each chunk to LDS (transposed,
+// split into bf16 hi + lo) for the products contracted over d, so no second
+// register copy is needed.
 #include "scan_common.hpp"
 
 namespace gradlev {
@@ -33,272 +32,318 @@ struct BArgs {
   const void* dY;
   const float* eta;
   float eta_scalar;
-  int64_t H, T, seg_len, nseg;
+  int64_t BH, H, T, seg_len, nseg;
   float* gtilde;
   float* dX;
   float* dG;
   float* deta;
-  const float* pin;   // [BH][nseg][m][d] inclusive prefix of write aggregates
-  const float* sfx;   // [BH][nseg][m][d] exclusive suffix of dY x^T aggregates, or null
-  float* rfin;        // [BH][m][d] full-sequence dY x^T (written by segment 0), or null
+  const float* wend;  // [BH][nseg][d][m]: W at each segment's end, transposed
+  const float* rend;  // [BH][nseg][d][m]: R at each segment's end, transposed, or null (nseg == 1)
+  float* rfin;        // [BH][m][d]: full-sequence dY x^T (written by segment 0), or null
 };
 
-template <class OP, int D, int M, int C, bool INCL>
-__global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
+// Output modes compiled separately so that no accumulator crosses a runtime
+// branch: kOutFull computes every backward term (stores are skipped for NULL
+// outputs); kOutRead computes only the read-side gtilde.
+enum OutMode { kOutFull = 0, kOutRead = 1 };
+
+template <class OP, int D, int M, int C, bool INCL, bool ETAV, int OUT>
+__global__ void __launch_bounds__(cmax(D, M) / 16 * 64, 128 / cmax(D, M))
 bwd_main_kernel(const BArgs a) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
   constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
   constexpr int TB = C / 16, JB = D / 16, IB = M / 16;
-  constexpr int LDD = D + 4, LDM = M + 4, LDC = C + 4;
-  __shared__ E Xr[C * LDD];  // X[t][j]
-  __shared__ E Gr[C * LDM];  // G[t][i]
-  __shared__ E Dr[C * LDM];  // dY[t][i]
-  __shared__ E Xt[D * LDC];  // X^T[j][t]
-  __shared__ E Gt[M * LDC];  // G^T[i][t]
-  __shared__ E Dt[M * LDC];  // dY^T[i][t]
-  __shared__ E Er[C * LDC];  // -E[t][s], E = eta_s dY_t.g_s (s before t), [t][s]
-  __shared__ E Et[C * LDC];  // +E stored [s][t]
+  constexpr bool SPLITV = ETAV && OP::kSplit == 2;
+  constexpr bool FULL = OUT == kOutFull;
+  __shared__ E Xs[C * D];                  // X[t][j]
+  __shared__ E Gs[C * M];                  // G[t][i]
+  __shared__ E Ds[C * M];                  // dY[t][i]
+  __shared__ E Es[C * C];                  // E[t][s] = eta_s dY_t . g_s (s before t)
+  __shared__ E Vh[ETAV ? C * M : 1];       // (eta G)[t][i] hi (per-token eta)
+  __shared__ E Vl[SPLITV ? C * M : 1];     // (eta G)[t][i] lo
+  __shared__ E Rh[FULL ? D * M : 1];       // R^T[j][i] hi
+  __shared__ E Rl[FULL && OP::kSplit == 2 ? D * M : 1];  // R^T[j][i] lo
   __shared__ float et[C];
   __shared__ float dpart[IB][C];
 
+  int64_t bh, seg;
+  if (!map_block(a.BH, a.nseg, bh, seg)) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
-  const int64_t seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
-  const E* X = static_cast<const E*>(a.X) + bh * T * D;
-  const E* G = static_cast<const E*>(a.G) + bh * T * M;
-  const E* Dy = static_cast<const E*>(a.dY) + bh * T * M;
-  const bool need_gx = a.gtilde || a.dX;
-  const bool need_u = a.dG || a.deta;
-  const bool need_dxw = a.dX != nullptr;
-  const bool need_ri = need_u || a.rfin;
+  const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
+  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t Dy = make_rsrc(static_cast<const E*>(a.dY) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  // Outputs: rows past T are dropped by the resource bounds.
+  const rsrc_t Og = make_rsrc(a.gtilde ? a.gtilde + bh * T * D : nullptr, a.gtilde ? (uint32_t)(T * D * 4) : 0u);
+  const rsrc_t Ox = make_rsrc(a.dX ? a.dX + bh * T * D : nullptr, a.dX ? (uint32_t)(T * D * 4) : 0u);
+  const rsrc_t Od = make_rsrc(a.dG ? a.dG + bh * T * M : nullptr, a.dG ? (uint32_t)(T * M * 4) : 0u);
+  const rsrc_t Oe = make_rsrc(a.deta ? a.deta + bh * T : nullptr, a.deta ? (uint32_t)(T * 4) : 0u);
+  const rsrc_t none = make_rsrc(nullptr, 0u);  // every access out of range
+  const int64_t nch = (t_end - t_begin + C - 1) / C;
 
-  for (int i = tid; i < C * LDC; i += NT) {
-    Er[i] = (E)0.f;
-    Et[i] = (E)0.f;
+  // Register staging, DEPTH chunks ahead (chunks are visited last to first).
+  // The full backward keeps twice the accumulators of the read-only one and
+  // fp32 tiles take twice the registers: those stage one chunk ahead, which
+  // keeps them free of spills.
+  constexpr int DEPTH = (FULL || OP::kSplit == 1) ? 1 : 2;
+  Tile4<OP, C, D, NT> xa, xb;
+  Tile4<OP, C, M, NT> ga, gb, da, db;
+  EtaReg<ETAV> ea, eb;
+  const rsrc_t Et = eta_rsrc(a.eta, bh, T);
+  typedef Tile4<OP, C, D, NT> TX;
+  typedef Tile4<OP, C, M, NT> TM;
+  auto fetch = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
+    const int64_t t0 = t_begin + n * C;
+    er.load(Et, n >= 0 ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    xr.load(X, n >= 0 ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
+    gr.load(G, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    dr.load(Dy, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+  };
+  fetch(xa, ga, da, ea, nch - 1);
+  if (DEPTH == 2) fetch(xb, gb, db, eb, nch - 2);
+
+  // Column-block state (wave w < JB): Wj[ib], Rj[ib] hold W/R[i = 16ib + 4q + r][j = 16w + c],
+  // i.e. row j of the transposed [d][m] layout the carry kernel leaves.
+  f32x4 Wj[IB], Rj[IB];
+  if (w < JB) {
+    const int64_t o = (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * M;
+#pragma unroll
+    for (int ib = 0; ib < IB; ++ib) {
+      Wj[ib] = *reinterpret_cast<const f32x4*>(a.wend + o + 16 * ib + 4 * q);
+      Rj[ib] = (FULL && a.rend) ? *reinterpret_cast<const f32x4*>(a.rend + o + 16 * ib + 4 * q) : zero4();
+    }
   }
+  for (int i = tid; i < C * C; i += NT) Es[i] = (E)0.f;
 
-  // Column-block state (wave w < JB): Wj[ib], Rj[ib] hold W/R[i = 16ib + 4q + r][j = 16w + c].
-  // Row-block copy of R (wave w < IB): Ri[jb] holds R[i = 16w + c][j = 16jb + 4q + r].
-  f32x4 Wj[IB], Rj[IB], Ri[JB];
-  {
-    const float* w0 = a.W0 + h * M * D;
-    const float* pin = a.pin ? a.pin + (bh * a.nseg + seg) * M * D : nullptr;
-    const float* sfx = a.sfx ? a.sfx + (bh * a.nseg + seg) * M * D : nullptr;
-    if (w < JB) {
+  auto chunk = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
+    // A step before the segment start (the second of a pair) sees zero
+    // tiles, leaves W and R unchanged and stores nothing.
+    const int64_t t0 = t_begin + n * C;
+    const bool live = n >= 0;
+    const int nvalid = live ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
+    const rsrc_t Ogc = live ? Og : none, Oxc = live ? Ox : none, Odc = live ? Od : none, Oec = live ? Oe : none;
+    __syncthreads();
+    er.stage(et, C, a.eta_scalar, nvalid, 1.f, tid);
+    xr.store(Xs, tid);
+    gr.store(Gs, tid);
+    dr.store(Ds, tid);
+    __syncthreads();
+    if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read after the next barrier
+    fetch(xr, gr, dr, er, n - DEPTH);
+
+    // (1) Intra-chunk tiles E[t][s], shared through LDS, and R_n^T (split).
+#pragma unroll
+    for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+      if (idx % NW != w) continue;
+      int tb = 0;
+      while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+      const int sb = idx - tb * (tb + 1) / 2;
+      // acc[r] = g_s . dY_t with s = 16sb + 4q + r, t = 16tb + c.
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < M / 32; ++kb)
+        acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, lane), OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+      const int t = 16 * tb + c;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int s = 16 * sb + 4 * q + r;
+        const bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
+        acc[r] = keep ? acc[r] * et[s] : 0.f;
+      }
+      OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
+    }
+    if (FULL && w < JB) {
 #pragma unroll
       for (int ib = 0; ib < IB; ++ib) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t o = (int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c;
-          Wj[ib][r] = pin ? w0[o] - pin[o] : 0.f;
-          Rj[ib][r] = sfx ? sfx[o] : 0.f;
-        }
-      }
-    }
-    if (w < IB) {
-#pragma unroll
-      for (int jb = 0; jb < JB; ++jb)
-        Ri[jb] = sfx ? *reinterpret_cast<const f32x4*>(sfx + (int64_t)(16 * w + c) * D + 16 * jb + 4 * q) : zero4();
-    }
-  }
-
-  const int64_t nch = (t_end - t_begin + C - 1) / C;
-  TileRegs<OP, C, D, NT> xr;
-  TileRegs<OP, C, M, NT> gr, dr;
-  {
-    const int64_t t0 = t_begin + (nch - 1) * C;
-    const int rows = (int)(t_end - t0);
-    xr.load(X + t0 * D, rows, tid);
-    gr.load(G + t0 * M, rows, tid);
-    dr.load(Dy + t0 * M, rows, tid);
-  }
-  for (int64_t n = nch - 1; n >= 0; --n) {
-    const int64_t t0 = t_begin + n * C;
-    const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
-    __syncthreads();
-    xr.store_rows(Xr, LDD, tid);
-    xr.store_cols(Xt, LDC, tid);
-    gr.store_rows(Gr, LDM, tid);
-    gr.store_cols(Gt, LDC, tid);
-    dr.store_rows(Dr, LDM, tid);
-    dr.store_cols(Dt, LDC, tid);
-    if (tid < C) et[tid] = tid < nvalid ? (a.eta ? a.eta[bh * T + t0 + tid] : a.eta_scalar) : 0.f;
-    __syncthreads();
-    if (n > 0) {
-      xr.load(X + (t0 - C) * D, C, tid);
-      gr.load(G + (t0 - C) * M, C, tid);
-      dr.load(Dy + (t0 - C) * M, C, tid);
-    }
-
-    // (1) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
-    if (w < JB && need_gx) {
-#pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) {
-        const F xq = OP::load(Xt, LDC, 16 * w, 32 * kb, lane);
-#pragma unroll
-        for (int ib = 0; ib < IB; ++ib) {
-          f32x8 gv = OP::load_f32(Gt, LDC, 16 * ib, 32 * kb, lane);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) gv[e] *= et[32 * kb + slot_k(e, q)];
-          F vh, vl;
-          OP::split(gv, vh, vl);
-          Wj[ib] = mma_split_a<OP>(Wj[ib], vh, vl, xq);
-        }
-      }
-    }
-
-    // (2) Intra-chunk tiles E[t][s] = eta_s dY_t . g_s (t after s), shared
-    //     through LDS in both orientations.
-    if (need_gx) {
-      for (int idx = w; idx < TB * (TB + 1) / 2; idx += NW) {
-        const int tb = tri_row(idx), sb = idx - tb * (tb + 1) / 2;
-        // acc[r] holds entry (t = 16tb + 4q + r, s = 16sb + c).
-        const int s = 16 * sb + c;
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kb = 0; kb < M / 32; ++kb)
-          acc = OP::mma(acc, OP::load(Dr, LDM, 16 * tb, 32 * kb, lane), OP::load(Gr, LDM, 16 * sb, 32 * kb, lane));
-        const float es = et[s];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = 16 * tb + 4 * q + r;
-          const bool keep = INCL ? (t >= s) : (t > s);
-          acc[r] = keep ? acc[r] * es : 0.f;
-          OP::store1(Er + t * LDC + s, -acc[r]);
-        }
-        OP::store4(Et + s * LDC + 16 * tb + 4 * q, acc);
+        const int o = lds_off(16 * w + c, 16 * ib + 4 * q, M);
+        OP::store4_split(Rh + o, Rl + o, Rj[ib]);
       }
     }
     __syncthreads();
 
-    // (3) gtilde and dX for columns j in [16w, 16w+16).
-    if (w < JB && need_gx) {
-      F Wh[M / 32], Wl[M / 32], Rh[M / 32], Rl[M / 32];
+    // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
+    if (w < JB) {
+      if constexpr (ETAV) {
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) {
+            const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, lane);
+            F vl = vh;
+            if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, lane);
+            Wj[ib] = mma_split_a<OP>(Wj[ib], vh, vl, xq);
+          }
+        }
+      } else {
+        f32x4 dw[IB];
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib) dw[ib] = zero4();
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, lane), xq);
+        }
+        const float e = a.eta_scalar;
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib) Wj[ib] += e * dw[ib];
+      }
+    }
+
+    // (3) gtilde and dX for columns j in [16w, 16w+16), all t blocks at once.
+    if (w < JB) {
+      f32x4 ga[TB], xa2[TB];
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) ga[tb] = xa2[tb] = zero4();
+      // gtilde^T[j][t] += sum_i W[i][j] dY[t][i];  dXw^T[j][s] += sum_i R[i][j] G[s][i]
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb) {
-        OP::split(cat(Wj[2 * kb], Wj[2 * kb + 1]), Wh[kb], Wl[kb]);
-        if (need_dxw) OP::split(cat(Rj[2 * kb], Rj[2 * kb + 1]), Rh[kb], Rl[kb]);
+        F wh, wl;
+        OP::split(cat(Wj[2 * kb], Wj[2 * kb + 1]), wh, wl);
+        F rh, rl;
+        if (FULL) {
+          rh = OP::load_n(Rh, M, 16 * w, 32 * kb, lane);
+          rl = rh;
+          if constexpr (OP::kSplit == 2) rl = OP::load_n(Rl, M, 16 * w, 32 * kb, lane);
+        }
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          ga[tb] = mma_split_a<OP>(ga[tb], wh, wl, OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+          if (FULL) xa2[tb] = mma_split_a<OP>(xa2[tb], rh, rl, OP::load_n(Gs, M, 16 * tb, 32 * kb, lane));
+        }
       }
+      if (FULL) {
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) xa2[tb] *= et[16 * tb + c];
+      }
+      // Intra-chunk terms: gtilde -= sum_{s<t} X[s][j] E[t][s];  dXw += sum_{t>s} X[t][j] E[t][s]
+#pragma unroll
+      for (int kb = 0; kb < C / 32; ++kb) {
+        const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+        const F xn = OP::neg(xq);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          if (kb <= tb / 2) ga[tb] = OP::mma(ga[tb], xn, OP::load_n(Es, C, 16 * tb, 32 * kb, lane));
+          if (FULL && kb >= tb / 2) xa2[tb] = OP::mma(xa2[tb], xq, OP::load_t(Es, C, 32 * kb, 16 * tb, lane));
+        }
+      }
+      // Lane holds row t = 16tb + c, columns j = 16w + 4q + r; dX = gtilde - xa2.
+#pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        // gtilde^T[j][t] = sum_i W[i][j] dY[t][i] - sum_s X[s][j] E[t][s]
-        f32x4 ga = zero4();
-#pragma unroll
-        for (int kb = 0; kb < M / 32; ++kb)
-          ga = mma_split_a<OP>(ga, Wh[kb], Wl[kb], OP::load(Dr, LDM, 16 * tb, 32 * kb, lane));
-        for (int kb = 0; kb <= tb / 2; ++kb)
-          ga = OP::mma(ga, OP::load(Xt, LDC, 16 * w, 32 * kb, lane), OP::load(Er, LDC, 16 * tb, 32 * kb, lane));
-        // Lane holds row t = 16tb + c, columns j = 16w + 4q + r.
-        const int t = 16 * tb + c;
-        f32x4 dx = ga;
-        if (need_dxw) {
-          // dXw^T[j][s] = -(eta_s sum_i R[i][j] G[s][i] + sum_t X[t][j] E[t][s]), s = t here.
-          f32x4 xa = zero4();
-#pragma unroll
-          for (int kb = 0; kb < M / 32; ++kb)
-            xa = mma_split_a<OP>(xa, Rh[kb], Rl[kb], OP::load(Gr, LDM, 16 * tb, 32 * kb, lane));
-          xa *= et[t];
-          for (int kb = tb / 2; kb < C / 32; ++kb)
-            xa = OP::mma(xa, OP::load(Xt, LDC, 16 * w, 32 * kb, lane), OP::load(Et, LDC, 16 * tb, 32 * kb, lane));
-          dx = ga - xa;
-        }
-        if (t < nvalid) {
-          const int64_t o = (t0 + t) * D + 16 * w + 4 * q;
-          if (a.gtilde) *reinterpret_cast<f32x4*>(a.gtilde + bh * T * D + o) = ga;
-          if (a.dX) *reinterpret_cast<f32x4*>(a.dX + bh * T * D + o) = dx;
-        }
+        const uint32_t o = (uint32_t)(((t0 + 16 * tb + c) * D + 16 * w + 4 * q) * 4);
+        if (a.gtilde) buf_store4(Ogc, o, ga[tb]);
+        if (FULL && a.dX) buf_store4(Oxc, o, ga[tb] - xa2[tb]);
       }
     }
 
-    // (4) U, dG and deta for rows i in [16w, 16w+16).
-    if (w < IB && need_u) {
-      F Rh[D / 32], Rl[D / 32];
+    if constexpr (FULL) {
+      // (4) U, dG and deta for rows i in [16w, 16w+16), all s blocks at once.
+      if (w < IB) {
+        f32x4 ua[TB];
 #pragma unroll
-      for (int kb = 0; kb < D / 32; ++kb) OP::split(cat(Ri[2 * kb], Ri[2 * kb + 1]), Rh[kb], Rl[kb]);
-      for (int sb = 0; sb < TB; ++sb) {
+        for (int sb = 0; sb < TB; ++sb) ua[sb] = zero4();
         // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
-        f32x4 ua = zero4();
 #pragma unroll
-        for (int kb = 0; kb < D / 32; ++kb)
-          ua = mma_split_a<OP>(ua, Rh[kb], Rl[kb], OP::load(Xr, LDD, 16 * sb, 32 * kb, lane));
+        for (int kb = 0; kb < D / 32; ++kb) {
+          const F rh = OP::load_t(Rh, M, 32 * kb, 16 * w, lane);
+          F rl = rh;
+          if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * w, lane);
+#pragma unroll
+          for (int sb = 0; sb < TB; ++sb)
+            ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane));
+        }
         // Intra-chunk term with S[t][s] = x_t . x_s computed here, per pair of
         // t blocks, and kept in fp32 registers (split for the matrix core):
         // the tile (rows t, cols s) is directly the operand contracted over t.
-        for (int kb = sb / 2; kb < C / 32; ++kb) {
-          f32x8 sv;
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int tb = 2 * kb + hh;
-            f32x4 st = zero4();
-            if (tb >= sb) {
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
 #pragma unroll
-              for (int kj = 0; kj < D / 32; ++kj)
-                st = OP::mma(st, OP::load(Xr, LDD, 16 * tb, 32 * kj, lane), OP::load(Xr, LDD, 16 * sb, 32 * kj, lane));
+          for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+            f32x8 sv;
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int t = 16 * tb + 4 * q + r, s = 16 * sb + c;
-                if (!(INCL ? (t >= s) : (t > s))) st[r] = 0.f;
+            for (int hh = 0; hh < 2; ++hh) {
+              const int tb = 2 * kb + hh;
+              f32x4 st = zero4();
+              if (tb >= sb) {
+#pragma unroll
+                for (int kj = 0; kj < D / 32; ++kj)
+                  st = OP::mma(st, OP::load_n(Xs, D, 16 * tb, 32 * kj, lane), OP::load_n(Xs, D, 16 * sb, 32 * kj, lane));
+                if (tb == sb) {
+#pragma unroll
+                  for (int r = 0; r < 4; ++r) {
+                    const int t = 4 * q + r;
+                    if (!(INCL ? (t >= c) : (t > c))) st[r] = 0.f;
+                  }
+                }
               }
+#pragma unroll
+              for (int r = 0; r < 4; ++r) sv[4 * hh + r] = st[r];
             }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sv[4 * hh + r] = st[r];
+            F sh, sl;
+            OP::split(sv, sh, sl);
+            ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
           }
-          F sh, sl;
-          OP::split(sv, sh, sl);
-          ua = mma_split_b<OP>(ua, OP::load(Dt, LDC, 16 * w, 32 * kb, lane), sh, sl);
         }
-        // Lane holds token s = 16sb + c, rows i = 16w + 4q + r; U = -ua.
-        const int s = 16 * sb + c;
-        const float es = et[s];
-        if (a.dG && s < nvalid)
-          *reinterpret_cast<f32x4*>(a.dG + (bh * T + t0 + s) * M + 16 * w + 4 * q) = -es * ua;
-        if (a.deta) {
-          const E* gp = Gr + s * LDM + 16 * w + 4 * q;
-          float p = 0.f;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) p -= (float)gp[r] * ua[r];
-          p += __shfl_xor(p, 16);
-          p += __shfl_xor(p, 32);
-          if (q == 0) dpart[w][s] = p;
+        for (int sb = 0; sb < TB; ++sb) {
+          // Lane holds token s = 16sb + c, rows i = 16w + 4q + r; U = -ua.
+          const int s = 16 * sb + c;
+          const float es = et[s];
+          if (a.dG) buf_store4(Odc, (uint32_t)(((t0 + s) * M + 16 * w + 4 * q) * 4), -es * ua[sb]);
+          if (a.deta) {
+            typedef typename Vec4<E>::type vec4;
+            const vec4 gv = *reinterpret_cast<const vec4*>(Gs + lds_off(s, 16 * w + 4 * q, M));
+            float p = 0.f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[sb][r];
+            p += __shfl_xor(p, 16);
+            p += __shfl_xor(p, 32);
+            if (q == 0) dpart[w][s] = p;
+          }
         }
       }
-    }
 
-    // (5) Suffix update: R_{n-1} = R_n + dY^T X (exact products).
-    if (w < JB && need_dxw) {
+      // (5) Suffix update: R_{n-1} = R_n + dY^T X (exact products).
+      if (w < JB) {
 #pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) {
-        const F xq = OP::load(Xt, LDC, 16 * w, 32 * kb, lane);
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load(Dt, LDC, 16 * ib, 32 * kb, lane), xq);
+          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, lane), xq);
+        }
       }
-    }
-    if (w < IB && need_ri) {
-#pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) {
-        const F dq = OP::load(Dt, LDC, 16 * w, 32 * kb, lane);
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) Ri[jb] = OP::mma(Ri[jb], OP::load(Xt, LDC, 16 * jb, 32 * kb, lane), dq);
-      }
-    }
-    if (a.deta) {
-      __syncthreads();
-      if (tid < nvalid) {
+      if (a.deta) {
+        __syncthreads();
+        const int tt = tid < C ? tid : 0;
         float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < IB; ++i) s += dpart[i][tid];
-        a.deta[bh * T + t0 + tid] = s;
+        for (int i = 0; i < IB; ++i) s += dpart[i][tt];
+        buf_store1(Oec, tid < C ? (uint32_t)((t0 + tid) * 4) : kOOB, s);
       }
     }
+  };
+
+  if constexpr (DEPTH == 2) {
+    for (int64_t n = nch - 1; n >= 0; n -= 2) {
+      chunk(xa, ga, da, ea, n);
+      chunk(xb, gb, db, eb, n - 1);
+    }
+  } else {
+    for (int64_t n = nch - 1; n >= 0; --n) chunk(xa, ga, da, ea, n);
   }
 
-  // Segment 0 ends holding sum over the whole sequence of dY x^T.
-  if (a.rfin && seg == 0 && w < IB) {
-    float* o = a.rfin + bh * M * D + (int64_t)(16 * w + c) * D;
+  // Segment 0 ends holding the sum over the whole sequence of dY x^T.
+  if (FULL && a.rfin && seg == 0 && w < JB) {
+    float* o = a.rfin + bh * M * D;
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb + 4 * q) = Ri[jb];
+    for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[(int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c] = Rj[ib][r];
   }
 }
 
@@ -316,32 +361,39 @@ reduce_dw0_kernel(const float* rfin, float* dW0, int64_t B, int64_t H, int64_t m
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-static int lds_bytes_bwd(int bf16, int d, int m, int C) {
+static constexpr int lds_bytes_bwd(int bf16, int d, int m, int C, int etav) {
   const int es = bf16 ? 2 : 4;
-  return es * (C * (d + 4) + 2 * C * (m + 4) + d * (C + 4) + 2 * m * (C + 4) + 2 * C * (C + 4)) +
-         4 * C + 4 * (m / 16) * C;
+  const int v = etav ? (bf16 ? 2 : 1) * C * m : 0;
+  const int r = (bf16 ? 2 : 1) * d * m;
+  return es * (C * d + 2 * C * m + C * C + v + r) + 4 * C + 4 * (m / 16) * C;
 }
 
+// Tile length of the backward (the same for both eta forms).  bf16 tiles use
+// 64 for every map; fp32 tiles take twice the LDS and registers and use 64
+// only for the 64 x 64 map.  launch_scan_bwd dispatches on exactly this value.
 int bwd_chunk_for(int bf16, int d, int m, int requested) {
   (void)requested;
-  int C = 64;
-  if (lds_bytes_bwd(bf16, d, m, C) > 160 * 1024) C = 32;
-  return C;
+  return (bf16 || (d == 64 && m == 64)) ? 64 : 32;
 }
+static_assert(lds_bytes_bwd(1, 128, 128, 64, 1) <= 160 * 1024, "bf16 backward tile does not fit LDS");
+static_assert(lds_bytes_bwd(0, 64, 64, 64, 1) <= 160 * 1024, "fp32 backward tile does not fit LDS");
+static_assert(lds_bytes_bwd(0, 128, 128, 32, 1) <= 160 * 1024, "fp32 backward tile does not fit LDS");
 
 int bwd_wgs_per_cu(int bf16, int d, int m, int C) {
-  int n = 160 * 1024 / lds_bytes_bwd(bf16, d, m, C);
+  int n = 160 * 1024 / lds_bytes_bwd(bf16, d, m, C, 0);
   const int waves = cmax(d, m) / 16;
-  if (n * waves > 32) n = 32 / waves;
+  if (n * waves > 8) n = 8 / waves;  // two waves per SIMD (register budget)
   return n < 1 ? 1 : n;
 }
 
-template <class OP, int D, int M, int C>
-static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream_t s) {
+template <class OP, int D, int M, int C, bool ETAV>
+static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStream_t s) {
   constexpr int NT = cmax(D, M) / 16 * 64;
   const int64_t BH = p.B * p.H;
-  const bool need_gx = f.gtilde || f.dX;
-  const bool need_sfx = p.nseg > 1 && (f.dX || f.dG || f.deta || f.dW0);
+  const unsigned grid = (unsigned)seg_grid(BH, p.nseg);
+  // Only gtilde requested: the reverse-time suffix is never needed.
+  const bool read_only = !f.dX && !f.dG && !f.deta && !f.dW0;
+  const bool need_sfx = p.nseg > 1 && !read_only;
 
   KArgs k{};
   k.W0 = f.W0;
@@ -350,28 +402,26 @@ static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream
   k.dY = f.dY;
   k.eta = f.eta;
   k.eta_scalar = f.eta_scalar;
+  k.BH = BH;
   k.H = p.H;
   k.T = p.T;
   k.seg_len = p.seg_len;
   k.nseg = p.nseg;
   k.aggA = f.aggA;
   k.aggB = f.aggB;
-  // Segment aggregates: writes (for the un-write start state) and, when a
-  // suffix is needed, dY x^T.  The write aggregate is skipped when only the
-  // reverse-time outputs are requested; W is then never read.
-  if (need_gx || need_sfx) {
-    timing_begin(GRADLEV_K_BWD_AGG, s);
-    if (need_sfx)
-      hipLaunchKernelGGL((agg_kernel<OP, D, M, C, true>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, k);
-    else
-      hipLaunchKernelGGL((agg_kernel<OP, D, M, C, false>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, k);
-    timing_end(GRADLEV_K_BWD_AGG, s);
-    if (p.nseg > 1) {
-      timing_begin(GRADLEV_K_BWD_CARRY, s);
-      (void)launch_carry(f.aggA, need_sfx ? f.aggB : nullptr, BH, p.nseg, (int64_t)D * M, need_sfx ? 1 : 2, s);
-      timing_end(GRADLEV_K_BWD_CARRY, s);
-    }
-  }
+  // Segment aggregates (writes, and dY x^T when a suffix is needed), then the
+  // carry that turns them into every segment's end state.
+  timing_begin(GRADLEV_K_BWD_AGG, s);
+  if (need_sfx)
+    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdAB, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+  else
+    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdA, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+  timing_end(GRADLEV_K_BWD_AGG, s);
+  timing_begin(GRADLEV_K_BWD_CARRY, s);
+  hipError_t e = launch_carry(f.W0, f.aggA, need_sfx ? f.aggB : nullptr, BH, p.H, p.nseg, D, M, 1, s);
+  timing_end(GRADLEV_K_BWD_CARRY, s);
+  if (e != hipSuccess) return e;
+
   BArgs b{};
   b.W0 = f.W0;
   b.X = f.X;
@@ -379,6 +429,7 @@ static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream
   b.dY = f.dY;
   b.eta = f.eta;
   b.eta_scalar = f.eta_scalar;
+  b.BH = BH;
   b.H = p.H;
   b.T = p.T;
   b.seg_len = p.seg_len;
@@ -387,14 +438,21 @@ static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream
   b.dX = f.dX;
   b.dG = f.dG;
   b.deta = f.deta;
-  b.pin = need_gx ? f.aggA : nullptr;
-  b.sfx = need_sfx ? f.aggB : nullptr;
+  b.wend = f.aggA;
+  b.rend = need_sfx ? f.aggB : nullptr;
   b.rfin = f.dW0 ? f.rfin : nullptr;
   timing_begin(GRADLEV_K_BWD_MAIN, s);
-  if (p.inclusive)
-    hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, true>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, b);
-  else
-    hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, b);
+  if (read_only) {
+    if (p.inclusive)
+      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, true, ETAV, kOutRead>), dim3(grid), dim3(NT), 0, s, b);
+    else
+      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutRead>), dim3(grid), dim3(NT), 0, s, b);
+  } else {
+    if (p.inclusive)
+      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, true, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
+    else
+      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
+  }
   timing_end(GRADLEV_K_BWD_MAIN, s);
   if (f.dW0) {
     const int64_t md4 = (int64_t)D * M / 4, n = p.H * md4;
@@ -403,6 +461,12 @@ static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream
     timing_end(GRADLEV_K_BWD_DW0, s);
   }
   return hipGetLastError();
+}
+
+template <class OP, int D, int M, int C>
+static hipError_t bwd_dispatch(const ScanProblem& p, const BwdPtrs& f, hipStream_t s) {
+  if (f.eta) return bwd_dispatch2<OP, D, M, C, true>(p, f, s);
+  return bwd_dispatch2<OP, D, M, C, false>(p, f, s);
 }
 
 template <class OP, int C>
@@ -415,11 +479,10 @@ static hipError_t bwd_by_dims(const ScanProblem& p, const BwdPtrs& f, hipStream_
 }
 
 hipError_t launch_scan_bwd(const ScanProblem& p, const BwdPtrs& f, hipStream_t s) {
+  if (p.chunk != bwd_chunk_for(p.bf16, p.d, p.m, 0)) return hipErrorInvalidValue;
   if (p.bf16) return bwd_by_dims<OpBF16, 64>(p, f, s);
-  // fp32 tiles double the LDS footprint: chunk 64 fits only the 64 x 64 map.
-  if (p.d == 64 && p.m == 64 && p.chunk == 64) return bwd_dispatch<OpF32, 64, 64, 64>(p, f, s);
-  if (p.chunk == 32) return bwd_by_dims<OpF32, 32>(p, f, s);
-  return hipErrorInvalidValue;
+  if (p.chunk == 64) return bwd_dispatch<OpF32, 64, 64, 64>(p, f, s);
+  return bwd_by_dims<OpF32, 32>(p, f, s);
 }
 
 }  // namespace gradlev

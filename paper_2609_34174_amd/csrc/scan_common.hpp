@@ -1,7 +1,9 @@
-// Pieces shared by the forward and backward scan launchers: kernel
-// arguments, the segment-aggregate kernel and the cross-segment carry.
+// Pieces shared by the forward and backward scan kernels: kernel arguments,
+// the block -> (sequence, segment) map, chunk-tile staging, the
+// segment-aggregate kernel and the cross-segment carry.
 #pragma once
 
+#include "../../include/gradlev.h"
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -14,101 +16,245 @@ struct KArgs {
   const void* dY;
   const float* eta;
   float eta_scalar;
-  int64_t H, T, seg_len, nseg;
+  int64_t BH, H, T, seg_len, nseg;
   float* out0;   // fwd: Y
-  float* aggA;
-  float* aggB;
+  float* aggA;   // [BH][nseg][m*d] write aggregates (fwd: [m][d]; bwd: transposed [d][m])
+  float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates
 };
 
 // ---------------------------------------------------------------------------
-// Segment aggregates: A_k = sum_{t in seg k} eta_t g_t x_t^T   ([m][d], fp32)
-// and, for the backward (BWD), B_k = sum_{t in seg k} dY_t x_t^T for k >= 1.
-// Grid (segments to aggregate, B*H); wave w owns rows i in [16w, 16w+16).
+// Workgroups are dealt round-robin over the 8 XCDs of an MI355X by linear
+// block id.  All segments of one sequence are mapped to the same XCD (block id
+// congruent mod 8), so the segment aggregates a sequence exchanges stay in
+// that XCD's L2.  Grid size: 8 * nseg * ceil(BH / 8); blocks past BH exit.
 // ---------------------------------------------------------------------------
-template <class OP, int D, int M, int C, bool BWD>
+constexpr int kXCD = 8;
+
+__host__ __device__ inline int64_t seg_grid(int64_t BH, int64_t nseg) {
+  return kXCD * nseg * ((BH + kXCD - 1) / kXCD);
+}
+
+__device__ __forceinline__ bool map_block(int64_t BH, int64_t nseg, int64_t& bh, int64_t& seg) {
+  const int64_t L = blockIdx.x;
+  const int64_t r = L / kXCD;
+  seg = r % nseg;
+  bh = L % kXCD + kXCD * (r / nseg);
+  return bh < BH;
+}
+
+// ---------------------------------------------------------------------------
+// Chunk tile staging by 4x4 element blocks.  A C x K tile of a row-major
+// [T][K] global matrix is held in registers (thread b owns rows 4*rb..4*rb+3
+// and the 4-element chunk cb; consecutive threads take consecutive chunks of
+// a row so the global loads coalesce) while earlier chunks compute, then
+// written row by row into a swizzled LDS tile: a 16-lane group writes 16
+// distinct chunks of one row.  The loads go through the sequence's buffer
+// resource, so rows past the sequence end arrive as zero, which masks a
+// partial chunk.  (Segments are whole chunks, so only the sequence end can
+// cut a chunk.)
+// ---------------------------------------------------------------------------
+template <typename T>
+struct Vec4;
+template <>
+struct Vec4<bf16> {
+  typedef bf16x4 type;
+};
+template <>
+struct Vec4<float> {
+  typedef f32x4 type;
+};
+
+template <class OP, int C, int K, int NT>
+struct Tile4 {
+  typedef typename OP::elem elem;
+  typedef typename Vec4<elem>::type vec4;
+  static constexpr int NCB = K / 4, NB = (C / 4) * NCB, PER = (NB + NT - 1) / NT;
+  vec4 v[PER][4];
+
+  // Loads the chunk whose first row starts at byte `off` of `src`; with
+  // off == kOOB the tile is zero and nothing is read.
+  __device__ __forceinline__ void load(rsrc_t src, uint32_t off, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int b = tid + i * NT, rb = b / NCB, cb = b % NCB;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t o = (off == kOOB || b >= NB) ? kOOB : off + (uint32_t)(((4 * rb + k) * K + 4 * cb) * sizeof(elem));
+        v[i][k] = buf_load4(src, o, (const elem*)nullptr);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(elem* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int b = tid + i * NT, rb = b / NCB, cb = b % NCB;
+      if (b >= NB) continue;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) *reinterpret_cast<vec4*>(lds + lds_off(4 * rb + k, 4 * cb, K)) = v[i][k];
+    }
+  }
+  // Store of s_row * value split into hi + lo tiles (one tile for fp32
+  // operands), with per-row scale s_row = et[row].
+  __device__ __forceinline__ void store_scaled(elem* hi, elem* lo, int tid, const float* et) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int b = tid + i * NT, rb = b / NCB, cb = b % NCB;
+      if (b >= NB) continue;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float s = et[4 * rb + k];
+        f32x4 f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f[e] = (float)v[i][k][e] * s;
+        const int o = lds_off(4 * rb + k, 4 * cb, K);
+        OP::store4_split(hi + o, lo + o, f);
+      }
+    }
+  }
+};
+
+// Step sizes of one chunk, loaded together with the chunk's tiles (thread
+// tid < C holds row tid; per-token values only), then staged into LDS as
+// sign * eta for the valid rows and 0 past them.
+template <bool ETAV>
+struct EtaReg {
+  float v;
+  __device__ __forceinline__ void load(rsrc_t r, uint32_t off_row0, int tid, int C) {
+    v = 0.f;
+    if constexpr (ETAV) v = buf_load1(r, (off_row0 == kOOB || tid >= C) ? kOOB : off_row0 + 4 * tid);
+  }
+  __device__ __forceinline__ void stage(float* et, int C, float eta_scalar, int nvalid, float sign, int tid) const {
+    if (tid < C) et[tid] = tid < nvalid ? sign * (ETAV ? v : eta_scalar) : 0.f;
+  }
+};
+
+__device__ __forceinline__ rsrc_t eta_rsrc(const float* eta, int64_t bh, int64_t T) {
+  return make_rsrc(eta ? eta + bh * T : nullptr, eta ? (uint32_t)(T * 4) : 0u);
+}
+
+// ---------------------------------------------------------------------------
+// Segment aggregates: A_k = sum_{t in seg k} eta_t g_t x_t^T (fp32) and, for
+// the backward (mode kAggBwdAB), B_k = sum_{t in seg k} dY_t x_t^T for k >= 1.
+// Forward: A row-major [m][d].  Backward: A and B transposed [d][m] (its waves
+// own column blocks of W and R).  Segments [0, nagg) of every sequence; wave
+// w owns rows i in [16w, 16w+16).  With a scalar eta the products are exact
+// bf16 products and eta scales the sum once; per-token eta is folded into a
+// hi + lo split operand staged once per chunk.
+// ---------------------------------------------------------------------------
+enum AggMode { kAggFwd = 0, kAggBwdA = 1, kAggBwdAB = 2 };
+
+template <class OP, int D, int M, int C, int MODE, bool ETAV>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
-agg_kernel(const KArgs a) {
+agg_kernel(const KArgs a, int64_t nagg) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
+  constexpr bool BWD = MODE == kAggBwdAB;    // also aggregate dY x^T
+  constexpr bool TRANS = MODE != kAggFwd;    // backward layout
+  constexpr bool SPLITV = ETAV && OP::kSplit == 2;
   constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
-  constexpr int JB = D / 16, IB = M / 16, LDC = C + 4;
-  __shared__ E Xt[D * LDC];
-  __shared__ E Gt[M * LDC];
-  __shared__ E Dt[BWD ? M * LDC : 1];
+  constexpr int JB = D / 16, IB = M / 16;
+  __shared__ E Xs[C * D];
+  __shared__ E Gs[C * M];                 // G, or eta G hi when ETAV
+  __shared__ E Gl[SPLITV ? C * M : 1];    // eta G lo
+  __shared__ E Ds[BWD ? C * M : 1];
   __shared__ float et[C];
 
+  int64_t bh, seg;
+  if (!map_block(a.BH, a.nseg, bh, seg) || seg >= nagg) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
-  const int64_t seg = blockIdx.x, bh = blockIdx.y;
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
   const bool with_b = BWD && seg >= 1;
-  const E* X = static_cast<const E*>(a.X) + bh * T * D;
-  const E* G = static_cast<const E*>(a.G) + bh * T * M;
-  const E* Dy = BWD ? static_cast<const E*>(a.dY) + bh * T * M : nullptr;
+  const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
+  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t Dy = make_rsrc(BWD ? static_cast<const E*>(a.dY) + bh * T * M : nullptr, BWD ? (uint32_t)(T * M * sizeof(E)) : 0u);
 
   f32x4 accA[JB], accB[JB];
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) accA[jb] = accB[jb] = zero4();
 
-  TileRegs<OP, C, D, NT> xr;
-  TileRegs<OP, C, M, NT> gr, dr;
-  {
-    const int rows = (int)(t_end - t_begin < C ? t_end - t_begin : C);
-    xr.load(X + t_begin * D, rows, tid);
-    gr.load(G + t_begin * M, rows, tid);
-    if (with_b) dr.load(Dy + t_begin * M, rows, tid);
-  }
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += C) {
-    const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
+  // The pass streams its inputs and does little arithmetic per byte, so its
+  // rate is set by the bytes in flight: chunks are staged DEPTH ahead.  Every
+  // group runs all DEPTH chunk steps (a step past the segment end sees zero
+  // tiles and adds nothing), which keeps the memory operations branch-free.
+  constexpr int DEPTH = 4;
+  Tile4<OP, C, D, NT> xr[DEPTH];
+  Tile4<OP, C, M, NT> gr[DEPTH], dr[DEPTH];
+  EtaReg<ETAV> er[DEPTH];
+  const rsrc_t Et = eta_rsrc(a.eta, bh, T);
+  auto fetch = [&](int k, int64_t t0) {
+    const bool ok = t0 < t_end;
+    er[k].load(Et, ok ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    xr[k].load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
+    gr[k].load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    if (with_b) dr[k].load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+  };
+#pragma unroll
+  for (int k = 0; k < DEPTH; ++k) fetch(k, t_begin + k * C);
+
+  auto chunk = [&](int k, int64_t t0) {
+    const int nvalid = (int)(t_end - t0 < C ? (t_end > t0 ? t_end - t0 : 0) : C);
     __syncthreads();
-    xr.store_cols(Xt, LDC, tid);
-    gr.store_cols(Gt, LDC, tid);
-    if (with_b) dr.store_cols(Dt, LDC, tid);
-    if (tid < C) et[tid] = tid < nvalid ? (a.eta ? a.eta[bh * T + t0 + tid] : a.eta_scalar) : 0.f;
-    __syncthreads();
-    if (t0 + C < t_end) {
-      const int rows = (int)(t_end - t0 - C < C ? t_end - t0 - C : C);
-      xr.load(X + (t0 + C) * D, rows, tid);
-      gr.load(G + (t0 + C) * M, rows, tid);
-      if (with_b) dr.load(Dy + (t0 + C) * M, rows, tid);
+    if (ETAV) er[k].stage(et, C, a.eta_scalar, nvalid, 1.f, tid);
+    xr[k].store(Xs, tid);
+    if (with_b) dr[k].store(Ds, tid);
+    if (!ETAV) gr[k].store(Gs, tid);
+    if (ETAV) {
+      __syncthreads();
+      gr[k].store_scaled(Gs, Gl, tid, et);
     }
+    __syncthreads();
+    fetch(k, t0 + DEPTH * C);
     if (w < IB) {
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
-        f32x8 gv = OP::load_f32(Gt, LDC, 16 * w, 32 * kb, lane);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) gv[e] *= et[32 * kb + slot_k(e, q)];
-        F vh, vl;
-        OP::split(gv, vh, vl);
-        F dv;
-        if (with_b) dv = OP::load(Dt, LDC, 16 * w, 32 * kb, lane);
+        // A^T[j][i] += sum_t X[t][j] (eta G)[t][i];  B^T[j][i] += sum_t X[t][j] dY[t][i]
+        const F gh = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
+        F gl = gh;
+        if constexpr (SPLITV) gl = OP::load_t(Gl, M, 32 * kb, 16 * w, lane);
+        F dv = gh;
+        if (with_b) dv = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) {
-          const F xa = OP::load(Xt, LDC, 16 * jb, 32 * kb, lane);
-          accA[jb] = mma_split_b<OP>(accA[jb], xa, vh, vl);
+          const F xa = OP::load_t(Xs, D, 32 * kb, 16 * jb, lane);
+          if constexpr (ETAV) accA[jb] = mma_split_b<OP>(accA[jb], xa, gh, gl);
+          else accA[jb] = OP::mma(accA[jb], xa, gh);
           if (with_b) accB[jb] = OP::mma(accB[jb], xa, dv);
         }
       }
     }
+  };
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += DEPTH * C) {
+#pragma unroll
+    for (int k = 0; k < DEPTH; ++k) chunk(k, t0 + k * C);
   }
   if (w < IB) {
     // accA[jb] holds A^T[j = 16jb + 4q + r][i = 16w + c].
-    const int64_t off = (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * D;
+    const int64_t base = (bh * a.nseg + seg) * M * D;
+    const float s = ETAV ? 1.f : a.eta_scalar;
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) {
-      *reinterpret_cast<f32x4*>(a.aggA + off + 16 * jb + 4 * q) = accA[jb];
-      if (with_b) *reinterpret_cast<f32x4*>(a.aggB + off + 16 * jb + 4 * q) = accB[jb];
+      if (TRANS) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) a.aggA[base + (int64_t)(16 * jb + 4 * q + r) * M + 16 * w + c] = s * accA[jb][r];
+      } else {
+        *reinterpret_cast<f32x4*>(a.aggA + base + (int64_t)(16 * w + c) * D + 16 * jb + 4 * q) = s * accA[jb];
+      }
+      if (with_b) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) a.aggB[base + (int64_t)(16 * jb + 4 * q + r) * M + 16 * w + c] = accB[jb][r];
+      }
     }
   }
 }
 
-// Carry across segments (defined in scan_fwd.hip).
-//   mode 0 (forward):  A[k] <- sum_{j<k} A[j]        (A[nseg-1] is not read)
-//   mode 1 (backward): A[k] <- sum_{j<=k} A[j];  B[k] <- sum_{j>k} B[j]
-//                      (B[0] is not read)
-//   mode 2 (backward, no suffix): A[k] <- sum_{j<=k} A[j]
-hipError_t launch_carry(float* A, float* B, int64_t BH, int64_t nseg, int64_t md, int mode,
-                        hipStream_t s);
+// Carry across segments (scan_fwd.hip), per sequence and element, in a fixed
+// summation order, with W0 folded in:
+//   mode 0 (forward):  A[k] <- W0 - sum_{j<k} A[j]            ([m][d])
+//   mode 1 (backward): A[k] <- W0^T - sum_{j<=k} A[j]         ([d][m])
+//                      B[k] <- sum_{j>k} B[j] if B != null    ([d][m]; B[0] unread)
+hipError_t launch_carry(const float* W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d,
+                        int m, int mode, hipStream_t s);
 
 }  // namespace gradlev

@@ -12,215 +12,290 @@
 //       S   = X X^T                        (C x C, causal mask, scaled by -eta)
 //       Y   = X W_n^T + S G                (state read + intra-chunk reads)
 //       W  <- W_n - (eta G)^T X            (carry to the next chunk)
-//   * segments are joined by their aggregated writes A_k = sum eta g x^T,
-//     computed by agg_kernel and turned into exclusive prefixes by
-//     carry_kernel, so each segment starts from W_0 - sum_{j<k} A_j.
-#include "../../include/gradlev.h"
+//   * segments are joined by their aggregated writes A_k = sum eta g x^T
+//     (agg_kernel) and the carry kernel, which leaves W_0 - sum_{j<k} A_j for
+//     every segment k; a workgroup loads its start state once.
+// Chunk inputs are staged through registers two chunks ahead of the compute
+// (about 3 us of loaded HBM latency has to be covered) into row-major LDS
+// tiles; operands with k along the tile rows use the transposing LDS read.
 #include "scan_common.hpp"
 
 namespace gradlev {
 
 // ---------------------------------------------------------------------------
-// Carry across segments, per sequence and element (fixed summation order).
-//   mode 0 (forward):  A[k] <- sum_{j<k} A[j]        (A[nseg-1] is not read)
-//   mode 1 (backward): A[k] <- sum_{j<=k} A[j];  B[k] <- sum_{j>k} B[j]
-//                      (B[0] is not read)
-//   mode 2 (backward, no suffix): A[k] <- sum_{j<=k} A[j]
+// Cross-segment carry.  One thread per (sequence, 4 elements); every segment
+// value is loaded before any is summed, so the whole carry costs one memory
+// latency.  Summation order is fixed (segment 0 first).
 // ---------------------------------------------------------------------------
+constexpr int kMaxSeg = 16;
+
 static __global__ void __launch_bounds__(256)
-carry_kernel(float* A, float* B, int64_t BH, int64_t nseg, int64_t md4, int mode) {
+carry_kernel(const float* __restrict__ W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d, int m,
+             int mode) {
+  const int64_t md4 = (int64_t)d * m / 4;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= BH * md4) return;
-  const int64_t bh = gid / md4, e = gid % md4;
-  f32x4* pa = reinterpret_cast<f32x4*>(A) + bh * nseg * md4 + e;
-  f32x4 run = zero4();
+  const int64_t bh = gid / md4, e4 = gid % md4, h = bh % H;
+  f32x4* pa = reinterpret_cast<f32x4*>(A) + bh * nseg * md4 + e4;
+  f32x4 w0;
   if (mode == 0) {
-    for (int64_t k = 0; k < nseg; ++k) {
-      const f32x4 v = k + 1 < nseg ? pa[k * md4] : zero4();
+    w0 = reinterpret_cast<const f32x4*>(W0 + h * m * d)[e4];
+  } else {
+    // element 4*e4 + r of the transposed [d][m] layout is W0[i][j], j = e / m, i = e % m
+    const int64_t e = 4 * e4, j = e / m, i = e % m;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w0[r] = W0[h * m * d + (i + r) * d + j];
+  }
+  f32x4 v[kMaxSeg];
+#pragma unroll
+  for (int k = 0; k < kMaxSeg; ++k)
+    if (k < nseg && (mode == 1 || k + 1 < nseg)) v[k] = pa[k * md4];
+  f32x4 run = w0;
+#pragma unroll
+  for (int k = 0; k < kMaxSeg; ++k) {
+    if (k >= nseg) break;
+    if (mode == 0) {
       pa[k * md4] = run;
-      run += v;
+      if (k + 1 < nseg) run -= v[k];
+    } else {
+      run -= v[k];
+      pa[k * md4] = run;
     }
-    return;
   }
-  for (int64_t k = 0; k < nseg; ++k) {
-    run += pa[k * md4];
-    pa[k * md4] = run;
+  if (mode == 1 && B) {
+    f32x4* pb = reinterpret_cast<f32x4*>(B) + bh * nseg * md4 + e4;
+#pragma unroll
+    for (int k = 1; k < kMaxSeg; ++k)
+      if (k < nseg) v[k] = pb[k * md4];
+    f32x4 acc = zero4();
+#pragma unroll
+    for (int k = kMaxSeg - 1; k >= 0; --k) {
+      if (k >= nseg) continue;
+      pb[k * md4] = acc;
+      if (k >= 1) acc += v[k];
+    }
   }
-  if (mode != 1) return;
-  f32x4* pb = reinterpret_cast<f32x4*>(B) + bh * nseg * md4 + e;
-  run = zero4();
-  for (int64_t k = nseg - 1; k >= 1; --k) {
-    const f32x4 v = pb[k * md4];
-    pb[k * md4] = run;
-    run += v;
-  }
-  pb[0] = run;
 }
 
-hipError_t launch_carry(float* A, float* B, int64_t BH, int64_t nseg, int64_t md, int mode,
-                        hipStream_t s) {
-  const int64_t md4 = md / 4, n = BH * md4;
-  hipLaunchKernelGGL(carry_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, A, B, BH, nseg, md4, mode);
+hipError_t launch_carry(const float* W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d, int m,
+                        int mode, hipStream_t s) {
+  if (nseg > kMaxSeg) return hipErrorInvalidValue;
+  const int64_t n = BH * (int64_t)d * m / 4;
+  hipLaunchKernelGGL(carry_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W0, A, B, BH, H, nseg, d, m,
+                     mode);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Main forward kernel.  Grid (nseg, B*H); NW = max(d, m)/16 waves.
-// Wave w < m/16 owns output rows i in [16w, 16w+16): it holds that slice of
-// the state as accumulator tiles of W^T (rows j, cols i) and produces the
-// matching columns of Y for every token of the chunk.
+// Main forward kernel.  NW = max(d, m)/16 waves.  Wave w < m/16 owns output
+// rows i in [16w, 16w+16): it holds that slice of the state as accumulator
+// tiles of W^T (rows j, cols i) and produces the matching columns of Y for
+// every token of the chunk.
 // ---------------------------------------------------------------------------
-template <class OP, int D, int M, int C, bool INCL>
-__global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
+template <class OP, int D, int M, int C, bool INCL, bool ETAV>
+__global__ void __launch_bounds__(cmax(D, M) / 16 * 64, 128 / cmax(D, M))
 fwd_main_kernel(const KArgs a) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
   constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
   constexpr int TB = C / 16, JB = D / 16, IB = M / 16;
-  constexpr int LDR = D + 4, LDC = C + 4;
-  __shared__ E Xr[C * LDR];   // X[t][j]
-  __shared__ E Xt[D * LDC];   // X^T[j][t]
-  __shared__ E Gt[M * LDC];   // G^T[i][t]
-  __shared__ E Pl[C * LDC];   // -eta_s (x_t . x_s) masked, [t][s]
+  constexpr bool SPLITV = ETAV && OP::kSplit == 2;
+  __shared__ E Xs[C * D];                 // X[t][j]
+  __shared__ E Gs[C * M];                 // G[t][i]
+  __shared__ E Pl[C * C];                 // -eta_s (x_t . x_s) masked, [t][s]
+  __shared__ E Vh[ETAV ? C * M : 1];      // -(eta G)[t][i] hi (per-token eta)
+  __shared__ E Vl[SPLITV ? C * M : 1];    // -(eta G)[t][i] lo
   __shared__ float et[C];
 
+  int64_t bh, seg;
+  if (!map_block(a.BH, a.nseg, bh, seg)) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
-  const int64_t seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int64_t h = bh % a.H;
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
-  const E* X = static_cast<const E*>(a.X) + bh * T * D;
-  const E* G = static_cast<const E*>(a.G) + bh * T * M;
-  float* Y = a.out0 + bh * T * M;
+  const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
+  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t Y = make_rsrc(a.out0 + bh * T * M, (uint32_t)(T * M * 4));
+  const rsrc_t none = make_rsrc(nullptr, 0u);  // every access out of range
 
-  for (int i = tid; i < C * LDC; i += NT) Pl[i] = (E)0.f;
+  // Register staging, two chunks ahead.
+  Tile4<OP, C, D, NT> xa, xb;
+  Tile4<OP, C, M, NT> ga, gb;
+  EtaReg<ETAV> ea, eb;
+  const rsrc_t Et = eta_rsrc(a.eta, bh, T);
+  auto fetch = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, int64_t t0) {
+    const bool ok = t0 < t_end;
+    er.load(Et, ok ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    xr.load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
+    gr.load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+  };
+  fetch(xa, ga, ea, t_begin);
+  fetch(xb, gb, eb, t_begin + C);
 
-  // State tiles: Ws[jb] holds W[i = 16w + c][j = 16jb + 4q + r].
+  // State tiles: Ws[jb] holds W[i = 16w + c][j = 16jb + 4q + r] = W^T tile (rows j, cols i).
   f32x4 Ws[JB];
   if (w < IB) {
-    const float* w0 = a.W0 + h * M * D + (int64_t)(16 * w + c) * D;
-    const float* pf = a.aggA ? a.aggA + (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * D : nullptr;
+    const float* w0 = a.aggA ? a.aggA + (bh * a.nseg + seg) * M * D : a.W0 + h * M * D;
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) {
-      f32x4 v = *reinterpret_cast<const f32x4*>(w0 + 16 * jb + 4 * q);
-      if (pf) v -= *reinterpret_cast<const f32x4*>(pf + 16 * jb + 4 * q);
-      Ws[jb] = v;
-    }
+    for (int jb = 0; jb < JB; ++jb)
+      Ws[jb] = *reinterpret_cast<const f32x4*>(w0 + (int64_t)(16 * w + c) * D + 16 * jb + 4 * q);
   }
+  for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
 
-  TileRegs<OP, C, D, NT> xr;
-  TileRegs<OP, C, M, NT> gr;
-  {
-    const int rows = (int)(t_end - t_begin < C ? t_end - t_begin : C);
-    xr.load(X + t_begin * D, rows, tid);
-    gr.load(G + t_begin * M, rows, tid);
-  }
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += C) {
-    const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
+  auto chunk = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, int64_t t0) {
+    // A step past the segment end (the second of a pair) sees zero tiles,
+    // leaves the state unchanged and stores nothing.
+    const bool live = t0 < t_end;
+    const int nvalid = live ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
+    const rsrc_t Yc = live ? Y : none;
     __syncthreads();
-    xr.store_rows(Xr, LDR, tid);
-    xr.store_cols(Xt, LDC, tid);
-    gr.store_cols(Gt, LDC, tid);
-    if (tid < C) et[tid] = tid < nvalid ? (a.eta ? a.eta[bh * T + t0 + tid] : a.eta_scalar) : 0.f;
+    er.stage(et, C, a.eta_scalar, nvalid, -1.f, tid);
+    xr.store(Xs, tid);
+    gr.store(Gs, tid);
     __syncthreads();
-    if (t0 + C < t_end) {
-      const int rows = (int)(t_end - t0 - C < C ? t_end - t0 - C : C);
-      xr.load(X + (t0 + C) * D, rows, tid);
-      gr.load(G + (t0 + C) * M, rows, tid);
-    }
+    if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read after the next barrier
+    fetch(xr, gr, er, t0 + 2 * C);
 
     // Intra-chunk scores, lower-triangular tiles (tb >= sb) shared by all waves.
-    for (int idx = w; idx < TB * (TB + 1) / 2; idx += NW) {
-      const int tb = tri_row(idx), sb = idx - tb * (tb + 1) / 2;
+#pragma unroll
+    for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+      if (idx % NW != w) continue;
+      int tb = 0;
+      while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+      const int sb = idx - tb * (tb + 1) / 2;
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < D / 32; ++kb)
-        acc = OP::mma(acc, OP::load(Xr, LDR, 16 * sb, 32 * kb, lane), OP::load(Xr, LDR, 16 * tb, 32 * kb, lane));
-      // acc[r] = x_s . x_t with s = 16sb + 4q + r, t = 16tb + c.
+        acc = OP::mma(acc, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+      // acc[r] = x_s . x_t with s = 16sb + 4q + r, t = 16tb + c; et holds -eta.
       const int t = 16 * tb + c;
       f32x4 v;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int s = 16 * sb + 4 * q + r;
-        const bool keep = INCL ? (s <= t) : (s < t);
-        v[r] = keep ? -acc[r] * et[s] : 0.f;
+        const bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
+        v[r] = keep ? acc[r] * et[s] : 0.f;
       }
-      OP::store4(Pl + t * LDC + 16 * sb + 4 * q, v);
+      OP::store4(Pl + lds_off(t, 16 * sb + 4 * q, C), v);
     }
     __syncthreads();
 
     if (w < IB) {
-      F Wh[D / 32], Wl[D / 32];
+      // Y^T[i][t] for all t blocks at once (independent accumulator chains).
+      f32x4 acc[TB];
 #pragma unroll
-      for (int kb = 0; kb < D / 32; ++kb) OP::split(cat(Ws[2 * kb], Ws[2 * kb + 1]), Wh[kb], Wl[kb]);
-      for (int tb = 0; tb < TB; ++tb) {
-        f32x4 acc = zero4();
+      for (int tb = 0; tb < TB; ++tb) acc[tb] = zero4();
 #pragma unroll
-        for (int kb = 0; kb < D / 32; ++kb)
-          acc = mma_split_a<OP>(acc, Wh[kb], Wl[kb], OP::load(Xr, LDR, 16 * tb, 32 * kb, lane));
-        for (int kb = 0; kb <= tb / 2; ++kb)
-          acc = OP::mma(acc, OP::load(Gt, LDC, 16 * w, 32 * kb, lane), OP::load(Pl, LDC, 16 * tb, 32 * kb, lane));
-        // acc[r] = y_t[i] with i = 16w + 4q + r, t = 16tb + c.
-        const int t = 16 * tb + c;
-        if (t < nvalid) *reinterpret_cast<f32x4*>(Y + (t0 + t) * M + 16 * w + 4 * q) = acc;
+      for (int kb = 0; kb < D / 32; ++kb) {
+        F wh, wl;
+        OP::split(cat(Ws[2 * kb], Ws[2 * kb + 1]), wh, wl);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+          acc[tb] = mma_split_a<OP>(acc[tb], wh, wl, OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
       }
-      if (t0 + C < t_end) {
+#pragma unroll
+      for (int kb = 0; kb < C / 32; ++kb) {
+        const F gq = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);  // G[s][i], k = s
+#pragma unroll
+        for (int tb = 2 * kb; tb < TB; ++tb) acc[tb] = OP::mma(acc[tb], gq, OP::load_n(Pl, C, 16 * tb, 32 * kb, lane));
+      }
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        // acc[tb][r] = y_t[i] with i = 16w + 4q + r, t = 16tb + c (rows past T are dropped).
+        const int t = 16 * tb + c;
+        buf_store4(Yc, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), acc[tb]);
+      }
+      // Carry to the next chunk (also after the last one, where it is unused).
+      if constexpr (ETAV) {
+        // W^T[j][i] += sum_t X[t][j] (-eta G)[t][i], eta folded into the split operand.
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          f32x8 gv = OP::load_f32(Gt, LDC, 16 * w, 32 * kb, lane);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) gv[e] *= -et[32 * kb + slot_k(e, q)];
-          F vh, vl;
-          OP::split(gv, vh, vl);
+          const F vh = OP::load_t(Vh, M, 32 * kb, 16 * w, lane);
+          F vl = vh;
+          if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * w, lane);
 #pragma unroll
           for (int jb = 0; jb < JB; ++jb)
-            Ws[jb] = mma_split_b<OP>(Ws[jb], OP::load(Xt, LDC, 16 * jb, 32 * kb, lane), vh, vl);
+            Ws[jb] = mma_split_b<OP>(Ws[jb], OP::load_t(Xs, D, 32 * kb, 16 * jb, lane), vh, vl);
         }
+      } else {
+        // Exact products G^T X, scaled once by the scalar eta.
+        f32x4 dw[JB];
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) dw[jb] = zero4();
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F gq = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
+#pragma unroll
+          for (int jb = 0; jb < JB; ++jb) dw[jb] = OP::mma(dw[jb], OP::load_t(Xs, D, 32 * kb, 16 * jb, lane), gq);
+        }
+        const float e = a.eta_scalar;
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) Ws[jb] -= e * dw[jb];
       }
     }
+  };
+
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += 2 * C) {
+    chunk(xa, ga, ea, t0);
+    chunk(xb, gb, eb, t0 + C);
   }
 }
 
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-static int lds_bytes_fwd(int bf16, int d, int m, int C) {
+static constexpr int lds_bytes_fwd(int bf16, int d, int m, int C, int etav) {
   const int es = bf16 ? 2 : 4;
-  return es * (C * (d + 4) + d * (C + 4) + m * (C + 4) + C * (C + 4)) + 4 * C;
+  const int v = etav ? (bf16 ? 2 : 1) * C * m : 0;
+  return es * (C * d + C * m + C * C + v) + 4 * C;
 }
 
 int fwd_chunk_for(int bf16, int d, int m, int requested) {
   int C = (bf16 && requested == 128) ? 128 : 64;
-  if (C == 128 && lds_bytes_fwd(bf16, d, m, 128) > 160 * 1024) C = 64;
+  if (C == 128 && lds_bytes_fwd(bf16, d, m, 128, 0) > 160 * 1024) C = 64;
   return C;
 }
 
 int fwd_wgs_per_cu(int bf16, int d, int m, int C) {
-  int n = 160 * 1024 / lds_bytes_fwd(bf16, d, m, C);
+  int n = 160 * 1024 / lds_bytes_fwd(bf16, d, m, C, 0);
   const int waves = cmax(d, m) / 16;
-  if (n * waves > 32) n = 32 / waves;
+  if (n * waves > 8) n = 8 / waves;  // two waves per SIMD (register budget)
   return n < 1 ? 1 : n;
+}
+
+template <class OP, int D, int M, int C, bool ETAV>
+static hipError_t fwd_dispatch2(const ScanProblem& p, const KArgs& k, hipStream_t s) {
+  constexpr int NT = cmax(D, M) / 16 * 64;
+  const unsigned grid = (unsigned)seg_grid(k.BH, p.nseg);
+  if (p.nseg > 1) {
+    timing_begin(GRADLEV_K_FWD_AGG, s);
+    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggFwd, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
+    timing_end(GRADLEV_K_FWD_AGG, s);
+    timing_begin(GRADLEV_K_FWD_CARRY, s);
+    const hipError_t e = launch_carry(k.W0, k.aggA, nullptr, k.BH, k.H, p.nseg, D, M, 0, s);
+    timing_end(GRADLEV_K_FWD_CARRY, s);
+    if (e != hipSuccess) return e;
+  }
+  timing_begin(GRADLEV_K_FWD_MAIN, s);
+  if (p.inclusive)
+    hipLaunchKernelGGL((fwd_main_kernel<OP, D, M, C, true, ETAV>), dim3(grid), dim3(NT), 0, s, k);
+  else
+    hipLaunchKernelGGL((fwd_main_kernel<OP, D, M, C, false, ETAV>), dim3(grid), dim3(NT), 0, s, k);
+  timing_end(GRADLEV_K_FWD_MAIN, s);
+  return hipGetLastError();
 }
 
 template <class OP, int D, int M, int C>
 static hipError_t fwd_dispatch(const ScanProblem& p, const KArgs& k, hipStream_t s) {
-  constexpr int NT = cmax(D, M) / 16 * 64;
-  const int64_t BH = p.B * p.H;
-  if (p.nseg > 1) {
-    timing_begin(GRADLEV_K_FWD_AGG, s);
-    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, false>), dim3((unsigned)(p.nseg - 1), (unsigned)BH), dim3(NT), 0, s, k);
-    timing_end(GRADLEV_K_FWD_AGG, s);
-    timing_begin(GRADLEV_K_FWD_CARRY, s);
-    (void)launch_carry(k.aggA, nullptr, BH, p.nseg, (int64_t)D * M, 0, s);
-    timing_end(GRADLEV_K_FWD_CARRY, s);
+  constexpr int bf = OP::kSplit == 2 ? 1 : 0;
+  if (k.eta) {
+    // The per-token split operands need two more tiles of LDS; where they do
+    // not fit at this tile length the chunk drops to 64 (same segments).
+    if constexpr (lds_bytes_fwd(bf, D, M, C, 1) <= 160 * 1024) return fwd_dispatch2<OP, D, M, C, true>(p, k, s);
+    else return fwd_dispatch2<OP, D, M, 64, true>(p, k, s);
   }
-  timing_begin(GRADLEV_K_FWD_MAIN, s);
-  if (p.inclusive)
-    hipLaunchKernelGGL((fwd_main_kernel<OP, D, M, C, true>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, k);
-  else
-    hipLaunchKernelGGL((fwd_main_kernel<OP, D, M, C, false>), dim3((unsigned)p.nseg, (unsigned)BH), dim3(NT), 0, s, k);
-  timing_end(GRADLEV_K_FWD_MAIN, s);
-  return hipGetLastError();
+  return fwd_dispatch2<OP, D, M, C, false>(p, k, s);
 }
 
 template <class OP, int C>
@@ -240,6 +315,7 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& f, hipStream_t s
   k.dY = nullptr;
   k.eta = f.eta;
   k.eta_scalar = f.eta_scalar;
+  k.BH = p.B * p.H;
   k.H = p.H;
   k.T = p.T;
   k.seg_len = p.seg_len;

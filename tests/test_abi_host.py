@@ -68,7 +68,7 @@ def plan_rc(s):
     (dict(d_in=0), gl.ERR_INVALID), (dict(dtype=7), gl.ERR_INVALID), (dict(prefix=3), gl.ERR_INVALID),
     (dict(chunk=-64), gl.ERR_INVALID), (dict(d_in=96), gl.ERR_UNSUPPORTED),
     (dict(d_out=256), gl.ERR_UNSUPPORTED), (dict(chunk=32), gl.ERR_UNSUPPORTED),
-    (dict(segment=100), gl.ERR_UNSUPPORTED),
+    (dict(segment=100), gl.ERR_UNSUPPORTED), (dict(T=1025, segment=64), gl.ERR_UNSUPPORTED),
 ])
 def test_plan_rejects(L, bad, code):
     rc, _ = plan_rc(shape(**bad))
@@ -78,7 +78,8 @@ def test_plan_rejects(L, bad, code):
 @pytest.mark.parametrize("kw", [dict(), dict(dtype=gl.F32), dict(d_in=128, d_out=128),
                                 dict(d_in=64, d_out=128), dict(d_in=128, d_out=64, dtype=gl.F32),
                                 dict(T=1), dict(T=16384, B=2, H=16, d_in=128, d_out=128, chunk=128),
-                                dict(segment=64), dict(prefix="inclusive")])
+                                dict(segment=64), dict(prefix="inclusive"), dict(T=1024, segment=64),
+                                dict(B=1, H=1, T=1 << 20), dict(B=1, H=1, T=1 << 20, segment=1 << 16)])
 def test_plan_is_consistent(L, kw):
     s = shape(**kw)
     rc, p = plan_rc(s)
@@ -90,13 +91,15 @@ def test_plan_is_consistent(L, kw):
     assert gl.workspace_bytes(s) == p.workspace_bytes
     if kw.get("segment"):
         assert p.fwd_segment == max(kw["segment"], p.fwd_chunk)
+    assert p.fwd_nseg <= 16 and p.bwd_nseg <= 16
 
 
 def test_workspace_covers_aggregates(L):
     s = shape(B=8, H=16, T=2048)
     p = gl.plan(s)
     md = 64 * 64 * 4
-    assert p.workspace_bytes >= 8 * 16 * max(p.fwd_nseg, 2 * p.bwd_nseg + 1) * md
+    bwd = (2 * p.bwd_nseg if p.bwd_nseg > 1 else 1) + 1
+    assert p.workspace_bytes >= 8 * 16 * max(p.fwd_nseg, bwd) * md
 
 
 def fwd_call(s, W0=FAKE, X=FAKE, G=FAKE, eta=None, Y=FAKE, ws=FAKE, wsn=1 << 40):

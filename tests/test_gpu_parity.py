@@ -107,6 +107,19 @@ def test_chunk_hint_and_segments_change_rounding_only(dtype):
             check(f"{k}", out[k], ref[k], dtype)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sixteen_segments(dtype):
+    """The largest carry: 16 segments of 64 tokens, the last one ragged."""
+    log(f"16 segments dtype={dtype}")
+    inp = small_inputs(1, 2, 1000, 64, 64, dtype, seed=21, eta_kind="token")
+    assert gl.plan(gl.make_shape(B=1, H=2, T=1000, d_in=64, d_out=64, dtype=gl.BF16 if dtype == "bf16" else gl.F32,
+                                 prefix="inclusive", segment=64)).bwd_nseg == 16
+    out = run_gpu(inp, dtype, "inclusive", segment=64)
+    ref = oracle_all(inp, "inclusive")
+    for k in KEYS:
+        check(k, out[k], ref[k], dtype)
+
+
 def test_eta_zero_reads_slow_weights():
     log("eta = 0")
     inp = small_inputs(2, 2, 150, 64, 64, "bf16", seed=9, eta_kind="scalar")
