@@ -164,13 +164,16 @@ int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                         const float* eta, float eta_scalar, float* y,
                         void* stream);
 
-/* Kernel timing for benchmarks and tracing.  While enabled, every kernel the
- * library launches is bracketed by HIP events recorded on the caller's stream
- * (events are created by the library on first use and reused; no device
- * memory is allocated).  gradlev_timing_read waits for the recorded events and
- * returns, for one kernel family, the summed duration in milliseconds and the
- * number of launches since the last reset.  Not thread-safe: use from one host
- * thread.  At most 65536 launches per family are kept between resets.
+/* Kernel timing for benchmarks and tracing.  While a family's bit is set in
+ * the mask given to gradlev_timing_enable (bit f = family f; 0 turns timing
+ * off), every launch of that family is bracketed by HIP events recorded on the
+ * caller's stream (events are created by the library on first use and reused;
+ * no device memory is allocated).  Recording works under stream capture: the
+ * events become nodes of the captured graph and are read after it has run.
+ * gradlev_timing_read waits for the recorded events and returns, for one
+ * family, the summed duration in milliseconds and the number of launches
+ * since the last reset.  Not thread-safe: use from one host thread.  At most
+ * 65536 launches per family are kept between resets.
  * Families: */
 enum {
   GRADLEV_K_FWD_AGG = 0,   /* per-segment write aggregates (forward)      */
@@ -183,7 +186,7 @@ enum {
   GRADLEV_K_DECODE = 7,    /* deployment step                              */
   GRADLEV_K_COUNT = 8
 };
-int gradlev_timing_enable(int on);   /* returns the previous setting */
+int gradlev_timing_enable(int mask); /* returns the previous mask */
 int gradlev_timing_reset(void);
 int gradlev_timing_read(int family, double* ms, int64_t* launches);
 

@@ -263,9 +263,19 @@ def decode_step(W, x, g, eta=0.1, *, out=None):
 KERNELS = ("fwd_agg", "fwd_carry", "fwd_main", "bwd_agg", "bwd_carry", "bwd_main", "bwd_dw0", "decode")
 
 
-def timing_enable(on: bool = True) -> bool:
-    """Turn per-launch event timing on or off; returns the previous setting."""
-    return bool(lib().gradlev_timing_enable(1 if on else 0))
+def timing_enable(on: bool = True, kernels=None) -> int:
+    """Turn per-launch event timing on (for ``kernels``, default all families) or off.
+
+    Returns the previous family mask."""
+    if not on:
+        mask = 0
+    elif kernels is None:
+        mask = (1 << len(KERNELS)) - 1
+    else:
+        mask = 0
+        for k in kernels:
+            mask |= 1 << KERNELS.index(k)
+    return int(lib().gradlev_timing_enable(mask))
 
 
 def timing_reset() -> None:

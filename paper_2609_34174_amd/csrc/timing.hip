@@ -17,7 +17,7 @@ struct Family {
   int64_t launches = 0;
 };
 
-bool g_enabled = false;
+unsigned g_mask = 0;  // bit f: family f is timed
 Family g_fam[GRADLEV_K_COUNT];
 
 void fold(Family& f) {
@@ -35,7 +35,7 @@ void fold(Family& f) {
 }  // namespace
 
 void timing_begin(int family, hipStream_t s) {
-  if (!g_enabled || family < 0 || family >= GRADLEV_K_COUNT) return;
+  if (family < 0 || family >= GRADLEV_K_COUNT || !(g_mask & (1u << family))) return;
   Family& f = g_fam[family];
   if (f.used == kMaxPairs) fold(f);
   if (f.used == f.start.size()) {
@@ -52,7 +52,7 @@ void timing_begin(int family, hipStream_t s) {
 }
 
 void timing_end(int family, hipStream_t s) {
-  if (!g_enabled || family < 0 || family >= GRADLEV_K_COUNT) return;
+  if (family < 0 || family >= GRADLEV_K_COUNT || !(g_mask & (1u << family))) return;
   Family& f = g_fam[family];
   if (!f.open) return;
   f.open = false;
@@ -65,9 +65,9 @@ using namespace gradlev;
 
 extern "C" {
 
-int gradlev_timing_enable(int on) {
-  const int prev = g_enabled ? 1 : 0;
-  g_enabled = on != 0;
+int gradlev_timing_enable(int mask) {
+  const int prev = (int)g_mask;
+  g_mask = (unsigned)mask & ((1u << GRADLEV_K_COUNT) - 1u);
   return prev;
 }
 
