@@ -177,14 +177,12 @@ int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
  * Families: */
 enum {
   GRADLEV_K_FWD_AGG = 0,   /* per-segment write aggregates (forward)      */
-  GRADLEV_K_FWD_CARRY = 1, /* cross-segment prefix (forward)              */
-  GRADLEV_K_FWD_MAIN = 2,  /* chunked forward scan                         */
-  GRADLEV_K_BWD_AGG = 3,   /* per-segment aggregates (backward)           */
-  GRADLEV_K_BWD_CARRY = 4, /* cross-segment prefix/suffix (backward)      */
-  GRADLEV_K_BWD_MAIN = 5,  /* chunked backward scan                        */
-  GRADLEV_K_BWD_DW0 = 6,   /* batch reduction of dW0                       */
-  GRADLEV_K_DECODE = 7,    /* deployment step                              */
-  GRADLEV_K_COUNT = 8
+  GRADLEV_K_FWD_MAIN = 1,  /* chunked forward scan                         */
+  GRADLEV_K_BWD_AGG = 2,   /* per-segment aggregates (backward)           */
+  GRADLEV_K_BWD_MAIN = 3,  /* chunked backward scan                        */
+  GRADLEV_K_BWD_DW0 = 4,   /* batch reduction of dW0                       */
+  GRADLEV_K_DECODE = 5,    /* deployment step                              */
+  GRADLEV_K_COUNT = 6
 };
 int gradlev_timing_enable(int mask); /* returns the previous mask */
 int gradlev_timing_reset(void);

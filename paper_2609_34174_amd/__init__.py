@@ -260,7 +260,7 @@ def decode_step(W, x, g, eta=0.1, *, out=None):
 # Kernel timing (HIP events recorded by the library around each launch)
 # ---------------------------------------------------------------------------
 
-KERNELS = ("fwd_agg", "fwd_carry", "fwd_main", "bwd_agg", "bwd_carry", "bwd_main", "bwd_dw0", "decode")
+KERNELS = ("fwd_agg", "fwd_main", "bwd_agg", "bwd_main", "bwd_dw0", "decode")
 
 
 def timing_enable(on: bool = True, kernels=None) -> int:

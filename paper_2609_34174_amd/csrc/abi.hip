@@ -35,7 +35,7 @@ int64_t pick_nseg(int64_t BH, int64_t T, int C, int wgs_per_cu, int64_t hint) {
     int64_t nseg = (target + BH - 1) / BH;
     if (nseg < 1) nseg = 1;
     if (nseg > nchunks) nseg = nchunks;
-    if (nseg > 16) nseg = 16;  // the carry kernel joins at most 16 segments
+    if (nseg > 16) nseg = 16;  // a main workgroup sums at most 15 predecessor aggregates
     seg_chunks = (nchunks + nseg - 1) / nseg;
   }
   if (seg_chunks < 1) seg_chunks = 1;

@@ -39,8 +39,8 @@ struct BwdPtrs {
   float* dG;
   float* deta;
   float* dW0;
-  float* aggA;   // [B*H][nseg][d][m]: segment write aggregates -> segment end states (transposed)
-  float* aggB;   // [B*H][nseg][d][m]: segment dY x^T aggregates -> suffixes (transposed)
+  float* aggA;   // [B*H][nseg][d][m]: segment write aggregates (transposed)
+  float* aggB;   // [B*H][nseg][d][m]: segment dY x^T aggregates (transposed)
   float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
 };
 

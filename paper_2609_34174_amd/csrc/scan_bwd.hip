@@ -17,7 +17,7 @@
 //   R_{n-1}= R_n + dY^T X
 // A workgroup walks its segment's chunks from last to first, carrying R in
 // reverse time and un-writing W from the state at the segment's end (both
-// provided by the aggregate and carry kernels).  Waves own column blocks of
+// summed in its prologue from the aggregate pass).  Waves own column blocks of
 // W and R in registers; R is also published each chunk to LDS (transposed,
 // split into bf16 hi + lo) for the products contracted over d, so no second
 // register copy is needed.
@@ -37,8 +37,8 @@ struct BArgs {
   float* dX;
   float* dG;
   float* deta;
-  const float* wend;  // [BH][nseg][d][m]: W at each segment's end, transposed
-  const float* rend;  // [BH][nseg][d][m]: R at each segment's end, transposed, or null (nseg == 1)
+  const float* aggA;  // [BH][nseg][d][m]: per-segment write aggregates A_k, transposed
+  const float* aggB;  // [BH][nseg][d][m]: per-segment dY x^T aggregates B_k (k >= 1), or null
   float* rfin;        // [BH][m][d]: full-sequence dY x^T (written by segment 0), or null
 };
 
@@ -46,6 +46,18 @@ struct BArgs {
 // branch: kOutFull computes every backward term (stores are skipped for NULL
 // outputs); kOutRead computes only the read-side gtilde.
 enum OutMode { kOutFull = 0, kOutRead = 1 };
+
+// LDS bytes of the main backward kernel (without the shared score tiles) and
+// whether the split score tiles fit beside it.
+static constexpr int lds_bytes_bwd(int bf16, int d, int m, int C, int etav) {
+  const int es = bf16 ? 2 : 4;
+  const int v = etav ? (bf16 ? 2 : 1) * C * m : 0;
+  const int r = (bf16 ? 2 : 1) * d * m;
+  return es * (C * d + 2 * C * m + C * C + v + r) + 4 * C + 4 * (m / 16) * C;
+}
+static constexpr bool s_shared_fits(bool bf16, int d, int m, int C, bool etav) {
+  return lds_bytes_bwd(bf16, d, m, C, etav) + (bf16 ? 2 : 1) * C * C * (bf16 ? 2 : 4) <= 160 * 1024;
+}
 
 template <class OP, int D, int M, int C, bool INCL, bool ETAV, int OUT>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64, 128 / cmax(D, M))
@@ -64,6 +76,11 @@ bwd_main_kernel(const BArgs a) {
   __shared__ E Vl[SPLITV ? C * M : 1];     // (eta G)[t][i] lo
   __shared__ E Rh[FULL ? D * M : 1];       // R^T[j][i] hi
   __shared__ E Rl[FULL && OP::kSplit == 2 ? D * M : 1];  // R^T[j][i] lo
+  // Intra-chunk scores S[t][s] = x_t . x_s (masked), split hi + lo, built once
+  // per chunk and shared by the waves (when they fit the LDS budget).
+  constexpr bool SSH = FULL && s_shared_fits(OP::kSplit == 2, D, M, C, ETAV);
+  __shared__ E Sh[SSH ? C * C : 1];
+  __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
   __shared__ float et[C];
   __shared__ float dpart[IB][C];
 
@@ -105,18 +122,54 @@ bwd_main_kernel(const BArgs a) {
   fetch(xa, ga, da, ea, nch - 1);
   if (DEPTH == 2) fetch(xb, gb, db, eb, nch - 2);
 
-  // Column-block state (wave w < JB): Wj[ib], Rj[ib] hold W/R[i = 16ib + 4q + r][j = 16w + c],
-  // i.e. row j of the transposed [d][m] layout the carry kernel leaves.
+  // Column-block state (wave w < JB): Wj[ib], Rj[ib] hold W/R[i = 16ib + 4q + r][j = 16w + c]
+  // at the segment's end: W_0 - sum_{j<=seg} A_j (subtracted in segment order)
+  // and R = sum_{j>seg} B_j (added from the last segment down).
   f32x4 Wj[IB], Rj[IB];
   if (w < JB) {
-    const int64_t o = (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * M;
+    const float* w0 = a.W0 + (bh % a.H) * M * D;
 #pragma unroll
-    for (int ib = 0; ib < IB; ++ib) {
-      Wj[ib] = *reinterpret_cast<const f32x4*>(a.wend + o + 16 * ib + 4 * q);
-      Rj[ib] = (FULL && a.rend) ? *reinterpret_cast<const f32x4*>(a.rend + o + 16 * ib + 4 * q) : zero4();
+    for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) Wj[ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c];
+    const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
+    for (int64_t j0 = 0; j0 <= seg; j0 += 4) {
+      f32x4 v[4][IB];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          v[u][ib] = j0 + u <= seg ? *reinterpret_cast<const f32x4*>(a.aggA + o + (j0 + u) * M * D + 16 * ib) : zero4();
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          if (j0 + u <= seg) Wj[ib] -= v[u][ib];
+    }
+#pragma unroll
+    for (int ib = 0; ib < IB; ++ib) Rj[ib] = zero4();
+    if (FULL && a.aggB) {
+      for (int64_t j0 = a.nseg - 1; j0 > seg; j0 -= 4) {
+        f32x4 v[4][IB];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib)
+            v[u][ib] = j0 - u > seg ? *reinterpret_cast<const f32x4*>(a.aggB + o + (j0 - u) * M * D + 16 * ib) : zero4();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib)
+            if (j0 - u > seg) Rj[ib] += v[u][ib];
+      }
     }
   }
   for (int i = tid; i < C * C; i += NT) Es[i] = (E)0.f;
+  if constexpr (SSH) {
+    for (int i = tid; i < C * C; i += NT) Sh[i] = (E)0.f;
+    if constexpr (OP::kSplit == 2)
+      for (int i = tid; i < C * C; i += NT) Sl[i] = (E)0.f;
+  }
 
   auto chunk = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
     // A step before the segment start (the second of a pair) sees zero
@@ -155,6 +208,28 @@ bwd_main_kernel(const BArgs a) {
       }
       OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
     }
+    if constexpr (SSH) {
+      // Score tiles st[r] = x_s . x_t for the same (s, t) pairs, masked alike.
+#pragma unroll
+      for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+        if ((idx + NW / 2) % NW != w) continue;
+        int tb = 0;
+        while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+        const int sb = idx - tb * (tb + 1) / 2;
+        f32x4 st = zero4();
+#pragma unroll
+        for (int kb = 0; kb < D / 32; ++kb)
+          st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+        const int t = 16 * tb + c;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * sb + 4 * q + r;
+          if (!(tb > sb || (INCL ? (t >= s) : (t > s)))) st[r] = 0.f;
+        }
+        const int o = lds_off(t, 16 * sb + 4 * q, C);
+        OP::store4_split(Sh + o, Sl + o, st);
+      }
+    }
     if (FULL && w < JB) {
 #pragma unroll
       for (int ib = 0; ib < IB; ++ib) {
@@ -164,12 +239,20 @@ bwd_main_kernel(const BArgs a) {
     }
     __syncthreads();
 
+    // X^T rows j of this wave's column block over the chunk's tokens: shared
+    // by the un-write, both intra-chunk terms and the suffix update.
+    F xt[C / 32];
+    if (w < JB) {
+#pragma unroll
+      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+    }
+
     // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
     if (w < JB) {
       if constexpr (ETAV) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+          const F xq = xt[kb];
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
             const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, lane);
@@ -184,9 +267,8 @@ bwd_main_kernel(const BArgs a) {
         for (int ib = 0; ib < IB; ++ib) dw[ib] = zero4();
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, lane), xq);
+          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, lane), xt[kb]);
         }
         const float e = a.eta_scalar;
 #pragma unroll
@@ -204,7 +286,7 @@ bwd_main_kernel(const BArgs a) {
       for (int kb = 0; kb < M / 32; ++kb) {
         F wh, wl;
         OP::split(cat(Wj[2 * kb], Wj[2 * kb + 1]), wh, wl);
-        F rh, rl;
+        F rh, rl;  // this wave's own R^T rows, as published (split) in step (1)
         if (FULL) {
           rh = OP::load_n(Rh, M, 16 * w, 32 * kb, lane);
           rl = rh;
@@ -223,7 +305,7 @@ bwd_main_kernel(const BArgs a) {
       // Intra-chunk terms: gtilde -= sum_{s<t} X[s][j] E[t][s];  dXw += sum_{t>s} X[t][j] E[t][s]
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
-        const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+        const F xq = xt[kb];
         const F xn = OP::neg(xq);
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
@@ -246,6 +328,21 @@ bwd_main_kernel(const BArgs a) {
         f32x4 ua[TB];
 #pragma unroll
         for (int sb = 0; sb < TB; ++sb) ua[sb] = zero4();
+        // Row fragments of X (rows t over j) serve both the R term and, when
+        // the scores are not shared, the intra-chunk scores; they are then read
+        // once when they fit the register budget (32 VGPRs), else per use.
+        constexpr bool XCACHE = !SSH && TB * (D / 32) * (int)(sizeof(F) / 4) <= 32;
+        F xr[XCACHE ? TB : 1][XCACHE ? D / 32 : 1];
+        if constexpr (XCACHE) {
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+            for (int kb = 0; kb < D / 32; ++kb) xr[tb][kb] = OP::load_n(Xs, D, 16 * tb, 32 * kb, lane);
+        }
+        auto xrow = [&](int tb, int kb) -> F {
+          if constexpr (XCACHE) return xr[tb][kb];
+          else return OP::load_n(Xs, D, 16 * tb, 32 * kb, lane);
+        };
         // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb) {
@@ -253,9 +350,23 @@ bwd_main_kernel(const BArgs a) {
           F rl = rh;
           if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * w, lane);
 #pragma unroll
-          for (int sb = 0; sb < TB; ++sb)
-            ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane));
+          for (int sb = 0; sb < TB; ++sb) ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, xrow(sb, kb));
         }
+        if constexpr (SSH) {
+          // Intra-chunk term from the shared split scores: the operand for
+          // row s over k = t is a transposing read of the [t][s] tile.
+#pragma unroll
+          for (int kb = 0; kb < C / 32; ++kb) {
+            const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
+#pragma unroll
+            for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+              const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, lane);
+              F sl = sh;
+              if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, lane);
+              ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
+            }
+          }
+        } else {
         // Intra-chunk term with S[t][s] = x_t . x_s computed here, per pair of
         // t blocks, and kept in fp32 registers (split for the matrix core):
         // the tile (rows t, cols s) is directly the operand contracted over t.
@@ -271,8 +382,7 @@ bwd_main_kernel(const BArgs a) {
               f32x4 st = zero4();
               if (tb >= sb) {
 #pragma unroll
-                for (int kj = 0; kj < D / 32; ++kj)
-                  st = OP::mma(st, OP::load_n(Xs, D, 16 * tb, 32 * kj, lane), OP::load_n(Xs, D, 16 * sb, 32 * kj, lane));
+                for (int kj = 0; kj < D / 32; ++kj) st = OP::mma(st, xrow(tb, kj), xrow(sb, kj));
                 if (tb == sb) {
 #pragma unroll
                   for (int r = 0; r < 4; ++r) {
@@ -288,6 +398,7 @@ bwd_main_kernel(const BArgs a) {
             OP::split(sv, sh, sl);
             ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
           }
+        }
         }
 #pragma unroll
         for (int sb = 0; sb < TB; ++sb) {
@@ -312,9 +423,8 @@ bwd_main_kernel(const BArgs a) {
       if (w < JB) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F xq = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, lane), xq);
+          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, lane), xt[kb]);
         }
       }
       if (a.deta) {
@@ -361,13 +471,6 @@ reduce_dw0_kernel(const float* rfin, float* dW0, int64_t B, int64_t H, int64_t m
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-static constexpr int lds_bytes_bwd(int bf16, int d, int m, int C, int etav) {
-  const int es = bf16 ? 2 : 4;
-  const int v = etav ? (bf16 ? 2 : 1) * C * m : 0;
-  const int r = (bf16 ? 2 : 1) * d * m;
-  return es * (C * d + 2 * C * m + C * C + v + r) + 4 * C + 4 * (m / 16) * C;
-}
-
 // Tile length of the backward (the same for both eta forms).  bf16 tiles use
 // 64 for every map; fp32 tiles take twice the LDS and registers and use 64
 // only for the 64 x 64 map.  launch_scan_bwd dispatches on exactly this value.
@@ -380,7 +483,8 @@ static_assert(lds_bytes_bwd(0, 64, 64, 64, 1) <= 160 * 1024, "fp32 backward tile
 static_assert(lds_bytes_bwd(0, 128, 128, 32, 1) <= 160 * 1024, "fp32 backward tile does not fit LDS");
 
 int bwd_wgs_per_cu(int bf16, int d, int m, int C) {
-  int n = 160 * 1024 / lds_bytes_bwd(bf16, d, m, C, 0);
+  const int s = s_shared_fits(bf16, d, m, C, false) ? (bf16 ? 2 : 1) * C * C * (bf16 ? 2 : 4) : 0;
+  int n = 160 * 1024 / (lds_bytes_bwd(bf16, d, m, C, 0) + s);
   const int waves = cmax(d, m) / 16;
   if (n * waves > 8) n = 8 / waves;  // two waves per SIMD (register budget)
   return n < 1 ? 1 : n;
@@ -409,18 +513,14 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   k.nseg = p.nseg;
   k.aggA = f.aggA;
   k.aggB = f.aggB;
-  // Segment aggregates (writes, and dY x^T when a suffix is needed), then the
-  // carry that turns them into every segment's end state.
+  // Segment aggregates (writes, and dY x^T when a suffix is needed); each
+  // workgroup of the main kernel sums the ones it needs in its prologue.
   timing_begin(GRADLEV_K_BWD_AGG, s);
   if (need_sfx)
     hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdAB, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
   else
     hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdA, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
   timing_end(GRADLEV_K_BWD_AGG, s);
-  timing_begin(GRADLEV_K_BWD_CARRY, s);
-  hipError_t e = launch_carry(f.W0, f.aggA, need_sfx ? f.aggB : nullptr, BH, p.H, p.nseg, D, M, 1, s);
-  timing_end(GRADLEV_K_BWD_CARRY, s);
-  if (e != hipSuccess) return e;
 
   BArgs b{};
   b.W0 = f.W0;
@@ -438,8 +538,8 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   b.dX = f.dX;
   b.dG = f.dG;
   b.deta = f.deta;
-  b.wend = f.aggA;
-  b.rend = need_sfx ? f.aggB : nullptr;
+  b.aggA = f.aggA;
+  b.aggB = need_sfx ? f.aggB : nullptr;
   b.rfin = f.dW0 ? f.rfin : nullptr;
   timing_begin(GRADLEV_K_BWD_MAIN, s);
   if (read_only) {

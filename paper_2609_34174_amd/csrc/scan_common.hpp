@@ -1,6 +1,6 @@
 // Pieces shared by the forward and backward scan kernels: kernel arguments,
-// the block -> (sequence, segment) map, chunk-tile staging, the
-// segment-aggregate kernel and the cross-segment carry.
+// the block -> (sequence, segment) map, chunk-tile staging and the
+// segment-aggregate kernel.
 #pragma once
 
 #include "../../include/gradlev.h"
@@ -18,8 +18,8 @@ struct KArgs {
   float eta_scalar;
   int64_t BH, H, T, seg_len, nseg;
   float* out0;   // fwd: Y
-  float* aggA;   // [BH][nseg][m*d] write aggregates (fwd: [m][d]; bwd: transposed [d][m])
-  float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates
+  float* aggA;   // [BH][nseg][m*d] write aggregates A_k (fwd: [m][d]; bwd: transposed [d][m])
+  float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates B_k (k >= 1)
 };
 
 // ---------------------------------------------------------------------------
@@ -248,13 +248,5 @@ agg_kernel(const KArgs a, int64_t nagg) {
     }
   }
 }
-
-// Carry across segments (scan_fwd.hip), per sequence and element, in a fixed
-// summation order, with W0 folded in:
-//   mode 0 (forward):  A[k] <- W0 - sum_{j<k} A[j]            ([m][d])
-//   mode 1 (backward): A[k] <- W0^T - sum_{j<=k} A[j]         ([d][m])
-//                      B[k] <- sum_{j>k} B[j] if B != null    ([d][m]; B[0] unread)
-hipError_t launch_carry(const float* W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d,
-                        int m, int mode, hipStream_t s);
 
 }  // namespace gradlev

@@ -13,78 +13,14 @@
 //       Y   = X W_n^T + S G                (state read + intra-chunk reads)
 //       W  <- W_n - (eta G)^T X            (carry to the next chunk)
 //   * segments are joined by their aggregated writes A_k = sum eta g x^T
-//     (agg_kernel) and the carry kernel, which leaves W_0 - sum_{j<k} A_j for
-//     every segment k; a workgroup loads its start state once.
+//     (agg_kernel, one pass before the main kernel); a workgroup starts from
+//     W_0 - sum_{j<k} A_j, summed in its prologue.
 // Chunk inputs are staged through registers two chunks ahead of the compute
 // (about 3 us of loaded HBM latency has to be covered) into row-major LDS
 // tiles; operands with k along the tile rows use the transposing LDS read.
 #include "scan_common.hpp"
 
 namespace gradlev {
-
-// ---------------------------------------------------------------------------
-// Cross-segment carry.  One thread per (sequence, 4 elements); every segment
-// value is loaded before any is summed, so the whole carry costs one memory
-// latency.  Summation order is fixed (segment 0 first).
-// ---------------------------------------------------------------------------
-constexpr int kMaxSeg = 16;
-
-static __global__ void __launch_bounds__(256)
-carry_kernel(const float* __restrict__ W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d, int m,
-             int mode) {
-  const int64_t md4 = (int64_t)d * m / 4;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= BH * md4) return;
-  const int64_t bh = gid / md4, e4 = gid % md4, h = bh % H;
-  f32x4* pa = reinterpret_cast<f32x4*>(A) + bh * nseg * md4 + e4;
-  f32x4 w0;
-  if (mode == 0) {
-    w0 = reinterpret_cast<const f32x4*>(W0 + h * m * d)[e4];
-  } else {
-    // element 4*e4 + r of the transposed [d][m] layout is W0[i][j], j = e / m, i = e % m
-    const int64_t e = 4 * e4, j = e / m, i = e % m;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) w0[r] = W0[h * m * d + (i + r) * d + j];
-  }
-  f32x4 v[kMaxSeg];
-#pragma unroll
-  for (int k = 0; k < kMaxSeg; ++k)
-    if (k < nseg && (mode == 1 || k + 1 < nseg)) v[k] = pa[k * md4];
-  f32x4 run = w0;
-#pragma unroll
-  for (int k = 0; k < kMaxSeg; ++k) {
-    if (k >= nseg) break;
-    if (mode == 0) {
-      pa[k * md4] = run;
-      if (k + 1 < nseg) run -= v[k];
-    } else {
-      run -= v[k];
-      pa[k * md4] = run;
-    }
-  }
-  if (mode == 1 && B) {
-    f32x4* pb = reinterpret_cast<f32x4*>(B) + bh * nseg * md4 + e4;
-#pragma unroll
-    for (int k = 1; k < kMaxSeg; ++k)
-      if (k < nseg) v[k] = pb[k * md4];
-    f32x4 acc = zero4();
-#pragma unroll
-    for (int k = kMaxSeg - 1; k >= 0; --k) {
-      if (k >= nseg) continue;
-      pb[k * md4] = acc;
-      if (k >= 1) acc += v[k];
-    }
-  }
-}
-
-hipError_t launch_carry(const float* W0, float* A, float* B, int64_t BH, int64_t H, int64_t nseg, int d, int m,
-                        int mode, hipStream_t s) {
-  if (nseg > kMaxSeg) return hipErrorInvalidValue;
-  const int64_t n = BH * (int64_t)d * m / 4;
-  hipLaunchKernelGGL(carry_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W0, A, B, BH, H, nseg, d, m,
-                     mode);
-  return hipGetLastError();
-}
 
 // ---------------------------------------------------------------------------
 // Main forward kernel.  NW = max(d, m)/16 waves.  Wave w < m/16 owns output
@@ -134,12 +70,27 @@ fwd_main_kernel(const KArgs a) {
   fetch(xb, gb, eb, t_begin + C);
 
   // State tiles: Ws[jb] holds W[i = 16w + c][j = 16jb + 4q + r] = W^T tile (rows j, cols i).
+  // The segment starts from W_0 - sum_{j<seg} A_j (the aggregate pass's sums),
+  // subtracted in segment order, four segments' loads in flight at a time.
   f32x4 Ws[JB];
   if (w < IB) {
-    const float* w0 = a.aggA ? a.aggA + (bh * a.nseg + seg) * M * D : a.W0 + h * M * D;
+    const int64_t o = (int64_t)(16 * w + c) * D + 4 * q;
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb)
-      Ws[jb] = *reinterpret_cast<const f32x4*>(w0 + (int64_t)(16 * w + c) * D + 16 * jb + 4 * q);
+    for (int jb = 0; jb < JB; ++jb) Ws[jb] = *reinterpret_cast<const f32x4*>(a.W0 + h * M * D + o + 16 * jb);
+    const float* ag = a.aggA + bh * a.nseg * M * D + o;
+    for (int64_t j0 = 0; j0 < seg; j0 += 4) {
+      f32x4 v[4][JB];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb)
+          v[u][jb] = j0 + u < seg ? *reinterpret_cast<const f32x4*>(ag + (j0 + u) * M * D + 16 * jb) : zero4();
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb)
+          if (j0 + u < seg) Ws[jb] -= v[u][jb];
+    }
   }
   for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
 
@@ -272,10 +223,6 @@ static hipError_t fwd_dispatch2(const ScanProblem& p, const KArgs& k, hipStream_
     timing_begin(GRADLEV_K_FWD_AGG, s);
     hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggFwd, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
     timing_end(GRADLEV_K_FWD_AGG, s);
-    timing_begin(GRADLEV_K_FWD_CARRY, s);
-    const hipError_t e = launch_carry(k.W0, k.aggA, nullptr, k.BH, k.H, p.nseg, D, M, 0, s);
-    timing_end(GRADLEV_K_FWD_CARRY, s);
-    if (e != hipSuccess) return e;
   }
   timing_begin(GRADLEV_K_FWD_MAIN, s);
   if (p.inclusive)
