@@ -7,9 +7,10 @@
 // The step is a pure stream over the fp32 state (0.5 flop per byte), so the
 // kernel is shaped for HBM: one workgroup per state matrix, each thread
 // owning one 16-byte column group of D/4 lanes' rows, consecutive lanes on
-// consecutive 16-byte words (fully coalesced loads and stores), the row dot
-// products reduced across the D/4 lanes that share a row, and the update
-// written back from the same registers (each byte read once, written once).
+// consecutive 16-byte words (fully coalesced loads and stores), four row
+// passes' loads in flight at once, the row dot products reduced across the
+// D/4 lanes that share a row, and the update written back from the same
+// registers (each byte read once, written once).
 #include "../../include/gradlev.h"
 #include "device_common.hpp"
 #include "internal.hpp"
@@ -22,23 +23,35 @@ decode_kernel(float* __restrict__ W, const float* __restrict__ x, const float* _
               const float* __restrict__ eta, float eta_scalar, float* __restrict__ y, int M) {
   constexpr int LPR = D / 4;          // lanes per row (each holds 4 columns)
   constexpr int RPI = 256 / LPR;      // rows per pass of the workgroup
+  constexpr int U = 4;                // passes whose loads are in flight together
   const int64_t sh = blockIdx.x;
   const int tid = threadIdx.x;
   const int col = 4 * (tid % LPR), row0 = tid / LPR;
-  float* Ws = W + sh * (int64_t)M * D;
+  // The state of one (sequence, head) as a buffer: rows past M read zero and
+  // their stores are dropped, so the passes need no branches.
+  const rsrc_t Ws = make_rsrc(W + sh * (int64_t)M * D, (uint32_t)(M * D * 4));
+  const rsrc_t Gs = make_rsrc(g + sh * (int64_t)M, (uint32_t)(M * 4));
+  const rsrc_t Ys = make_rsrc(y + sh * (int64_t)M, (uint32_t)(M * 4));
   const f32x4 xv = *reinterpret_cast<const f32x4*>(x + sh * D + col);
   const float e = eta ? eta[sh] : eta_scalar;
-  const float* gs = g + sh * (int64_t)M;
-  float* ys = y + sh * (int64_t)M;
-  for (int i = row0; i < M; i += RPI) {
-    f32x4* p = reinterpret_cast<f32x4*>(Ws + (int64_t)i * D + col);
-    f32x4 wv = *p;
-    float s = wv[0] * xv[0] + wv[1] * xv[1] + wv[2] * xv[2] + wv[3] * xv[3];
+  for (int i0 = row0; i0 < M; i0 += U * RPI) {
+    f32x4 wv[U];
+    float gv[U];
 #pragma unroll
-    for (int o = LPR / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, LPR);
-    if (tid % LPR == 0) ys[i] = s;
-    const float eg = e * gs[i];
-    *p = wv - eg * xv;
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u * RPI;
+      wv[u] = buf_load4(Ws, (uint32_t)((i * D + col) * 4), (const float*)nullptr);
+      gv[u] = buf_load1(Gs, (uint32_t)(i * 4));
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u * RPI;
+      float s = wv[u][0] * xv[0] + wv[u][1] * xv[1] + wv[u][2] * xv[2] + wv[u][3] * xv[3];
+#pragma unroll
+      for (int o = LPR / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, LPR);
+      buf_store1<kStoreDefault>(Ys, tid % LPR == 0 ? (uint32_t)(i * 4) : kOOB, s);
+      buf_store4<kStoreDefault>(Ws, (uint32_t)((i * D + col) * 4), wv[u] - (e * gv[u]) * xv);
+    }
   }
 }
 

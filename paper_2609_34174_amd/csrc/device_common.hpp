@@ -211,16 +211,21 @@ __device__ __forceinline__ f32x4 buf_load4(rsrc_t r, uint32_t off, const float*)
 __device__ __forceinline__ float buf_load1(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
 }
-// Output streams are written once and read by later kernels only, so they
-// are stored non-temporal at device scope (cache-policy bits SC1 | NT): the
-// lines do not stay dirty in the XCD's L2, which otherwise has to be written
-// back before the next kernel starts (about 15% of a scan step when measured).
+// Store cache policies.  Scan outputs are written once and read by later
+// kernels only, so they are stored non-temporal at device scope (cache-policy
+// bits SC1 | NT): the lines do not stay dirty in the XCD's L2, which otherwise
+// has to be written back before the next kernel starts (about 15% of a scan
+// step when measured).  The decode state is read again by the next step and
+// keeps the default policy (measured: streaming stores cost it 15%).
 constexpr int kStoreStream = 16 | 2;
+constexpr int kStoreDefault = 0;
+template <int POLICY = kStoreStream>
 __device__ __forceinline__ void buf_store4(rsrc_t r, uint32_t off, f32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, (int)off, 0, kStoreStream);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), r, (int)off, 0, POLICY);
 }
+template <int POLICY = kStoreStream>
 __device__ __forceinline__ void buf_store1(rsrc_t r, uint32_t off, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, kStoreStream);
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, POLICY);
 }
 
 }  // namespace gradlev
