@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes 5 times (for scaling "
                          "rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes) and exit")
+    ap.add_argument("--ingest-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+                    help="only turn four rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE and WRITE_SIZE "
+                         "of a bench run and of a --copy-calibration 256 run) into profiles/traffic.json and exit")
     return ap.parse_args()
 
 
@@ -190,6 +193,61 @@ def load_traffic(kernel):
     return rec.get("bytes_per_launch")
 
 
+TRAFFIC_SOURCES = ["include/gradlev.h"] + [f"paper_2609_34174_amd/csrc/{n}" for n in (
+    "abi.hip", "decode.hip", "device_common.hpp", "internal.hpp", "scan_bwd.hip", "scan_common.hpp",
+    "scan_fwd.hip", "timing.hip")]
+TRAFFIC_KERNELS = {"bwd_main": "bwd_main_kernel", "fwd_main": "fwd_main_kernel"}
+CALIBRATION_MIB = 256
+
+
+def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv):
+    """HBM bytes per launch of the main kernels from rocprofv3 --pmc runs.
+
+    FETCH_SIZE and WRITE_SIZE are read in KiB per dispatch and scaled by what
+    the same counters read for a plain device copy of CALIBRATION_MIB MiB
+    (bytes read and written by the copy / counter value).
+    """
+    import csv
+    import hashlib
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    copy_bytes = CALIBRATION_MIB * 2 ** 20
+    cal = {}
+    for name, path in (("FETCH_SIZE", cal_fetch_csv), ("WRITE_SIZE", cal_write_csv)):
+        v = [x for k, xs in per_kernel(path, name).items() if "copyBuffer" in k for x in xs]
+        cal[name] = copy_bytes / statistics.median(v)  # bytes per counter unit
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    out = {"calibration": {"copy_mib": CALIBRATION_MIB, "bytes_per_unit": cal}}
+    for fam, pat in TRAFFIC_KERNELS.items():
+        fk = [k for k in fetch if pat in k]
+        wk = [k for k in write if pat in k]
+        if not fk or not wk:
+            continue
+        # the lm-bf16 kernel is the instantiation launched most often in the bench run
+        fk = max(fk, key=lambda k: len(fetch[k]))
+        wk = max(wk, key=lambda k: len(write[k]))
+        fb = statistics.median(fetch[fk]) * cal["FETCH_SIZE"]
+        wb = statistics.median(write[wk]) * cal["WRITE_SIZE"]
+        out[fam] = {"kernel": fk.split("(")[0], "read_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb,
+                    "sources": TRAFFIC_SOURCES, "source_sha256": h.hexdigest()}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def cpu_baseline(W, wl, min_seconds):
     """The float64 oracle, as it stands, on the workload's first batch rows.
 
@@ -319,6 +377,9 @@ def secondary_decode(gl, torch, W, device):
 
 def main():
     args = parse()
+    if args.ingest_traffic:
+        ingest_traffic(*args.ingest_traffic)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the GradLev scan shards over (batch, head) with no "
