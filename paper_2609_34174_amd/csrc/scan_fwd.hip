@@ -38,10 +38,13 @@ fwd_main_kernel(const KArgs a) {
   constexpr bool SPLITV = ETAV && OP::kSplit == 2;
   __shared__ E Xs[C * D];                 // X[t][j]
   __shared__ E Gs[C * M];                 // G[t][i]
-  __shared__ E Pl[C * C];                 // -eta_s (x_t . x_s) masked, [t][s]
+  // Scores -eta_s (x_t . x_s): built per wave in registers for bf16 tiles of up
+  // to 64 tokens (no LDS round trip, no barrier); otherwise shared through LDS.
+  constexpr bool RS = C <= 64 && OP::kSplit == 2;
+  __shared__ E Pl[RS ? 1 : C * C];        // -eta_s (x_t . x_s) masked, [t][s]
   __shared__ E Vh[ETAV ? C * M : 1];      // -(eta G)[t][i] hi (per-token eta)
   __shared__ E Vl[SPLITV ? C * M : 1];    // -(eta G)[t][i] lo
-  __shared__ float et[C];
+  __shared__ __attribute__((aligned(16))) float et[C];
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg)) return;
@@ -92,7 +95,8 @@ fwd_main_kernel(const KArgs a) {
           if (j0 + u < seg) Ws[jb] -= v[u][jb];
     }
   }
-  for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
+  if constexpr (!RS)
+    for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
 
   auto chunk = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, int64_t t0) {
     // A step past the segment end (the second of a pair) sees zero tiles,
@@ -109,29 +113,30 @@ fwd_main_kernel(const KArgs a) {
     fetch(xr, gr, er, t0 + 2 * C);
 
     // Intra-chunk scores, lower-triangular tiles (tb >= sb) shared by all waves.
+    if constexpr (!RS) {
 #pragma unroll
-    for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
-      if (idx % NW != w) continue;
-      int tb = 0;
-      while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
-      const int sb = idx - tb * (tb + 1) / 2;
-      f32x4 acc = zero4();
+      for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+        if (idx % NW != w) continue;
+        int tb = 0;
+        while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+        const int sb = idx - tb * (tb + 1) / 2;
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int kb = 0; kb < D / 32; ++kb)
-        acc = OP::mma(acc, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
-      // acc[r] = x_s . x_t with s = 16sb + 4q + r, t = 16tb + c; et holds -eta.
-      const int t = 16 * tb + c;
-      f32x4 v;
+        for (int kb = 0; kb < D / 32; ++kb)
+          acc = OP::mma(acc, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+        // acc[r] = x_s . x_t with s = 16sb + 4q + r, t = 16tb + c; et holds -eta.
+        const int t = 16 * tb + c;
+        f32x4 v;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int s = 16 * sb + 4 * q + r;
-        const bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
-        v[r] = keep ? acc[r] * et[s] : 0.f;
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * sb + 4 * q + r;
+          const bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
+          v[r] = keep ? acc[r] * et[s] : 0.f;
+        }
+        OP::store4(Pl + lds_off(t, 16 * sb + 4 * q, C), v);
       }
-      OP::store4(Pl + lds_off(t, 16 * sb + 4 * q, C), v);
+      __syncthreads();
     }
-    __syncthreads();
-
     if (w < IB) {
       // Y^T[i][t] for all t blocks at once (independent accumulator chains).
       f32x4 acc[TB];
@@ -149,7 +154,37 @@ fwd_main_kernel(const KArgs a) {
       for (int kb = 0; kb < C / 32; ++kb) {
         const F gq = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);  // G[s][i], k = s
 #pragma unroll
-        for (int tb = 2 * kb; tb < TB; ++tb) acc[tb] = OP::mma(acc[tb], gq, OP::load_n(Pl, C, 16 * tb, 32 * kb, lane));
+        for (int tb = 2 * kb; tb < TB; ++tb) {
+          F sq;  // row t of -eta_s (x_t . x_s), masked, over k = s in [32kb, 32kb + 32)
+          if constexpr (RS) {
+            // The tile with rows s, cols t is the operand contracted over s:
+            // built here from the X row fragments the state term already read.
+            f32x8 sv;
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int sb = 2 * kb + hh;
+              f32x4 st = zero4();
+              if (sb <= tb) {
+#pragma unroll
+                for (int kj = 0; kj < D / 32; ++kj)
+                  st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kj, lane), OP::load_n(Xs, D, 16 * tb, 32 * kj, lane));
+                const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                  const bool keep = sb < tb || (INCL ? (4 * q + r <= c) : (4 * q + r < c));
+                  st[r] = keep ? st[r] * es[r] : 0.f;
+                }
+              }
+#pragma unroll
+              for (int r = 0; r < 4; ++r) sv[4 * hh + r] = st[r];
+            }
+            F lo;
+            OP::split(sv, sq, lo);  // hi part only: the same rounding as a bf16 score tile
+          } else {
+            sq = OP::load_n(Pl, C, 16 * tb, 32 * kb, lane);
+          }
+          acc[tb] = OP::mma(acc[tb], gq, sq);
+        }
       }
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
