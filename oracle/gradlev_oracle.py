@@ -162,6 +162,40 @@ def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE):
     }
 
 
+def outer_sum(A, Bm, w, lo, hi):
+    """sum_{lo <= i < hi} w_i a_i b_i^T over tokens [lo, hi) of one sequence.
+
+    A [T, m], Bm [T, d], w a scalar or [T].  Returns [m, d].  With A = G and
+    w = eta this is minus the accumulated fast weights of Section 3, Eq. 2
+    (Delta_t = -outer_sum(G, X, eta, 0, t)); with A = dY and w = 1 it is the
+    costate suffix R of the reverse-time sweep.  Sums over disjoint ranges add
+    up (linearity), which is how long sequences are handled a block at a time.
+    """
+    a, b = _as_array(A)[lo:hi], _as_array(Bm)[lo:hi]
+    wv = _as_array(w)
+    if wv.ndim:
+        wv = wv[lo:hi, None]
+    return (a * wv).T @ b
+
+
+def token_outputs(W_read, R, x, g, eta_t, dy):
+    """Every scan output at one token from the closed forms of the sums.
+
+    W_read is the weight matrix the token's read sees (W_0 minus the writes
+    before it, or up to and including it for the inclusive convention), R the
+    suffix sum of dY_u x_u^T over the reads that see the token's write.  The
+    formulas are those of the sequential sweeps in :func:`scan_fwd` and
+    :func:`scan_bwd`: y = W x, gtilde = W^T dY, u = -R x, dg = eta u,
+    deta = <g, u>, dx = gtilde - eta R^T g.
+    """
+    W_read, R = _as_array(W_read), _as_array(R)
+    x, g, dy, e = _as_array(x), _as_array(g), _as_array(dy), _as_array(eta_t)
+    gt = W_read.T @ dy
+    u = -(R @ x)
+    return {"y": W_read @ x, "gtilde": gt, "dx": gt - e * (R.T @ g), "dg": e * u,
+            "deta": g @ u}
+
+
 def decode_step(W, x, g, eta):
     """One deployment step for every (sequence, head): score, then write.
 

@@ -120,6 +120,20 @@ def test_sixteen_segments(dtype):
         check(k, out[k], ref[k], dtype)
 
 
+@pytest.mark.parametrize("dtype,d,m", [("f32", 64, 64), ("bf16", 64, 64), ("bf16", 128, 64)])
+def test_heads_not_multiple_of_eight(dtype, d, m):
+    """B*H = 15 with automatic segments: the XCD-ordered grid has idle slots."""
+    log(f"B*H=15 auto segments dtype={dtype} d={d} m={m}")
+    inp = small_inputs(3, 5, 3000, d, m, dtype, seed=33 + d, eta_kind="token")
+    p = gl.plan(gl.make_shape(B=3, H=5, T=3000, d_in=d, d_out=m,
+                              dtype=gl.BF16 if dtype == "bf16" else gl.F32))
+    assert p.fwd_nseg > 1 and p.bwd_nseg > 1
+    out = run_gpu(inp, dtype, "exclusive")
+    ref = oracle_all(inp, "exclusive")
+    for k in KEYS:
+        check(k, out[k], ref[k], dtype)
+
+
 def test_eta_zero_reads_slow_weights():
     log("eta = 0")
     inp = small_inputs(2, 2, 150, 64, 64, "bf16", seed=9, eta_kind="scalar")
@@ -166,7 +180,7 @@ def test_small_f32_config():
             check(k, out[k], ref[k], "f32")
 
 
-def _sampled_config(wl, layer, heads):
+def _sampled_config(wl, layer, heads, prefix="exclusive", token_eta=False):
     """Full-size GPU run; the oracle checks every output of the sampled heads.
 
     Inputs are drawn on the device with the workload's seeded generator (the
@@ -176,17 +190,22 @@ def _sampled_config(wl, layer, heads):
     """
     log(f"config {wl.name} layer={layer}: drawing inputs on the device")
     inp = W.device_scan_inputs(wl, layer, "cuda", torch=torch)
-    log(f"config {wl.name} layer={layer}: GPU fwd+bwd (full size)")
-    Y = gl.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"], chunk=wl.chunk)
-    out = gl.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["dY"], inp["eta"], chunk=wl.chunk)
+    eta = inp["eta"]
+    if token_eta:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(wl.layer_seed(layer) + 7)
+        eta = (torch.rand(wl.B, wl.H, wl.T, device="cuda", generator=gen) * 0.2).contiguous()
+    log(f"config {wl.name} layer={layer} prefix={prefix} token_eta={token_eta}: GPU fwd+bwd (full size)")
+    Y = gl.scan_fwd(inp["W0"], inp["X"], inp["G"], eta, prefix=prefix, chunk=wl.chunk)
+    out = gl.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["dY"], eta, prefix=prefix, chunk=wl.chunk)
     out["y"] = Y
     torch.cuda.synchronize()
     for h in heads:
         log(f"  oracle on head h={h} (all {wl.B} batch rows, T={wl.T})")
         sl = {"W0": to_host(inp["W0"][h:h + 1]), "X": to_host(inp["X"][:, h:h + 1]),
               "G": to_host(inp["G"][:, h:h + 1]), "dY": to_host(inp["dY"][:, h:h + 1]),
-              "eta": inp["eta"]}
-        ref = oracle_all(sl, "exclusive")
+              "eta": to_host(eta[:, h:h + 1]) if token_eta else eta}
+        ref = oracle_all(sl, prefix)
         for k in ("y", "gtilde", "dx", "dg", "deta"):
             check(k, to_host(out[k][:, h:h + 1]), ref[k], wl.dtype)
         check("dw0", to_host(out["dw0"][h:h + 1]), ref["dw0"], wl.dtype)
@@ -198,6 +217,13 @@ def test_lm_bf16_config():
 
 
 @pytest.mark.timeout(300)
+@pytest.mark.parametrize("prefix,token_eta", [("inclusive", False), ("exclusive", True), ("inclusive", True)])
+def test_lm_bf16_config_conventions(prefix, token_eta):
+    """The lm-bf16 shape with the inclusive read and per-token step sizes."""
+    _sampled_config(W.SCAN_WORKLOADS["lm-bf16"], 0, [5], prefix, token_eta)
+
+
+@pytest.mark.timeout(300)
 def test_long_bf16_config():
     _sampled_config(W.SCAN_WORKLOADS["long-bf16"], 0, [3])
 
@@ -206,6 +232,100 @@ def test_long_bf16_config():
 @pytest.mark.parametrize("layer", [0, 23])
 def test_stack_bf16_config_layers(layer):
     _sampled_config(W.SCAN_WORKLOADS["stack-bf16"], layer, [31])
+
+
+# ---------------------------------------------------------------------------
+# Longest accepted sequences (per-sequence byte offsets just under 2^31)
+# ---------------------------------------------------------------------------
+
+def _longest_T(width):
+    """The largest T the library accepts for this map width: T * width * 4 < 2^31."""
+    return (1 << 31) // (4 * width) - 1
+
+
+def _point_check(inp, eta, prefix, out, ts, dtype, block=1 << 20):
+    """Check sampled tokens of one sequence against the closed-form oracle.
+
+    The writes before each sampled read and the costate suffix after it are
+    summed block by block on the host in float64 (sums over disjoint token
+    ranges add up), then every output of the token is evaluated from them.
+    """
+    X, G, dY = inp["X"][0, 0], inp["G"][0, 0], inp["dY"][0, 0]
+    T = X.shape[0]
+    inc = prefix == "inclusive"
+    tok_eta = not isinstance(eta, float)
+    eh = to_host(eta[0, 0]) if tok_eta else eta
+
+    def ew(lo, hi):
+        return eh[lo:hi] if tok_eta else eh
+
+    ts = sorted(set(int(t) for t in ts))
+    W0h = to_host(inp["W0"][0])
+    P = np.zeros_like(W0h)
+    pos, Wread = 0, {}
+    for t in ts:
+        end = t + 1 if inc else t
+        while pos < end:
+            hi = min(end, pos + block)
+            P += orc.outer_sum(to_host(G[pos:hi]), to_host(X[pos:hi]), ew(pos, hi), 0, hi - pos)
+            pos = hi
+        Wread[t] = W0h - P
+    R = np.zeros_like(W0h)
+    pos, Rs = T, {}
+    for t in reversed(ts):
+        start = t if inc else t + 1
+        while pos > start:
+            lo = max(start, pos - block)
+            R += orc.outer_sum(to_host(dY[lo:pos]), to_host(X[lo:pos]), 1.0, 0, pos - lo)
+            pos = lo
+        Rs[t] = R.copy()
+    while pos > 0:
+        lo = max(0, pos - block)
+        R += orc.outer_sum(to_host(dY[lo:pos]), to_host(X[lo:pos]), 1.0, 0, pos - lo)
+        pos = lo
+    idx = torch.tensor(ts, device=X.device)
+    rows = {k: to_host(out[k][0, 0].index_select(0, idx)) for k in ("y", "gtilde", "dx", "dg", "deta")}
+    xs, gs, ds = to_host(X.index_select(0, idx)), to_host(G.index_select(0, idx)), to_host(dY.index_select(0, idx))
+    ref = {k: [] for k in rows}
+    for i, t in enumerate(ts):
+        o = orc.token_outputs(Wread[t], Rs[t], xs[i], gs[i], eh[t] if tok_eta else eh, ds[i])
+        for k in rows:
+            ref[k].append(o[k])
+    for k in rows:
+        check(k, rows[k], np.array(ref[k]), dtype)
+    check("dw0", to_host(out["dw0"][0]), R, dtype)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("d,prefix,token_eta", [(64, "exclusive", False), (128, "inclusive", True)])
+def test_longest_sequence(d, prefix, token_eta):
+    """One bf16 sequence of the longest accepted length, sampled at the chunk
+    and segment seams, the ragged tail and random tokens."""
+    T = _longest_T(d)
+    p = gl.plan(gl.make_shape(B=1, H=1, T=T, d_in=d, d_out=d, dtype=gl.BF16, prefix=prefix))
+    log(f"longest sequence T={T} d=m={d} prefix={prefix} token_eta={token_eta} "
+        f"fwd {p.fwd_nseg}x{p.fwd_segment} bwd {p.bwd_nseg}x{p.bwd_segment}")
+    with pytest.raises(gl.GradLevError):
+        gl.plan(gl.make_shape(B=1, H=1, T=T + 1, d_in=d, d_out=d, dtype=gl.BF16))
+    wl = dataclasses.replace(W.SCAN_WORKLOADS["lm-bf16"], B=1, H=1, T=T, d=d, m=d, seed=40 + d)
+    inp = W.device_scan_inputs(wl, 0, "cuda", torch=torch)
+    eta = inp["eta"]
+    if token_eta:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(41 + d)
+        eta = (torch.rand(1, 1, T, device="cuda", generator=gen) * 0.2).contiguous()
+    out = {"y": gl.scan_fwd(inp["W0"], inp["X"], inp["G"], eta, prefix=prefix)}
+    out.update(gl.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["dY"], eta, prefix=prefix))
+    torch.cuda.synchronize()
+    log("  GPU done; oracle on sampled tokens")
+    seams = [0, 1, p.fwd_chunk - 1, p.fwd_chunk, p.bwd_chunk - 1, p.bwd_chunk]
+    for seg in (p.fwd_segment, p.bwd_segment):
+        for k in (1, p.fwd_nseg // 2, (T - 1) // seg):
+            seams += [k * seg - 1, k * seg, k * seg + 1]
+    seams += [T // 2, T - p.bwd_chunk, T - 2, T - 1]
+    rng = np.random.default_rng(d)
+    seams += list(rng.integers(0, T, 8))
+    _point_check(inp, eta, prefix, out, [t for t in seams if 0 <= t < T], "bf16")
 
 
 # ---------------------------------------------------------------------------

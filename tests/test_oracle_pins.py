@@ -318,3 +318,42 @@ def test_oracle_rejects_unknown_prefix():
     W0, X, G, e, dY = rand_problem(1, 1, 2, 2, 2)
     with pytest.raises(ValueError):
         orc.scan_fwd(W0, X, G, e, "shifted")
+
+
+# --------------------------------------------------------------------------
+# Point evaluation from the closed-form sums (used for sampled checks of
+# sequences too long for the sequential sweeps)
+# --------------------------------------------------------------------------
+
+def test_outer_sum_of_repeated_token():
+    """n copies of (a, b) with step w sum to n w a b^T; ranges add up."""
+    rng = np.random.default_rng(31)
+    a, b = rng.standard_normal(5), rng.standard_normal(3)
+    A, Bm = np.tile(a, (40, 1)), np.tile(b, (40, 1))
+    np.testing.assert_allclose(orc.outer_sum(A, Bm, 0.25, 7, 19), 12 * 0.25 * np.outer(a, b), rtol=1e-13)
+    w = rng.uniform(0, 1, 40)
+    whole = orc.outer_sum(A, Bm, w, 0, 40)
+    parts = orc.outer_sum(A, Bm, w, 0, 13) + orc.outer_sum(A, Bm, w, 13, 40)
+    np.testing.assert_allclose(parts, whole, rtol=1e-13)
+    np.testing.assert_allclose(whole, w.sum() * np.outer(a, b), rtol=1e-13)
+    assert np.all(orc.outer_sum(A, Bm, w, 5, 5) == 0.0)
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_token_outputs_match_sweeps(prefix):
+    """Closed-form point outputs equal the sequential sweeps at every token."""
+    W0, X, G, e, dY = rand_problem(1, 1, 23, 6, 4, seed=17)
+    Y = orc.scan_fwd(W0, X, G, e, prefix)
+    ref = orc.scan_bwd(W0, X, G, e, dY, prefix)
+    x, g, dy, et = X[0, 0], G[0, 0], dY[0, 0], e[0, 0]
+    T = x.shape[0]
+    inc = prefix == orc.INCLUSIVE
+    for t in range(T):
+        Wr = W0[0] - orc.outer_sum(g, x, et, 0, t + 1 if inc else t)
+        R = orc.outer_sum(dy, x, 1.0, t if inc else t + 1, T)
+        o = orc.token_outputs(Wr, R, x[t], g[t], et[t], dy[t])
+        assert rel_err(o["y"], Y[0, 0, t]) < 1e-12
+        for k in ("gtilde", "dx", "dg"):
+            assert rel_err(o[k], ref[k][0, 0, t]) < 1e-12, (k, t)
+        assert abs(o["deta"] - ref["deta"][0, 0, t]) <= 1e-12 * max(1.0, np.max(np.abs(ref["deta"])))
+    np.testing.assert_allclose(orc.outer_sum(dy, x, 1.0, 0, T), ref["dw0"][0], rtol=1e-12)
