@@ -29,6 +29,19 @@ What is computed (GradLev, arXiv 2609.34174):
   returned and callers drop what they detach.
 * Deployment (Section 3, "Training objective", last sentences): score with
   the current weights, then write the true costate: y = W x, W <- W - eta g x^T.
+* Retention (Section 3, Eq. 2, general form): with per-token alpha_t in [0, 1]
+  the write is centered weight decay, W_{t+1} = W_0 + alpha_t (W_t - W_0)
+  - eta_t g_t x_t^T, so that Delta_t = W_t - W_0 discounts write i by the
+  retentions alpha_{i+1} .. alpha_{t-1}.  The reverse sweep then carries
+  Lambda_t = dL/dDelta_t = dY_t x_t^T + alpha_t Lambda_{t+1} (the retention
+  scales the suffix), and the gate gradient is dalpha_t = <Lambda_{t+1},
+  Delta_t>_F (Appendix E keeps gate derivatives).  Without alpha every
+  retention is one and the arithmetic is the plain prefix sum above.
+* Resets (Section 3, Eq. 2 holds within each reset segment): a token flagged
+  as a reset reads W_0 again, i.e. Delta_t = 0.  That is the same as a zero
+  retention and a zero step size at the token before it, which is how the
+  sweeps apply it; the gate gradients of that token are then reported as 0
+  (its gates have no effect).
 
 Everything here is the plain sequential definition, token by token, in float64
 (complex inputs are also accepted, which the tests use for complex-step
@@ -41,6 +54,8 @@ Shapes (row-major):
   G   [B, H, T, m]   proposed costates g_hat_t
   eta [B, H, T]      step sizes (a Python scalar is broadcast)
   dY  [B, H, T, m]   upstream costates dL/dy_hat_t
+  alpha [B, H, T]    retentions (optional; a Python scalar is broadcast)
+  reset [B, T]       optional 0/1 flags, 1 = the token starts a new segment
 """
 
 from __future__ import annotations
@@ -69,38 +84,73 @@ def _eta_array(eta, B, H, T):
     return e
 
 
+def _gates(eta, alpha, reset, B, H, T):
+    """Per-token (eta, alpha) with resets applied; alpha None means one.
+
+    A reset at token t (t > 0) clears the fast weights before t's read: the
+    write of token t - 1 is dropped and the state it would carry is
+    forgotten (eta_{t-1} = alpha_{t-1} = 0).  A reset at t = 0 changes
+    nothing (Delta_0 = 0).  Returns (eta, alpha_or_None, gate_mask) where
+    gate_mask zeroes the gate gradients of the tokens a reset overrides.
+    """
+    e = _eta_array(eta, B, H, T)
+    a = None if alpha is None else _eta_array(alpha, B, H, T)
+    keep = np.ones((B, H, T))
+    if reset is not None:
+        r = np.asarray(reset)
+        if r.shape != (B, T):
+            raise ValueError(f"reset must be [B,T]={B,T}, got {r.shape}")
+        cut = np.zeros((B, T), bool)
+        cut[:, :-1] = r[:, 1:] != 0
+        cut = np.broadcast_to(cut[:, None, :], (B, H, T))
+        e = np.where(cut, 0.0, e)
+        a = np.where(cut, 0.0, 1.0 if a is None else a)
+        keep = np.where(cut, 0.0, keep)
+    return e, a, keep
+
+
 def _check(prefix):
     if prefix not in (EXCLUSIVE, INCLUSIVE):
         raise ValueError(f"prefix must be '{EXCLUSIVE}' or '{INCLUSIVE}'")
 
 
-def scan_fwd(W0, X, G, eta, prefix=EXCLUSIVE):
+def _write(W, W0, a_t, e_t, g, x):
+    """One write of Eq. 2: W_0 + alpha (W - W_0) - eta g x^T (alpha None: W - eta g x^T)."""
+    write = e_t[:, :, None, None] * g[:, :, :, None] * x[:, :, None, :]
+    if a_t is None:
+        return W - write
+    return W0 + a_t[:, :, None, None] * (W - W0) - write
+
+
+def scan_fwd(W0, X, G, eta, prefix=EXCLUSIVE, alpha=None, reset=None):
     """Adapted outputs y_hat_t = W_t x_t of the sequential online learner.
 
     Follows Section 3, Eq. 3: Delta_0 = 0, read y_t with the current weights,
-    then write W <- W - eta_t g_t x_t^T (exclusive).  The inclusive reading
-    writes first.  Returns Y [B, H, T, m].
+    then write (exclusive).  The inclusive reading writes first.  The write
+    is W <- W - eta_t g_t x_t^T, or the centered decay of Eq. 2 when
+    retentions are given.  Returns Y [B, H, T, m].
     """
     _check(prefix)
     W0, X, G = _as_array(W0), _as_array(X), _as_array(G)
     B, H, T, d = X.shape
     m = G.shape[-1]
-    e = _eta_array(eta, B, H, T)
-    dt = np.result_type(W0, X, G, e)
-    W = np.broadcast_to(W0, (B, H, m, d)).astype(dt).copy()
+    e, a, _ = _gates(eta, alpha, reset, B, H, T)
+    dt = np.result_type(W0, X, G, e, 0.0 if a is None else a)
+    W0b = np.broadcast_to(W0, (B, H, m, d)).astype(dt)
+    W = W0b.copy()
     Y = np.zeros((B, H, T, m), dt)
     for t in range(T):
         x, g = X[:, :, t, :], G[:, :, t, :]
-        write = e[:, :, t, None, None] * g[:, :, :, None] * x[:, :, None, :]
+        at = None if a is None else a[:, :, t]
         if prefix == INCLUSIVE:
-            W -= write
+            W = _write(W, W0b, at, e[:, :, t], g, x)
         Y[:, :, t, :] = np.einsum("bhmd,bhd->bhm", W, x)
         if prefix == EXCLUSIVE:
-            W -= write
+            W = _write(W, W0b, at, e[:, :, t], g, x)
     return Y
 
 
-def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE):
+def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE, alpha=None, reset=None):
     """Backward of the forward scan for L = sum_t <dY_t, y_hat_t>.
 
     Two sweeps, each the plain definition:
@@ -108,58 +158,94 @@ def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE):
     * forward-time sweep (Section 3, Eq. 4 and Appendix C, Eq. 16): the
       transpose read gtilde_t = W_t^T dY_t with the same weights the forward
       read used (W_0 + Delta_hat_t, or Delta_hat_{t+1} when inclusive);
-    * reverse-time sweep: with R the suffix sum of dY_u x_u^T over the reads
-      that see write t (u > t, or u >= t when inclusive),
-      u_t = -R x_t, dG_t = eta_t u_t, deta_t = <g_t, u_t>,
-      write-side dx_t = -eta_t R^T g_t.
+    * reverse-time sweep: Lambda is dL/dDelta of the state that token t's
+      write produces: the suffix sum of dY_u x_u^T over the reads that see
+      write t (u > t, or u >= t when inclusive), each discounted by the
+      retentions between (Lambda_t = dY_t x_t^T + alpha_t Lambda_{t+1}).
+      u_t = -Lambda x_t, dG_t = eta_t u_t, deta_t = <g_t, u_t>,
+      write-side dx_t = -eta_t Lambda^T g_t and, with retentions,
+      dalpha_t = <Lambda, Delta_t>_F (Delta_t = W_t - W_0 before t's write).
 
     Returns a dict with
       gtilde [B,H,T,d]  read-side gradient (the paper's grounded target),
       dx     [B,H,T,d]  total dL/dx = gtilde + write-side term,
-      dg     [B,H,T,m], deta [B,H,T], dw0 [H,m,d] (summed over the batch).
+      dg     [B,H,T,m], deta [B,H,T], dw0 [H,m,d] (summed over the batch),
+      dalpha [B,H,T]    (only when alpha is given).
     """
     _check(prefix)
     W0, X, G, dY = _as_array(W0), _as_array(X), _as_array(G), _as_array(dY)
     B, H, T, d = X.shape
     m = G.shape[-1]
-    e = _eta_array(eta, B, H, T)
-    dt = np.result_type(W0, X, G, e, dY)
+    e, a, keep = _gates(eta, alpha, reset, B, H, T)
+    dt = np.result_type(W0, X, G, e, dY, 0.0 if a is None else a)
+    W0b = np.broadcast_to(W0, (B, H, m, d)).astype(dt)
 
-    # Forward-time sweep: transpose reads over the historical writes.
-    W = np.broadcast_to(W0, (B, H, m, d)).astype(dt).copy()
+    def write(W, t):
+        return _write(W, W0b, None if a is None else a[:, :, t], e[:, :, t], G[:, :, t], X[:, :, t])
+
+    # Forward-time sweep: transpose reads over the historical writes.  With
+    # retentions, the weights before every block of K writes are kept so the
+    # reverse sweep can replay each block (Delta_t is needed there).
+    K = 64
+    ckpt = {}
+    W = W0b.copy()
     gtilde = np.zeros((B, H, T, d), dt)
     for t in range(T):
-        x, g = X[:, :, t, :], G[:, :, t, :]
-        write = e[:, :, t, None, None] * g[:, :, :, None] * x[:, :, None, :]
+        if a is not None and t % K == 0:
+            ckpt[t] = W.copy()
         if prefix == INCLUSIVE:
-            W -= write
+            W = write(W, t)
         gtilde[:, :, t, :] = np.einsum("bhmd,bhm->bhd", W, dY[:, :, t, :])
         if prefix == EXCLUSIVE:
-            W -= write
+            W = write(W, t)
 
     # Reverse-time sweep: explicit suffix accumulation.
-    R = np.zeros((B, H, m, d), dt)
+    Lam = np.zeros((B, H, m, d), dt)
     dg = np.zeros((B, H, T, m), dt)
     deta = np.zeros((B, H, T), dt)
+    dalpha = np.zeros((B, H, T), dt)
     dxw = np.zeros((B, H, T, d), dt)
+    hist = []
     for t in range(T - 1, -1, -1):
         x, g, dy = X[:, :, t, :], G[:, :, t, :], dY[:, :, t, :]
+        if a is not None and not hist:
+            # Replay the block holding t: hist[i] = W_{b0 + i} before its write.
+            b0 = t - t % K
+            Wr = ckpt[b0].copy()
+            for s in range(b0, t + 1):
+                hist.append(Wr)
+                Wr = write(Wr, s)
+        read = dy[:, :, :, None] * x[:, :, None, :]
         if prefix == INCLUSIVE:
-            R += dy[:, :, :, None] * x[:, :, None, :]
-        u = -np.einsum("bhmd,bhd->bhm", R, x)
+            # Lambda becomes dL/dDelta_{t+1}; the next token's retention
+            # discounts what lies beyond it.
+            if a is not None and t + 1 < T:
+                Lam = a[:, :, t + 1, None, None] * Lam
+            Lam = Lam + read
+        u = -np.einsum("bhmd,bhd->bhm", Lam, x)
         dg[:, :, t, :] = e[:, :, t, None] * u
         deta[:, :, t] = np.einsum("bhm,bhm->bh", g, u)
-        dxw[:, :, t, :] = -e[:, :, t, None] * np.einsum("bhmd,bhm->bhd", R, g)
+        dxw[:, :, t, :] = -e[:, :, t, None] * np.einsum("bhmd,bhm->bhd", Lam, g)
+        if a is not None:
+            Delta = hist.pop() - W0b
+            dalpha[:, :, t] = np.einsum("bhmd,bhmd->bh", Lam, Delta)
         if prefix == EXCLUSIVE:
-            R += dy[:, :, :, None] * x[:, :, None, :]
-    # After the sweep R = sum over all t of dY_t x_t^T, which is dL/dW_0.
-    return {
+            if a is not None:
+                Lam = a[:, :, t, None, None] * Lam
+            Lam = Lam + read
+    # dL/dW_0: every read sees W_0 undiscounted (the decay is centered), so it
+    # is sum_t dY_t x_t^T, which the sweep accumulates when alpha is one.
+    dw0 = np.einsum("bhtm,bhtd->hmd", dY, X) if a is not None else Lam.sum(axis=0)
+    out = {
         "gtilde": gtilde,
         "dx": gtilde + dxw,
         "dg": dg,
-        "deta": deta,
-        "dw0": R.sum(axis=0),
+        "deta": deta * keep,
+        "dw0": dw0,
     }
+    if alpha is not None:
+        out["dalpha"] = dalpha * keep
+    return out
 
 
 def outer_sum(A, Bm, w, lo, hi):
@@ -196,17 +282,27 @@ def token_outputs(W_read, R, x, g, eta_t, dy):
             "deta": g @ u}
 
 
-def decode_step(W, x, g, eta):
+def decode_step(W, x, g, eta, alpha=None, W0=None):
     """One deployment step for every (sequence, head): score, then write.
 
     W [S,H,m,d], x [S,H,d], g [S,H,m], eta scalar or [S,H].
     Returns (y, W_next) with y = W x computed before the write and
-    W_next = W - eta g x^T.
+    W_next = W - eta g x^T, or, with retentions alpha (scalar or [S,H]) and
+    the slow weights W0 [H,m,d], the centered decay of Eq. 2:
+    W_next = W0 + alpha (W - W0) - eta g x^T.
     """
     W, x, g = _as_array(W), _as_array(x), _as_array(g)
     e = _as_array(eta)
     if e.ndim == 0:
         e = np.broadcast_to(e, W.shape[:2])
     y = np.einsum("shmd,shd->shm", W, x)
-    W_next = W - e[:, :, None, None] * g[:, :, :, None] * x[:, :, None, :]
-    return y, W_next
+    write = e[:, :, None, None] * g[:, :, :, None] * x[:, :, None, :]
+    if alpha is None:
+        return y, W - write
+    if W0 is None:
+        raise ValueError("retention needs the slow weights W0")
+    a = _as_array(alpha)
+    if a.ndim == 0:
+        a = np.broadcast_to(a, W.shape[:2])
+    W0b = np.broadcast_to(_as_array(W0), W.shape)
+    return y, W0b + a[:, :, None, None] * (W - W0b) - write

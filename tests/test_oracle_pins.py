@@ -357,3 +357,181 @@ def test_token_outputs_match_sweeps(prefix):
             assert rel_err(o[k], ref[k][0, 0, t]) < 1e-12, (k, t)
         assert abs(o["deta"] - ref["deta"][0, 0, t]) <= 1e-12 * max(1.0, np.max(np.abs(ref["deta"])))
     np.testing.assert_allclose(orc.outer_sum(dy, x, 1.0, 0, T), ref["dw0"][0], rtol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Retention (Section 3, Eq. 2 general form) and resets
+# --------------------------------------------------------------------------
+
+def rand_alpha(B, H, T, seed, lo=0.0, hi=1.0):
+    return np.random.default_rng(seed).uniform(lo, hi, size=(B, H, T))
+
+
+def closed_form_retention(W0, X, G, eta, alpha, prefix):
+    """Eq. 2 expanded: each write discounted by the explicit product of the
+    retentions between it and the read (empty products are one)."""
+    B, H, T, d = X.shape
+    e = np.broadcast_to(np.asarray(eta, float), (B, H, T))
+    Y = np.empty(G.shape)
+    for b in range(B):
+        for h in range(H):
+            for t in range(T):
+                y = W0[h] @ X[b, h, t]
+                last = t if prefix == orc.EXCLUSIVE else t + 1
+                for i in range(last):
+                    hi = t if prefix == orc.EXCLUSIVE else t + 1
+                    f = np.prod(alpha[b, h, i + 1:hi])
+                    y = y - e[b, h, i] * f * (X[b, h, i] @ X[b, h, t]) * G[b, h, i]
+                Y[b, h, t] = y
+    return Y
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_retention_equals_expanded_sum(prefix):
+    W0, X, G, e, _ = rand_problem(2, 2, 9, 4, 3, seed=40)
+    a = rand_alpha(2, 2, 9, 41)
+    Y = orc.scan_fwd(W0, X, G, e, prefix, alpha=a)
+    assert rel_err(Y, closed_form_retention(W0, X, G, e, a, prefix)) < 1e-12
+
+
+def test_unit_retention_is_the_plain_scan():
+    W0, X, G, e, dY = rand_problem(2, 2, 10, 4, 3, seed=42)
+    for prefix in PREFIXES:
+        np.testing.assert_allclose(orc.scan_fwd(W0, X, G, e, prefix, alpha=1.0),
+                                   orc.scan_fwd(W0, X, G, e, prefix), rtol=1e-13, atol=1e-13)
+        r1 = orc.scan_bwd(W0, X, G, e, dY, prefix, alpha=1.0)
+        r0 = orc.scan_bwd(W0, X, G, e, dY, prefix)
+        for k in r0:
+            np.testing.assert_allclose(r1[k], r0[k], rtol=1e-12, atol=1e-12)
+
+
+def test_zero_retention_keeps_only_the_last_write():
+    """alpha = 0: y_t = W0 x_t - eta_{t-1} (x_{t-1} . x_t) g_{t-1} (exclusive)."""
+    W0, X, G, e, _ = rand_problem(1, 2, 8, 4, 3, seed=43)
+    Y = orc.scan_fwd(W0, X, G, e, alpha=0.0)
+    for h in range(2):
+        x, g = X[0, h], G[0, h]
+        ref = x @ W0[h].T
+        ref[1:] -= (e[0, h, :-1] * np.sum(x[:-1] * x[1:], axis=1))[:, None] * g[:-1]
+        np.testing.assert_allclose(Y[0, h], ref, rtol=0, atol=1e-13)
+
+
+def test_constant_retention_on_unit_inputs_is_an_ema():
+    """x_t = e_k, constant alpha: y_t = W0 e_k - sum_{s<t} alpha^(t-1-s) eta_s g_s."""
+    rng = np.random.default_rng(44)
+    T, d, m, k, al = 12, 4, 3, 1, 0.7
+    W0 = rng.standard_normal((1, m, d))
+    X = np.zeros((1, 1, T, d))
+    X[..., k] = 1.0
+    G = rng.standard_normal((1, 1, T, m))
+    e = rng.uniform(0.1, 0.5, size=(1, 1, T))
+    Y = orc.scan_fwd(W0, X, G, e, alpha=al)
+    for t in range(T):
+        ref = W0[0][:, k] - sum(al ** (t - 1 - s) * e[0, 0, s] * G[0, 0, s] for s in range(t))
+        np.testing.assert_allclose(Y[0, 0, t], ref, rtol=0, atol=1e-13)
+
+
+def test_retention_without_writes_is_static():
+    """eta = 0 keeps W = W0 whatever alpha is: no gate gradient, gtilde = W0^T dY."""
+    W0, X, G, _, dY = rand_problem(2, 1, 7, 4, 3, seed=45)
+    a = rand_alpha(2, 1, 7, 46)
+    Y = orc.scan_fwd(W0, X, G, 0.0, alpha=a)
+    np.testing.assert_allclose(Y, np.einsum("hmd,bhtd->bhtm", W0, X), atol=1e-14)
+    out = orc.scan_bwd(W0, X, G, 0.0, dY, alpha=a)
+    np.testing.assert_array_equal(out["dalpha"], 0.0)
+    np.testing.assert_allclose(out["gtilde"], np.einsum("hmd,bhtm->bhtd", W0, dY), atol=1e-14)
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_retention_gradients_complex_step(prefix):
+    """Every gradient, dalpha included, against per-element complex-step
+    derivatives of L = sum <dY, y> (exact to rounding)."""
+    W0, X, G, e, dY = rand_problem(1, 1, 6, 3, 2, seed=47)
+    a = rand_alpha(1, 1, 6, 48, 0.2, 1.0)
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix, alpha=a)
+    h = 1e-30
+
+    def cs(which, arr):
+        g = np.zeros(arr.shape)
+        for i in np.ndindex(arr.shape):
+            args = {"W0": W0, "X": X, "G": G, "e": e, "a": a}
+            p = arr.astype(complex)
+            p[i] += 1j * h
+            args[which] = p
+            Y = orc.scan_fwd(args["W0"], args["X"], args["G"], args["e"], prefix, alpha=args["a"])
+            g[i] = np.sum(np.imag(Y) * dY) / h
+        return g
+
+    assert rel_err(out["dalpha"], cs("a", a)) < 1e-12
+    assert rel_err(out["deta"], cs("e", e)) < 1e-12
+    assert rel_err(out["dg"], cs("G", G)) < 1e-12
+    assert rel_err(out["dx"], cs("X", X)) < 1e-12
+    assert rel_err(out["dw0"], cs("W0", W0)) < 1e-12
+
+
+@pytest.mark.parametrize("prefix", PREFIXES)
+def test_retention_gtilde_is_read_side(prefix):
+    """gtilde stays the transpose read (W_0 + Delta_t)^T dY_t of Eq. 4."""
+    W0, X, G, e, dY = rand_problem(1, 2, 7, 3, 4, seed=49)
+    a = rand_alpha(1, 2, 7, 50)
+    out = orc.scan_bwd(W0, X, G, e, dY, prefix, alpha=a)
+    # The read weights follow from the expanded sum with x replaced by basis vectors.
+    B, H, T, d = X.shape
+    for h in range(H):
+        for t in range(T):
+            W = W0[h].copy()
+            last = t if prefix == orc.EXCLUSIVE else t + 1
+            for i in range(last):
+                f = np.prod(a[0, h, i + 1:last])
+                W -= e[0, h, i] * f * np.outer(G[0, h, i], X[0, h, i])
+            np.testing.assert_allclose(out["gtilde"][0, h, t], W.T @ dY[0, h, t], rtol=1e-12, atol=1e-12)
+
+
+def test_decode_with_retention_equals_scan():
+    rng = np.random.default_rng(51)
+    S, H, T, d, m = 3, 2, 10, 5, 4
+    W0 = rng.standard_normal((H, m, d))
+    X = rng.standard_normal((S, H, T, d))
+    G = rng.standard_normal((S, H, T, m))
+    e = rng.uniform(0.1, 0.4, size=(S, H, T))
+    a = rng.uniform(0.0, 1.0, size=(S, H, T))
+    Y = orc.scan_fwd(W0, X, G, e, alpha=a)
+    W = np.broadcast_to(W0, (S, H, m, d)).copy()
+    for t in range(T):
+        y, W = orc.decode_step(W, X[:, :, t], G[:, :, t], e[:, :, t], alpha=a[:, :, t], W0=W0)
+        np.testing.assert_allclose(y, Y[:, :, t], rtol=0, atol=1e-12)
+    final = np.broadcast_to(W0, (S, H, m, d)).copy()
+    for s in range(S):
+        for h in range(H):
+            for i in range(T):
+                final[s, h] -= e[s, h, i] * np.prod(a[s, h, i + 1:T]) * np.outer(G[s, h, i], X[s, h, i])
+    np.testing.assert_allclose(W, final, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("with_alpha", [False, True])
+def test_reset_equals_separate_segments(with_alpha):
+    """A reset splits the sequence: every output and gradient equals running
+    the two segments on their own (the cut token's gates have no effect)."""
+    W0, X, G, e, dY = rand_problem(2, 2, 11, 4, 3, seed=52)
+    a = rand_alpha(2, 2, 11, 53) if with_alpha else None
+    r = np.zeros((2, 11), np.int8)
+    r[:, 0] = 1                      # a reset at t = 0 is a no-op
+    r[0, 4] = r[1, 7] = 1
+    Y = orc.scan_fwd(W0, X, G, e, alpha=a, reset=r)
+    out = orc.scan_bwd(W0, X, G, e, dY, alpha=a, reset=r)
+    for b, cut in ((0, 4), (1, 7)):
+        for lo, hi in ((0, cut), (cut, 11)):
+            sl = (slice(b, b + 1), slice(None), slice(lo, hi))
+            asl = None if a is None else a[sl]
+            Yp = orc.scan_fwd(W0, X[sl], G[sl], e[sl], alpha=asl)
+            np.testing.assert_allclose(Y[sl], Yp, rtol=1e-13, atol=1e-13)
+            op = orc.scan_bwd(W0, X[sl], G[sl], e[sl], dY[sl], alpha=asl)
+            for k in ("gtilde", "dx", "dg", "deta") + (("dalpha",) if with_alpha else ()):
+                np.testing.assert_allclose(out[k][sl], op[k], rtol=1e-12, atol=1e-12, err_msg=k)
+    np.testing.assert_allclose(out["dw0"], np.einsum("bhtm,bhtd->hmd", dY, X), rtol=1e-13)
+
+
+def test_retention_dw0_is_plain_product():
+    W0, X, G, e, dY = rand_problem(3, 2, 9, 4, 5, seed=54)
+    out = orc.scan_bwd(W0, X, G, e, dY, alpha=rand_alpha(3, 2, 9, 55))
+    assert rel_err(out["dw0"], np.einsum("bhtm,bhtd->hmd", dY, X)) < 1e-13
