@@ -109,7 +109,7 @@ fwd_main_kernel(const KArgs a) {
     xr.store(Xs, tid);
     gr.store(Gs, tid);
     __syncthreads();
-    if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read after the next barrier
+    if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read by the carry, after a barrier
     fetch(xr, gr, er, t0 + 2 * C);
 
     // Intra-chunk scores, lower-triangular tiles (tb >= sb) shared by all waves.
@@ -192,6 +192,11 @@ fwd_main_kernel(const KArgs a) {
         const int t = 16 * tb + c;
         buf_store4(Yc, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), acc[tb]);
       }
+    }
+    // The eta-scaled V tiles were written by every wave; with register scores
+    // no barrier has passed since (the shared-score path had one).
+    if constexpr (RS && ETAV) __syncthreads();
+    if (w < IB) {
       // Carry to the next chunk (also after the last one, where it is unused).
       if constexpr (ETAV) {
         // W^T[j][i] += sum_t X[t][j] (-eta G)[t][i], eta folded into the split operand.
