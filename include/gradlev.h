@@ -164,6 +164,75 @@ int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                         const float* eta, float eta_scalar, float* y,
                         void* stream);
 
+/* ------------------------------------------------------------------------
+ * Gated scans: retention and document resets (Section 3, Eq. 2, general form)
+ * ------------------------------------------------------------------------
+ * With a retention alpha_t in [0, 1] per token the write is centered weight
+ * decay,
+ *
+ *     W_{t+1} = W_0 + alpha_t (W_t - W_0) - eta_t g_t x_t^T,
+ *     Delta_t = - sum_{i<t} eta_i (prod_{i<j<t} alpha_j) g_i x_i^T,
+ *
+ * so every earlier write is discounted by the retentions after it and decay
+ * pulls towards W_0, not towards zero.  Eq. 2 holds within each reset
+ * segment: a token flagged as a reset reads W_0 again (Delta_t = 0).  That
+ * is the recurrence with alpha_{t-1} = eta_{t-1} = 0, which is how the kernels
+ * apply it; the gate gradients (dalpha, deta) of such a token t-1 are 0.
+ *
+ *   alpha   [B, H, T] fp32 in [0, 1], or NULL to use alpha_scalar for every token
+ *   reset   [B, T] uint8 (0 or 1, shared by the heads of a batch row), or NULL
+ *
+ * Only the exclusive read is supported (GRADLEV_ERR_UNSUPPORTED otherwise),
+ * and one sequence's chunk-start states must stay under 2 GiB:
+ * ceil(T / 32) * d_in * d_out * 4 < 2^31 (T below 2^20 at 128 x 128). */
+typedef struct gradlev_gates {
+  const float* alpha;
+  float alpha_scalar;
+  const uint8_t* reset;
+} gradlev_gates;
+
+/* Workspace bytes for gradlev_scan_fwd_gated and gradlev_scan_bwd_gated
+ * (same rules as gradlev_scan_workspace_bytes).  The backward keeps the
+ * fast-weight state at every chunk start of its plan (fp32, B*H*ceil(T/chunk)
+ * matrices): retention makes the writes impossible to take back stably. */
+int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes);
+
+/* Gated forward scan: Y[b,h,t,:] = (W0[h] + Delta_t) X[b,h,t,:] with Delta_t
+ * as above.  Arguments as in gradlev_scan_fwd; gates must not be NULL. */
+int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates,
+                           const float* W0, const void* X, const void* G,
+                           const float* eta, float eta_scalar, float* Y,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of the gated forward scan.  With Lambda_t = dL/dDelta_t, carried
+ * in reverse time as Lambda_t = dY_t X_t^T + alpha_t Lambda_{t+1}:
+ *   gtilde[t] = (W0 + Delta_t)^T dY_t
+ *   u_t       = -Lambda_{t+1} X_t,   dG[t] = eta_t u_t,   deta[t] = <G_t, u_t>
+ *   dX[t]     = gtilde_t - eta_t Lambda_{t+1}^T G_t
+ *   dalpha[t] = <Lambda_{t+1}, Delta_t>_F           dL/dalpha (Appendix E keeps gate derivatives)
+ *   dW0[h]    = sum_b sum_t dY_t X_t^T              (the decay is centered on W0)
+ *   dalpha  [B, H, T] fp32 or NULL; other arguments as in gradlev_scan_bwd. */
+int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates,
+                           const float* W0, const void* X, const void* G,
+                           const float* eta, float eta_scalar, const void* dY,
+                           float* gtilde, float* dX, float* dG, float* deta,
+                           float* dalpha, float* dW0, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* Gated deployment step: score with the current weights, then write with
+ * centered decay,
+ *   y[s,h,:]  = W[s,h] x[s,h,:]            (W[s,h] replaced by W0[h] first if reset[s])
+ *   W[s,h]   <- W0[h] + alpha[s,h] (W[s,h] - W0[h]) - eta[s,h] g[s,h,:] x[s,h,:]^T
+ *   W0     [H, d_out, d_in] fp32 slow weights
+ *   alpha  [S, H] fp32 or NULL (then alpha_scalar)
+ *   reset  [S] uint8 or NULL: 1 = this step starts a new document
+ * Other arguments and supported sizes as in gradlev_decode_step. */
+int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
+                              float* W, const float* W0, const float* x,
+                              const float* g, const float* eta, float eta_scalar,
+                              const float* alpha, float alpha_scalar,
+                              const uint8_t* reset, float* y, void* stream);
+
 /* Kernel timing for benchmarks and tracing.  While a family's bit is set in
  * the mask given to gradlev_timing_enable (bit f = family f; 0 turns timing
  * off), every launch of that family is bracketed by HIP events recorded on the
@@ -182,7 +251,11 @@ enum {
   GRADLEV_K_BWD_MAIN = 3,  /* chunked backward scan                        */
   GRADLEV_K_BWD_DW0 = 4,   /* batch reduction of dW0                       */
   GRADLEV_K_DECODE = 5,    /* deployment step                              */
-  GRADLEV_K_COUNT = 6
+  GRADLEV_K_GATED_AGG = 6, /* gated scans: per-segment aggregates          */
+  GRADLEV_K_GATED_FWD = 7, /* gated forward scan                           */
+  GRADLEV_K_GATED_STATES = 8, /* gated backward: chunk-start states        */
+  GRADLEV_K_GATED_BWD = 9, /* gated backward scan                          */
+  GRADLEV_K_COUNT = 10
 };
 int gradlev_timing_enable(int mask); /* returns the previous mask */
 int gradlev_timing_reset(void);

@@ -44,6 +44,11 @@ class Plan(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
+class Gates(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_void_p), ("alpha_scalar", ctypes.c_float),
+                ("reset", ctypes.c_void_p)]
+
+
 class GradLevError(RuntimeError):
     def __init__(self, code, what):
         super().__init__(f"{what}: {error_string(code)} (status {code})")
@@ -73,11 +78,21 @@ def lib():
                                        vp, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_decode_step.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p,
                                           ctypes.c_float, f32p, vp]
+        gp = ctypes.POINTER(Gates)
+        L.gradlev_scan_gated_workspace_bytes.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(ctypes.c_size_t)]
+        L.gradlev_scan_fwd_gated.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
+                                             f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_bwd_gated.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
+                                             vp, f32p, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_decode_step_gated.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p, f32p,
+                                                ctypes.c_float, f32p, ctypes.c_float, vp, f32p, vp]
         L.gradlev_timing_enable.argtypes = [ctypes.c_int]
         L.gradlev_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]
         for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd",
-                     "gradlev_scan_bwd", "gradlev_decode_step", "gradlev_timing_enable",
+                     "gradlev_scan_bwd", "gradlev_decode_step", "gradlev_scan_gated_workspace_bytes",
+                     "gradlev_scan_fwd_gated", "gradlev_scan_bwd_gated", "gradlev_decode_step_gated",
+                     "gradlev_timing_enable",
                      "gradlev_timing_reset", "gradlev_timing_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -257,10 +272,132 @@ def decode_step(W, x, g, eta=0.1, *, out=None):
 
 
 # ---------------------------------------------------------------------------
+# Gated scans: retention alpha and document resets
+# ---------------------------------------------------------------------------
+
+def gated_workspace_bytes(shape: Shape) -> int:
+    n = ctypes.c_size_t(0)
+    rc = lib().gradlev_scan_gated_workspace_bytes(ctypes.byref(shape), ctypes.byref(n))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_gated_workspace_bytes")
+    return int(n.value)
+
+
+def _gates(alpha, reset, B, H, T, X, name="alpha", alpha_shape=None):
+    torch = _torch()
+    g = Gates()
+    if isinstance(alpha, torch.Tensor):
+        _check_dev(name, alpha, torch.float32, alpha_shape or (B, H, T))
+        g.alpha, g.alpha_scalar = alpha.data_ptr(), 0.0
+    else:
+        g.alpha, g.alpha_scalar = None, float(alpha)
+    if reset is not None:
+        _check_dev("reset", reset, torch.uint8, (B, T) if alpha_shape is None else (B,))
+        g.reset = reset.data_ptr()
+    else:
+        g.reset = None
+    return g
+
+
+def _gated_ws(shape, device, workspace):
+    torch = _torch()
+    need = gated_workspace_bytes(shape)
+    if need == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def scan_fwd_gated(W0, X, G, eta=0.1, alpha=1.0, reset=None, *, chunk=0, segment=0, out=None,
+                   workspace=None):
+    """Gated forward scan (retention alpha: float or fp32 [B,H,T]; reset: uint8 [B,T] or None)."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", chunk, segment)
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    if out is None:
+        out = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    _check_dev("out", out, torch.float32, (s.B, s.H, s.T, s.d_out))
+    ws, wsn = _gated_ws(s, X.device, workspace)
+    rc = lib().gradlev_scan_fwd_gated(ctypes.byref(s), ctypes.byref(gt), _ptr(W0), _ptr(X), _ptr(G), _ptr(e),
+                                      es, _ptr(out), _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_fwd_gated")
+    return out
+
+
+GATED_OUTPUTS = ("gtilde", "dx", "dg", "deta", "dalpha", "dw0")
+
+
+def scan_bwd_gated(W0, X, G, dY, eta=0.1, alpha=1.0, reset=None, *, chunk=0, segment=0,
+                   outputs=GATED_OUTPUTS, out=None, workspace=None):
+    """Backward of the gated forward scan; dict with the requested outputs (``dalpha`` [B,H,T] too)."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", chunk, segment)
+    _check_dev("dY", dY, X.dtype, (s.B, s.H, s.T, s.d_out))
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    shapes = {"gtilde": (s.B, s.H, s.T, s.d_in), "dx": (s.B, s.H, s.T, s.d_in),
+              "dg": (s.B, s.H, s.T, s.d_out), "deta": (s.B, s.H, s.T), "dalpha": (s.B, s.H, s.T),
+              "dw0": (s.H, s.d_out, s.d_in)}
+    res = dict(out or {})
+    for k in outputs:
+        if k not in shapes:
+            raise ValueError(f"unknown output {k!r}")
+        if k not in res:
+            res[k] = torch.empty(shapes[k], dtype=torch.float32, device=X.device)
+        _check_dev(k, res[k], torch.float32, shapes[k])
+    ws, wsn = _gated_ws(s, X.device, workspace)
+    rc = lib().gradlev_scan_bwd_gated(ctypes.byref(s), ctypes.byref(gt), _ptr(W0), _ptr(X), _ptr(G), _ptr(e),
+                                      es, _ptr(dY), _ptr(res.get("gtilde")), _ptr(res.get("dx")),
+                                      _ptr(res.get("dg")), _ptr(res.get("deta")), _ptr(res.get("dalpha")),
+                                      _ptr(res.get("dw0")), _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_bwd_gated")
+    return res
+
+
+def decode_step_gated(W, W0, x, g, eta=0.1, alpha=1.0, reset=None, *, out=None):
+    """Gated deployment step: y = W x (W0 after a reset), then W <- W0 + alpha (W - W0) - eta g x^T."""
+    torch = _torch()
+    _check_dev("W", W, torch.float32)
+    if W.dim() != 4:
+        raise ValueError("W must be [S, H, m, d]")
+    S, H, m, d = W.shape
+    _check_dev("W0", W0, torch.float32, (H, m, d))
+    _check_dev("x", x, torch.float32, (S, H, d))
+    _check_dev("g", g, torch.float32, (S, H, m))
+    if isinstance(eta, torch.Tensor):
+        _check_dev("eta", eta, torch.float32, (S, H))
+        e, es = eta, 0.0
+    else:
+        e, es = None, float(eta)
+    if isinstance(alpha, torch.Tensor):
+        _check_dev("alpha", alpha, torch.float32, (S, H))
+        a, as_ = alpha, 0.0
+    else:
+        a, as_ = None, float(alpha)
+    if reset is not None:
+        _check_dev("reset", reset, torch.uint8, (S,))
+    if out is None:
+        out = torch.empty(S, H, m, dtype=torch.float32, device=W.device)
+    _check_dev("out", out, torch.float32, (S, H, m))
+    rc = lib().gradlev_decode_step_gated(S, H, d, m, _ptr(W), _ptr(W0), _ptr(x), _ptr(g), _ptr(e), es,
+                                         _ptr(a), as_, _ptr(reset), _ptr(out), _stream(W.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_decode_step_gated")
+    return out
+
+
+# ---------------------------------------------------------------------------
 # Kernel timing (HIP events recorded by the library around each launch)
 # ---------------------------------------------------------------------------
 
-KERNELS = ("fwd_agg", "fwd_main", "bwd_agg", "bwd_main", "bwd_dw0", "decode")
+KERNELS = ("fwd_agg", "fwd_main", "bwd_agg", "bwd_main", "bwd_dw0", "decode",
+           "gated_agg", "gated_fwd", "gated_states", "gated_bwd")
 
 
 def timing_enable(on: bool = True, kernels=None) -> int:
@@ -294,6 +431,8 @@ def timing_read() -> dict:
     return out
 
 
-__all__ = ["timing_enable", "timing_reset", "timing_read", "KERNELS", "scan_fwd", "scan_bwd", "decode_step", "plan", "workspace_bytes", "make_shape",
+__all__ = ["timing_enable", "timing_reset", "timing_read", "KERNELS", "scan_fwd", "scan_bwd", "decode_step",
+           "scan_fwd_gated", "scan_bwd_gated", "decode_step_gated", "gated_workspace_bytes", "Gates",
+           "GATED_OUTPUTS", "plan", "workspace_bytes", "make_shape",
            "error_string", "lib", "GradLevError", "Shape", "Plan", "F32", "BF16",
            "EXCLUSIVE", "INCLUSIVE", "BWD_OUTPUTS"]

@@ -95,6 +95,54 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   return GRADLEV_OK;
 }
 
+// Gated plan: tile lengths of the gated kernels, segments picked as for the
+// unit-retention scans, and the workspace layout of GatedPtrs.
+struct GatedPlan {
+  ScanProblem fwd, bwd;
+  size_t ws_fwd, ws_bwd;
+  size_t off_A, off_B, off_Bu, off_D, off_S;  // backward layout (forward: A then D)
+};
+
+int make_gated_plan(const gradlev_shape* s, GatedPlan* out) {
+  Plan base;
+  const int rc = make_plan(s, &base);
+  if (rc != GRADLEV_OK) return rc;
+  if (s->prefix != GRADLEV_EXCLUSIVE) return GRADLEV_ERR_UNSUPPORTED;
+  const int64_t BH = s->B * s->H;
+  const size_t md = (size_t)s->d_out * s->d_in * sizeof(float);
+  const int bf = s->in_dtype == GRADLEV_BF16;
+  const int d = (int)s->d_in, m = (int)s->d_out;
+  for (int k = 0; k < 2; ++k) {
+    ScanProblem& q = k == 0 ? out->fwd : out->bwd;
+    q = k == 0 ? base.fwd : base.bwd;
+    q.chunk = k == 0 ? gated_fwd_chunk(bf, d, m) : gated_bwd_chunk(bf, d, m);
+    const int64_t sc = pick_nseg(BH, s->T, q.chunk, gated_wgs_per_cu(k == 0, bf, d, m), s->segment);
+    q.seg_len = sc * q.chunk;
+    q.nseg = (s->T + q.seg_len - 1) / q.seg_len;
+    if (q.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
+  }
+  // The backward addresses one sequence's chunk-start states with 32-bit
+  // buffer offsets: ceil(T / chunk) * m * d * 4 < 2^31.
+  const int64_t nchunk = (s->T + out->bwd.chunk - 1) / out->bwd.chunk;
+  if (nchunk > ((int64_t(1) << 31) - 1) / (int64_t)md) return GRADLEV_ERR_UNSUPPORTED;
+  const size_t nf = (size_t)BH * out->fwd.nseg, nb = (size_t)BH * out->bwd.nseg;
+  out->ws_fwd = out->fwd.nseg > 1 ? round_up(nf * md, 256) + round_up(nf * 4, 256) : 0;
+  const size_t nch = (size_t)BH * ((s->T + out->bwd.chunk - 1) / out->bwd.chunk);
+  out->off_A = 0;
+  out->off_B = round_up(nb * md, 256);
+  out->off_Bu = out->off_B + round_up(nb * md, 256);
+  out->off_D = out->off_Bu + round_up(nb * md, 256);
+  out->off_S = out->off_D + round_up(nb * 4, 256);
+  out->ws_bwd = out->off_S + round_up(nch * md, 256);
+  return GRADLEV_OK;
+}
+
+int check_gates(const gradlev_gates* g) {
+  if (!g) return GRADLEV_ERR_INVALID;
+  if (g->alpha && !aligned16(g->alpha)) return GRADLEV_ERR_ALIGN;
+  return GRADLEV_OK;
+}
+
 int check_workspace(void* ws, size_t have, size_t need) {
   if (need == 0) return GRADLEV_OK;
   if (!ws || have < need) return GRADLEV_ERR_WORKSPACE;
@@ -115,7 +163,7 @@ const char* gradlev_error_string(int code) {
   switch (code) {
     case GRADLEV_OK: return "success";
     case GRADLEV_ERR_INVALID: return "invalid argument (null pointer, non-positive size or unknown enum)";
-    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64 giving at most 16 segments)";
+    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64 giving at most 16 segments; gated scans read exclusively)";
     case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
     case GRADLEV_ERR_HIP: return "HIP launch failed";
@@ -201,6 +249,109 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, con
   b.aggB = reinterpret_cast<float*>(ws + p.off_aggB);
   b.rfin = reinterpret_cast<float*>(ws + p.off_rfin);
   const hipError_t e = launch_scan_bwd(p.bwd, b, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
+  if (!bytes) return GRADLEV_ERR_INVALID;
+  GatedPlan p;
+  const int rc = make_gated_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  *bytes = p.ws_fwd > p.ws_bwd ? p.ws_fwd : p.ws_bwd;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
+                           const void* X, const void* G, const float* eta, float eta_scalar, float* Y,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  GatedPlan p;
+  int rc = make_gated_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  rc = check_gates(gates);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
+  if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
+    return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.ws_fwd);
+  if (rc != GRADLEV_OK) return rc;
+  GatedPtrs f{};
+  f.W0 = W0;
+  f.X = X;
+  f.G = G;
+  f.eta = eta;
+  f.eta_scalar = eta_scalar;
+  f.alpha = gates->alpha;
+  f.alpha_scalar = gates->alpha_scalar;
+  f.reset = gates->reset;
+  f.Y = Y;
+  if (p.fwd.nseg > 1) {
+    char* ws = static_cast<char*>(workspace);
+    const size_t nf = (size_t)(s->B * s->H) * p.fwd.nseg;
+    f.aggA = reinterpret_cast<float*>(ws);
+    f.aggD = reinterpret_cast<float*>(ws + round_up(nf * (size_t)s->d_out * s->d_in * sizeof(float), 256));
+  }
+  const hipError_t e = launch_scan_fwd_gated(p.fwd, f, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
+                           const void* X, const void* G, const float* eta, float eta_scalar,
+                           const void* dY, float* gtilde, float* dX, float* dG, float* deta,
+                           float* dalpha, float* dW0, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  GatedPlan p;
+  int rc = make_gated_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  rc = check_gates(gates);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
+  if (!gtilde && !dX && !dG && !deta && !dalpha && !dW0) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dalpha, dW0};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.ws_bwd);
+  if (rc != GRADLEV_OK) return rc;
+  char* ws = static_cast<char*>(workspace);
+  GatedPtrs b{};
+  b.W0 = W0;
+  b.X = X;
+  b.G = G;
+  b.dY = dY;
+  b.eta = eta;
+  b.eta_scalar = eta_scalar;
+  b.alpha = gates->alpha;
+  b.alpha_scalar = gates->alpha_scalar;
+  b.reset = gates->reset;
+  b.gtilde = gtilde;
+  b.dX = dX;
+  b.dG = dG;
+  b.deta = deta;
+  b.dalpha = dalpha;
+  b.dW0 = dW0;
+  b.aggA = reinterpret_cast<float*>(ws + p.off_A);
+  b.aggB = reinterpret_cast<float*>(ws + p.off_B);
+  b.aggBu = reinterpret_cast<float*>(ws + p.off_Bu);
+  b.aggD = reinterpret_cast<float*>(ws + p.off_D);
+  b.states = reinterpret_cast<float*>(ws + p.off_S);
+  const hipError_t e = launch_scan_bwd_gated(p.bwd, b, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out, float* W,
+                              const float* W0, const float* x, const float* g, const float* eta,
+                              float eta_scalar, const float* alpha, float alpha_scalar,
+                              const uint8_t* reset, float* y, void* stream) {
+  if (S < 1 || H < 1 || d_in < 1 || d_out < 1) return GRADLEV_ERR_INVALID;
+  if (!W || !W0 || !x || !g || !y) return GRADLEV_ERR_INVALID;
+  if (d_in != 16 && d_in != 32 && d_in != 64 && d_in != 128 && d_in != 256) return GRADLEV_ERR_UNSUPPORTED;
+  if (d_out > 1024) return GRADLEV_ERR_UNSUPPORTED;
+  if (S > kMaxElems / H || S * H > 0x7fffffff) return GRADLEV_ERR_UNSUPPORTED;
+  if (!aligned16(W) || !aligned16(W0) || !aligned16(x) || !aligned16(g) || !aligned16(y) ||
+      (eta && !aligned16(eta)) || (alpha && !aligned16(alpha)))
+    return GRADLEV_ERR_ALIGN;
+  DecodeGates gt{W0, alpha, alpha_scalar, reset};
+  const hipError_t e = launch_decode(S, H, (int)d_in, (int)d_out, W, x, g, eta, eta_scalar, y,
+                                     static_cast<hipStream_t>(stream), &gt);
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }
 

@@ -44,6 +44,47 @@ struct BwdPtrs {
   float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
 };
 
+// Gated scans (retention and resets).  Workspace: segment aggregates
+// A_k = sum eta_s (prod_{s<j<end} alpha_j) g_s x_s^T, B_k = sum (prod_{start<=j<u}
+// alpha_j) dY_u x_u^T, Bu_k = sum dY_u x_u^T (all [m][d]), the segment decays
+// D_k = prod alpha, and for the backward the state at every chunk start.
+struct GatedPtrs {
+  const float* W0;
+  const void* X;
+  const void* G;
+  const void* dY;
+  const float* eta;
+  float eta_scalar;
+  const float* alpha;
+  float alpha_scalar;
+  const uint8_t* reset;
+  float* Y;
+  float* gtilde;
+  float* dX;
+  float* dG;
+  float* deta;
+  float* dalpha;
+  float* dW0;
+  float* aggA;    // [B*H][nseg][m][d]
+  float* aggB;    // [B*H][nseg][m][d] (backward)
+  float* aggBu;   // [B*H][nseg][m][d] (backward)
+  float* aggD;    // [B*H][nseg]
+  float* states;  // [B*H][ceil(T/chunk)][m*d] (backward), in the backward's register order
+};
+
+struct DecodeGates {
+  const float* W0;
+  const float* alpha;
+  float alpha_scalar;
+  const uint8_t* reset;
+};
+
+int gated_fwd_chunk(int bf16, int d, int m);
+int gated_bwd_chunk(int bf16, int d, int m);
+int gated_wgs_per_cu(int fwd, int bf16, int d, int m);
+hipError_t launch_scan_fwd_gated(const ScanProblem& p, const GatedPtrs& a, hipStream_t s);
+hipError_t launch_scan_bwd_gated(const ScanProblem& p, const GatedPtrs& a, hipStream_t s);
+
 // Tile lengths each kernel family supports for a shape (LDS budget).
 int fwd_chunk_for(int bf16, int d, int m, int requested);
 int bwd_chunk_for(int bf16, int d, int m, int requested);
@@ -59,6 +100,6 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& a, hipStream_t s
 hipError_t launch_scan_bwd(const ScanProblem& p, const BwdPtrs& a, hipStream_t s);
 hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const float* x,
                          const float* g, const float* eta, float eta_scalar, float* y,
-                         hipStream_t s);
+                         hipStream_t s, const DecodeGates* gates = nullptr);
 
 }  // namespace gradlev

@@ -154,6 +154,39 @@ def eta_tokens(B, H, T, seed, lo=0.0, hi=0.2):
     return rng.uniform(lo, hi, size=(B, H, T)).astype(np.float32)
 
 
+def gate_tokens(B, H, T, d, seed, a_mean=1.5, a_std=0.5, mu_max=4.0, b_std=0.5):
+    """Per-token retention and step size from the paper's gate family.
+
+    alpha = sigmoid(a) and eta = (mu_max / d) sigmoid(b) (Section 3, "Practical
+    architecture and training"), with the logits drawn around the values the
+    paper starts from: a ~ N(1.5, 0.5^2) (the toy of Appendix D uses a bias of
+    1.5) and b ~ N(log(0.9 / 3.1), 0.5^2) (write strength starting at 0.9 with
+    mu_max = 4, Appendix E).  Returns (alpha, eta) as fp32 [B, H, T].
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    a = rng.normal(a_mean, a_std, size=(B, H, T))
+    b = rng.normal(np.log(0.9 / 3.1), b_std, size=(B, H, T))
+    alpha = 1.0 / (1.0 + np.exp(-a))
+    eta = mu_max / d / (1.0 + np.exp(-b))
+    return alpha.astype(np.float32), eta.astype(np.float32)
+
+
+def reset_flags(B, T, seed, mean_len=300):
+    """Document starts for packed rows: uint8 [B, T], 1 where a document begins.
+
+    Document lengths are geometric with the given mean (a packed stream of
+    variable-length documents); token 0 always starts one.
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    r = np.zeros((B, T), np.uint8)
+    for b in range(B):
+        t = 0
+        while t < T:
+            r[b, t] = 1
+            t += int(rng.geometric(1.0 / mean_len))
+    return r
+
+
 def decode_initial_state(wl: DecodeWorkload, S=None):
     S = wl.S if S is None else S
     rng = np.random.Generator(np.random.PCG64(wl.seed))

@@ -148,3 +148,46 @@ def test_binding_refuses_cpu_tensors(L):
     W0 = torch.zeros(1, 64, 64)
     with pytest.raises(ValueError, match="ROCm GPU"):
         gl.scan_fwd(W0, X, G, 0.1)
+
+
+# ---------------------------------------------------------------------------
+# Gated entry points
+# ---------------------------------------------------------------------------
+
+def gates(alpha=None, scalar=0.9, reset=None):
+    g = gl.Gates()
+    g.alpha, g.alpha_scalar, g.reset = alpha, scalar, reset
+    return g
+
+
+def test_gated_workspace_covers_states(L):
+    s = shape(B=2, H=4, T=300)
+    n = gl.gated_workspace_bytes(s)
+    # the backward keeps one fp32 m x d state per chunk start (chunks of at most 64 tokens)
+    assert n >= 2 * 4 * ((300 + 63) // 64) * 64 * 64 * 4
+    with pytest.raises(gl.GradLevError) as e:
+        gl.gated_workspace_bytes(shape(prefix="inclusive"))
+    assert e.value.code == gl.ERR_UNSUPPORTED
+
+
+def test_gated_validation_before_launch(L):
+    s = shape()
+    g = gates()
+    fwd = gl.lib().gradlev_scan_fwd_gated
+    bwd = gl.lib().gradlev_scan_bwd_gated
+    assert fwd(ctypes.byref(s), None, FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, 1 << 40, None) == gl.ERR_INVALID
+    assert fwd(ctypes.byref(s), ctypes.byref(gates(alpha=MISALIGNED)), FAKE, FAKE, FAKE, None, 0.1, FAKE,
+               FAKE, 1 << 40, None) == gl.ERR_ALIGN
+    assert fwd(ctypes.byref(s), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE, None, 0, None) == gl.ERR_WORKSPACE
+    si = shape(prefix="inclusive")
+    assert fwd(ctypes.byref(si), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, 1 << 40, None) == gl.ERR_UNSUPPORTED
+    outs = (None,) * 6
+    assert bwd(ctypes.byref(s), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE, *outs, FAKE, 1 << 40, None) == gl.ERR_INVALID
+    outs = (None, None, None, None, MISALIGNED, None)
+    assert bwd(ctypes.byref(s), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE, *outs, FAKE, 1 << 40, None) == gl.ERR_ALIGN
+    outs = (None, None, None, None, FAKE, None)
+    assert bwd(ctypes.byref(s), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE, *outs, FAKE, 1024, None) == gl.ERR_WORKSPACE
+    dec = gl.lib().gradlev_decode_step_gated
+    assert dec(4, 16, 64, 64, FAKE, None, FAKE, FAKE, None, 0.1, None, 0.9, None, FAKE, None) == gl.ERR_INVALID
+    assert dec(4, 16, 64, 64, FAKE, FAKE, FAKE, FAKE, None, 0.1, MISALIGNED, 0.9, None, FAKE, None) == gl.ERR_ALIGN
+    assert dec(4, 16, 48, 64, FAKE, FAKE, FAKE, FAKE, None, 0.1, None, 0.9, None, FAKE, None) == gl.ERR_UNSUPPORTED
