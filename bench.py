@@ -329,24 +329,77 @@ def secondary_scan(gl, torch, W, name, steps, warmup, device):
     return res
 
 
-def secondary_decode(gl, torch, W, device):
+def secondary_gated(gl, torch, W, device, steps=5, warmup=1):
+    """Gated fwd+bwd (retention, per-token gates, packed-document resets) on the
+    lm-bf16 shape, every gradient including dalpha."""
+    wl = W.SCAN_WORKLOADS["lm-bf16"]
+    B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
+    inp = W.device_scan_inputs(wl, 0, device, torch=torch)
+    a, e = W.gate_tokens(B, H, T, d, wl.seed + 11)
+    alpha = torch.from_numpy(a).to(device)
+    eta = torch.from_numpy(e).to(device)
+    reset = torch.from_numpy(W.reset_flags(B, T, wl.seed + 12, mean_len=512)).to(device)
+    shape = gl.make_shape(B, H, T, d, m, gl.BF16)
+    ws = torch.empty(max(gl.gated_workspace_bytes(shape), 256), dtype=torch.uint8, device=device)
+    f32 = dict(dtype=torch.float32, device=device)
+    Y = torch.empty(B, H, T, m, **f32)
+    outs = {"gtilde": torch.empty(B, H, T, d, **f32), "dx": torch.empty(B, H, T, d, **f32),
+            "dg": torch.empty(B, H, T, m, **f32), "deta": torch.empty(B, H, T, **f32),
+            "dalpha": torch.empty(B, H, T, **f32), "dw0": torch.empty(H, m, d, **f32)}
+
+    def fn(_=0):
+        gl.scan_fwd_gated(inp["W0"], inp["X"], inp["G"], eta, alpha, reset, out=Y, workspace=ws)
+        gl.scan_bwd_gated(inp["W0"], inp["X"], inp["G"], inp["dY"], eta, alpha, reset, out=outs, workspace=ws)
+    for _ in range(warmup):
+        fn()
+    ms, _ = graph_timed(torch, gl, fn, steps, kernels=[])
+    _, k = graph_timed(torch, gl, fn, steps,
+                       kernels=["gated_agg", "gated_fwd", "gated_states", "gated_bwd", "bwd_dw0"])
+    # Algorithmic bytes: x, g (and dY) in bf16, alpha and eta per token; outputs fp32
+    # (y; gtilde, dX, dG, deta, dalpha).  Flops as the unit-retention scan.
+    nbytes = B * H * T * (2 * (d + m) + 8 + 4 * m + 2 * (d + 2 * m) + 8 + 4 * (2 * d + m) + 8)
+    flops = B * H * T * (flops_fwd(d, m, 64) + flops_bwd(d, m, 32))
+    res = {"workload": "lm-bf16 shape, gated: alpha = sigmoid(N(1.5, 0.5^2)), eta = 4/d sigmoid(N(log(0.9/3.1), 0.5^2)) "
+                       "per token, documents of geometric length (mean 512) packed per row",
+           "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3),
+           "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9, "frac_hbm_peak": nbytes / (ms * 1e-3) / PEAK_HBM,
+           "tflops_algorithmic": flops / (ms * 1e-3) / 1e12,
+           "kernel_avg_us": {n: round(v[0], 2) for n, v in k.items() if v[0] is not None}}
+    del inp, outs, Y, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
+    """Decode steps of the decode-f32 workload (optionally more sequences, fewer
+    steps, or the gated update with per-state retention)."""
     wl = W.DECODE_WORKLOADS["decode-f32"]
-    S, H, d, m, n = wl.S, wl.H, wl.d, wl.m, wl.steps
+    S = wl.S if S is None else S
+    n = wl.steps if steps is None else steps
+    H, d, m = wl.H, wl.d, wl.m
     gen = torch.Generator(device=device)
     gen.manual_seed(wl.seed)
     state = (torch.randn(S, H, m, d, device=device, generator=gen) * wl.w_std).contiguous()
     xs = (torch.randn(n, S, H, d, device=device, generator=gen) * wl.x_std).contiguous()
     gs = (torch.randn(n, S, H, m, device=device, generator=gen) * wl.g_std).contiguous()
     ys = torch.empty(n, S, H, m, device=device)
+    if gated:
+        W0 = (torch.randn(H, m, d, device=device, generator=gen) * wl.w_std).contiguous()
+        alpha = torch.sigmoid(1.5 + 0.5 * torch.randn(S, H, device=device, generator=gen)).contiguous()
 
     def run_all(_=0):
         for t in range(n):
-            gl.decode_step(state, xs[t], gs[t], wl.eta, out=ys[t])
+            if gated:
+                gl.decode_step_gated(state, W0, xs[t], gs[t], wl.eta, alpha, out=ys[t])
+            else:
+                gl.decode_step(state, xs[t], gs[t], wl.eta, out=ys[t])
 
-    per_step_bytes = 4 * (2 * S * H * m * d + S * H * (d + m) + S * H * m)
+    # W read and written, x, g read, y written (gated: alpha read too; W0 is
+    # H matrices shared by every sequence and stays in cache).
+    per_step_bytes = 4 * (2 * S * H * m * d + S * H * (d + m) + S * H * m) + (4 * S * H if gated else 0)
     run_all()  # warm-up
     torch.cuda.synchronize()
-    mode = "hip graph of 512 launches"
+    mode = f"hip graph of {n} launches"
     try:
         ms, _ = graph_timed(torch, gl, lambda i: run_all(), 1, kernels=[])
         _, k = graph_timed(torch, gl, lambda i: run_all(), 1, kernels=["decode"])
@@ -361,7 +414,7 @@ def secondary_decode(gl, torch, W, device):
         k = kernel_avgs(gl)
     step_us = ms * 1e3 / n
     kern_us = k["decode"][0]
-    res = {"mode": mode, "us_per_step": step_us,
+    res = {"mode": mode, "S": S, "steps": n, "us_per_step": step_us,
            "seq_tokens_per_s": S * n / (ms * 1e-3),
            "hbm_GBps_algorithmic": per_step_bytes / (step_us * 1e-6) / 1e9,
            "frac_hbm_peak": per_step_bytes / (step_us * 1e-6) / PEAK_HBM,
@@ -474,8 +527,14 @@ def main():
         for name in ("long-bf16", "stack-bf16"):
             log(f"secondary {name}")
             sec[name] = secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
+        log("secondary lm-bf16-gated")
+        sec["lm-bf16-gated"] = secondary_gated(gl, torch, W, device)
         log("secondary decode-f32")
         sec["decode-f32"] = secondary_decode(gl, torch, W, device)
+        log("secondary decode-f32 with 2048 sequences (state larger than the MALL)")
+        sec["decode-f32-S2048"] = secondary_decode(gl, torch, W, device, S=2048, steps=64)
+        log("secondary decode-f32 gated")
+        sec["decode-f32-gated"] = secondary_decode(gl, torch, W, device, gated=True)
         result["secondary"] = sec
 
     if not args.no_cpu_baseline:

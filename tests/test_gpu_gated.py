@@ -159,3 +159,29 @@ def test_gated_decode(d, m, alpha_kind, with_reset):
         yr, Wr = orc.decode_step(Wr, x, g, eta, alpha=al, W0=W0)
         check("y", to_host(y), yr, "f32")
     check("W", to_host(Wd), Wr, "f32")
+
+
+@pytest.mark.timeout(300)
+def test_gated_lm_bf16_config():
+    """The lm-bf16 shape with the paper's gate family and packed-document
+    resets at full size; the oracle checks every output of sampled heads."""
+    wl = W.SCAN_WORKLOADS["lm-bf16"]
+    B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
+    log("gated lm-bf16 config: drawing inputs on the device")
+    inp = W.device_scan_inputs(wl, 0, "cuda", torch=torch)
+    a, e = W.gate_tokens(B, H, T, d, wl.seed + 11)
+    rs = W.reset_flags(B, T, wl.seed + 12, mean_len=512)
+    ad, ed, rd = (torch.from_numpy(v).to("cuda") for v in (a, e, rs))
+    out = {"y": gl.scan_fwd_gated(inp["W0"], inp["X"], inp["G"], ed, ad, rd)}
+    out.update(gl.scan_bwd_gated(inp["W0"], inp["X"], inp["G"], inp["dY"], ed, ad, rd))
+    torch.cuda.synchronize()
+    for h in (2, 13):
+        log(f"  oracle on head h={h} (all {B} batch rows, T={T})")
+        sl = {"W0": to_host(inp["W0"][h:h + 1]), "X": to_host(inp["X"][:, h:h + 1]),
+              "G": to_host(inp["G"][:, h:h + 1]), "dY": to_host(inp["dY"][:, h:h + 1]),
+              "eta": e[:, h:h + 1].astype(np.float64), "alpha": a[:, h:h + 1].astype(np.float64),
+              "reset": rs}
+        ref = oracle_all(sl)
+        for k in ("y", "gtilde", "dx", "dg", "deta", "dalpha"):
+            check(k, to_host(out[k][:, h:h + 1]), ref[k], "bf16")
+        check("dw0", to_host(out["dw0"][h:h + 1]), ref["dw0"], "bf16")
