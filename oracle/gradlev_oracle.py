@@ -37,6 +37,12 @@ What is computed (GradLev, arXiv 2609.34174):
   scales the suffix), and the gate gradient is dalpha_t = <Lambda_{t+1},
   Delta_t>_F (Appendix E keeps gate derivatives).  Without alpha every
   retention is one and the arithmetic is the plain prefix sum above.
+* Two-map online MLP (Appendix A): z = W1 x, h = sigma(z), y = W2 h, both
+  maps written with the shared retention and eta_1 = mu / d, eta_2 = mu / m.
+  Given costate proposals the forward is two exclusive scans in layer order;
+  the reverse target of the hidden layer is sigma'(z) times the transpose
+  read of the second scan (mlp_fwd, mlp_reverse), and the serial learner it
+  must reproduce is mlp_serial.
 * Resets (Section 3, Eq. 2 holds within each reset segment): a token flagged
   as a reset reads W_0 again, i.e. Delta_t = 0.  That is the same as a zero
   retention and a zero step size at the token before it, which is how the
@@ -246,6 +252,120 @@ def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE, alpha=None, reset=None):
     if alpha is not None:
         out["dalpha"] = dalpha * keep
     return out
+
+
+# ---------------------------------------------------------------------------
+# Two-map online MLP (Appendix A): z = W1 x, h = sigma(z), y = W2 h
+# ---------------------------------------------------------------------------
+
+ACTS = ("tanh", "gelu")
+
+
+def act(z, kind):
+    """sigma(z): tanh, or GELU written with the Gaussian CDF (erf form)."""
+    if kind == "tanh":
+        return np.tanh(z)
+    if kind == "gelu":
+        from scipy.special import erf
+        return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+    raise ValueError(kind)
+
+
+def act_grad(z, kind):
+    """sigma'(z)."""
+    if kind == "tanh":
+        return 1.0 - np.tanh(z) ** 2
+    if kind == "gelu":
+        from scipy.special import erf
+        return 0.5 * (1.0 + erf(z / np.sqrt(2.0))) + z * np.exp(-0.5 * z * z) / np.sqrt(2.0 * np.pi)
+    raise ValueError(kind)
+
+
+def round_bf16(a):
+    """Nearest bfloat16 value (ties to even), as float64; for hidden
+    activations stored in bf16 between the two scans."""
+    f = np.asarray(a, np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def mlp_serial(W10, W20, X, C, alpha, mu, kind="tanh"):
+    """Serial test-time training of the two-map MLP on l_t = |y_t - c_t|^2 / 2.
+
+    Appendix A, Eqs. for the online forward, reverse and simultaneous writes:
+    both gradients use the pre-update weights, eta_1 = mu / d, eta_2 = mu / m,
+    centered decay with the shared retention.  One sequence: X [T, d],
+    C [T, o], alpha and mu [T].  Returns y, h, z, the costates g_y = y - c,
+    g_z = sigma'(z) * W2^T g_y and g_x = W1^T g_z, and the first-matrix
+    gradients g_z x^T [T, m, d].
+    """
+    W10, W20, X, C = (_as_array(a) for a in (W10, W20, X, C))
+    a, mu = _as_array(alpha), _as_array(mu)
+    T, d = X.shape
+    m = W10.shape[0]
+    W1, W2 = W10.copy(), W20.copy()
+    out = {k: [] for k in ("y", "h", "z", "gy", "gz", "gx", "dW1")}
+    for t in range(T):
+        x = X[t]
+        z = W1 @ x
+        h = act(z, kind)
+        y = W2 @ h
+        gy = y - C[t]
+        gz = act_grad(z, kind) * (W2.T @ gy)
+        gx = W1.T @ gz
+        W1 = W10 + a[t] * (W1 - W10) - (mu[t] / d) * np.outer(gz, x)
+        W2 = W20 + a[t] * (W2 - W20) - (mu[t] / m) * np.outer(gy, h)
+        for k, v in (("y", y), ("h", h), ("z", z), ("gy", gy), ("gz", gz), ("gx", gx),
+                     ("dW1", np.outer(gz, x))):
+            out[k].append(v)
+    return {k: np.array(v) for k, v in out.items()}
+
+
+def mlp_fwd(W10, W20, X, Gz, Gy, alpha, mu, kind="tanh", hidden_bf16=False, reset=None):
+    """Parallel forward of Appendix A with costate proposals: z_hat by the
+    first exclusive scan, h_hat = sigma(z_hat), y_hat by the second scan.
+
+    Batched like the scans: W10 [H, m, d], W20 [H, o, m], X [B, H, T, d],
+    Gz [B, H, T, m], Gy [B, H, T, o], alpha and mu scalars or [B, H, T].
+    hidden_bf16 rounds h_hat to bfloat16 before the second scan (the storage
+    of a bf16 pipeline).  Returns dict(z, h, y).
+    """
+    X = _as_array(X)
+    B, H, T, d = X.shape
+    m = _as_array(W10).shape[1]
+    e1 = _as_array(mu) / d
+    e2 = _as_array(mu) / m
+    z = scan_fwd(W10, X, Gz, e1, alpha=alpha, reset=reset)
+    h = act(z, kind)
+    if hidden_bf16:
+        h = round_bf16(h)
+    y = scan_fwd(W20, h, Gy, e2, alpha=alpha, reset=reset)
+    return {"z": z, "h": h, "y": y}
+
+
+def mlp_reverse(W10, W20, X, Gz, Gy, alpha, mu, gy, kind="tanh", hidden_bf16=False,
+                slow_transpose=False, reset=None):
+    """Reconstructed costates of Appendix A (Eq. for the reverse targets):
+    g_z = sigma'(z_hat) * (W2_0 + Delta2_hat_t)^T g_y, a transpose read of the
+    second scan queried by the output costate g_y [B, H, T, o], and the input
+    costate g_x = (W1_0 + Delta1_hat_t)^T g_z.  slow_transpose keeps only W2_0
+    (the control of Section 5.1).  Returns dict(z, h, gh, gz, gx).
+    """
+    f = mlp_fwd(W10, W20, X, Gz, Gy, alpha, mu, kind, hidden_bf16, reset)
+    X = _as_array(X)
+    B, H, T, d = X.shape
+    m = _as_array(W10).shape[1]
+    e1 = _as_array(mu) / d
+    e2 = _as_array(mu) / m
+    gy = _as_array(gy)
+    if slow_transpose:
+        gh = np.einsum("hom,bhto->bhtm", _as_array(W20), gy)
+    else:
+        gh = scan_bwd(W20, f["h"], Gy, e2, gy, alpha=alpha, reset=reset)["gtilde"]
+    gz = act_grad(f["z"], kind) * gh
+    gx = scan_bwd(W10, X, Gz, e1, gz, alpha=alpha, reset=reset)["gtilde"]
+    return {"z": f["z"], "h": f["h"], "gh": gh, "gz": gz, "gx": gx}
 
 
 def outer_sum(A, Bm, w, lo, hi):

@@ -535,3 +535,90 @@ def test_retention_dw0_is_plain_product():
     W0, X, G, e, dY = rand_problem(3, 2, 9, 4, 5, seed=54)
     out = orc.scan_bwd(W0, X, G, e, dY, alpha=rand_alpha(3, 2, 9, 55))
     assert rel_err(out["dw0"], np.einsum("bhtm,bhtd->hmd", dY, X)) < 1e-13
+
+
+# --------------------------------------------------------------------------
+# Two-map online MLP (Appendix A) and the FP64 recovery experiment
+# (Section 5.1, Appendix B): tests/golden/mlp_toy.json
+# --------------------------------------------------------------------------
+
+def _toy(seed):
+    rng = np.random.default_rng(seed)
+    W10 = rng.normal(0, 0.5 / np.sqrt(4), (7, 4))
+    W20 = rng.normal(0, 0.5 / np.sqrt(7), (3, 7))
+    va, vm = rng.normal(0, 0.25, 4), rng.normal(0, 0.25, 4)
+    X, C = rng.standard_normal((32, 4)), rng.standard_normal((32, 3))
+    al = 1 / (1 + np.exp(-(X @ va + 1.5)))
+    mu = 1 / (1 + np.exp(-(X @ vm - 0.2)))
+    return W10, W20, X, C, al, mu
+
+
+def test_mlp_toy_recovers_serial_ttt(golden_dir):
+    """Serial TTT supplies exact costates; the parallel scans reproduce its
+    outputs, hidden costates, input costates and first-matrix gradients at
+    rounding level, and the slow-transpose control misses by O(0.1-1)."""
+    gd = json.load(open(os.path.join(golden_dir, "mlp_toy.json")))
+    paper, ctrl = gd["paper_max_abs_error"], gd["paper_slow_transpose_control"]
+    worst = {"y": 0.0, "gz": 0.0, "gx": 0.0, "dW1": 0.0}
+    cworst = {"gz": 0.0, "dW1": 0.0, "y": 0.0}
+    for seed in gd["protocol"]["seeds"]:
+        W10, W20, X, C, al, mu = _toy(seed)
+        ser = orc.mlp_serial(W10, W20, X, C, al, mu)
+        b = lambda a: a[None, None]  # noqa: E731
+        f = orc.mlp_fwd(W10[None], W20[None], b(X), b(ser["gz"]), b(ser["gy"]), b(al), b(mu))
+        gy = f["y"][0, 0] - C           # the reverse target from the scanned output
+        r = orc.mlp_reverse(W10[None], W20[None], b(X), b(ser["gz"]), b(ser["gy"]), b(al), b(mu), b(gy))
+        rc = orc.mlp_reverse(W10[None], W20[None], b(X), b(ser["gz"]), b(ser["gy"]), b(al), b(mu), b(gy),
+                             slow_transpose=True)
+        worst["y"] = max(worst["y"], np.max(np.abs(f["y"][0, 0] - ser["y"])))
+        worst["gz"] = max(worst["gz"], np.max(np.abs(r["gz"][0, 0] - ser["gz"])))
+        worst["gx"] = max(worst["gx"], np.max(np.abs(r["gx"][0, 0] - ser["gx"])))
+        dW1 = np.einsum("tm,td->tmd", r["gz"][0, 0], X)
+        worst["dW1"] = max(worst["dW1"], np.max(np.abs(dW1 - ser["dW1"])))
+        cworst["gz"] = max(cworst["gz"], np.max(np.abs(rc["gz"][0, 0] - ser["gz"])))
+        cworst["dW1"] = max(cworst["dW1"], np.max(np.abs(np.einsum("tm,td->tmd", rc["gz"][0, 0], X) - ser["dW1"])))
+        cworst["y"] = max(cworst["y"], np.max(np.abs(rc["h"][0, 0] - ser["h"])))
+    # Rounding level: within a few ulps of the paper's maxima.
+    assert worst["y"] <= 4 * paper["outputs"]
+    assert worst["gz"] <= 4 * paper["hidden_costates"]
+    assert worst["dW1"] <= 4 * paper["first_matrix_gradients"]
+    assert worst["gx"] <= 1e-15
+    # The control changes only the reverse: same forward, gradients off by the
+    # paper's order of magnitude.
+    assert cworst["y"] <= 4 * paper["outputs"]
+    for k, name in (("gz", "hidden_costates"), ("dW1", "first_matrix_gradients")):
+        assert ctrl[name] / 10 <= cworst[k] <= 10 * ctrl[name], (k, cworst[k])
+
+
+def test_mlp_with_unit_gates_is_two_scans():
+    """alpha = 1, constant mu: the MLP forward is the plain scans of the two maps."""
+    rng = np.random.default_rng(60)
+    B, H, T, d, m, o = 2, 2, 9, 4, 5, 3
+    W10, W20 = rng.standard_normal((H, m, d)), rng.standard_normal((H, o, m))
+    X = rng.standard_normal((B, H, T, d))
+    Gz, Gy = rng.standard_normal((B, H, T, m)), rng.standard_normal((B, H, T, o))
+    f = orc.mlp_fwd(W10, W20, X, Gz, Gy, 1.0, 0.6)
+    z = closed_form_fwd(W10, X, Gz, 0.6 / d, orc.EXCLUSIVE)
+    np.testing.assert_allclose(f["z"], z, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(f["y"], closed_form_fwd(W20, np.tanh(z), Gy, 0.6 / m, orc.EXCLUSIVE),
+                               rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", orc.ACTS)
+def test_activation_derivatives(kind):
+    z = np.linspace(-4, 4, 41)
+    h = 1e-6
+    fd = (orc.act(z + h, kind) - orc.act(z - h, kind)) / (2 * h)
+    np.testing.assert_allclose(orc.act_grad(z, kind), fd, rtol=0, atol=1e-8)
+    if kind == "gelu":
+        # GELU(z) - GELU(-z) = z, GELU(0) = 0, GELU -> z for large z
+        np.testing.assert_allclose(orc.act(z, kind) - orc.act(-z, kind), z, atol=1e-15)
+        assert orc.act(np.array(0.0), kind) == 0.0
+        np.testing.assert_allclose(orc.act(np.array(10.0), kind), 10.0, rtol=1e-15)
+
+
+def test_bf16_rounding_of_hidden_activations():
+    v = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -7, -2.5, 3.0 + 2 ** -6 + 2 ** -9, 0.0])
+    r = orc.round_bf16(v)
+    # representable values are kept; ties go to the even mantissa
+    np.testing.assert_array_equal(r, [1.0, 1.0, 1.0 + 2 ** -6, 1.0 + 2 ** -7, -2.5, 3.0 + 2 ** -6 + 2 ** -9 - 2 ** -9, 0.0])
