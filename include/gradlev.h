@@ -184,7 +184,8 @@ int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
  *
  * Only the exclusive read is supported (GRADLEV_ERR_UNSUPPORTED otherwise),
  * and one sequence's chunk-start states must stay under 2 GiB:
- * ceil(T / 32) * d_in * d_out * 4 < 2^31 (T below 2^20 at 128 x 128). */
+ * ceil(T / chunk) * d_in * d_out * 4 < 2^31 with the backward's chunk of 32
+ * tokens (64 for bf16 64 x 64 maps): T below 2^20 at 128 x 128. */
 typedef struct gradlev_gates {
   const float* alpha;
   float alpha_scalar;
@@ -232,6 +233,58 @@ int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                               const float* g, const float* eta, float eta_scalar,
                               const float* alpha, float alpha_scalar,
                               const uint8_t* reset, float* y, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Two-map online MLP (Appendix A)
+ * ------------------------------------------------------------------------
+ *   z_t = W1_t x_t,   h_t = sigma(z_t),   y_t = W2_t h_t,
+ * both maps written with centered decay, the shared retention alpha_t and the
+ * shared write strength mu_t divided by each map's input width:
+ *   eta_1 = mu_t / d_in,   eta_2 = mu_t / hidden.
+ * Given costate proposals g_z (for W1) and g_y (for W2) the forward is two
+ * gated exclusive scans in layer order, and the reverse target of the hidden
+ * layer is sigma'(z_hat) times the transpose read of the second scan,
+ *   g_z~ = sigma'(z_hat_t) (W2_0 + Delta2_t)^T g_y~,
+ * optionally continued to the input: g_x~ = (W1_0 + Delta1_t)^T g_z~. */
+enum { GRADLEV_ACT_TANH = 0, GRADLEV_ACT_GELU = 1 /* z Phi(z), erf form */ };
+
+/* d_in, hidden, d_out in {64, 128}; in_dtype is the storage of X, Gz, Gy,
+ * the hidden activations between the scans and gY; segment as in
+ * gradlev_shape; act a GRADLEV_ACT_* value. */
+typedef struct gradlev_mlp_shape {
+  int64_t B, H, T, d_in, hidden, d_out;
+  int64_t segment;
+  int32_t in_dtype;
+  int32_t act;
+} gradlev_mlp_shape;
+
+/* Workspace for gradlev_mlp_fwd and gradlev_mlp_reverse (same rules as
+ * gradlev_scan_workspace_bytes). */
+int gradlev_mlp_workspace_bytes(const gradlev_mlp_shape* s, size_t* bytes);
+
+/* Forward.
+ *   W1_0 [H, hidden, d_in], W2_0 [H, d_out, hidden] fp32 slow weights
+ *   X [B,H,T,d_in], Gz [B,H,T,hidden], Gy [B,H,T,d_out]   in_dtype
+ *   mu [B,H,T] fp32 or NULL (then mu_scalar)
+ *   Z   [B,H,T,hidden] fp32 out: z_hat
+ *   Hid [B,H,T,hidden] in_dtype out: h_hat = sigma(z_hat) as stored for the second scan
+ *   Y   [B,H,T,d_out]  fp32 out: y_hat */
+int gradlev_mlp_fwd(const gradlev_mlp_shape* s, const gradlev_gates* gates,
+                    const float* W1_0, const float* W2_0, const void* X,
+                    const void* Gz, const void* Gy, const float* mu, float mu_scalar,
+                    float* Z, void* Hid, float* Y, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Reverse targets, from the forward's Z and Hid and the output costate
+ *   gY [B,H,T,d_out] in_dtype.
+ *   gZ [B,H,T,hidden] fp32 out: g_z~
+ *   gX [B,H,T,d_in]   fp32 out or NULL: g_x~ (the hidden target is stored in
+ *                     in_dtype before it queries the first scan) */
+int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates,
+                        const float* W1_0, const float* W2_0, const void* X,
+                        const void* Gz, const void* Gy, const float* mu, float mu_scalar,
+                        const float* Z, const void* Hid, const void* gY, float* gZ,
+                        float* gX, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Kernel timing for benchmarks and tracing.  While a family's bit is set in
  * the mask given to gradlev_timing_enable (bit f = family f; 0 turns timing

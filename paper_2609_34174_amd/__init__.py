@@ -49,6 +49,15 @@ class Gates(ctypes.Structure):
                 ("reset", ctypes.c_void_p)]
 
 
+class MlpShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("H", ctypes.c_int64), ("T", ctypes.c_int64),
+                ("d_in", ctypes.c_int64), ("hidden", ctypes.c_int64), ("d_out", ctypes.c_int64),
+                ("segment", ctypes.c_int64), ("in_dtype", ctypes.c_int32), ("act", ctypes.c_int32)]
+
+
+ACT = {"tanh": 0, "gelu": 1}
+
+
 class GradLevError(RuntimeError):
     def __init__(self, code, what):
         super().__init__(f"{what}: {error_string(code)} (status {code})")
@@ -86,12 +95,19 @@ def lib():
                                              vp, f32p, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_decode_step_gated.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p, f32p,
                                                 ctypes.c_float, f32p, ctypes.c_float, vp, f32p, vp]
+        mp = ctypes.POINTER(MlpShape)
+        L.gradlev_mlp_workspace_bytes.argtypes = [mp, ctypes.POINTER(ctypes.c_size_t)]
+        L.gradlev_mlp_fwd.argtypes = [mp, gp, f32p, f32p, vp, vp, vp, f32p, ctypes.c_float,
+                                      f32p, vp, f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_mlp_reverse.argtypes = [mp, gp, f32p, f32p, vp, vp, vp, f32p, ctypes.c_float,
+                                          f32p, vp, vp, f32p, f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_timing_enable.argtypes = [ctypes.c_int]
         L.gradlev_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]
         for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd",
                      "gradlev_scan_bwd", "gradlev_decode_step", "gradlev_scan_gated_workspace_bytes",
                      "gradlev_scan_fwd_gated", "gradlev_scan_bwd_gated", "gradlev_decode_step_gated",
+                     "gradlev_mlp_workspace_bytes", "gradlev_mlp_fwd", "gradlev_mlp_reverse",
                      "gradlev_timing_enable",
                      "gradlev_timing_reset", "gradlev_timing_read"):
             getattr(L, name).restype = ctypes.c_int
@@ -393,6 +409,84 @@ def decode_step_gated(W, W0, x, g, eta=0.1, alpha=1.0, reset=None, *, out=None):
 
 
 # ---------------------------------------------------------------------------
+# Two-map online MLP
+# ---------------------------------------------------------------------------
+
+def _mlp_shape(W10, W20, X, Gz, Gy, act, segment):
+    torch = _torch()
+    _check_dev("X", X)
+    if X.dim() != 4:
+        raise ValueError("X must be [B, H, T, d_in]")
+    B, H, T, d = X.shape
+    if X.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError("X must be float32 or bfloat16")
+    _check_dev("W1_0", W10, torch.float32)
+    if W10.dim() != 3 or W10.shape[0] != H or W10.shape[2] != d:
+        raise ValueError("W1_0 must be [H, hidden, d_in]")
+    hid = W10.shape[1]
+    _check_dev("W2_0", W20, torch.float32)
+    if W20.dim() != 3 or W20.shape[0] != H or W20.shape[2] != hid:
+        raise ValueError("W2_0 must be [H, d_out, hidden]")
+    o = W20.shape[1]
+    _check_dev("Gz", Gz, X.dtype, (B, H, T, hid))
+    _check_dev("Gy", Gy, X.dtype, (B, H, T, o))
+    return MlpShape(B, H, T, d, hid, o, int(segment), BF16 if X.dtype == torch.bfloat16 else F32, ACT[act])
+
+
+def _mlp_ws(s, device, workspace):
+    torch = _torch()
+    n = ctypes.c_size_t(0)
+    rc = lib().gradlev_mlp_workspace_bytes(ctypes.byref(s), ctypes.byref(n))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_mlp_workspace_bytes")
+    need = max(int(n.value), 256)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def mlp_fwd(W10, W20, X, Gz, Gy, mu=0.9, alpha=1.0, reset=None, *, act="tanh", segment=0, workspace=None):
+    """Two-map MLP forward from costate proposals; returns (Z fp32, Hid in X's dtype, Y fp32)."""
+    torch = _torch()
+    s = _mlp_shape(W10, W20, X, Gz, Gy, act, segment)
+    m, ms = _eta_args(mu, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    Z = torch.empty(s.B, s.H, s.T, s.hidden, dtype=torch.float32, device=X.device)
+    Hid = torch.empty(s.B, s.H, s.T, s.hidden, dtype=X.dtype, device=X.device)
+    Y = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    ws, wsn = _mlp_ws(s, X.device, workspace)
+    rc = lib().gradlev_mlp_fwd(ctypes.byref(s), ctypes.byref(gt), _ptr(W10), _ptr(W20), _ptr(X), _ptr(Gz),
+                               _ptr(Gy), _ptr(m), ms, _ptr(Z), _ptr(Hid), _ptr(Y), _ptr(ws), wsn,
+                               _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_mlp_fwd")
+    return Z, Hid, Y
+
+
+def mlp_reverse(W10, W20, X, Gz, Gy, Z, Hid, gY, mu=0.9, alpha=1.0, reset=None, *, act="tanh",
+                with_gx=True, segment=0, workspace=None):
+    """Reverse targets of the MLP: returns (gZ, gX or None), fp32."""
+    torch = _torch()
+    s = _mlp_shape(W10, W20, X, Gz, Gy, act, segment)
+    _check_dev("Z", Z, torch.float32, (s.B, s.H, s.T, s.hidden))
+    _check_dev("Hid", Hid, X.dtype, (s.B, s.H, s.T, s.hidden))
+    _check_dev("gY", gY, X.dtype, (s.B, s.H, s.T, s.d_out))
+    m, ms = _eta_args(mu, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    gZ = torch.empty(s.B, s.H, s.T, s.hidden, dtype=torch.float32, device=X.device)
+    gX = torch.empty(s.B, s.H, s.T, s.d_in, dtype=torch.float32, device=X.device) if with_gx else None
+    ws, wsn = _mlp_ws(s, X.device, workspace)
+    rc = lib().gradlev_mlp_reverse(ctypes.byref(s), ctypes.byref(gt), _ptr(W10), _ptr(W20), _ptr(X), _ptr(Gz),
+                                   _ptr(Gy), _ptr(m), ms, _ptr(Z), _ptr(Hid), _ptr(gY), _ptr(gZ), _ptr(gX),
+                                   _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_mlp_reverse")
+    return gZ, gX
+
+
+# ---------------------------------------------------------------------------
 # Kernel timing (HIP events recorded by the library around each launch)
 # ---------------------------------------------------------------------------
 
@@ -433,6 +527,6 @@ def timing_read() -> dict:
 
 __all__ = ["timing_enable", "timing_reset", "timing_read", "KERNELS", "scan_fwd", "scan_bwd", "decode_step",
            "scan_fwd_gated", "scan_bwd_gated", "decode_step_gated", "gated_workspace_bytes", "Gates",
-           "GATED_OUTPUTS", "plan", "workspace_bytes", "make_shape",
+           "GATED_OUTPUTS", "mlp_fwd", "mlp_reverse", "MlpShape", "ACT", "plan", "workspace_bytes", "make_shape",
            "error_string", "lib", "GradLevError", "Shape", "Plan", "F32", "BF16",
            "EXCLUSIVE", "INCLUSIVE", "BWD_OUTPUTS"]

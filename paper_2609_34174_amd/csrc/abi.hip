@@ -143,6 +143,67 @@ int check_gates(const gradlev_gates* g) {
   return GRADLEV_OK;
 }
 
+// The two scans of the MLP, as gated scan shapes.
+int make_mlp_shapes(const gradlev_mlp_shape* m, gradlev_shape* s1, gradlev_shape* s2) {
+  if (!m) return GRADLEV_ERR_INVALID;
+  if (m->act != GRADLEV_ACT_TANH && m->act != GRADLEV_ACT_GELU) return GRADLEV_ERR_INVALID;
+  *s1 = gradlev_shape{m->B, m->H, m->T, m->d_in, m->hidden, 0, m->segment, m->in_dtype, GRADLEV_EXCLUSIVE};
+  *s2 = gradlev_shape{m->B, m->H, m->T, m->hidden, m->d_out, 0, m->segment, m->in_dtype, GRADLEV_EXCLUSIVE};
+  return GRADLEV_OK;
+}
+
+struct MlpPlan {
+  GatedPlan p1, p2;
+  size_t scan_ws;  // the larger of the two scans' workspaces (they run in turn)
+  size_t off_q;    // in_dtype copy of the hidden target (reverse with gX)
+  size_t total;
+};
+
+int make_mlp_plan(const gradlev_mlp_shape* m, MlpPlan* out) {
+  gradlev_shape s1, s2;
+  int rc = make_mlp_shapes(m, &s1, &s2);
+  if (rc != GRADLEV_OK) return rc;
+  rc = make_gated_plan(&s1, &out->p1);
+  if (rc != GRADLEV_OK) return rc;
+  rc = make_gated_plan(&s2, &out->p2);
+  if (rc != GRADLEV_OK) return rc;
+  size_t w = out->p1.ws_fwd;
+  for (size_t v : {out->p1.ws_bwd, out->p2.ws_fwd, out->p2.ws_bwd}) w = v > w ? v : w;
+  out->scan_ws = round_up(w, 256);
+  out->off_q = out->scan_ws;
+  const size_t es = m->in_dtype == GRADLEV_BF16 ? 2 : 4;
+  out->total = out->off_q + round_up((size_t)(m->B * m->H * m->T * m->hidden) * es, 256);
+  return GRADLEV_OK;
+}
+
+GatedPtrs gated_ptrs(const GatedPlan& p, const gradlev_gates* g, const float* W0, const void* X,
+                     const void* G, const float* mu, float mu_scalar, float eta_mul, void* ws, bool bwd,
+                     int64_t BH) {
+  GatedPtrs f{};
+  f.W0 = W0;
+  f.X = X;
+  f.G = G;
+  f.eta = mu;
+  f.eta_scalar = mu_scalar;
+  f.eta_mul = eta_mul;
+  f.alpha = g->alpha;
+  f.alpha_scalar = g->alpha_scalar;
+  f.reset = g->reset;
+  char* w = static_cast<char*>(ws);
+  if (bwd) {
+    f.aggA = reinterpret_cast<float*>(w + p.off_A);
+    f.aggB = reinterpret_cast<float*>(w + p.off_B);
+    f.aggBu = reinterpret_cast<float*>(w + p.off_Bu);
+    f.aggD = reinterpret_cast<float*>(w + p.off_D);
+    f.states = reinterpret_cast<float*>(w + p.off_S);
+  } else if (p.fwd.nseg > 1) {
+    const size_t nf = (size_t)BH * p.fwd.nseg;
+    f.aggA = reinterpret_cast<float*>(w);
+    f.aggD = reinterpret_cast<float*>(w + round_up(nf * (size_t)p.fwd.m * p.fwd.d * sizeof(float), 256));
+  }
+  return f;
+}
+
 int check_workspace(void* ws, size_t have, size_t need) {
   if (need == 0) return GRADLEV_OK;
   if (!ws || have < need) return GRADLEV_ERR_WORKSPACE;
@@ -280,6 +341,7 @@ int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
   f.G = G;
   f.eta = eta;
   f.eta_scalar = eta_scalar;
+  f.eta_mul = 1.f;
   f.alpha = gates->alpha;
   f.alpha_scalar = gates->alpha_scalar;
   f.reset = gates->reset;
@@ -319,6 +381,7 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
   b.dY = dY;
   b.eta = eta;
   b.eta_scalar = eta_scalar;
+  b.eta_mul = 1.f;
   b.alpha = gates->alpha;
   b.alpha_scalar = gates->alpha_scalar;
   b.reset = gates->reset;
@@ -335,6 +398,77 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
   b.states = reinterpret_cast<float*>(ws + p.off_S);
   const hipError_t e = launch_scan_bwd_gated(p.bwd, b, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_mlp_workspace_bytes(const gradlev_mlp_shape* s, size_t* bytes) {
+  if (!bytes) return GRADLEV_ERR_INVALID;
+  MlpPlan p;
+  const int rc = make_mlp_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  *bytes = p.total;
+  return GRADLEV_OK;
+}
+
+int gradlev_mlp_fwd(const gradlev_mlp_shape* s, const gradlev_gates* gates, const float* W1_0,
+                    const float* W2_0, const void* X, const void* Gz, const void* Gy, const float* mu,
+                    float mu_scalar, float* Z, void* Hid, float* Y, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  MlpPlan p;
+  int rc = make_mlp_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  rc = check_gates(gates);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W1_0 || !W2_0 || !X || !Gz || !Gy || !Z || !Hid || !Y) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W1_0, W2_0, X, Gz, Gy, mu, Z, Hid, Y};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.total);
+  if (rc != GRADLEV_OK) return rc;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t BH = s->B * s->H;
+  GatedPtrs f1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, false, BH);
+  f1.Y = Z;
+  if (launch_scan_fwd_gated(p.p1.fwd, f1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  if (launch_act_fwd(s->in_dtype == GRADLEV_BF16, Z, Hid, BH * s->T * s->hidden, s->act, st) != hipSuccess)
+    return GRADLEV_ERR_HIP;
+  GatedPtrs f2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, false, BH);
+  f2.Y = Y;
+  if (launch_scan_fwd_gated(p.p2.fwd, f2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  return GRADLEV_OK;
+}
+
+int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates, const float* W1_0,
+                        const float* W2_0, const void* X, const void* Gz, const void* Gy, const float* mu,
+                        float mu_scalar, const float* Z, const void* Hid, const void* gY, float* gZ,
+                        float* gX, void* workspace, size_t workspace_bytes, void* stream) {
+  MlpPlan p;
+  int rc = make_mlp_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  rc = check_gates(gates);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W1_0 || !W2_0 || !X || !Gz || !Gy || !Z || !Hid || !gY || !gZ) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W1_0, W2_0, X, Gz, Gy, mu, Z, Hid, gY, gZ, gX};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.total);
+  if (rc != GRADLEV_OK) return rc;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t BH = s->B * s->H;
+  // Transpose read of the second scan: g_h = (W2_0 + Delta2_t)^T gY, written into gZ.
+  GatedPtrs b2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, true, BH);
+  b2.dY = gY;
+  b2.gtilde = gZ;
+  if (launch_scan_bwd_gated(p.p2.bwd, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  void* q = gX ? static_cast<void*>(static_cast<char*>(workspace) + p.off_q) : nullptr;
+  if (launch_act_bwd(s->in_dtype == GRADLEV_BF16, Z, gZ, q, BH * s->T * s->hidden, s->act, st) != hipSuccess)
+    return GRADLEV_ERR_HIP;
+  if (gX) {
+    GatedPtrs b1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, true, BH);
+    b1.dY = q;
+    b1.gtilde = gX;
+    if (launch_scan_bwd_gated(p.p1.bwd, b1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  }
+  return GRADLEV_OK;
 }
 
 int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out, float* W,

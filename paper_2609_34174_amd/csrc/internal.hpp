@@ -55,6 +55,7 @@ struct GatedPtrs {
   const void* dY;
   const float* eta;
   float eta_scalar;
+  float eta_mul;  // step size = eta_mul * (eta ? eta[t] : eta_scalar)
   const float* alpha;
   float alpha_scalar;
   const uint8_t* reset;
@@ -78,6 +79,10 @@ struct DecodeGates {
   float alpha_scalar;
   const uint8_t* reset;
 };
+
+// Two-map MLP elementwise stages (n values, a multiple of 4).
+hipError_t launch_act_fwd(int bf16, const float* Z, void* H, int64_t n, int kind, hipStream_t s);
+hipError_t launch_act_bwd(int bf16, const float* Z, float* G, void* Gq, int64_t n, int kind, hipStream_t s);
 
 int gated_fwd_chunk(int bf16, int d, int m);
 int gated_bwd_chunk(int bf16, int d, int m);

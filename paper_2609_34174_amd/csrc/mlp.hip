@@ -1,0 +1,88 @@
+// Elementwise stages of the two-map online MLP (Appendix A): the hidden
+// activation between the two scans, h = sigma(z), and the reverse target of
+// the hidden layer, g_z = sigma'(z) * g_h.  Both are pure streams (a few
+// flops per 8-16 bytes), so each thread handles 4 consecutive values with
+// 16-byte accesses in a grid-stride loop.
+#include "../../include/gradlev.h"
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace gradlev {
+
+// tanh, or GELU in its Gaussian-CDF form z * Phi(z).
+__device__ __forceinline__ float act_value(float z, int kind) {
+  if (kind == GRADLEV_ACT_TANH) return tanhf(z);
+  return 0.5f * z * (1.f + erff(z * 0.70710678118654752f));
+}
+__device__ __forceinline__ float act_slope(float z, int kind) {
+  if (kind == GRADLEV_ACT_TANH) {
+    const float t = tanhf(z);
+    return 1.f - t * t;
+  }
+  // Phi(z) + z phi(z), phi the standard normal density.
+  return 0.5f * (1.f + erff(z * 0.70710678118654752f)) + z * expf(-0.5f * z * z) * 0.39894228040143268f;
+}
+
+template <typename E>
+__device__ __forceinline__ void store4e(E* p, f32x4 v);
+template <>
+__device__ __forceinline__ void store4e<float>(float* p, f32x4 v) {
+  *reinterpret_cast<f32x4*>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store4e<bf16>(bf16* p, f32x4 v) {
+  bf16x4 o;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) o[r] = (bf16)v[r];
+  *reinterpret_cast<bf16x4*>(p) = o;
+}
+
+template <typename E>
+__global__ void __launch_bounds__(256)
+act_fwd_kernel(const float* __restrict__ Z, E* __restrict__ H, int64_t n4, int kind) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const f32x4 z = *reinterpret_cast<const f32x4*>(Z + 4 * i);
+    f32x4 h;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) h[r] = act_value(z[r], kind);
+    store4e<E>(H + 4 * i, h);
+  }
+}
+
+template <typename E>
+__global__ void __launch_bounds__(256)
+act_bwd_kernel(const float* __restrict__ Z, float* __restrict__ G, E* __restrict__ Gq, int64_t n4, int kind) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const f32x4 z = *reinterpret_cast<const f32x4*>(Z + 4 * i);
+    f32x4 g = *reinterpret_cast<const f32x4*>(G + 4 * i);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) g[r] *= act_slope(z[r], kind);
+    *reinterpret_cast<f32x4*>(G + 4 * i) = g;
+    if (Gq) store4e<E>(Gq + 4 * i, g);
+  }
+}
+
+static unsigned act_grid(int64_t n4) {
+  const int64_t b = (n4 + 255) / 256;
+  return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
+}
+
+hipError_t launch_act_fwd(int is_bf16, const float* Z, void* H, int64_t n, int kind, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (is_bf16)
+    hipLaunchKernelGGL(act_fwd_kernel<bf16>, dim3(act_grid(n4)), dim3(256), 0, s, Z, static_cast<bf16*>(H), n4, kind);
+  else
+    hipLaunchKernelGGL(act_fwd_kernel<float>, dim3(act_grid(n4)), dim3(256), 0, s, Z, static_cast<float*>(H), n4, kind);
+  return hipGetLastError();
+}
+
+hipError_t launch_act_bwd(int is_bf16, const float* Z, float* G, void* Gq, int64_t n, int kind, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (is_bf16)
+    hipLaunchKernelGGL(act_bwd_kernel<bf16>, dim3(act_grid(n4)), dim3(256), 0, s, Z, G, static_cast<bf16*>(Gq), n4, kind);
+  else
+    hipLaunchKernelGGL(act_bwd_kernel<float>, dim3(act_grid(n4)), dim3(256), 0, s, Z, G, static_cast<float*>(Gq), n4, kind);
+  return hipGetLastError();
+}
+
+}  // namespace gradlev

@@ -43,7 +43,7 @@ struct GArgs {
   const void* G;
   const void* dY;
   const float* eta;
-  float eta_scalar;
+  float eta_scalar, eta_mul;
   const float* alpha;
   float alpha_scalar;
   const uint8_t* reset;
@@ -69,7 +69,7 @@ struct GArgs {
 // ---------------------------------------------------------------------------
 struct GateSrc {
   rsrc_t al, et, rs;
-  float a_s, e_s;
+  float a_s, e_s, e_mul;
   bool has_a, has_e, has_r;
 };
 
@@ -84,6 +84,7 @@ __device__ __forceinline__ GateSrc gate_src(const GArgs& a, int64_t bh) {
   g.rs = make_rsrc(g.has_r ? a.reset + (bh / a.H) * T : nullptr, g.has_r ? (uint32_t)T : 0u);
   g.a_s = a.alpha_scalar;
   g.e_s = a.eta_scalar;
+  g.e_mul = a.eta_mul;
   return g;
 }
 
@@ -94,7 +95,7 @@ struct GateReg {
     const bool mine = ok && tid < C;
     const uint32_t o = mine ? (uint32_t)(t0 + tid) : kOOB;
     a = g.has_a ? buf_load1(g.al, o == kOOB ? kOOB : 4 * o) : g.a_s;
-    e = g.has_e ? buf_load1(g.et, o == kOOB ? kOOB : 4 * o) : g.e_s;
+    e = g.e_mul * (g.has_e ? buf_load1(g.et, o == kOOB ? kOOB : 4 * o) : g.e_s);
     // Reset flag of the next token (past the sequence end the load reads 0).
     r = g.has_r ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(g.rs, o == kOOB ? kOOB : (int)(o + 1), 0, 0) : 0u;
   }
@@ -920,7 +921,9 @@ reduce_gated_dw0_kernel(const float* __restrict__ Bu, float* __restrict__ dW0, i
 // Host side
 // ---------------------------------------------------------------------------
 int gated_fwd_chunk(int, int, int) { return 64; }
-int gated_bwd_chunk(int, int, int) { return 32; }
+// The backward's LDS holds five C x C split tiles besides the chunk inputs and
+// the published Lambda: 64-token tiles fit for bf16 64 x 64 maps only.
+int gated_bwd_chunk(int bf16, int d, int m) { return (bf16 && d == 64 && m == 64) ? 64 : 32; }
 
 static constexpr int lds_gated_bwd(int es, int lo, int d, int m, int C) {
   return es * (C * d + 3 * C * m + lo * C * m + (1 + lo) * 5 * C * C + (1 + lo) * d * m) +
@@ -934,7 +937,7 @@ int gated_wgs_per_cu(int fwd, int bf16, int d, int m) {
     const int es = bf16 ? 2 : 4;
     n = 160 * 1024 / (es * 64 * (d + 2 * m + (bf16 ? m : 0)) + 1024);
   } else {
-    n = 160 * 1024 / lds_gated_bwd(bf16 ? 2 : 4, bf16 ? 1 : 0, d, m, 32);
+    n = 160 * 1024 / lds_gated_bwd(bf16 ? 2 : 4, bf16 ? 1 : 0, d, m, gated_bwd_chunk(bf16, d, m));
   }
   if (n * waves > 8) n = 8 / waves;
   return n < 1 ? 1 : n;
@@ -948,6 +951,7 @@ static GArgs gargs(const ScanProblem& p, const GatedPtrs& f) {
   k.dY = f.dY;
   k.eta = f.eta;
   k.eta_scalar = f.eta_scalar;
+  k.eta_mul = f.eta_mul;
   k.alpha = f.alpha;
   k.alpha_scalar = f.alpha_scalar;
   k.reset = f.reset;
@@ -986,10 +990,9 @@ static hipError_t fwd_gated_dims(const ScanProblem& p, const GArgs& k, hipStream
   return hipGetLastError();
 }
 
-template <class OP, int D, int M>
-static hipError_t bwd_gated_dims(const ScanProblem& p, const GArgs& k, float* dW0, hipStream_t s) {
+template <class OP, int D, int M, int C>
+static hipError_t bwd_gated_dims_c(const ScanProblem& p, const GArgs& k, float* dW0, hipStream_t s) {
   constexpr int NT = cmax(D, M) / 16 * 64;
-  constexpr int C = 32;
   const unsigned grid = (unsigned)seg_grid(k.BH, p.nseg);
   timing_begin(GRADLEV_K_GATED_AGG, s);
   hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, C, true>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
@@ -1008,6 +1011,14 @@ static hipError_t bwd_gated_dims(const ScanProblem& p, const GArgs& k, float* dW
     timing_end(GRADLEV_K_BWD_DW0, s);
   }
   return hipGetLastError();
+}
+
+template <class OP, int D, int M>
+static hipError_t bwd_gated_dims(const ScanProblem& p, const GArgs& k, float* dW0, hipStream_t s) {
+  if constexpr (OP::kSplit == 2 && D == 64 && M == 64) {
+    if (p.chunk == 64) return bwd_gated_dims_c<OP, D, M, 64>(p, k, dW0, s);
+  }
+  return bwd_gated_dims_c<OP, D, M, 32>(p, k, dW0, s);
 }
 
 hipError_t launch_scan_fwd_gated(const ScanProblem& p, const GatedPtrs& f, hipStream_t s) {
