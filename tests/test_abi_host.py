@@ -191,3 +191,29 @@ def test_gated_validation_before_launch(L):
     assert dec(4, 16, 64, 64, FAKE, None, FAKE, FAKE, None, 0.1, None, 0.9, None, FAKE, None) == gl.ERR_INVALID
     assert dec(4, 16, 64, 64, FAKE, FAKE, FAKE, FAKE, None, 0.1, MISALIGNED, 0.9, None, FAKE, None) == gl.ERR_ALIGN
     assert dec(4, 16, 48, 64, FAKE, FAKE, FAKE, FAKE, None, 0.1, None, 0.9, None, FAKE, None) == gl.ERR_UNSUPPORTED
+
+
+def test_mlp_validation_before_launch(L):
+    def ms(**kw):
+        base = dict(B=2, H=2, T=100, d_in=64, hidden=128, d_out=64, segment=0, in_dtype=gl.BF16, act=0)
+        base.update(kw)
+        return gl.MlpShape(**base)
+    n = ctypes.c_size_t(0)
+    assert L.gradlev_mlp_workspace_bytes(ctypes.byref(ms()), ctypes.byref(n)) == gl.OK and n.value > 0
+    assert L.gradlev_mlp_workspace_bytes(ctypes.byref(ms(act=7)), ctypes.byref(n)) == gl.ERR_INVALID
+    assert L.gradlev_mlp_workspace_bytes(ctypes.byref(ms(hidden=96)), ctypes.byref(n)) == gl.ERR_UNSUPPORTED
+    g = gates(scalar=1.0)
+    fwd = L.gradlev_mlp_fwd
+    args = [FAKE] * 5 + [None, 0.9, FAKE, FAKE, FAKE, FAKE, 1 << 40, None]
+    bad = list(args)
+    bad[7] = None                      # Z missing
+    assert fwd(ctypes.byref(ms()), ctypes.byref(g), *bad) == gl.ERR_INVALID
+    bad = list(args)
+    bad[2] = MISALIGNED                # X misaligned
+    assert fwd(ctypes.byref(ms()), ctypes.byref(g), *bad) == gl.ERR_ALIGN
+    bad = list(args)
+    bad[11] = 16                       # workspace too small
+    assert fwd(ctypes.byref(ms()), ctypes.byref(g), *bad) == gl.ERR_WORKSPACE
+    rev = L.gradlev_mlp_reverse
+    rargs = [FAKE] * 5 + [None, 0.9, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None]
+    assert rev(ctypes.byref(ms()), ctypes.byref(g), *rargs) == gl.ERR_INVALID   # gZ missing
