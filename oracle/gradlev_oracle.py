@@ -258,16 +258,25 @@ def scan_bwd(W0, X, G, eta, dY, prefix=EXCLUSIVE, alpha=None, reset=None):
 # Two-map online MLP (Appendix A): z = W1 x, h = sigma(z), y = W2 h
 # ---------------------------------------------------------------------------
 
-ACTS = ("tanh", "gelu")
+ACTS = ("tanh", "gelu", "gelu_tanh")
+
+# Constants of the tanh approximation of GELU (Hendrycks and Gimpel, 2016):
+# GELU(z) ~ z/2 (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))).
+_GELU_K0 = np.sqrt(2.0 / np.pi)
+_GELU_K1 = 0.044715
 
 
 def act(z, kind):
-    """sigma(z): tanh, or GELU written with the Gaussian CDF (erf form)."""
+    """sigma(z): tanh; GELU written with the Gaussian CDF (erf form); or the
+    tanh-approximate GELU that the paper's backbone uses (Appendix E,
+    "Model and prefiller")."""
     if kind == "tanh":
         return np.tanh(z)
     if kind == "gelu":
         from scipy.special import erf
         return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+    if kind == "gelu_tanh":
+        return 0.5 * z * (1.0 + np.tanh(_GELU_K0 * (z + _GELU_K1 * z ** 3)))
     raise ValueError(kind)
 
 
@@ -278,6 +287,9 @@ def act_grad(z, kind):
     if kind == "gelu":
         from scipy.special import erf
         return 0.5 * (1.0 + erf(z / np.sqrt(2.0))) + z * np.exp(-0.5 * z * z) / np.sqrt(2.0 * np.pi)
+    if kind == "gelu_tanh":
+        th = np.tanh(_GELU_K0 * (z + _GELU_K1 * z ** 3))
+        return 0.5 * (1.0 + th) + 0.5 * z * (1.0 - th * th) * _GELU_K0 * (1.0 + 3.0 * _GELU_K1 * z * z)
     raise ValueError(kind)
 
 

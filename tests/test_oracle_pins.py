@@ -610,11 +610,22 @@ def test_activation_derivatives(kind):
     h = 1e-6
     fd = (orc.act(z + h, kind) - orc.act(z - h, kind)) / (2 * h)
     np.testing.assert_allclose(orc.act_grad(z, kind), fd, rtol=0, atol=1e-8)
-    if kind == "gelu":
-        # GELU(z) - GELU(-z) = z, GELU(0) = 0, GELU -> z for large z
+    if kind in ("gelu", "gelu_tanh"):
+        # GELU(z) - GELU(-z) = z, GELU(0) = 0, GELU -> z for large z (both forms)
         np.testing.assert_allclose(orc.act(z, kind) - orc.act(-z, kind), z, atol=1e-15)
         assert orc.act(np.array(0.0), kind) == 0.0
         np.testing.assert_allclose(orc.act(np.array(10.0), kind), 10.0, rtol=1e-15)
+    if kind == "gelu_tanh":
+        # The tanh form approximates z Phi(z) to within 5e-4 everywhere
+        # (largest gap near |z| = 2.7), slopes to within 1e-3; a dropped cubic
+        # term or a wrong sqrt(2/pi) factor breaks both bounds.
+        from scipy.special import erf
+        zz = np.linspace(-8, 8, 20001)
+        exact = 0.5 * zz * (1.0 + erf(zz / np.sqrt(2.0)))
+        slope = 0.5 * (1.0 + erf(zz / np.sqrt(2.0))) + zz * np.exp(-0.5 * zz * zz) / np.sqrt(2.0 * np.pi)
+        gap = np.abs(orc.act(zz, kind) - exact)
+        assert gap.max() < 5e-4 and gap.max() > 1e-4
+        assert np.abs(orc.act_grad(zz, kind) - slope).max() < 1e-3
 
 
 def test_bf16_rounding_of_hidden_activations():
