@@ -246,7 +246,10 @@ int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
  * layer is sigma'(z_hat) times the transpose read of the second scan,
  *   g_z~ = sigma'(z_hat_t) (W2_0 + Delta2_t)^T g_y~,
  * optionally continued to the input: g_x~ = (W1_0 + Delta1_t)^T g_z~. */
-enum { GRADLEV_ACT_TANH = 0, GRADLEV_ACT_GELU = 1 /* z Phi(z), erf form */ };
+/* GRADLEV_ACT_GELU_TANH is the tanh-approximate GELU,
+ *   z/2 (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))),
+ * which the paper's backbone uses (Appendix E, "Model and prefiller"). */
+enum { GRADLEV_ACT_TANH = 0, GRADLEV_ACT_GELU = 1 /* z Phi(z), erf form */, GRADLEV_ACT_GELU_TANH = 2 };
 
 /* d_in, hidden, d_out in {64, 128}; in_dtype is the storage of X, Gz, Gy,
  * the hidden activations between the scans and gY; segment as in

@@ -55,7 +55,7 @@ class MlpShape(ctypes.Structure):
                 ("segment", ctypes.c_int64), ("in_dtype", ctypes.c_int32), ("act", ctypes.c_int32)]
 
 
-ACT = {"tanh": 0, "gelu": 1}
+ACT = {"tanh": 0, "gelu": 1, "gelu_tanh": 2}
 
 
 class GradLevError(RuntimeError):

@@ -146,7 +146,7 @@ int check_gates(const gradlev_gates* g) {
 // The two scans of the MLP, as gated scan shapes.
 int make_mlp_shapes(const gradlev_mlp_shape* m, gradlev_shape* s1, gradlev_shape* s2) {
   if (!m) return GRADLEV_ERR_INVALID;
-  if (m->act != GRADLEV_ACT_TANH && m->act != GRADLEV_ACT_GELU) return GRADLEV_ERR_INVALID;
+  if (m->act != GRADLEV_ACT_TANH && m->act != GRADLEV_ACT_GELU && m->act != GRADLEV_ACT_GELU_TANH) return GRADLEV_ERR_INVALID;
   *s1 = gradlev_shape{m->B, m->H, m->T, m->d_in, m->hidden, 0, m->segment, m->in_dtype, GRADLEV_EXCLUSIVE};
   *s2 = gradlev_shape{m->B, m->H, m->T, m->hidden, m->d_out, 0, m->segment, m->in_dtype, GRADLEV_EXCLUSIVE};
   return GRADLEV_OK;

@@ -9,15 +9,23 @@
 
 namespace gradlev {
 
-// tanh, or GELU in its Gaussian-CDF form z * Phi(z).
+// tanh; GELU in its Gaussian-CDF form z * Phi(z); or the tanh-approximate
+// GELU z/2 (1 + tanh(u)), u = sqrt(2/pi) (z + 0.044715 z^3).
+constexpr float kGeluK0 = 0.79788456080286536f;  // sqrt(2/pi)
+constexpr float kGeluK1 = 0.044715f;
 __device__ __forceinline__ float act_value(float z, int kind) {
   if (kind == GRADLEV_ACT_TANH) return tanhf(z);
+  if (kind == GRADLEV_ACT_GELU_TANH) return 0.5f * z * (1.f + tanhf(kGeluK0 * (z + kGeluK1 * z * z * z)));
   return 0.5f * z * (1.f + erff(z * 0.70710678118654752f));
 }
 __device__ __forceinline__ float act_slope(float z, int kind) {
   if (kind == GRADLEV_ACT_TANH) {
     const float t = tanhf(z);
     return 1.f - t * t;
+  }
+  if (kind == GRADLEV_ACT_GELU_TANH) {
+    const float t = tanhf(kGeluK0 * (z + kGeluK1 * z * z * z));
+    return 0.5f * (1.f + t) + 0.5f * z * (1.f - t * t) * kGeluK0 * (1.f + 3.f * kGeluK1 * z * z);
   }
   // Phi(z) + z phi(z), phi the standard normal density.
   return 0.5f * (1.f + erff(z * 0.70710678118654752f)) + z * expf(-0.5f * z * z) * 0.39894228040143268f;
