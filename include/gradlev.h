@@ -311,7 +311,9 @@ enum {
   GRADLEV_K_GATED_FWD = 7, /* gated forward scan                           */
   GRADLEV_K_GATED_STATES = 8, /* gated backward: chunk-start states        */
   GRADLEV_K_GATED_BWD = 9, /* gated backward scan                          */
-  GRADLEV_K_COUNT = 10
+  GRADLEV_K_WIDE_SCORE = 10, /* wide maps: gates and causal score tiles   */
+  GRADLEV_K_WIDE_OUT = 11,   /* wide maps: W_0 term plus score-weighted sum */
+  GRADLEV_K_COUNT = 12
 };
 int gradlev_timing_enable(int mask); /* returns the previous mask */
 int gradlev_timing_reset(void);

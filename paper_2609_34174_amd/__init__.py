@@ -491,7 +491,7 @@ def mlp_reverse(W10, W20, X, Gz, Gy, Z, Hid, gY, mu=0.9, alpha=1.0, reset=None, 
 # ---------------------------------------------------------------------------
 
 KERNELS = ("fwd_agg", "fwd_main", "bwd_agg", "bwd_main", "bwd_dw0", "decode",
-           "gated_agg", "gated_fwd", "gated_states", "gated_bwd")
+           "gated_agg", "gated_fwd", "gated_states", "gated_bwd", "wide_score", "wide_out")
 
 
 def timing_enable(on: bool = True, kernels=None) -> int:

@@ -95,6 +95,66 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   return GRADLEV_OK;
 }
 
+// Wide maps: widths that are multiples of 128 with one of them above 128 run
+// the parallel form (scan_wide.hip).  Its workspace holds the gate prefixes
+// and the causal score matrix, B*H*Tp*Tp*4 bytes, so the sequence length is
+// capped; reads are exclusive (the paper's convention).
+constexpr int64_t kWideMaxWidth = 8192;
+constexpr int64_t kWideMaxT = 16384;
+
+bool wide_shape(const gradlev_shape* s) { return s && (s->d_in > 128 || s->d_out > 128); }
+
+int make_wide(const gradlev_shape* s, WideProblem* out) {
+  if (!s || !out) return GRADLEV_ERR_INVALID;
+  if (s->B < 1 || s->H < 1 || s->T < 1 || s->d_in < 1 || s->d_out < 1) return GRADLEV_ERR_INVALID;
+  if (s->in_dtype != GRADLEV_F32 && s->in_dtype != GRADLEV_BF16) return GRADLEV_ERR_INVALID;
+  if (s->prefix != GRADLEV_EXCLUSIVE && s->prefix != GRADLEV_INCLUSIVE) return GRADLEV_ERR_INVALID;
+  if (s->chunk < 0 || s->segment < 0) return GRADLEV_ERR_INVALID;
+  if (s->prefix != GRADLEV_EXCLUSIVE) return GRADLEV_ERR_UNSUPPORTED;
+  if (s->d_in % 128 != 0 || s->d_out % 128 != 0) return GRADLEV_ERR_UNSUPPORTED;
+  if (s->d_in > kWideMaxWidth || s->d_out > kWideMaxWidth || s->T > kWideMaxT) return GRADLEV_ERR_UNSUPPORTED;
+  if (s->B > kMaxElems / s->H || s->B * s->H > (int64_t(1) << 20)) return GRADLEV_ERR_UNSUPPORTED;
+  out->B = s->B;
+  out->H = s->H;
+  out->T = s->T;
+  out->Tp = (s->T + 127) / 128 * 128;
+  out->d = (int)s->d_in;
+  out->m = (int)s->d_out;
+  out->bf16 = s->in_dtype == GRADLEV_BF16;
+  out->fmode = 0;
+  // Grid sizes (work-items are counted in 32 bits) and 32-bit byte offsets
+  // within one sequence's score matrix and rows.
+  const int64_t BH = s->B * s->H, Kp = out->Tp / 128;
+  const int64_t wmax = s->d_in > s->d_out ? s->d_in : s->d_out;
+  if (BH * Kp * (wmax / 128) > (int64_t(1) << 23) || BH * 2 * Kp * (Kp + 1) > (int64_t(1) << 24))
+    return GRADLEV_ERR_UNSUPPORTED;
+  return GRADLEV_OK;
+}
+
+WidePtrs wide_ptrs(const gradlev_gates* g, const float* W0, const void* X, const void* G, const float* eta,
+                   float eta_scalar, float eta_mul, void* ws) {
+  WidePtrs f{};
+  f.W0 = W0;
+  f.X = X;
+  f.G = G;
+  f.eta = eta;
+  f.eta_scalar = eta_scalar;
+  f.eta_mul = eta_mul;
+  f.alpha = g ? g->alpha : nullptr;
+  f.alpha_scalar = g ? g->alpha_scalar : 1.f;
+  f.reset = g ? g->reset : nullptr;
+  f.ws = ws;
+  return f;
+}
+
+// Retention mode of the wide kernels: products of ones, resets only, or
+// general retentions.
+int wide_fmode(const gradlev_gates* g) {
+  if (!g) return 0;
+  if (g->alpha || g->alpha_scalar != 1.f) return 2;
+  return g->reset ? 1 : 0;
+}
+
 // Gated plan: tile lengths of the gated kernels, segments picked as for the
 // unit-retention scans, and the workspace layout of GatedPtrs.
 struct GatedPlan {
@@ -154,6 +214,8 @@ int make_mlp_shapes(const gradlev_mlp_shape* m, gradlev_shape* s1, gradlev_shape
 
 struct MlpPlan {
   GatedPlan p1, p2;
+  bool wide1, wide2;  // the scan runs the wide-map kernels (w1, w2) instead
+  WideProblem w1, w2;
   size_t scan_ws;  // the larger of the two scans' workspaces (they run in turn)
   size_t off_q;    // in_dtype copy of the hidden target (reverse with gX)
   size_t total;
@@ -163,12 +225,24 @@ int make_mlp_plan(const gradlev_mlp_shape* m, MlpPlan* out) {
   gradlev_shape s1, s2;
   int rc = make_mlp_shapes(m, &s1, &s2);
   if (rc != GRADLEV_OK) return rc;
-  rc = make_gated_plan(&s1, &out->p1);
-  if (rc != GRADLEV_OK) return rc;
-  rc = make_gated_plan(&s2, &out->p2);
-  if (rc != GRADLEV_OK) return rc;
-  size_t w = out->p1.ws_fwd;
-  for (size_t v : {out->p1.ws_bwd, out->p2.ws_fwd, out->p2.ws_bwd}) w = v > w ? v : w;
+  size_t w = 0;
+  const gradlev_shape* sh[2] = {&s1, &s2};
+  GatedPlan* gp[2] = {&out->p1, &out->p2};
+  WideProblem* wp[2] = {&out->w1, &out->w2};
+  bool* wd[2] = {&out->wide1, &out->wide2};
+  for (int k = 0; k < 2; ++k) {
+    *wd[k] = wide_shape(sh[k]);
+    size_t need;
+    if (*wd[k]) {
+      rc = make_wide(sh[k], wp[k]);
+      need = rc == GRADLEV_OK ? wide_workspace_bytes(*wp[k]) : 0;
+    } else {
+      rc = make_gated_plan(sh[k], gp[k]);
+      need = gp[k]->ws_fwd > gp[k]->ws_bwd ? gp[k]->ws_fwd : gp[k]->ws_bwd;
+    }
+    if (rc != GRADLEV_OK) return rc;
+    w = need > w ? need : w;
+  }
   out->scan_ws = round_up(w, 256);
   out->off_q = out->scan_ws;
   const size_t es = m->in_dtype == GRADLEV_BF16 ? 2 : 4;
@@ -224,7 +298,7 @@ const char* gradlev_error_string(int code) {
   switch (code) {
     case GRADLEV_OK: return "success";
     case GRADLEV_ERR_INVALID: return "invalid argument (null pointer, non-positive size or unknown enum)";
-    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out must be 64 or 128, chunk 0/64/128, segment a multiple of 64 giving at most 16 segments; gated scans read exclusively)";
+    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out 64 or 128, or multiples of 128 up to 8192 with T <= 16384 and exclusive reads for wide maps; chunk 0/64/128, segment a multiple of 64 giving at most 16 segments; gated scans read exclusively; wide maps return gtilde only from the backward)";
     case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
     case GRADLEV_ERR_HIP: return "HIP launch failed";
@@ -234,6 +308,16 @@ const char* gradlev_error_string(int code) {
 
 int gradlev_scan_plan(const gradlev_shape* s, gradlev_plan* plan) {
   if (!plan) return GRADLEV_ERR_INVALID;
+  if (wide_shape(s)) {
+    WideProblem w;
+    const int rc = make_wide(s, &w);
+    if (rc != GRADLEV_OK) return rc;
+    plan->fwd_chunk = plan->bwd_chunk = w.Tp;
+    plan->fwd_segment = plan->bwd_segment = w.Tp;
+    plan->fwd_nseg = plan->bwd_nseg = 1;
+    plan->workspace_bytes = wide_workspace_bytes(w);
+    return GRADLEV_OK;
+  }
   Plan p;
   const int rc = make_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -249,6 +333,12 @@ int gradlev_scan_plan(const gradlev_shape* s, gradlev_plan* plan) {
 
 int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
   if (!bytes) return GRADLEV_ERR_INVALID;
+  if (wide_shape(s)) {
+    WideProblem w;
+    const int rc = make_wide(s, &w);
+    if (rc == GRADLEV_OK) *bytes = wide_workspace_bytes(w);
+    return rc;
+  }
   Plan p;
   const int rc = make_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -259,6 +349,10 @@ int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
 int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
                      const float* eta, float eta_scalar, float* Y, void* workspace,
                      size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) {
+    const gradlev_gates none{nullptr, 1.f, nullptr};
+    return gradlev_scan_fwd_gated(s, &none, W0, X, G, eta, eta_scalar, Y, workspace, workspace_bytes, stream);
+  }
   Plan p;
   int rc = make_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -283,6 +377,11 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, con
                      const float* eta, float eta_scalar, const void* dY, float* gtilde,
                      float* dX, float* dG, float* deta, float* dW0, void* workspace,
                      size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) {
+    const gradlev_gates none{nullptr, 1.f, nullptr};
+    return gradlev_scan_bwd_gated(s, &none, W0, X, G, eta, eta_scalar, dY, gtilde, dX, dG, deta, nullptr, dW0,
+                                  workspace, workspace_bytes, stream);
+  }
   Plan p;
   int rc = make_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -315,6 +414,7 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, con
 
 int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
   if (!bytes) return GRADLEV_ERR_INVALID;
+  if (wide_shape(s)) return gradlev_scan_workspace_bytes(s, bytes);
   GatedPlan p;
   const int rc = make_gated_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -325,6 +425,22 @@ int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
 int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
                            const void* X, const void* G, const float* eta, float eta_scalar, float* Y,
                            void* workspace, size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) {
+    WideProblem w;
+    int rc = make_wide(s, &w);
+    if (rc != GRADLEV_OK) return rc;
+    rc = check_gates(gates);
+    if (rc != GRADLEV_OK) return rc;
+    if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
+    if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
+      return GRADLEV_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, wide_workspace_bytes(w));
+    if (rc != GRADLEV_OK) return rc;
+    w.fmode = wide_fmode(gates);
+    WidePtrs f = wide_ptrs(gates, W0, X, G, eta, eta_scalar, 1.f, workspace);
+    f.Y = Y;
+    return launch_wide_fwd(w, f, static_cast<hipStream_t>(stream)) == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+  }
   GatedPlan p;
   int rc = make_gated_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -361,6 +477,27 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
                            const void* dY, float* gtilde, float* dX, float* dG, float* deta,
                            float* dalpha, float* dW0, void* workspace, size_t workspace_bytes,
                            void* stream) {
+  if (wide_shape(s)) {
+    // Wide maps compute the transpose read (the grounded target) only.
+    WideProblem w;
+    int rc = make_wide(s, &w);
+    if (rc != GRADLEV_OK) return rc;
+    rc = check_gates(gates);
+    if (rc != GRADLEV_OK) return rc;
+    if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
+    if (!gtilde && !dX && !dG && !deta && !dalpha && !dW0) return GRADLEV_ERR_INVALID;
+    if (dX || dG || deta || dalpha || dW0) return GRADLEV_ERR_UNSUPPORTED;
+    const void* ptrs[] = {W0, X, G, dY, eta, gtilde};
+    for (const void* q : ptrs)
+      if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes, wide_workspace_bytes(w));
+    if (rc != GRADLEV_OK) return rc;
+    w.fmode = wide_fmode(gates);
+    WidePtrs f = wide_ptrs(gates, W0, X, G, eta, eta_scalar, 1.f, workspace);
+    f.dY = dY;
+    f.gtilde = gtilde;
+    return launch_wide_read(w, f, static_cast<hipStream_t>(stream)) == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+  }
   GatedPlan p;
   int rc = make_gated_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
@@ -426,14 +563,29 @@ int gradlev_mlp_fwd(const gradlev_mlp_shape* s, const gradlev_gates* gates, cons
   if (rc != GRADLEV_OK) return rc;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t BH = s->B * s->H;
-  GatedPtrs f1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, false, BH);
-  f1.Y = Z;
-  if (launch_scan_fwd_gated(p.p1.fwd, f1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  const int fm = wide_fmode(gates);
+  if (p.wide1) {
+    WidePtrs f1 = wide_ptrs(gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace);
+    f1.Y = Z;
+    p.w1.fmode = fm;
+    if (launch_wide_fwd(p.w1, f1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  } else {
+    GatedPtrs f1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, false, BH);
+    f1.Y = Z;
+    if (launch_scan_fwd_gated(p.p1.fwd, f1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  }
   if (launch_act_fwd(s->in_dtype == GRADLEV_BF16, Z, Hid, BH * s->T * s->hidden, s->act, st) != hipSuccess)
     return GRADLEV_ERR_HIP;
-  GatedPtrs f2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, false, BH);
-  f2.Y = Y;
-  if (launch_scan_fwd_gated(p.p2.fwd, f2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  if (p.wide2) {
+    WidePtrs f2 = wide_ptrs(gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace);
+    f2.Y = Y;
+    p.w2.fmode = fm;
+    if (launch_wide_fwd(p.w2, f2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  } else {
+    GatedPtrs f2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, false, BH);
+    f2.Y = Y;
+    if (launch_scan_fwd_gated(p.p2.fwd, f2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  }
   return GRADLEV_OK;
 }
 
@@ -455,14 +607,29 @@ int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates, 
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t BH = s->B * s->H;
   // Transpose read of the second scan: g_h = (W2_0 + Delta2_t)^T gY, written into gZ.
-  GatedPtrs b2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, true, BH);
-  b2.dY = gY;
-  b2.gtilde = gZ;
-  if (launch_scan_bwd_gated(p.p2.bwd, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  const int fm = wide_fmode(gates);
+  if (p.wide2) {
+    WidePtrs b2 = wide_ptrs(gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace);
+    b2.dY = gY;
+    b2.gtilde = gZ;
+    p.w2.fmode = fm;
+    if (launch_wide_read(p.w2, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  } else {
+    GatedPtrs b2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, true, BH);
+    b2.dY = gY;
+    b2.gtilde = gZ;
+    if (launch_scan_bwd_gated(p.p2.bwd, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  }
   void* q = gX ? static_cast<void*>(static_cast<char*>(workspace) + p.off_q) : nullptr;
   if (launch_act_bwd(s->in_dtype == GRADLEV_BF16, Z, gZ, q, BH * s->T * s->hidden, s->act, st) != hipSuccess)
     return GRADLEV_ERR_HIP;
-  if (gX) {
+  if (gX && p.wide1) {
+    WidePtrs b1 = wide_ptrs(gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace);
+    b1.dY = q;
+    b1.gtilde = gX;
+    p.w1.fmode = fm;
+    if (launch_wide_read(p.w1, b1, st) != hipSuccess) return GRADLEV_ERR_HIP;
+  } else if (gX) {
     GatedPtrs b1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, true, BH);
     b1.dY = q;
     b1.gtilde = gX;

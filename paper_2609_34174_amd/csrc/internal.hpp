@@ -97,6 +97,36 @@ int bwd_chunk_for(int bf16, int d, int m, int requested);
 int fwd_wgs_per_cu(int bf16, int d, int m, int chunk);
 int bwd_wgs_per_cu(int bf16, int d, int m, int chunk);
 
+// Wide maps (parallel form, scan_wide.hip): d and m multiples of 128, at
+// least one above 128; exclusive reads.  fmode: 0 no retention or resets
+// (F = 1), 1 resets only (F in {0, 1}), 2 general retention.
+struct WideProblem {
+  int64_t B, H, T, Tp;  // Tp: T rounded up to a multiple of 128
+  int d, m;
+  int bf16;
+  int fmode;
+};
+
+struct WidePtrs {
+  const float* W0;
+  const void* X;
+  const void* G;
+  const void* dY;
+  const float* eta;
+  float eta_scalar;
+  float eta_mul;
+  const float* alpha;
+  float alpha_scalar;
+  const uint8_t* reset;
+  float* Y;
+  float* gtilde;
+  void* ws;  // wide_workspace_bytes
+};
+
+size_t wide_workspace_bytes(const WideProblem& p);
+hipError_t launch_wide_fwd(const WideProblem& p, const WidePtrs& a, hipStream_t s);
+hipError_t launch_wide_read(const WideProblem& p, const WidePtrs& a, hipStream_t s);
+
 // Optional event timing around each kernel launch (see gradlev_timing_*).
 void timing_begin(int family, hipStream_t s);
 void timing_end(int family, hipStream_t s);

@@ -217,3 +217,44 @@ def test_mlp_validation_before_launch(L):
     rev = L.gradlev_mlp_reverse
     rargs = [FAKE] * 5 + [None, 0.9, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None]
     assert rev(ctypes.byref(ms()), ctypes.byref(g), *rargs) == gl.ERR_INVALID   # gZ missing
+
+
+# ---------------------------------------------------------------------------
+# Wide maps (parallel form): widths that are multiples of 128, one above 128
+# ---------------------------------------------------------------------------
+
+def test_wide_plan_is_one_chunk(L):
+    s = shape(B=2, H=1, T=1000, d_in=1024, d_out=4096)
+    rc, p = plan_rc(s)
+    assert rc == gl.OK
+    assert p.fwd_chunk == p.bwd_chunk == 1024 and p.fwd_nseg == p.bwd_nseg == 1
+    # gate prefixes (16 B per padded token) plus the causal score matrix (4 B per pair)
+    BH, Tp = 2, 1024
+    gates = (BH * Tp * 16 + 255) // 256 * 256
+    assert p.workspace_bytes == gates + BH * Tp * Tp * 4
+    assert gl.workspace_bytes(s) == p.workspace_bytes
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(d_in=192, d_out=256), gl.ERR_UNSUPPORTED), (dict(d_in=256, d_out=64), gl.ERR_UNSUPPORTED),
+    (dict(d_in=256, prefix="inclusive"), gl.ERR_UNSUPPORTED), (dict(d_in=256, T=16385), gl.ERR_UNSUPPORTED),
+    (dict(d_in=8320, d_out=128), gl.ERR_UNSUPPORTED), (dict(d_in=256, B=0), gl.ERR_INVALID),
+    (dict(d_in=256, d_out=128, chunk=-1), gl.ERR_INVALID),
+])
+def test_wide_plan_rejects(L, bad, code):
+    base = dict(d_out=128)
+    base.update(bad)
+    rc, _ = plan_rc(shape(**base))
+    assert rc == code
+
+
+def test_wide_backward_refuses_unbuilt_outputs_before_launch(L):
+    s = shape(B=1, H=1, T=100, d_in=256, d_out=128)
+    g = gl.Gates()
+    g.alpha, g.alpha_scalar, g.reset = None, 1.0, None
+    args = [ctypes.byref(s), ctypes.byref(g)] + [FAKE] * 4 + [ctypes.c_float(0.1), FAKE]
+    # gtilde, dX, dG, deta, dalpha, dW0, ws, bytes, stream
+    rc = L.gradlev_scan_bwd_gated(*args, FAKE, FAKE, None, None, None, None, FAKE, ctypes.c_size_t(1 << 30), None)
+    assert rc == gl.ERR_UNSUPPORTED
+    rc = L.gradlev_scan_bwd_gated(*args, FAKE, None, None, None, None, None, FAKE, ctypes.c_size_t(16), None)
+    assert rc == gl.ERR_WORKSPACE

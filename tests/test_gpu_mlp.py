@@ -36,7 +36,9 @@ def q(a, dtype):
 
 CASES = [("f32", "tanh", 64, 128, 64, 0), ("bf16", "tanh", 64, 128, 64, 64), ("bf16", "gelu", 128, 64, 128, 0),
          ("f32", "gelu", 64, 64, 128, 128), ("bf16", "tanh", 128, 128, 64, 0),
-         ("f32", "gelu_tanh", 64, 128, 64, 0), ("bf16", "gelu_tanh", 64, 128, 128, 0)]
+         ("f32", "gelu_tanh", 64, 128, 64, 0), ("bf16", "gelu_tanh", 64, 128, 128, 0),
+         # wide maps (parallel form): both scans above 128 wide
+         ("bf16", "gelu_tanh", 128, 256, 128, 0), ("f32", "tanh", 256, 384, 128, 0)]
 
 
 @pytest.mark.parametrize("dtype,act,d,hid,o,seg", CASES)

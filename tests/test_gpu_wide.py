@@ -1,0 +1,173 @@
+"""GPU parity of the wide-map scans (the parallel form, widths above 128).
+
+The HIP path runs through the C ABI (gated and unit-retention entry points,
+the two-map MLP); the float64 oracle (the sequential learner of Section 3,
+Eq. 2 general form) checks the forward outputs and the transpose read
+gtilde.  Small cases compare every element, with ragged tails (T not a
+multiple of the 128-token tile), T = 1, and the three retention modes the
+kernels distinguish (none, resets only, general retention with exact zeros
+and negative values).  The paper's adapted MLP at its LM width
+(1024 -> 4096 -> 1024, 1024-token context, two sequences, unit retention with
+document resets) is checked on sampled tokens against closed-form sums over
+each token's document.
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import gradlev_oracle as orc
+from paper_2609_34174_amd import workloads as W
+from parity_util import check, log, to_dev, to_host
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2609_34174_amd as gl  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no ROCm GPU visible")
+    gl.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def inputs(B, H, T, d, m, dtype, seed, alpha_kind, eta_kind, with_reset):
+    base = W.SCAN_WORKLOADS["lm-bf16"]
+    wl = dataclasses.replace(base, B=B, H=H, T=T, d=d, m=m, dtype=dtype, x_dist="normal",
+                             x_std=d ** -0.5, g_std=0.1, seed=seed)
+    inp = W.scan_inputs(wl)
+    a, e = W.gate_tokens(B, H, T, d, seed + 1)
+    rng = np.random.default_rng(seed + 2)
+    if alpha_kind == "family":
+        inp["alpha"] = a
+    elif alpha_kind == "uniform":
+        al = rng.uniform(0, 1, (B, H, T)).astype(np.float32)
+        al[..., ::11] = 0.0
+        inp["alpha"] = al
+    elif alpha_kind == "signed":
+        al = rng.uniform(0.6, 1.0, (B, H, T)).astype(np.float32)
+        al *= np.where(rng.uniform(size=(B, H, T)) < 0.1, -1, 1).astype(np.float32)
+        inp["alpha"] = al
+    else:
+        inp["alpha"] = float(alpha_kind)
+    inp["eta"] = e * 8 if eta_kind == "token" else 0.1
+    inp["reset"] = W.reset_flags(B, T, seed + 3, mean_len=60) if with_reset else None
+    return inp
+
+
+def dev_inputs(inp, dtype):
+    W0 = to_dev(inp["W0"], "f32", torch)
+    X, G, dY = (to_dev(inp[k], dtype, torch) for k in ("X", "G", "dY"))
+    eta, al = inp["eta"], inp["alpha"]
+    e = to_dev(eta, "f32", torch) if isinstance(eta, np.ndarray) else eta
+    a = to_dev(al, "f32", torch) if isinstance(al, np.ndarray) else al
+    r = None if inp["reset"] is None else torch.from_numpy(inp["reset"]).to("cuda")
+    return W0, X, G, dY, e, a, r
+
+
+CASES = [
+    ("f32", 256, 128, 300, "1", "scalar", False),
+    ("bf16", 256, 128, 300, "1", "scalar", False),
+    ("f32", 128, 384, 200, "1", "token", True),
+    ("bf16", 384, 256, 333, "family", "token", True),
+    ("f32", 256, 256, 129, "uniform", "token", False),
+    ("bf16", 128, 256, 1, "family", "scalar", False),
+    ("bf16", 512, 128, 128, "0.9", "token", True),
+    ("f32", 128, 256, 250, "signed", "token", True),
+    ("bf16", 256, 512, 700, "family", "token", True),
+]
+
+
+@pytest.mark.parametrize("dtype,d,m,T,ak,ek,rs", CASES)
+def test_wide_gated_parity(dtype, d, m, T, ak, ek, rs):
+    log(f"wide gated dtype={dtype} d={d} m={m} T={T} alpha={ak} eta={ek} reset={rs}")
+    inp = inputs(2, 2, T, d, m, dtype, seed=T + d + 3 * m, alpha_kind=ak, eta_kind=ek, with_reset=rs)
+    W0, X, G, dY, e, a, r = dev_inputs(inp, dtype)
+    y = gl.scan_fwd_gated(W0, X, G, e, a, r)
+    gt = gl.scan_bwd_gated(W0, X, G, dY, e, a, r, outputs=("gtilde",))["gtilde"]
+    torch.cuda.synchronize()
+    kw = dict(alpha=inp["alpha"], reset=inp["reset"])
+    args = (inp["W0"], inp["X"], inp["G"], inp["eta"])
+    check("y", to_host(y), orc.scan_fwd(*args, **kw), dtype)
+    check("gtilde", to_host(gt), orc.scan_bwd(*args, inp["dY"], **kw)["gtilde"], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_wide_unit_entry_points(dtype):
+    """The unit-retention entry points route wide shapes to the same kernels."""
+    log(f"wide unit dtype={dtype}")
+    inp = inputs(3, 1, 270, 128, 256, dtype, seed=11, alpha_kind="1", eta_kind="token", with_reset=False)
+    W0, X, G, dY, e, _, _ = dev_inputs(inp, dtype)
+    y = gl.scan_fwd(W0, X, G, e)
+    gt = gl.scan_bwd(W0, X, G, dY, e, outputs=("gtilde",))["gtilde"]
+    torch.cuda.synchronize()
+    args = (inp["W0"], inp["X"], inp["G"], inp["eta"])
+    check("y", to_host(y), orc.scan_fwd(*args), dtype)
+    check("gtilde", to_host(gt), orc.scan_bwd(*args, inp["dY"])["gtilde"], dtype)
+
+
+def test_wide_rejects_unbuilt_outputs():
+    """The wide backward returns the transpose read only; other outputs are refused."""
+    inp = inputs(1, 1, 64, 256, 128, "bf16", seed=5, alpha_kind="1", eta_kind="scalar", with_reset=False)
+    W0, X, G, dY, e, _, _ = dev_inputs(inp, "bf16")
+    with pytest.raises(gl.GradLevError) as ex:
+        gl.scan_bwd(W0, X, G, dY, e, outputs=("gtilde", "dx"))
+    assert ex.value.code == gl.ERR_UNSUPPORTED
+
+
+def doc_start(reset_row, t):
+    r = np.nonzero(reset_row[: t + 1])[0]
+    return int(r[-1]) if len(r) else 0
+
+
+@pytest.mark.timeout(600)
+def test_mlp_at_lm_width_sampled():
+    """The paper's adapted final MLP at its LM shape: d = 1024, hidden = 4096,
+    1024-token context, two sequences per GPU, bf16 activations, tanh-GELU,
+    unit retention with document resets and the write gate of the gate family.
+    Sampled tokens of both sequences are checked against W_read = W_0 minus the
+    sum of the writes of the token's own document (closed form of the
+    sequential learner), through the forward and both transpose reads."""
+    B, H, T, d, hid, o = 2, 1, 1024, 1024, 4096, 1024
+    log(f"mlp lm width B={B} T={T} {d}->{hid}->{o} bf16 gelu_tanh resets")
+    rng = np.random.default_rng(2024)
+    W10 = (rng.standard_normal((H, hid, d)) * d ** -0.5).astype(np.float32)
+    W20 = (rng.standard_normal((H, o, hid)) * hid ** -0.5).astype(np.float32)
+    X = W.quantise(rng.standard_normal((B, H, T, d)), "bf16")
+    Gz = W.quantise(rng.standard_normal((B, H, T, hid)) * 0.3, "bf16")
+    Gy = W.quantise(rng.standard_normal((B, H, T, o)) * 0.3, "bf16")
+    gY = W.quantise(rng.standard_normal((B, H, T, o)), "bf16")
+    _, mu = W.gate_tokens(B, H, T, 1, 77)        # mu = 4 sigmoid(b), the write strength
+    rs = W.reset_flags(B, T, 78, mean_len=400)
+    dv = lambda a, dt="bf16": to_dev(a, dt, torch)  # noqa: E731
+    args = (dv(W10, "f32"), dv(W20, "f32"), dv(X), dv(Gz), dv(Gy))
+    mud, rsd = dv(mu, "f32"), torch.from_numpy(rs).to("cuda")
+    Z, Hid, Y = gl.mlp_fwd(*args, mud, 1.0, rsd, act="gelu_tanh")
+    gZ, gX = gl.mlp_reverse(*args, Z, Hid, dv(gY), mud, 1.0, rsd, act="gelu_tanh")
+    torch.cuda.synchronize()
+    Zh, Hh, Yh, gZh, gXh = (to_host(t) for t in (Z, Hid, Y, gZ, gX))
+    picks = sorted({0, 1, 63, 64, 127, 128, 129, 511, 512, 1000, 1023,
+                    *rng.integers(0, T, 5).tolist()})
+    got = {k: [] for k in ("z", "h", "y", "gz", "gx")}
+    ref = {k: [] for k in got}
+    for b in range(B):
+        for t in picks:
+            lo = doc_start(rs[b], t)
+            e1, e2 = mu[b, 0] / d, mu[b, 0] / hid
+            W1r = W10[0].astype(np.float64) - orc.outer_sum(Gz[b, 0], X[b, 0], e1, lo, t)
+            z = W1r @ X[b, 0, t]
+            W2r = W20[0].astype(np.float64) - orc.outer_sum(Gy[b, 0], Hh[b, 0], e2, lo, t)
+            gz = orc.act_grad(z, "gelu_tanh") * (W2r.T @ gY[b, 0, t])
+            pairs = (("z", Zh[b, 0, t], z), ("h", Hh[b, 0, t], orc.round_bf16(orc.act(z, "gelu_tanh"))),
+                     ("y", Yh[b, 0, t], W2r @ Hh[b, 0, t]), ("gz", gZh[b, 0, t], gz),
+                     ("gx", gXh[b, 0, t], W1r.T @ orc.round_bf16(gZh[b, 0, t])))
+            for k, g_, r_ in pairs:
+                got[k].append(g_)
+                ref[k].append(r_)
+    for k in got:
+        check(k, np.array(got[k]), np.array(ref[k]), "bf16")
