@@ -74,11 +74,13 @@ __device__ __forceinline__ int zc_join(int l, int r) { return ((l & ~1) + (r & ~
 
 static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g) {
   const int64_t bh = blockIdx.x, b = bh / g.H;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t per = (g.Tp + 255) / 256;
   const int64_t t0 = tid * per, t1 = t0 + per < g.Tp ? t0 + per : g.Tp;
-  __shared__ int sz[256];
-  __shared__ double sl[256];
+  __shared__ int sz[4];
+  __shared__ double sl[4];
+  // Thread totals over its span, then an exclusive scan over the block:
+  // inclusive scan inside each wave (shuffles), wave totals through LDS.
   int z = 0;
   double l = 0.0;
   for (int64_t t = t0; t < t1; ++t) {
@@ -87,24 +89,35 @@ static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g
     z = zc_step(z, a);
     if (a != 0.f) l += log(fabs((double)a));
   }
-  sz[tid] = z;
-  sl[tid] = l;
-  __syncthreads();
-  if (tid == 0) {
-    int zz = 0;
-    double ll = 0.0;
-    for (int i = 0; i < 256; ++i) {
-      const int tz = sz[i];
-      const double tl = sl[i];
-      sz[i] = zz;
-      sl[i] = ll;
-      zz = zc_join(zz, tz);
-      ll += tl;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int zo = __shfl_up(z, o);
+    const double lo = __shfl_up(l, o);
+    if (lane >= o) {
+      z = zc_join(zo, z);
+      l = lo + l;
     }
   }
+  if (lane == 63) {
+    sz[w] = z;
+    sl[w] = l;
+  }
+  // exclusive within the wave
+  int ze = __shfl_up(z, 1);
+  double le = __shfl_up(l, 1);
+  if (lane == 0) {
+    ze = 0;
+    le = 0.0;
+  }
   __syncthreads();
-  z = sz[tid];
-  l = sl[tid];
+  int zp = 0;
+  double lp = 0.0;
+  for (int i = 0; i < w; ++i) {
+    zp = zc_join(zp, sz[i]);
+    lp += sl[i];
+  }
+  z = zc_join(zp, ze);
+  l = lp + le;
   for (int64_t t = t0; t < t1; ++t) {
     float a, e;
     gate_at(g, bh, b, t, a, e);
@@ -138,21 +151,19 @@ struct GTile {
                                             src, (int)(row_off + (uint32_t)r * stride + col0 + 16u * cu), 0, 0));
     }
   }
+  // One 16-byte LDS store per unit.  A bf16 unit is the chunk pair
+  // (2c, 2c + 1); the swizzle XORs chunk indices, so the pair stays an aligned
+  // pair, in swapped order when the row's swizzle is odd.
   __device__ __forceinline__ void store(E* lds, int tid) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int u = tid + i * NT, r = u / UPR, k = (u % UPR) * EPU;
-#pragma unroll
-      for (int h = 0; h < EPU / 4; ++h) {
-        typedef typename Vec4<E>::type vec4;
-        vec4 x;
-        if constexpr (sizeof(E) == 2) {
-          const i32x2 p = {v[i][2 * h], v[i][2 * h + 1]};
-          x = __builtin_bit_cast(vec4, p);
-        } else {
-          x = __builtin_bit_cast(vec4, v[i]);
-        }
-        *reinterpret_cast<vec4*>(lds + lds_off(r, k + 4 * h, COLS)) = x;
+      if constexpr (sizeof(E) == 2) {
+        const int ch = (k >> 2) ^ swz(r, COLS);
+        const i32x4 x = (ch & 1) ? i32x4{v[i][2], v[i][3], v[i][0], v[i][1]} : v[i];
+        *reinterpret_cast<i32x4*>(lds + r * COLS + 4 * (ch & ~1)) = x;
+      } else {
+        *reinterpret_cast<i32x4*>(lds + lds_off(r, k, COLS)) = v[i];
       }
     }
   }
@@ -170,45 +181,85 @@ struct GTile {
 };
 
 // ---------------------------------------------------------------------------
-// Score tiles.  Tile (tb, sb) covers rows t in [64 tb, 64 tb + 64) and
-// columns s in [64 sb, 64 sb + 64).  The output kernel reads, for its
-// 128-row tile p, the columns [0, 128 (p + 1)), so every tile with
-// sb <= (tb | 1) is written: those above the diagonal as zeros.  Per
-// sequence that is 2 K (K + 1) tiles, K = Tp / 128.
+// Score tiles.  Tile (tb, sb), sb <= tb, covers rows t in [128 tb, +128) and
+// columns s in [128 sb, +128): the lower triangle of 128-token blocks, which
+// is exactly what an output tile of rows [128 tb, +128) reads.  Workgroup of
+// 4 waves; wave (wt, ws) owns rows t in [64 wt, +64), columns s in
+// [64 ws, +64) as 4 x 4 accumulator blocks D[s][t] (lane: 4 consecutive s of
+// one t, so the score rows are stored 8 bytes at a time).
+//
+// When the triangle has too few tiles to fill the chip, the contraction is
+// split into KS ranges of the query width: each workgroup writes its fp32
+// partial tile and wide_score_finish sums the partials in a fixed order, so
+// results do not depend on scheduling.
 // ---------------------------------------------------------------------------
 struct WScoreArgs {
   const void* Q;
   const void* K;
   int64_t T, Tp, w, BH;
+  int KS;
   const float* cw;
   const int* zc;
   const double* lc;
   void* Sh;
   void* Sl;
+  float* part;  // [KS][BH][Tp][Tp] fp32 partial tiles (KS > 1)
 };
 
-template <class OP, int FMODE>
-static __global__ void __launch_bounds__(64) wide_score_kernel(const WScoreArgs a) {
-  typedef typename OP::elem E;
-  typedef typename OP::frag F;
-  constexpr int BK = 64;
-  __shared__ E Ps[64 * BK];  // K rows s
-  __shared__ E Qs[64 * BK];  // Q rows t
+// Tile index within one sequence's lower triangle of 128-token blocks.
+__device__ __forceinline__ void tri_tile(int64_t L, int64_t& tb, int64_t& sb) {
+  tb = (int64_t)((sqrt(8.0 * (double)L + 1.0) - 1.0) * 0.5);
+  while ((tb + 1) * (tb + 2) / 2 <= L) ++tb;
+  while (tb > 0 && tb * (tb + 1) / 2 > L) --tb;
+  sb = L - tb * (tb + 1) / 2;
+}
 
-  const int64_t Kp = a.Tp / 128, per_seq = 2 * Kp * (Kp + 1);
-  const int64_t bh = blockIdx.x / per_seq;
-  int64_t L = blockIdx.x % per_seq;
-  // Pair row p holds tile rows 2p and 2p + 1 with 2p + 2 tiles each; the
-  // rows before it hold 2 p (p + 1) tiles.
-  int64_t p = (int64_t)((sqrt(1.0 + 2.0 * (double)L) - 1.0) * 0.5);
-  while (2 * (p + 1) * (p + 2) <= L) ++p;
-  while (p > 0 && 2 * p * (p + 1) > L) --p;
-  L -= 2 * p * (p + 1);
-  const int64_t tb = 2 * p + L / (2 * p + 2), sb = L % (2 * p + 2);
-  const int lane = threadIdx.x, c = lane & 15, q = lane >> 4;
-  const int64_t t0 = 64 * tb, s0 = 64 * sb;
+// Scales 4 consecutive scores (t; s .. s+3) by F[t][s] c_s, masks s >= t and
+// padding rows, and stores them split (bf16 hi + lo) or as fp32.  F is
+// rebased on the log sum at the end of the 64-column block holding s, so that
+// the fp32 exponent argument stays small wherever F is not negligible.
+template <class OP, int FMODE>
+__device__ __forceinline__ void score_store(const WScoreArgs& a, int64_t bh, int64_t t, int64_t s, f32x4 acc) {
+  typedef typename OP::elem E;
+  const float* cw = a.cw + bh * a.Tp;
+  const int* zc = a.zc + bh * a.Tp;
+  const double* lc = a.lc + bh * a.Tp;
+  const double ref = FMODE == 2 ? lc[s | 63] : 0.0;
+  int zt = 0;
+  float at = 0.f;
+  if (FMODE >= 1 && t >= 1) zt = zc[t - 1];
+  if (FMODE == 2 && t >= 1) at = (float)(lc[t - 1] - ref);
+  const f32x4 cv = *reinterpret_cast<const f32x4*>(cw + s);
+  f32x4 v;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float f = (s + r < t && t < a.T) ? cv[r] : 0.f;
+    const int zs = FMODE >= 1 ? zc[s + r] : 0;
+    if (FMODE >= 1 && (zs >> 1) != (zt >> 1)) f = 0.f;
+    if (FMODE == 2 && f != 0.f) f *= ((zs ^ zt) & 1 ? -1.f : 1.f) * expf(at + (float)(ref - lc[s + r]));
+    v[r] = acc[r] * f;
+  }
   E* Sh = static_cast<E*>(a.Sh) + bh * a.Tp * a.Tp;
   E* Sl = static_cast<E*>(a.Sl) + bh * a.Tp * a.Tp;
+  OP::store4_split(Sh + t * a.Tp + s, Sl + t * a.Tp + s, v);
+}
+
+template <class OP, int FMODE>
+static __global__ void __launch_bounds__(256) wide_score_kernel(const WScoreArgs a) {
+  typedef typename OP::elem E;
+  typedef typename OP::frag F;
+  constexpr int BT = 128, BK = 64, NT = 256;
+  __shared__ __attribute__((aligned(16))) E Ps[BT * BK];  // K rows s
+  __shared__ __attribute__((aligned(16))) E Qs[BT * BK];  // Q rows t
+
+  const int64_t Kp = a.Tp / BT, per_seq = Kp * (Kp + 1) / 2;
+  const int64_t ks = blockIdx.x % a.KS, tile = blockIdx.x / a.KS;
+  const int64_t bh = tile / per_seq;
+  int64_t tb, sb;
+  tri_tile(tile % per_seq, tb, sb);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wt = w >> 1, ws = w & 1;
+  const int c = lane & 15, q = lane >> 4;
+  const int64_t wk = a.w / a.KS, kbeg = ks * wk;
 
   f32x4 acc[4][4];  // [s block][t block]: D[s][t] = K_s . Q_t
 #pragma unroll
@@ -216,78 +267,108 @@ static __global__ void __launch_bounds__(64) wide_score_kernel(const WScoreArgs 
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
 
-  if (sb <= tb) {
+  {
     const size_t es = sizeof(E);
     const rsrc_t Qr = make_rsrc(static_cast<const E*>(a.Q) + bh * a.T * a.w, (uint32_t)(a.T * a.w * es));
     const rsrc_t Kr = make_rsrc(static_cast<const E*>(a.K) + bh * a.T * a.w, (uint32_t)(a.T * a.w * es));
     const uint32_t stride = (uint32_t)(a.w * es);
-    GTile<E, 64, BK, 64> qt, kt;
-    qt.load(Qr, (uint32_t)(t0 * stride), stride, 0, lane);
-    kt.load(Kr, (uint32_t)(s0 * stride), stride, 0, lane);
-    for (int64_t k0 = 0; k0 < a.w; k0 += BK) {
+    const uint32_t qoff = (uint32_t)(BT * tb * stride), koff = (uint32_t)(BT * sb * stride);
+    // Two-deep register pipeline as in wide_out_kernel (the step count
+    // wk / 64 is even: the split rule keeps every range a multiple of 128).
+    struct Set {
+      GTile<E, BT, BK, NT> qt, kt;
+    } st[2];
+    const int64_t nk = wk / BK;
+    auto fetch = [&](Set& x, int64_t k) {
+      const bool ok = k < nk;
+      const uint32_t col = (uint32_t)((kbeg + k * BK) * es);
+      x.qt.load(Qr, ok ? qoff : kOOB, stride, col, tid);
+      x.kt.load(Kr, ok ? koff : kOOB, stride, col, tid);
+    };
+    auto step = [&](Set& x, int64_t k) {
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
-      qt.store(Qs, lane);
-      kt.store(Ps, lane);
+      x.qt.store(Qs, tid);
+      x.kt.store(Ps, tid);
       __syncthreads();
-      if (k0 + BK < a.w) {
-        qt.load(Qr, (uint32_t)(t0 * stride), stride, (uint32_t)((k0 + BK) * es), lane);
-        kt.load(Kr, (uint32_t)(s0 * stride), stride, (uint32_t)((k0 + BK) * es), lane);
-      }
+      fetch(x, k + 2);
 #pragma unroll
       for (int kk = 0; kk < BK; kk += 32) {
         F qf[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 16 * j, kk, lane);
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const F pf = OP::load_n(Ps, BK, 16 * i, kk, lane);
+          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[i][j] = OP::mma(acc[i][j], pf, qf[j]);
         }
       }
+    };
+    fetch(st[0], 0);
+    fetch(st[1], 1);
+    for (int64_t k = 0; k < nk; k += 2) {
+      step(st[0], k);
+      step(st[1], k + 1);
     }
   }
 
-  // Epilogue: lane (c, q) of block (i, j) holds s = s0 + 16 i + 4 q + r and
-  // t = t0 + 16 j + c.
-  const float* cw = a.cw + bh * a.Tp;
-  const int* zc = a.zc + bh * a.Tp;
-  const double* lc = a.lc + bh * a.Tp;
-  const double ref = FMODE == 2 ? lc[s0 + 63] : 0.0;
+  // Lane (c, q) of block (i, j) holds s = s0 + 16 i + 4 q + r, t = t0 + 16 j + c.
+  const int64_t s0 = BT * sb + 64 * ws, t0 = BT * tb + 64 * wt;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t t = t0 + 16 * j + c;
-    int zt = 0;
-    float at = 0.f;
-    if (FMODE >= 1 && t >= 1) zt = zc[t - 1];
-    if (FMODE == 2 && t >= 1) at = (float)(lc[t - 1] - ref);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t s = s0 + 16 * i + 4 * q;
-      const f32x4 cv = *reinterpret_cast<const f32x4*>(cw + s);
-      f32x4 v;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float f = (s + r < t && t < a.T) ? cv[r] : 0.f;
-        const int zs = FMODE >= 1 ? zc[s + r] : 0;
-        if (FMODE >= 1 && (zs >> 1) != (zt >> 1)) f = 0.f;
-        if (FMODE == 2 && f != 0.f) f *= ((zs ^ zt) & 1 ? -1.f : 1.f) * expf(at + (float)(ref - lc[s + r]));
-        v[r] = acc[i][j][r] * f;
-      }
-      OP::store4_split(Sh + t * a.Tp + s, Sl + t * a.Tp + s, v);
+      if (a.KS == 1) score_store<OP, FMODE>(a, bh, t, s, acc[i][j]);
+      else *reinterpret_cast<f32x4*>(a.part + ((ks * a.BH + bh) * a.Tp + t) * a.Tp + s) = acc[i][j];
     }
   }
 }
 
+// Sum of the KS partial tiles in order, then the scaling and split of
+// score_store.  Thread: 4 consecutive columns of one row; workgroup: 8 rows
+// of one tile (16 workgroups per tile).
+template <class OP, int FMODE>
+static __global__ void __launch_bounds__(256) wide_score_finish(const WScoreArgs a) {
+  const int64_t Kp = a.Tp / 128, per_seq = Kp * (Kp + 1) / 2;
+  const int64_t tile = blockIdx.x / 16, part = blockIdx.x % 16;
+  const int64_t bh = tile / per_seq;
+  int64_t tb, sb;
+  tri_tile(tile % per_seq, tb, sb);
+  const int tid = threadIdx.x;
+  const size_t plane = (size_t)a.BH * a.Tp * a.Tp;
+  const int64_t t = 128 * tb + 8 * part + tid / 32, s = 128 * sb + 4 * (tid % 32);
+  const float* p = a.part + (bh * a.Tp + t) * a.Tp + s;
+  f32x4 v = *reinterpret_cast<const f32x4*>(p);
+  for (int k = 1; k < a.KS; ++k) v += *reinterpret_cast<const f32x4*>(p + k * plane);
+  score_store<OP, FMODE>(a, bh, t, s, v);
+}
+
 // ---------------------------------------------------------------------------
-// Output tiles.  Workgroup of 4 waves, tile 128 (t) x 128 (n); wave (wt, wn)
-// owns rows [64 wt, +64) and columns [64 wn, +64) as 4 x 4 accumulator
-// blocks D[n][t] (a lane holds 4 consecutive n of one t: 16-byte stores).
+// Output tiles.  Workgroup of 8 waves, tile 128 (t) x BN (n), BN 128 or 64
+// (64 when 128-wide tiles would leave compute units idle).  Wave
+// (kh, wt, wn) owns rows [64 wt, +64) and columns [BN/2 wn, +BN/2) as
+// accumulator blocks D[n][t] (a lane holds 4 consecutive n of one t:
+// 16-byte stores) and contracts the k sub-step kh of every staged 64-wide
+// slice; the two halves are added through LDS at the end.
 // Phase 1 contracts Q with W_0 over the query width, phase 2 contracts S with
 // V over s < 128 (tile + 1).  Tiles are issued heaviest (last rows) first.
 // ---------------------------------------------------------------------------
+// fp32 W_0 split once per call into bf16 hi and lo planes of the same
+// layout (the output tiles then stage bf16 directly; the split costs one
+// pass over W_0 instead of one per row tile).
+static __global__ void __launch_bounds__(256) wide_split_w0(const float* __restrict__ W0, bf16* __restrict__ hi,
+                                                            bf16* __restrict__ lo, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
+    OpBF16::store4_split(hi + 4 * i, lo + 4 * i, *reinterpret_cast<const f32x4*>(W0 + 4 * i));
+}
+
 struct WOutArgs {
   const void* Q;
+  const bf16* Wh;  // bf16 operands: W_0 split into hi and lo planes [H][m][d]
+  const bf16* Wl;
   const float* W0;
   const void* Sh;
   const void* Sl;
@@ -296,18 +377,22 @@ struct WOutArgs {
   int64_t wq, wout, BH, H, T, Tp;
 };
 
-template <class OP, bool TRANS>
-static __global__ void __launch_bounds__(256) wide_out_kernel(const WOutArgs a) {
+template <class OP, bool TRANS, int BN>
+static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
-  constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
-  constexpr int TILE = BM * BK;  // elements of one staged tile (all are 128 x 64 or 64 x 128)
+  constexpr int BM = 128, BK = 64, NT = 512, NB = BN / 32;  // NB: 16-column blocks per wave
+  constexpr int TILE = BM * BK, PT = BN * BK;
   constexpr bool SPLIT = OP::kSplit == 2;
-  __shared__ E lds[(SPLIT ? 3 : 2) * TILE];
+  constexpr int P1 = TILE + (SPLIT ? 2 : 1) * PT, P2 = (SPLIT ? 2 : 1) * TILE + PT;
+  constexpr int PR = BM * BN * 4 / (int)sizeof(E);  // the kh = 1 waves' accumulators: a BM x BN fp32 partial
+  static_assert(4 * NB * 4 * 64 * 16 == BM * BN * 4, "reduction layout covers the tile once");
+  constexpr int PM = P1 > P2 ? P1 : P2;
+  __shared__ __attribute__((aligned(16))) E lds[PM > PR ? PM : PR];
   // Phase 1: Qs | Ph | Pl.  Phase 2: Shs | Sls | Vs (fp32: Qs | Ph and Shs | Vs).
   E* const Qs = lds;
   E* const Ph = lds + TILE;
-  E* const Pl = SPLIT ? lds + 2 * TILE : Ph;
+  E* const Pl = SPLIT ? lds + TILE + PT : Ph;
   E* const Shs = lds;
   E* const Sls = SPLIT ? lds + TILE : lds;
   E* const Vs = lds + (SPLIT ? 2 : 1) * TILE;
@@ -317,114 +402,160 @@ static __global__ void __launch_bounds__(256) wide_out_kernel(const WOutArgs a) 
   const int64_t tb = nTB - 1 - L / per_row;
   const int64_t bh = (L % per_row) / nNB, nb = L % nNB;
   const int64_t h = bh % a.H;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wt = w >> 1, wn = w & 1;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, kh = w >> 2, wt = (w >> 1) & 1, wn = w & 1;
   const int c = lane & 15, q = lane >> 4;
   const int64_t t0 = BM * tb, n0 = BN * nb;
   const size_t es = sizeof(E);
 
-  f32x4 acc[4][4];  // [n block][t block]
+  f32x4 acc[NB][4];  // [n block][t block]
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NB; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
 
+  // Both phases run a two-deep register pipeline: the tiles of step k + 2
+  // are requested while step k computes, by two staging sets used in turn.
+  // Step counts are even (widths are multiples of 128 and the causal range is
+  // whole 128-token blocks), and a request past the last step reads from an
+  // offset beyond the buffer (zeros, no branch), so the outstanding-load
+  // counts stay exact across the barriers.
   // Phase 1: acc += W_0-term over k in [0, wq).
   {
     const rsrc_t Qr = make_rsrc(static_cast<const E*>(a.Q) + bh * a.T * a.wq, (uint32_t)(a.T * a.wq * es));
     const int64_t md = a.wq * a.wout;
     const rsrc_t Wr = make_rsrc(a.W0 + h * md, (uint32_t)(md * 4));
     const uint32_t qstride = (uint32_t)(a.wq * es);
-    GTile<E, BM, BK, NT> qt;
-    // W_0 is [m][d]: forward rows n over k (row length wq), read rows k over n (row length wout).
-    typedef GTile<float, TRANS ? BK : BN, TRANS ? BN : BK, NT> WT;
-    WT wtile;
-    auto wload = [&](int64_t k0) {
-      if constexpr (TRANS) wtile.load(Wr, (uint32_t)(k0 * a.wout * 4), (uint32_t)(a.wout * 4), (uint32_t)(n0 * 4), tid);
-      else wtile.load(Wr, (uint32_t)(n0 * a.wq * 4), (uint32_t)(a.wq * 4), (uint32_t)(k0 * 4), tid);
+    // W_0 is [m][d]: forward rows n over k (row length wq), read rows k over n
+    // (row length wout).  bf16 operands stage the hi and lo planes, fp32 W_0.
+    const rsrc_t Whr = make_rsrc(SPLIT ? a.Wh + h * md : nullptr, SPLIT ? (uint32_t)(md * 2) : 0u);
+    const rsrc_t Wlr = make_rsrc(SPLIT ? a.Wl + h * md : nullptr, SPLIT ? (uint32_t)(md * 2) : 0u);
+    typedef GTile<E, TRANS ? BK : BN, TRANS ? BN : BK, NT> WT;
+    struct Set {
+      GTile<E, BM, BK, NT> qt;
+      WT wh, wl;
+    } st[2];
+    const int64_t n1 = a.wq / BK;
+    auto fetch = [&](Set& x, int64_t k) {
+      const bool ok = k < n1;
+      const int64_t k0 = k * BK;
+      x.qt.load(Qr, ok ? (uint32_t)(t0 * qstride) : kOOB, qstride, (uint32_t)(k0 * es), tid);
+      const rsrc_t r0 = SPLIT ? Whr : Wr;
+      const uint32_t rows = TRANS ? (uint32_t)(k0 * a.wout * es) : (uint32_t)(n0 * a.wq * es);
+      const uint32_t stride = TRANS ? (uint32_t)(a.wout * es) : (uint32_t)(a.wq * es);
+      const uint32_t col = TRANS ? (uint32_t)(n0 * es) : (uint32_t)(k0 * es);
+      x.wh.load(r0, ok ? rows : kOOB, stride, col, tid);
+      if constexpr (SPLIT) x.wl.load(Wlr, ok ? rows : kOOB, stride, col, tid);
     };
-    qt.load(Qr, (uint32_t)(t0 * qstride), qstride, 0, tid);
-    wload(0);
-    for (int64_t k0 = 0; k0 < a.wq; k0 += BK) {
+    auto step = [&](Set& x, int64_t k) {
+      // Keep each step's work inside the step: hoisting the other set's
+      // stores would make the compiler wait for its loads here.
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
-      qt.store(Qs, tid);
-      if constexpr (SPLIT) wtile.template store_split<OP>(Ph, Pl, tid);
-      else wtile.store(reinterpret_cast<float*>(Ph), tid);
+      x.qt.store(Qs, tid);
+      x.wh.store(Ph, tid);
+      if constexpr (SPLIT) x.wl.store(Pl, tid);
       __syncthreads();
-      if (k0 + BK < a.wq) {
-        qt.load(Qr, (uint32_t)(t0 * qstride), qstride, (uint32_t)((k0 + BK) * es), tid);
-        wload(k0 + BK);
-      }
+      fetch(x, k + 2);
+      const int kk = 32 * kh;
+      F qf[4];
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 32) {
-        F qf[4];
+      for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          F ph, pl;
-          if constexpr (TRANS) {
-            ph = OP::load_t(Ph, BN, kk, 64 * wn + 16 * i, lane);
-            pl = SPLIT ? OP::load_t(Pl, BN, kk, 64 * wn + 16 * i, lane) : ph;
-          } else {
-            ph = OP::load_n(Ph, BK, 64 * wn + 16 * i, kk, lane);
-            pl = SPLIT ? OP::load_n(Pl, BK, 64 * wn + 16 * i, kk, lane) : ph;
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mma_split_a<OP>(acc[i][j], ph, pl, qf[j]);
+      for (int i = 0; i < NB; ++i) {
+        F ph, pl;
+        if constexpr (TRANS) {
+          ph = OP::load_t(Ph, BN, kk, BN / 2 * wn + 16 * i, lane);
+          pl = SPLIT ? OP::load_t(Pl, BN, kk, BN / 2 * wn + 16 * i, lane) : ph;
+        } else {
+          ph = OP::load_n(Ph, BK, BN / 2 * wn + 16 * i, kk, lane);
+          pl = SPLIT ? OP::load_n(Pl, BK, BN / 2 * wn + 16 * i, kk, lane) : ph;
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma_split_a<OP>(acc[i][j], ph, pl, qf[j]);
       }
+    };
+    fetch(st[0], 0);
+    fetch(st[1], 1);
+    for (int64_t k = 0; k < n1; k += 2) {
+      step(st[0], k);
+      step(st[1], k + 1);
     }
   }
 
   // Phase 2: acc += S V over s in [0, 128 (tb + 1)).
   {
-    const int64_t send = BM * (tb + 1);
     const rsrc_t Shr = make_rsrc(static_cast<const E*>(a.Sh) + bh * a.Tp * a.Tp, (uint32_t)(a.Tp * a.Tp * es));
     const rsrc_t Slr = make_rsrc(SPLIT ? static_cast<const E*>(a.Sl) + bh * a.Tp * a.Tp : nullptr,
                                  SPLIT ? (uint32_t)(a.Tp * a.Tp * es) : 0u);
     const rsrc_t Vr = make_rsrc(static_cast<const E*>(a.V) + bh * a.T * a.wout, (uint32_t)(a.T * a.wout * es));
     const uint32_t sstride = (uint32_t)(a.Tp * es), vstride = (uint32_t)(a.wout * es);
-    GTile<E, BM, BK, NT> sh, sl;
-    GTile<E, BK, BN, NT> vt;
-    auto load = [&](int64_t s0) {
-      sh.load(Shr, (uint32_t)(t0 * sstride), sstride, (uint32_t)(s0 * es), tid);
-      if constexpr (SPLIT) sl.load(Slr, (uint32_t)(t0 * sstride), sstride, (uint32_t)(s0 * es), tid);
-      vt.load(Vr, (uint32_t)(s0 * vstride), vstride, (uint32_t)(n0 * es), tid);
+    struct Set {
+      GTile<E, BM, BK, NT> sh, sl;
+      GTile<E, BK, BN, NT> vt;
+    } st[2];
+    const int64_t n2 = 2 * (tb + 1);
+    auto fetch = [&](Set& x, int64_t k) {
+      const bool ok = k < n2;
+      const int64_t s0 = k * BK;
+      x.sh.load(Shr, ok ? (uint32_t)(t0 * sstride) : kOOB, sstride, (uint32_t)(s0 * es), tid);
+      if constexpr (SPLIT) x.sl.load(Slr, ok ? (uint32_t)(t0 * sstride) : kOOB, sstride, (uint32_t)(s0 * es), tid);
+      x.vt.load(Vr, ok ? (uint32_t)(s0 * vstride) : kOOB, vstride, (uint32_t)(n0 * es), tid);
     };
-    load(0);
-    for (int64_t s0 = 0; s0 < send; s0 += BK) {
+    auto step = [&](Set& x, int64_t k) {
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
-      sh.store(Shs, tid);
-      if constexpr (SPLIT) sl.store(Sls, tid);
-      vt.store(Vs, tid);
+      x.sh.store(Shs, tid);
+      if constexpr (SPLIT) x.sl.store(Sls, tid);
+      x.vt.store(Vs, tid);
       __syncthreads();
-      if (s0 + BK < send) load(s0 + BK);
+      fetch(x, k + 2);
+      const int kk = 32 * kh;
+      F sfh[4], sfl[4];
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 32) {
-        F sfh[4], sfl[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          sfh[j] = OP::load_n(Shs, BK, 64 * wt + 16 * j, kk, lane);
-          sfl[j] = SPLIT ? OP::load_n(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const F vf = OP::load_t(Vs, BN, kk, 64 * wn + 16 * i, lane);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mma_split_b<OP>(acc[i][j], vf, sfh[j], sfl[j]);
-        }
+      for (int j = 0; j < 4; ++j) {
+        sfh[j] = OP::load_n(Shs, BK, 64 * wt + 16 * j, kk, lane);
+        sfl[j] = SPLIT ? OP::load_n(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
       }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const F vf = OP::load_t(Vs, BN, kk, BN / 2 * wn + 16 * i, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma_split_b<OP>(acc[i][j], vf, sfh[j], sfl[j]);
+      }
+    };
+    fetch(st[0], 0);
+    fetch(st[1], 1);
+    for (int64_t k = 0; k < n2; k += 2) {
+      step(st[0], k);
+      step(st[1], k + 1);
     }
   }
 
-  // Lane (c, q) of block (i, j): n = n0 + 64 wn + 16 i + 4 q + r, t = t0 + 64 wt + 16 j + c.
+  // The kh = 1 waves hand their accumulators to the kh = 0 waves of the same
+  // (wt, wn) through LDS (16 bytes per lane, one contiguous block per wave).
+  f32x4* red = reinterpret_cast<f32x4*>(lds) + (w & 3) * NB * 4 * 64 + lane;
+  __syncthreads();
+  if (kh == 1) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) red[(i * 4 + j) * 64] = acc[i][j];
+  }
+  __syncthreads();
+  if (kh == 1) return;
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] += red[(i * 4 + j) * 64];
+
+  // Lane (c, q) of block (i, j): n = n0 + BN/2 wn + 16 i + 4 q + r, t = t0 + 64 wt + 16 j + c.
   const rsrc_t Or = make_rsrc(a.out + bh * a.T * a.wout, (uint32_t)(a.T * a.wout * 4));
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t t = t0 + 64 * wt + 16 * j + c;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t n = n0 + 64 * wn + 16 * i + 4 * q;
+    for (int i = 0; i < NB; ++i) {
+      const int64_t n = n0 + BN / 2 * wn + 16 * i + 4 * q;
       buf_store4(Or, (uint32_t)((t * a.wout + n) * 4), acc[i][j]);
     }
   }
@@ -433,11 +564,25 @@ static __global__ void __launch_bounds__(256) wide_out_kernel(const WOutArgs a) 
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
+// Splits of the score contraction: enough workgroups for two per compute
+// unit, at most 4 ranges, each at least 256 wide and a whole number of the
+// kernel's 64-wide steps.
+static int wide_score_splits(int64_t BH, int64_t Tp, int64_t w) {
+  const int64_t tiles = BH * (Tp / 128) * (Tp / 128 + 1) / 2;
+  int ks = 1;
+  while (ks < 4 && tiles * ks < 2 * 256 && w / (2 * ks) >= 256 && w % (2 * ks * 64) == 0) ks *= 2;
+  return ks;
+}
+
 size_t wide_workspace_bytes(const WideProblem& p) {
   const size_t BH = (size_t)(p.B * p.H), Tp = (size_t)p.Tp;
   const size_t gates = BH * Tp * (4 + 4 + 8);
-  const size_t S = BH * Tp * Tp * (p.bf16 ? 4 : 4);  // bf16 hi + lo, or fp32
-  return (gates + 255) / 256 * 256 + (S + 255) / 256 * 256;
+  const size_t S = BH * Tp * Tp * 4;  // bf16 hi + lo, or fp32
+  const int kd = wide_score_splits((int64_t)BH, (int64_t)Tp, p.d), km = wide_score_splits((int64_t)BH, (int64_t)Tp, p.m);
+  const int ks = kd > km ? kd : km;  // the forward contracts over d, the read over m
+  const size_t part = ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0;
+  const size_t planes = p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0;  // W_0 hi + lo
+  return (gates + 255) / 256 * 256 + (S + 255) / 256 * 256 + (part + 255) / 256 * 256 + planes;
 }
 
 namespace {
@@ -448,6 +593,9 @@ struct WideWs {
   double* lc;
   void* Sh;
   void* Sl;
+  float* part;
+  bf16* Wh;
+  bf16* Wl;
 };
 
 WideWs wide_ws(const WideProblem& p, void* ws) {
@@ -460,6 +608,13 @@ WideWs wide_ws(const WideProblem& p, void* ws) {
   char* s = w + (BH * Tp * 16 + 255) / 256 * 256;
   o.Sh = s;
   o.Sl = s + BH * Tp * Tp * 2;  // bf16 only
+  char* pt = s + (BH * Tp * Tp * 4 + 255) / 256 * 256;
+  o.part = reinterpret_cast<float*>(pt);
+  const int kd = wide_score_splits((int64_t)BH, (int64_t)Tp, p.d), km = wide_score_splits((int64_t)BH, (int64_t)Tp, p.m);
+  const int ks = kd > km ? kd : km;
+  char* wp = pt + ((ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0) + 255) / 256 * 256;
+  o.Wh = reinterpret_cast<bf16*>(wp);
+  o.Wl = reinterpret_cast<bf16*>(wp + (size_t)p.H * p.m * p.d * 2);
   return o;
 }
 
@@ -484,16 +639,30 @@ hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, hipStrea
   sa.lc = ws.lc;
   sa.Sh = ws.Sh;
   sa.Sl = OP::kSplit == 2 ? ws.Sl : ws.Sh;
+  sa.part = ws.part;
+  sa.KS = wide_score_splits(BH, p.Tp, sa.w);
   const int64_t Kp = p.Tp / 128;
-  const unsigned sgrid = (unsigned)(BH * 2 * Kp * (Kp + 1));
-  if (p.fmode == 0) hipLaunchKernelGGL((wide_score_kernel<OP, 0>), dim3(sgrid), dim3(64), 0, s, sa);
-  else if (p.fmode == 1) hipLaunchKernelGGL((wide_score_kernel<OP, 1>), dim3(sgrid), dim3(64), 0, s, sa);
-  else hipLaunchKernelGGL((wide_score_kernel<OP, 2>), dim3(sgrid), dim3(64), 0, s, sa);
+  const unsigned tiles = (unsigned)(BH * Kp * (Kp + 1) / 2), sgrid = tiles * sa.KS;
+  if (p.fmode == 0) hipLaunchKernelGGL((wide_score_kernel<OP, 0>), dim3(sgrid), dim3(256), 0, s, sa);
+  else if (p.fmode == 1) hipLaunchKernelGGL((wide_score_kernel<OP, 1>), dim3(sgrid), dim3(256), 0, s, sa);
+  else hipLaunchKernelGGL((wide_score_kernel<OP, 2>), dim3(sgrid), dim3(256), 0, s, sa);
+  if (sa.KS > 1) {
+    if (p.fmode == 0) hipLaunchKernelGGL((wide_score_finish<OP, 0>), dim3(16 * tiles), dim3(256), 0, s, sa);
+    else if (p.fmode == 1) hipLaunchKernelGGL((wide_score_finish<OP, 1>), dim3(16 * tiles), dim3(256), 0, s, sa);
+    else hipLaunchKernelGGL((wide_score_finish<OP, 2>), dim3(16 * tiles), dim3(256), 0, s, sa);
+  }
   timing_end(GRADLEV_K_WIDE_SCORE, s);
 
   WOutArgs oa{};
   oa.Q = sa.Q;
   oa.W0 = f.W0;
+  if (OP::kSplit == 2) {
+    const int64_t n4 = p.H * (int64_t)p.m * p.d / 4;
+    const unsigned g = (unsigned)(n4 / 256 < 4096 ? (n4 + 255) / 256 : 4096);
+    hipLaunchKernelGGL(wide_split_w0, dim3(g), dim3(256), 0, s, f.W0, ws.Wh, ws.Wl, n4);
+    oa.Wh = ws.Wh;
+    oa.Wl = ws.Wl;
+  }
   oa.Sh = ws.Sh;
   oa.Sl = sa.Sl;
   oa.V = read ? f.X : f.G;
@@ -504,10 +673,15 @@ hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, hipStrea
   oa.H = p.H;
   oa.T = p.T;
   oa.Tp = p.Tp;
-  const unsigned ogrid = (unsigned)(BH * (p.Tp / 128) * (oa.wout / 128));
+  // 128-wide column tiles unless that leaves fewer than two tiles per compute unit.
+  const int64_t t128 = BH * (p.Tp / 128) * (oa.wout / 128);
+  const bool narrow = t128 < 2 * 256;
+  const unsigned ogrid = (unsigned)(narrow ? 2 * t128 : t128);
   timing_begin(GRADLEV_K_WIDE_OUT, s);
-  if (read) hipLaunchKernelGGL((wide_out_kernel<OP, true>), dim3(ogrid), dim3(256), 0, s, oa);
-  else hipLaunchKernelGGL((wide_out_kernel<OP, false>), dim3(ogrid), dim3(256), 0, s, oa);
+  if (read && narrow) hipLaunchKernelGGL((wide_out_kernel<OP, true, 64>), dim3(ogrid), dim3(512), 0, s, oa);
+  else if (read) hipLaunchKernelGGL((wide_out_kernel<OP, true, 128>), dim3(ogrid), dim3(512), 0, s, oa);
+  else if (narrow) hipLaunchKernelGGL((wide_out_kernel<OP, false, 64>), dim3(ogrid), dim3(512), 0, s, oa);
+  else hipLaunchKernelGGL((wide_out_kernel<OP, false, 128>), dim3(ogrid), dim3(512), 0, s, oa);
   timing_end(GRADLEV_K_WIDE_OUT, s);
   return hipGetLastError();
 }

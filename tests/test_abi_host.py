@@ -228,10 +228,20 @@ def test_wide_plan_is_one_chunk(L):
     rc, p = plan_rc(s)
     assert rc == gl.OK
     assert p.fwd_chunk == p.bwd_chunk == 1024 and p.fwd_nseg == p.bwd_nseg == 1
-    # gate prefixes (16 B per padded token) plus the causal score matrix (4 B per pair)
+    # gate prefixes (16 B per padded token), the causal score matrix (4 B per
+    # pair), with 72 triangle tiles for 256 compute units the fp32 partials
+    # of a 4-way split of the score contraction, and the bf16 hi + lo planes
+    # of W_0
     BH, Tp = 2, 1024
     gates = (BH * Tp * 16 + 255) // 256 * 256
-    assert p.workspace_bytes == gates + BH * Tp * Tp * 4
+    planes = 1024 * 4096 * 4
+    assert p.workspace_bytes == gates + BH * Tp * Tp * 4 + 4 * BH * Tp * Tp * 4 + planes
+    # many sequences fill the chip without splitting
+    _, p2 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096))
+    assert p2.workspace_bytes == (64 * Tp * 16 + 255) // 256 * 256 + 64 * Tp * Tp * 4 + 4 * planes
+    # fp32 operands need no planes
+    _, p3 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096, dtype=gl.F32))
+    assert p3.workspace_bytes == p2.workspace_bytes - 4 * planes
     assert gl.workspace_bytes(s) == p.workspace_bytes
 
 

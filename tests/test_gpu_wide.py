@@ -80,6 +80,9 @@ CASES = [
     ("bf16", 512, 128, 128, "0.9", "token", True),
     ("f32", 128, 256, 250, "signed", "token", True),
     ("bf16", 256, 512, 700, "family", "token", True),
+    # contractions of 1024 and 768 split four and two ways (fp32 partials)
+    ("f32", 1024, 128, 200, "family", "token", True),
+    ("bf16", 128, 768, 260, "uniform", "scalar", True),
 ]
 
 
