@@ -17,7 +17,9 @@ host, and secondary measurements of the other workloads (long-context scan,
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
+import math
 import os
 import sys
 import time
@@ -370,6 +372,57 @@ def secondary_gated(gl, torch, W, device, steps=5, warmup=1):
     return res
 
 
+def secondary_mlp_lm(gl, torch, device, steps=5, warmup=2):
+    """The paper's adapted final MLP at its LM width (Appendix E: d = 1024,
+    hidden = 4096, 1024-token context, two sequences per GPU, bf16 activations,
+    tanh-approximate GELU, unit retention, document resets, per-token write
+    strength): forward from costate proposals plus both reverse targets.  Every
+    scan runs the parallel form on the matrix cores."""
+    B, H, T, d, hid, o = 2, 1, 1024, 1024, 4096, 1024
+    gen = torch.Generator(device=device)
+    gen.manual_seed(5)
+
+    def rn(*s, sc=1.0):
+        return (torch.randn(*s, device=device, generator=gen) * sc).contiguous()
+    W10, W20 = rn(H, hid, d, sc=d ** -0.5), rn(H, o, hid, sc=hid ** -0.5)
+    X, Gz, Gy, gY = (rn(B, H, T, w, sc=s).bfloat16() for w, s in ((d, 1.0), (hid, 0.3), (o, 0.3), (o, 1.0)))
+    # write strength mu = 4 sigmoid(b), b ~ N(log(0.9/3.1), 0.5^2); documents of mean length 512
+    mu = (4 * torch.sigmoid(math.log(0.9 / 3.1) + 0.5 * torch.randn(B, H, T, device=device, generator=gen))).contiguous()
+    rs = (torch.rand(B, T, device=device, generator=gen) < 1 / 512).to(torch.uint8)
+    rs[:, 0] = 1
+    args = (W10, W20, X, Gz, Gy)
+    s = gl.MlpShape(B, H, T, d, hid, o, 0, gl.BF16, gl.ACT["gelu_tanh"])
+    n = ctypes.c_size_t(0)
+    gl.lib().gradlev_mlp_workspace_bytes(ctypes.byref(s), ctypes.byref(n))
+    ws = torch.empty(int(n.value), dtype=torch.uint8, device=device)
+
+    def fn(_=0):
+        Z, Hd, Y = gl.mlp_fwd(*args, mu, 1.0, rs, act="gelu_tanh", workspace=ws)
+        gl.mlp_reverse(*args, Z, Hd, gY, mu, 1.0, rs, act="gelu_tanh", workspace=ws)
+    for _ in range(warmup):
+        fn()
+    ms = timed(torch, fn, steps, 1)
+    gl.timing_reset()
+    gl.timing_enable(True, kernels=["wide_score", "wide_out"])
+    timed(torch, fn, steps, 0)
+    gl.timing_enable(False)
+    k = kernel_avgs(gl)
+
+    def scan_flops(din, dout):  # parallel form: W_0 read plus the causal pair sums, per token
+        return B * H * T * (2 * din * dout + (T - 1) * (din + dout))
+    flops = 2 * (scan_flops(d, hid) + scan_flops(hid, o))  # two forward scans, two transpose reads
+    res = {"workload": "paper LM final MLP: B=2, T=1024, 1024 -> 4096 -> 1024, bf16, tanh-GELU, unit retention, "
+                       "document resets (mean 512), per-token write strength; mlp_fwd + mlp_reverse",
+           "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3),
+           "tflops_algorithmic": flops / (ms * 1e-3) / 1e12, "frac_bf16_peak": flops / (ms * 1e-3) / PEAK_BF16,
+           "kernel_avg_us": {k_: round(v[0], 2) for k_, v in k.items() if v[0] is not None},
+           "timing": "K eager steps between two synchronisations (outputs from torch's caching allocator); "
+                     "kernel_avg_us from a second pass with the wide families bracketed by HIP events"}
+    del args, X, Gz, Gy, gY, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
     """Decode steps of the decode-f32 workload (optionally more sequences, fewer
     steps, or the gated update with per-state retention)."""
@@ -529,6 +582,8 @@ def main():
             sec[name] = secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
         log("secondary lm-bf16-gated")
         sec["lm-bf16-gated"] = secondary_gated(gl, torch, W, device)
+        log("secondary mlp-lm (paper LM-width adapted MLP, wide maps)")
+        sec["mlp-lm"] = secondary_mlp_lm(gl, torch, device)
         log("secondary decode-f32")
         sec["decode-f32"] = secondary_decode(gl, torch, W, device)
         log("secondary decode-f32 with 2048 sequences (state larger than the MALL)")
