@@ -423,6 +423,45 @@ def secondary_mlp_lm(gl, torch, device, steps=5, warmup=2):
     return res
 
 
+def secondary_decode_mlp_lm(gl, torch, device, S=16, steps=8):
+    """Deployment steps of the LM-width adapted MLP for S concurrent sequences:
+    per token, the decode step of the 1024 -> 4096 map and of the 4096 -> 1024
+    map on resident fp32 states (16 MiB per map per sequence).  The costates
+    are synthetic (deployment computes them from the LM's backward)."""
+    d, hid = 1024, 4096
+    gen = torch.Generator(device=device)
+    gen.manual_seed(6)
+
+    def rn(*s, sc=1.0):
+        return (torch.randn(*s, device=device, generator=gen) * sc).contiguous()
+    W1, W2 = rn(S, 1, hid, d, sc=d ** -0.5), rn(S, 1, d, hid, sc=hid ** -0.5)
+    xs, g1, g2 = rn(steps, S, 1, d), rn(steps, S, 1, hid, sc=0.1), rn(steps, S, 1, d, sc=0.1)
+    hs = rn(steps, S, 1, hid)
+    y1, y2 = torch.empty(steps, S, 1, hid, device=device), torch.empty(steps, S, 1, d, device=device)
+
+    def run_all(_=0):
+        for t in range(steps):
+            gl.decode_step(W1, xs[t], g1[t], 0.9 / d, out=y1[t])
+            gl.decode_step(W2, hs[t], g2[t], 0.9 / hid, out=y2[t])
+    per_step_bytes = 2 * 4 * (2 * S * hid * d + S * (d + hid) + S * hid + S * d)
+    run_all()
+    torch.cuda.synchronize()
+    ms, _ = graph_timed(torch, gl, lambda i: run_all(), 1, kernels=[])
+    _, k = graph_timed(torch, gl, lambda i: run_all(), 1, kernels=["decode"])
+    step_us = ms * 1e3 / steps
+    res = {"workload": f"LM-width MLP deployment: {S} sequences, 1024 -> 4096 and 4096 -> 1024 fp32 states, "
+                       f"{steps} token steps (two decode launches each) in a HIP graph",
+           "us_per_token_step": step_us, "seq_tokens_per_s": S * steps / (ms * 1e-3),
+           "hbm_GBps_algorithmic": per_step_bytes / (step_us * 1e-6) / 1e9,
+           "frac_hbm_peak": per_step_bytes / (step_us * 1e-6) / PEAK_HBM,
+           "bytes_per_token_step": per_step_bytes}
+    if k["decode"][0]:
+        res["decode_kernel_avg_us"] = k["decode"][0]
+    del W1, W2, xs, g1, g2, hs, y1, y2
+    torch.cuda.empty_cache()
+    return res
+
+
 def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
     """Decode steps of the decode-f32 workload (optionally more sequences, fewer
     steps, or the gated update with per-state retention)."""
@@ -584,6 +623,8 @@ def main():
         sec["lm-bf16-gated"] = secondary_gated(gl, torch, W, device)
         log("secondary mlp-lm (paper LM-width adapted MLP, wide maps)")
         sec["mlp-lm"] = secondary_mlp_lm(gl, torch, device)
+        log("secondary decode-mlp-lm (wide decode states)")
+        sec["decode-mlp-lm"] = secondary_decode_mlp_lm(gl, torch, device)
         log("secondary decode-f32")
         sec["decode-f32"] = secondary_decode(gl, torch, W, device)
         log("secondary decode-f32 with 2048 sequences (state larger than the MALL)")

@@ -157,7 +157,10 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X,
  *   x    [S, H, d_in]  fp32        g [S, H, d_out] fp32
  *   eta  [S, H] fp32 or NULL (then eta_scalar)
  *   y    [S, H, d_out] fp32 output
- * Supported: d_in in {16, 32, 64, 128, 256}; d_out in [1, 1024].
+ * Supported: d_in in {16, 32, 64, 128, 256} with d_out in [1, 1024], or wide
+ * states, d_in in {512, 1024, 2048, 4096, 8192} with d_out in [1, 65536] and
+ * d_in * d_out * 4 < 2^31 (the paper's LM-width MLP maps are 1024 -> 4096 and
+ * 4096 -> 1024).
  * Exclusive only: deployment needs y before the costate g exists. */
 int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                         float* W, const float* x, const float* g,

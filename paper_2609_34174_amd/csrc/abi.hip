@@ -278,6 +278,19 @@ GatedPtrs gated_ptrs(const GatedPlan& p, const gradlev_gates* g, const float* W0
   return f;
 }
 
+// Decode shapes: d_in in {16, ..., 256} with d_out <= 1024, or a wide state
+// with d_in in {512, 1024, 2048, 4096, 8192} and d_out <= 65536 (one state
+// must stay under 2 GiB for 32-bit buffer offsets, and the grid of
+// S * H * ceil(d_out / rows per workgroup) workgroups within 2^31 work-items).
+bool decode_shape_ok(int64_t S, int64_t H, int64_t d_in, int64_t d_out) {
+  if (S > kMaxElems / H || S * H > 0x7fffffff) return false;
+  if (d_in == 16 || d_in == 32 || d_in == 64 || d_in == 128 || d_in == 256) return d_out <= 1024;
+  if (d_in != 512 && d_in != 1024 && d_in != 2048 && d_in != 4096 && d_in != 8192) return false;
+  if (d_out > 65536 || d_in * d_out * 4 >= (int64_t(1) << 31)) return false;
+  const int64_t nch = d_in / 256, rows = 4 * (nch >= 16 ? 1 : 16 / nch);
+  return S * H * ((d_out + rows - 1) / rows) * 256 < (int64_t(1) << 31);
+}
+
 int check_workspace(void* ws, size_t have, size_t need) {
   if (need == 0) return GRADLEV_OK;
   if (!ws || have < need) return GRADLEV_ERR_WORKSPACE;
@@ -644,9 +657,7 @@ int gradlev_decode_step_gated(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                               const uint8_t* reset, float* y, void* stream) {
   if (S < 1 || H < 1 || d_in < 1 || d_out < 1) return GRADLEV_ERR_INVALID;
   if (!W || !W0 || !x || !g || !y) return GRADLEV_ERR_INVALID;
-  if (d_in != 16 && d_in != 32 && d_in != 64 && d_in != 128 && d_in != 256) return GRADLEV_ERR_UNSUPPORTED;
-  if (d_out > 1024) return GRADLEV_ERR_UNSUPPORTED;
-  if (S > kMaxElems / H || S * H > 0x7fffffff) return GRADLEV_ERR_UNSUPPORTED;
+  if (!decode_shape_ok(S, H, d_in, d_out)) return GRADLEV_ERR_UNSUPPORTED;
   if (!aligned16(W) || !aligned16(W0) || !aligned16(x) || !aligned16(g) || !aligned16(y) ||
       (eta && !aligned16(eta)) || (alpha && !aligned16(alpha)))
     return GRADLEV_ERR_ALIGN;
@@ -660,9 +671,7 @@ int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out, float
                         const float* g, const float* eta, float eta_scalar, float* y, void* stream) {
   if (S < 1 || H < 1 || d_in < 1 || d_out < 1) return GRADLEV_ERR_INVALID;
   if (!W || !x || !g || !y) return GRADLEV_ERR_INVALID;
-  if (d_in != 16 && d_in != 32 && d_in != 64 && d_in != 128 && d_in != 256) return GRADLEV_ERR_UNSUPPORTED;
-  if (d_out > 1024) return GRADLEV_ERR_UNSUPPORTED;
-  if (S > kMaxElems / H || S * H > 0x7fffffff) return GRADLEV_ERR_UNSUPPORTED;
+  if (!decode_shape_ok(S, H, d_in, d_out)) return GRADLEV_ERR_UNSUPPORTED;
   if (!aligned16(W) || !aligned16(x) || !aligned16(g) || !aligned16(y) || (eta && !aligned16(eta)))
     return GRADLEV_ERR_ALIGN;
   const hipError_t e = launch_decode(S, H, (int)d_in, (int)d_out, W, x, g, eta, eta_scalar, y,

@@ -72,6 +72,97 @@ decode_kernel(float* __restrict__ W, const float* __restrict__ x, const float* _
   }
 }
 
+// Wide states (d_in = 256 NCH, NCH in {2, 4, ..., 32}): one wave per state
+// row, the row streamed in 256-column chunks (lane l holds columns 4l..4l+3
+// of each chunk: every load and store is a contiguous 1 KiB per wave).  A
+// wave takes U rows at a time with all their chunks' loads issued together
+// (U * NCH = 16 or more 16-byte loads in flight per lane), computes the dot
+// products from the loaded (pre-update) values, writes the update from the
+// same registers and reduces each row's dot product across the wave.  x sits
+// in LDS, loaded once per workgroup.  Workgroup: 4 waves, 4 U rows.
+template <int NCH, bool GATED>
+__global__ void __launch_bounds__(256)
+decode_wide_kernel(float* __restrict__ W, const float* __restrict__ x, const float* __restrict__ g,
+                   const float* __restrict__ eta, float eta_scalar, float* __restrict__ y, int M,
+                   const float* __restrict__ W0, int64_t H, const float* __restrict__ alpha,
+                   float alpha_scalar, const uint8_t* __restrict__ reset, int64_t blocks_per_state) {
+  constexpr int D = 256 * NCH;
+  constexpr int U = NCH >= 16 ? 1 : 16 / NCH;  // rows per wave per pass
+  __shared__ __attribute__((aligned(16))) float xs[D];
+  const int64_t sh = blockIdx.x / blocks_per_state;
+  const int64_t rb = blockIdx.x % blocks_per_state;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int i = tid; i < D / 4; i += 256)
+    reinterpret_cast<f32x4*>(xs)[i] = reinterpret_cast<const f32x4*>(x + sh * D)[i];
+  __syncthreads();
+  const rsrc_t Ws = make_rsrc(W + sh * (int64_t)M * D, (uint32_t)((int64_t)M * D * 4));
+  const rsrc_t Gs = make_rsrc(g + sh * (int64_t)M, (uint32_t)(M * 4));
+  const rsrc_t Ys = make_rsrc(y + sh * (int64_t)M, (uint32_t)(M * 4));
+  const rsrc_t W0s = make_rsrc(GATED ? W0 + (sh % H) * (int64_t)M * D : nullptr,
+                               GATED ? (uint32_t)((int64_t)M * D * 4) : 0u);
+  const float al = GATED ? (alpha ? alpha[sh] : alpha_scalar) : 1.f;
+  const bool fresh = GATED && reset && reset[sh / H] != 0;
+  const float e = eta ? eta[sh] : eta_scalar;
+  // Rows of this wave; rows past M read zero and their stores are dropped.
+  const int r0 = (int)(rb * 4 * U) + w * U;
+  f32x4 wv[U][NCH], w0[GATED ? U : 1][GATED ? NCH : 1];
+  float gv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    gv[u] = buf_load1(Gs, (uint32_t)((r0 + u) * 4));
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const uint32_t o = (uint32_t)((((int64_t)(r0 + u)) * D + 256 * c + 4 * lane) * 4);
+      wv[u][c] = buf_load4(Ws, o, (const float*)nullptr);
+      if constexpr (GATED) w0[u][c] = buf_load4(W0s, o, (const float*)nullptr);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const f32x4 xv = *reinterpret_cast<const f32x4*>(xs + 256 * c + 4 * lane);
+      f32x4 v = wv[u][c];
+      if constexpr (GATED) {
+        if (fresh) v = w0[u][c];
+      }
+      s += v[0] * xv[0] + v[1] * xv[1] + v[2] * xv[2] + v[3] * xv[3];
+      f32x4 nw;
+      if constexpr (GATED) nw = w0[u][c] + al * (v - w0[u][c]) - (e * gv[u]) * xv;
+      else nw = v - (e * gv[u]) * xv;
+      buf_store4<kStoreDefault>(Ws, (uint32_t)((((int64_t)(r0 + u)) * D + 256 * c + 4 * lane) * 4), nw);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+    buf_store1<kStoreDefault>(Ys, lane == 0 ? (uint32_t)((r0 + u) * 4) : kOOB, s);
+  }
+}
+
+static hipError_t launch_decode_wide(int64_t S, int64_t H, int d, int m, float* W, const float* x,
+                                     const float* g, const float* eta, float eta_scalar, float* y,
+                                     hipStream_t s, const DecodeGates* gt) {
+  const float* W0 = gt ? gt->W0 : nullptr;
+  const float* al = gt ? gt->alpha : nullptr;
+  const float as = gt ? gt->alpha_scalar : 1.f;
+  const uint8_t* rs = gt ? gt->reset : nullptr;
+  const int nch = d / 256;
+  const int U = nch >= 16 ? 1 : 16 / nch;
+  const int64_t bps = (m + 4 * U - 1) / (4 * U);
+  const dim3 grid((unsigned)(S * H * bps)), block(256);
+#define GL_DECODE_W(N)                                                                                    if (gt)                                                                                                   hipLaunchKernelGGL((decode_wide_kernel<N, true>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs, bps);   else                                                                                                      hipLaunchKernelGGL((decode_wide_kernel<N, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs, bps);
+  switch (nch) {
+    case 2: GL_DECODE_W(2) break;
+    case 4: GL_DECODE_W(4) break;
+    case 8: GL_DECODE_W(8) break;
+    case 16: GL_DECODE_W(16) break;
+    case 32: GL_DECODE_W(32) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef GL_DECODE_W
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const float* x,
                          const float* g, const float* eta, float eta_scalar, float* y,
                          hipStream_t s, const DecodeGates* gt) {
@@ -86,6 +177,11 @@ hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const flo
   else                                                                                                  \
     hipLaunchKernelGGL((decode_kernel<DD, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs);
   timing_begin(GRADLEV_K_DECODE, s);
+  if (d > 256) {
+    const hipError_t e = launch_decode_wide(S, H, d, m, W, x, g, eta, eta_scalar, y, s, gt);
+    timing_end(GRADLEV_K_DECODE, s);
+    return e;
+  }
   switch (d) {
     case 16: GL_DECODE(16) break;
     case 32: GL_DECODE(32) break;

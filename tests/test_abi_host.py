@@ -268,3 +268,15 @@ def test_wide_backward_refuses_unbuilt_outputs_before_launch(L):
     assert rc == gl.ERR_UNSUPPORTED
     rc = L.gradlev_scan_bwd_gated(*args, FAKE, None, None, None, None, None, FAKE, ctypes.c_size_t(16), None)
     assert rc == gl.ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("d_in,d_out,ok", [(512, 4096, True), (1024, 4096, True), (4096, 1024, True),
+                                           (8192, 65536, False), (8192, 65535, True), (8192, 8192, True), (384, 64, False),
+                                           (1024, 65537, False), (256, 1025, False), (3072, 64, False)])
+def test_decode_shapes(L, d_in, d_out, ok):
+    """Decode validates its state shape before any launch (fake pointers are
+    never touched: an accepted shape is checked here only through the
+    alignment error that a misaligned y produces)."""
+    rc = L.gradlev_decode_step(ctypes.c_int64(2), ctypes.c_int64(1), ctypes.c_int64(d_in), ctypes.c_int64(d_out),
+                               FAKE, FAKE, FAKE, None, ctypes.c_float(0.1), MISALIGNED, None)
+    assert rc == (gl.ERR_ALIGN if ok else gl.ERR_UNSUPPORTED)

@@ -135,7 +135,8 @@ def test_gated_optional_outputs():
 
 
 @pytest.mark.parametrize("d,m,alpha_kind,with_reset", [(64, 64, "state", True), (16, 7, "scalar", False),
-                                                        (128, 128, "state", False), (256, 64, "scalar", True)])
+                                                        (128, 128, "state", False), (256, 64, "scalar", True),
+                                                        (1024, 200, "state", True), (4096, 17, "scalar", False)])
 def test_gated_decode(d, m, alpha_kind, with_reset):
     log(f"gated decode d={d} m={m} alpha={alpha_kind} reset={with_reset}")
     rng = np.random.default_rng(d + m)

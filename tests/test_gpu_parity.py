@@ -333,7 +333,10 @@ def test_longest_sequence(d, prefix, token_eta):
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("d,m,eta_kind", [(64, 64, "scalar"), (16, 7, "state"), (32, 300, "scalar"),
-                                          (128, 128, "state"), (256, 64, "scalar"), (64, 1, "state")])
+                                          (128, 128, "state"), (256, 64, "scalar"), (64, 1, "state"),
+                                          # wide states: one wave per row, ragged row blocks
+                                          (512, 300, "scalar"), (1024, 129, "state"), (2048, 33, "state"),
+                                          (4096, 64, "scalar"), (8192, 5, "state")])
 def test_decode_small(d, m, eta_kind):
     log(f"decode small d={d} m={m} eta={eta_kind}")
     rng = np.random.default_rng(d * 1000 + m)

@@ -174,3 +174,36 @@ def test_mlp_at_lm_width_sampled():
                 ref[k].append(r_)
     for k in got:
         check(k, np.array(got[k]), np.array(ref[k]), "bf16")
+
+
+@pytest.mark.timeout(300)
+def test_decode_at_lm_width():
+    """Deployment steps of the paper's LM-width MLP maps (1024 -> 4096 and
+    4096 -> 1024, fp32 states of 16 MiB per sequence), plain and gated with a
+    document reset, against the float64 decode step of the oracle."""
+    rng = np.random.default_rng(31)
+    S, H, steps = 2, 1, 3
+    for d, m in ((1024, 4096), (4096, 1024)):
+        log(f"decode lm width {d}->{m}, S={S}, {steps} steps, plain then gated")
+        W0 = (rng.standard_normal((H, m, d)) * d ** -0.5).astype(np.float32)
+        for gated in (False, True):
+            Wh = (W0[None] + 0.02 * rng.standard_normal((S, H, m, d))).astype(np.float32)
+            Wd, W0d = to_dev(Wh, "f32", torch), to_dev(W0, "f32", torch)
+            Wr = Wh.astype(np.float64)
+            for step in range(steps):
+                x = rng.standard_normal((S, H, d)).astype(np.float32)
+                g = (rng.standard_normal((S, H, m)) * 0.1).astype(np.float32)
+                eta = (rng.uniform(0.5, 1.5, (S, H)) / d).astype(np.float32)
+                if gated:
+                    al = rng.uniform(0.8, 1.0, (S, H)).astype(np.float32)
+                    rs = np.array([0, 1 if step == 1 else 0], np.uint8)
+                    y = gl.decode_step_gated(Wd, W0d, to_dev(x, "f32", torch), to_dev(g, "f32", torch),
+                                             to_dev(eta, "f32", torch), to_dev(al, "f32", torch),
+                                             torch.from_numpy(rs).to("cuda"))
+                    Wr = np.where(rs[:, None, None, None] != 0, np.broadcast_to(W0, Wr.shape), Wr)
+                    yr, Wr = orc.decode_step(Wr, x, g, eta, alpha=al, W0=W0)
+                else:
+                    y = gl.decode_step(Wd, to_dev(x, "f32", torch), to_dev(g, "f32", torch), to_dev(eta, "f32", torch))
+                    yr, Wr = orc.decode_step(Wr, x, g, eta)
+                check("y", to_host(y), yr, "f32")
+            check("W", to_host(Wd), Wr, "f32")
