@@ -356,6 +356,222 @@ static __global__ void __launch_bounds__(256) wide_score_finish(const WScoreArgs
 // Phase 1 contracts Q with W_0 over the query width, phase 2 contracts S with
 // V over s < 128 (tile + 1).  Tiles are issued heaviest (last rows) first.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Gate gradient of the write strengths (Appendix E keeps gate derivatives):
+//   deta_s = -sum_{t>s} F[t][s] (x_s . x_t) (g_s . dY_t).
+// Each lower-triangle 128 x 128 tile contracts dY G^T (over m) and X X^T
+// (over d) into two accumulators, multiplies them with F and the causal mask,
+// and sums its columns over the rows t of each wave's 64-row half; the partial
+// column sums [BH][2 Tp/128][Tp] are added in a fixed order by
+// wide_deta_reduce, which zeroes the tokens a reset overrides.
+// ---------------------------------------------------------------------------
+struct WDetaArgs {
+  const void* X;
+  const void* G;
+  const void* dY;
+  int64_t T, Tp, d, m, BH, H;
+  const int* zc;
+  const double* lc;
+  float* dpart;
+  float* deta;
+  const uint8_t* reset;
+};
+
+template <class OP, int FMODE>
+static __global__ void __launch_bounds__(256) wide_deta_kernel(const WDetaArgs a) {
+  typedef typename OP::elem E;
+  typedef typename OP::frag F;
+  constexpr int BT = 128, BK = 64, NT = 256;
+  __shared__ __attribute__((aligned(16))) E Ps[BT * BK];
+  __shared__ __attribute__((aligned(16))) E Qs[BT * BK];
+  __shared__ float csum[2][BT];
+
+  const int64_t Kp = a.Tp / BT, per_seq = Kp * (Kp + 1) / 2;
+  const int64_t bh = blockIdx.x / per_seq;
+  int64_t tb, sb;
+  tri_tile(blockIdx.x % per_seq, tb, sb);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wt = w >> 1, ws = w & 1;
+  const int c = lane & 15, q = lane >> 4;
+  const size_t es = sizeof(E);
+
+  f32x4 acc[2][4][4];  // [contraction][s block][t block]: 0: dY_t . g_s, 1: x_t . x_s
+#pragma unroll
+  for (int z = 0; z < 2; ++z)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[z][i][j] = zero4();
+
+#pragma unroll
+  for (int z = 0; z < 2; ++z) {
+    const int64_t w_ = z == 0 ? a.m : a.d;
+    const rsrc_t Qr = make_rsrc(static_cast<const E*>(z == 0 ? a.dY : a.X) + bh * a.T * w_, (uint32_t)(a.T * w_ * es));
+    const rsrc_t Kr = make_rsrc(static_cast<const E*>(z == 0 ? a.G : a.X) + bh * a.T * w_, (uint32_t)(a.T * w_ * es));
+    const uint32_t stride = (uint32_t)(w_ * es);
+    const uint32_t qoff = (uint32_t)(BT * tb * stride), koff = (uint32_t)(BT * sb * stride);
+    GTile<E, BT, BK, NT> qt, kt;
+    qt.load(Qr, qoff, stride, 0, tid);
+    kt.load(Kr, koff, stride, 0, tid);
+    for (int64_t k0 = 0; k0 < w_; k0 += BK) {
+      __syncthreads();
+      qt.store(Qs, tid);
+      kt.store(Ps, tid);
+      __syncthreads();
+      const bool more = k0 + BK < w_;
+      qt.load(Qr, more ? qoff : kOOB, stride, (uint32_t)((k0 + BK) * es), tid);
+      kt.load(Kr, more ? koff : kOOB, stride, (uint32_t)((k0 + BK) * es), tid);
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 32) {
+        F qf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[z][i][j] = OP::mma(acc[z][i][j], pf, qf[j]);
+        }
+      }
+    }
+  }
+
+  // Lane (c, q) of block (i, j): s = s0 + 16 i + 4 q + r, t = t0 + 16 j + c.
+  const int64_t s0 = BT * sb + 64 * ws, t0 = BT * tb + 64 * wt;
+  const int* zc = a.zc + bh * a.Tp;
+  const double* lc = a.lc + bh * a.Tp;
+  const double ref = FMODE == 2 ? lc[s0 + 63] : 0.0;
+  float col[4][4];  // [i][r]: this lane's partial column sums
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) col[i][r] = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t t = t0 + 16 * j + c;
+    int zt = 0;
+    float at = 0.f;
+    if (FMODE >= 1 && t >= 1) zt = zc[t - 1];
+    if (FMODE == 2 && t >= 1) at = (float)(lc[t - 1] - ref);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t s = s0 + 16 * i + 4 * q;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float f = (s + r < t && t < a.T) ? 1.f : 0.f;
+        const int zs = FMODE >= 1 ? zc[s + r] : 0;
+        if (FMODE >= 1 && (zs >> 1) != (zt >> 1)) f = 0.f;
+        if (FMODE == 2 && f != 0.f) f = ((zs ^ zt) & 1 ? -1.f : 1.f) * expf(at + (float)(ref - lc[s + r]));
+        col[i][r] += f * acc[0][i][j][r] * acc[1][i][j][r];
+      }
+    }
+  }
+  // Sum over the 16 rows t held by lanes c = 0..15, then write this wave's
+  // 64-row partial for its 64 columns.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = col[i][r];
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 16);
+      col[i][r] = v;
+    }
+  if (c == 0) {
+    float* out = a.dpart + ((bh * 2 * (a.Tp / BT)) + 2 * tb + wt) * a.Tp;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<f32x4*>(out + s0 + 16 * i + 4 * q) = f32x4{col[i][0], col[i][1], col[i][2], col[i][3]};
+  }
+}
+
+// deta[bh][s] = -(sum of the partial column sums of the row halves at or
+// below s's block, in order), 0 for a token whose write a reset overrides.
+static __global__ void __launch_bounds__(256) wide_deta_reduce(const WDetaArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.BH * a.T) return;
+  const int64_t bh = i / a.T, s = i % a.T, b = bh / a.H;
+  const int64_t nh = 2 * (a.Tp / 128);
+  const float* p = a.dpart + bh * nh * a.Tp + s;
+  float v = 0.f;
+  for (int64_t h = 2 * (s / 128); h < nh; ++h) v += p[h * a.Tp];
+  const bool cut = a.reset && s + 1 < a.T && a.reset[b * a.T + s + 1];
+  a.deta[bh * a.T + s] = cut ? 0.f : -v;
+}
+
+// ---------------------------------------------------------------------------
+// dW0[h] = sum_b sum_t dY_t x_t^T (the decay is centered on W_0, so every read
+// sees W_0 undiscounted).  Tile 128 (i over d_out) x 128 (j over d_in) per
+// head; the contraction runs over the batch rows and tokens in a fixed order,
+// 64 tokens per step, both operands read transposed from row-major token
+// tiles.  Wave (wj, wi) owns a 64 x 64 block D[j][i] (a lane holds 4
+// consecutive j of one i: 16-byte stores into the row-major dW0).
+// ---------------------------------------------------------------------------
+struct WDw0Args {
+  const void* X;
+  const void* dY;
+  float* dW0;
+  int64_t B, H, T, d, m;
+};
+
+template <class OP>
+static __global__ void __launch_bounds__(256) wide_dw0_kernel(const WDw0Args a) {
+  typedef typename OP::elem E;
+  typedef typename OP::frag F;
+  constexpr int BT = 64, BN = 128, NT = 256;
+  __shared__ __attribute__((aligned(16))) E Xs[BT * BN];  // [t][j]
+  __shared__ __attribute__((aligned(16))) E Ds[BT * BN];  // [t][i]
+  const int64_t nJ = a.d / BN, nI = a.m / BN;
+  const int64_t h = blockIdx.x / (nI * nJ), rest = blockIdx.x % (nI * nJ);
+  const int64_t i0 = BN * (rest / nJ), j0 = BN * (rest % nJ);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wj = w >> 1, wi = w & 1;
+  const int c = lane & 15, q = lane >> 4;
+  const size_t es = sizeof(E);
+  f32x4 acc[4][4];  // [j block][i block]
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = zero4();
+  const int64_t nsteps = (a.T + BT - 1) / BT;
+  GTile<E, BT, BN, NT> xt, dt;
+  auto fetch = [&](int64_t k) {
+    const bool ok = k < a.B * nsteps;
+    const int64_t b = ok ? k / nsteps : 0, t0 = ok ? BT * (k % nsteps) : 0;
+    const int64_t bh = b * a.H + h;
+    const rsrc_t Xr = make_rsrc(static_cast<const E*>(a.X) + bh * a.T * a.d, (uint32_t)(a.T * a.d * es));
+    const rsrc_t Dr = make_rsrc(static_cast<const E*>(a.dY) + bh * a.T * a.m, (uint32_t)(a.T * a.m * es));
+    xt.load(Xr, ok ? (uint32_t)(t0 * a.d * es) : kOOB, (uint32_t)(a.d * es), (uint32_t)(j0 * es), tid);
+    dt.load(Dr, ok ? (uint32_t)(t0 * a.m * es) : kOOB, (uint32_t)(a.m * es), (uint32_t)(i0 * es), tid);
+  };
+  fetch(0);
+  for (int64_t k = 0; k < a.B * nsteps; ++k) {
+    __syncthreads();
+    xt.store(Xs, tid);
+    dt.store(Ds, tid);
+    __syncthreads();
+    fetch(k + 1);
+#pragma unroll
+    for (int kk = 0; kk < BT; kk += 32) {
+      F df[4];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) df[y] = OP::load_t(Ds, BN, kk, 64 * wi + 16 * y, lane);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const F xf = OP::load_t(Xs, BN, kk, 64 * wj + 16 * x, lane);
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = OP::mma(acc[x][y], xf, df[y]);
+      }
+    }
+  }
+  // Lane (c, q) of block (x, y): j = j0 + 64 wj + 16 x + 4 q + r, i = i0 + 64 wi + 16 y + c.
+#pragma unroll
+  for (int y = 0; y < 4; ++y) {
+    const int64_t i = i0 + 64 * wi + 16 * y + c;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+      *reinterpret_cast<f32x4*>(a.dW0 + (h * a.m + i) * a.d + j0 + 64 * wj + 16 * x + 4 * q) = acc[x][y];
+  }
+}
+
 // fp32 W_0 split once per call into bf16 hi and lo planes of the same
 // layout (the output tiles then stage bf16 directly; the split costs one
 // pass over W_0 instead of one per row tile).
@@ -582,7 +798,9 @@ size_t wide_workspace_bytes(const WideProblem& p) {
   const int ks = kd > km ? kd : km;  // the forward contracts over d, the read over m
   const size_t part = ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0;
   const size_t planes = p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0;  // W_0 hi + lo
-  return (gates + 255) / 256 * 256 + (S + 255) / 256 * 256 + (part + 255) / 256 * 256 + planes;
+  const size_t dpart = BH * 2 * (Tp / 128) * Tp * 4;               // deta partial column sums
+  return (gates + 255) / 256 * 256 + (S + 255) / 256 * 256 + (part + 255) / 256 * 256 + (planes + 255) / 256 * 256 +
+         dpart;
 }
 
 namespace {
@@ -596,6 +814,7 @@ struct WideWs {
   float* part;
   bf16* Wh;
   bf16* Wl;
+  float* dpart;
 };
 
 WideWs wide_ws(const WideProblem& p, void* ws) {
@@ -615,6 +834,7 @@ WideWs wide_ws(const WideProblem& p, void* ws) {
   char* wp = pt + ((ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0) + 255) / 256 * 256;
   o.Wh = reinterpret_cast<bf16*>(wp);
   o.Wl = reinterpret_cast<bf16*>(wp + (size_t)p.H * p.m * p.d * 2);
+  o.dpart = reinterpret_cast<float*>(wp + ((p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0) + 255) / 256 * 256);
   return o;
 }
 
@@ -692,8 +912,41 @@ hipError_t launch_wide_fwd(const WideProblem& p, const WidePtrs& f, hipStream_t 
   return p.bf16 ? wide_run<OpBF16>(p, f, false, s) : wide_run<OpF32>(p, f, false, s);
 }
 
+// The backward of a wide map: the transpose read (gtilde), the write-strength
+// gradient (deta) and dW0, each when requested.
+template <class OP>
+static hipError_t wide_bwd(const WideProblem& p, const WidePtrs& f, hipStream_t s) {
+  const int64_t BH = p.B * p.H;
+  const WideWs ws = wide_ws(p, f.ws);
+  if (f.gtilde) {
+    const hipError_t e = wide_run<OP>(p, f, true, s);
+    if (e != hipSuccess) return e;
+  } else if (f.deta) {
+    WGateArgs g{f.eta, f.eta_scalar, f.eta_mul, f.alpha, f.alpha_scalar, f.reset, p.H, p.T, p.Tp, ws.cw, ws.zc, ws.lc};
+    hipLaunchKernelGGL(wide_gate_kernel, dim3((unsigned)BH), dim3(256), 0, s, g);
+  }
+  if (f.deta) {
+    WDetaArgs da{f.X, f.G, f.dY, p.T, p.Tp, p.d, p.m, BH, p.H, ws.zc, ws.lc, ws.dpart, f.deta, f.reset};
+    const int64_t Kp = p.Tp / 128;
+    const unsigned grid = (unsigned)(BH * Kp * (Kp + 1) / 2);
+    timing_begin(GRADLEV_K_WIDE_SCORE, s);
+    if (p.fmode == 0) hipLaunchKernelGGL((wide_deta_kernel<OP, 0>), dim3(grid), dim3(256), 0, s, da);
+    else if (p.fmode == 1) hipLaunchKernelGGL((wide_deta_kernel<OP, 1>), dim3(grid), dim3(256), 0, s, da);
+    else hipLaunchKernelGGL((wide_deta_kernel<OP, 2>), dim3(grid), dim3(256), 0, s, da);
+    hipLaunchKernelGGL(wide_deta_reduce, dim3((unsigned)((BH * p.T + 255) / 256)), dim3(256), 0, s, da);
+    timing_end(GRADLEV_K_WIDE_SCORE, s);
+  }
+  if (f.dW0) {
+    WDw0Args wa{f.X, f.dY, f.dW0, p.B, p.H, p.T, p.d, p.m};
+    timing_begin(GRADLEV_K_WIDE_OUT, s);
+    hipLaunchKernelGGL((wide_dw0_kernel<OP>), dim3((unsigned)(p.H * (p.m / 128) * (p.d / 128))), dim3(256), 0, s, wa);
+    timing_end(GRADLEV_K_WIDE_OUT, s);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_wide_read(const WideProblem& p, const WidePtrs& f, hipStream_t s) {
-  return p.bf16 ? wide_run<OpBF16>(p, f, true, s) : wide_run<OpF32>(p, f, true, s);
+  return p.bf16 ? wide_bwd<OpBF16>(p, f, s) : wide_bwd<OpF32>(p, f, s);
 }
 
 }  // namespace gradlev

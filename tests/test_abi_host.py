@@ -231,14 +231,17 @@ def test_wide_plan_is_one_chunk(L):
     # gate prefixes (16 B per padded token), the causal score matrix (4 B per
     # pair), with 72 triangle tiles for 256 compute units the fp32 partials
     # of a 4-way split of the score contraction, and the bf16 hi + lo planes
-    # of W_0
+    # of W_0, and the write-strength gradient's partial column sums (two row
+    # halves per 128-token block)
     BH, Tp = 2, 1024
     gates = (BH * Tp * 16 + 255) // 256 * 256
     planes = 1024 * 4096 * 4
-    assert p.workspace_bytes == gates + BH * Tp * Tp * 4 + 4 * BH * Tp * Tp * 4 + planes
+    dpart = BH * 2 * (Tp // 128) * Tp * 4
+    assert p.workspace_bytes == gates + BH * Tp * Tp * 4 + 4 * BH * Tp * Tp * 4 + planes + dpart
     # many sequences fill the chip without splitting
     _, p2 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096))
-    assert p2.workspace_bytes == (64 * Tp * 16 + 255) // 256 * 256 + 64 * Tp * Tp * 4 + 4 * planes
+    assert p2.workspace_bytes == ((64 * Tp * 16 + 255) // 256 * 256 + 64 * Tp * Tp * 4 + 4 * planes
+                                  + 64 * 2 * (Tp // 128) * Tp * 4)
     # fp32 operands need no planes
     _, p3 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096, dtype=gl.F32))
     assert p3.workspace_bytes == p2.workspace_bytes - 4 * planes

@@ -86,18 +86,25 @@ CASES = [
 ]
 
 
+# The wide backward's outputs: the transpose read, the write-strength
+# gradient and dW0 (what remains when writes are detached).
+WIDE_BWD = ("gtilde", "deta", "dw0")
+
+
 @pytest.mark.parametrize("dtype,d,m,T,ak,ek,rs", CASES)
 def test_wide_gated_parity(dtype, d, m, T, ak, ek, rs):
     log(f"wide gated dtype={dtype} d={d} m={m} T={T} alpha={ak} eta={ek} reset={rs}")
     inp = inputs(2, 2, T, d, m, dtype, seed=T + d + 3 * m, alpha_kind=ak, eta_kind=ek, with_reset=rs)
     W0, X, G, dY, e, a, r = dev_inputs(inp, dtype)
     y = gl.scan_fwd_gated(W0, X, G, e, a, r)
-    gt = gl.scan_bwd_gated(W0, X, G, dY, e, a, r, outputs=("gtilde",))["gtilde"]
+    out = gl.scan_bwd_gated(W0, X, G, dY, e, a, r, outputs=WIDE_BWD)
     torch.cuda.synchronize()
     kw = dict(alpha=inp["alpha"], reset=inp["reset"])
     args = (inp["W0"], inp["X"], inp["G"], inp["eta"])
     check("y", to_host(y), orc.scan_fwd(*args, **kw), dtype)
-    check("gtilde", to_host(gt), orc.scan_bwd(*args, inp["dY"], **kw)["gtilde"], dtype)
+    ref = orc.scan_bwd(*args, inp["dY"], **kw)
+    for k in WIDE_BWD:
+        check(k, to_host(out[k]), ref[k], dtype)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -107,20 +114,23 @@ def test_wide_unit_entry_points(dtype):
     inp = inputs(3, 1, 270, 128, 256, dtype, seed=11, alpha_kind="1", eta_kind="token", with_reset=False)
     W0, X, G, dY, e, _, _ = dev_inputs(inp, dtype)
     y = gl.scan_fwd(W0, X, G, e)
-    gt = gl.scan_bwd(W0, X, G, dY, e, outputs=("gtilde",))["gtilde"]
+    out = gl.scan_bwd(W0, X, G, dY, e, outputs=WIDE_BWD)
     torch.cuda.synchronize()
     args = (inp["W0"], inp["X"], inp["G"], inp["eta"])
     check("y", to_host(y), orc.scan_fwd(*args), dtype)
-    check("gtilde", to_host(gt), orc.scan_bwd(*args, inp["dY"])["gtilde"], dtype)
+    ref = orc.scan_bwd(*args, inp["dY"])
+    for k in WIDE_BWD:
+        check(k, to_host(out[k]), ref[k], dtype)
 
 
 def test_wide_rejects_unbuilt_outputs():
-    """The wide backward returns the transpose read only; other outputs are refused."""
+    """The wide backward refuses the write-side outputs (dX, dG, dalpha)."""
     inp = inputs(1, 1, 64, 256, 128, "bf16", seed=5, alpha_kind="1", eta_kind="scalar", with_reset=False)
     W0, X, G, dY, e, _, _ = dev_inputs(inp, "bf16")
-    with pytest.raises(gl.GradLevError) as ex:
-        gl.scan_bwd(W0, X, G, dY, e, outputs=("gtilde", "dx"))
-    assert ex.value.code == gl.ERR_UNSUPPORTED
+    for outs in (("gtilde", "dx"), ("dg",), ("deta", "dalpha")):
+        with pytest.raises(gl.GradLevError) as ex:
+            gl.scan_bwd_gated(W0, X, G, dY, e, 0.9, outputs=outs)
+        assert ex.value.code == gl.ERR_UNSUPPORTED
 
 
 def doc_start(reset_row, t):
@@ -207,3 +217,50 @@ def test_decode_at_lm_width():
                     yr, Wr = orc.decode_step(Wr, x, g, eta)
                 check("y", to_host(y), yr, "f32")
             check("W", to_host(Wd), Wr, "f32")
+
+
+@pytest.mark.timeout(600)
+def test_lm_width_training_gradients_sampled():
+    """The first map of the paper's adapted MLP (1024 -> 4096) at its training
+    shape: two 1024-token sequences, bf16, per-token step sizes from the gate
+    family, unit retention, document resets.  The forward, the transpose read
+    and the write-strength gradient of sampled tokens are checked against the
+    closed forms of the sequential learner restricted to the token's
+    document (W_read = W_0 minus the writes before it, R = the dY x^T sum
+    after it), and dW0 = sum dY^T X in full."""
+    B, H, T, d, m = 2, 1, 1024, 1024, 4096
+    log(f"lm width training gradients B={B} T={T} {d}->{m} bf16 resets")
+    rng = np.random.default_rng(99)
+    W0 = (rng.standard_normal((H, m, d)) * d ** -0.5).astype(np.float32)
+    X = W.quantise(rng.standard_normal((B, H, T, d)), "bf16")
+    G = W.quantise(rng.standard_normal((B, H, T, m)) * 0.3, "bf16")
+    dY = W.quantise(rng.standard_normal((B, H, T, m)), "bf16")
+    _, eta = W.gate_tokens(B, H, T, d, 101)
+    rs = W.reset_flags(B, T, 102, mean_len=400)
+    dv = lambda a, dt="bf16": to_dev(a, dt, torch)  # noqa: E731
+    args = (dv(W0, "f32"), dv(X), dv(G))
+    y = gl.scan_fwd_gated(*args, dv(eta, "f32"), 1.0, torch.from_numpy(rs).to("cuda"))
+    out = gl.scan_bwd_gated(*args, dv(dY), dv(eta, "f32"), 1.0, torch.from_numpy(rs).to("cuda"), outputs=WIDE_BWD)
+    torch.cuda.synchronize()
+    yh, gth, deh, dwh = to_host(y), to_host(out["gtilde"]), to_host(out["deta"]), to_host(out["dw0"])
+    picks = sorted({0, 1, 127, 128, 500, 1022, 1023, *rng.integers(0, T, 5).tolist()})
+    got = {k: [] for k in ("y", "gtilde", "deta")}
+    ref = {k: [] for k in got}
+    for b in range(B):
+        starts = np.nonzero(rs[b])[0].tolist() + [T]
+        for t in picks:
+            lo = max(s for s in starts if s <= t)
+            hi = min(s for s in starts if s > t)
+            W_read = W0[0].astype(np.float64) - orc.outer_sum(G[b, 0], X[b, 0], eta[b, 0], lo, t)
+            R = orc.outer_sum(dY[b, 0], X[b, 0], 1.0, t + 1, hi)
+            r = orc.token_outputs(W_read, R, X[b, 0, t], G[b, 0, t], eta[b, 0, t], dY[b, 0, t])
+            # a token whose write the next document's reset drops has deta = 0
+            de = 0.0 if hi == t + 1 and t + 1 < T else r["deta"]
+            for k, g_, r_ in (("y", yh[b, 0, t], r["y"]), ("gtilde", gth[b, 0, t], r["gtilde"]),
+                              ("deta", deh[b, 0, t], de)):
+                got[k].append(g_)
+                ref[k].append(r_)
+    for k in got:
+        check(k, np.array(got[k]), np.array(ref[k]), "bf16")
+    dw_ref = np.einsum("bhtm,bhtd->hmd", dY.astype(np.float64), X.astype(np.float64))
+    check("dw0", dwh, dw_ref, "bf16")
