@@ -63,8 +63,8 @@ enum {
 /* Problem description for the scans.
  *   B, H      batch and heads; each (b, h) is an independent sequence (>= 1)
  *   T         tokens per sequence (>= 1, any value; a partial last chunk is masked)
- *   d_in      input width d of the adapted map  (64 or 128)
- *   d_out     output width m of the adapted map (64 or 128)
+ *   d_in      input width d of the adapted map  (64 or 128, or wide: see below)
+ *   d_out     output width m of the adapted map (64 or 128, or wide: see below)
  *   chunk     intra-chunk tile length hint: 0 (library default), 64 or 128.
  *             It changes the rounding order only, never the result in exact
  *             arithmetic; the library may use a smaller tile where a kernel's
@@ -77,6 +77,19 @@ enum {
  *             GRADLEV_ERR_UNSUPPORTED (the default never does).
  *   in_dtype  GRADLEV_F32 or GRADLEV_BF16
  *   prefix    GRADLEV_EXCLUSIVE or GRADLEV_INCLUSIVE */
+/* Wide maps.  When d_in or d_out is above 128 (both multiples of 128, at most
+ * 8192 - the paper's adapted MLP is 1024 -> 4096 -> 1024) the scans run the
+ * parallel form: the chunked form of Appendix C with one chunk spanning the
+ * sequence, i.e. y_t = W0 x_t + sum_{s<t} F_ts c_s (x_s . x_t) g_s with
+ * c_s = -eta_s and F_ts the retention product (1 without gates), and the
+ * transpose read alike.  Results are those of the sequential definition up to
+ * rounding.  Limits: exclusive reads only, T <= 16384 (the workspace holds
+ * the causal B*H*T*T score matrix: gradlev_scan_workspace_bytes), chunk and
+ * segment hints are ignored (the plan reports one chunk of T rounded up to
+ * 128).  The backward returns gtilde, deta and dW0 - the gradients that remain
+ * when writes are detached (Appendix E); dX, dG and dalpha give
+ * GRADLEV_ERR_UNSUPPORTED.  Calls are deterministic: every reduction,
+ * including the split of long score contractions, runs in a fixed order. */
 typedef struct gradlev_shape {
   int64_t B, H, T, d_in, d_out;
   int64_t chunk;
