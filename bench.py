@@ -39,7 +39,9 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The GPU clocks ramp for about 150 steps (~25 ms) of this workload before
+    # settling; the default warm-up covers that twice.
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default="lm-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
