@@ -35,6 +35,10 @@ PEAK_FP32_MFMA = 157.3e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
+SECONDARY_NAMES = ("long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
+                   "decode-f32-S2048", "decode-f32-gated")
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -45,6 +49,8 @@ def parse():
     ap.add_argument("--workload", default="lm-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--only", default=None, choices=SECONDARY_NAMES,
+                    help="run only this secondary workload (after the warm-up) and print its JSON; for profiling")
     ap.add_argument("--cpu-sample-seconds", type=float, default=12.0,
                     help="minimum host time spent timing the float64 oracle")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -522,6 +528,24 @@ def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
     return res
 
 
+def run_secondary(name, gl, torch, W, device):
+    if name in ("long-bf16", "stack-bf16"):
+        return secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
+    if name == "lm-bf16-gated":
+        return secondary_gated(gl, torch, W, device)
+    if name == "mlp-lm":
+        return secondary_mlp_lm(gl, torch, device)
+    if name == "decode-mlp-lm":
+        return secondary_decode_mlp_lm(gl, torch, device)
+    if name == "decode-f32":
+        return secondary_decode(gl, torch, W, device)
+    if name == "decode-f32-S2048":  # state larger than the 256 MB Infinity Cache
+        return secondary_decode(gl, torch, W, device, S=2048, steps=64)
+    if name == "decode-f32-gated":
+        return secondary_decode(gl, torch, W, device, gated=True)
+    raise ValueError(name)
+
+
 def main():
     args = parse()
     if args.ingest_traffic:
@@ -553,6 +577,18 @@ def main():
         log(f"copied {args.copy_calibration} MiB 5 times")
         return
     gl.lib()
+    if args.only:
+        # Profiling aid: the headline workload warms the clocks, then one
+        # secondary runs alone.
+        wl = W.SCAN_WORKLOADS["lm-bf16"]
+        run = ScanRunner(gl, torch, W, wl, 1, device)
+        for i in range(args.warmup):
+            run.step(i)
+        del run
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        print(json.dumps({args.only: run_secondary(args.only, gl, torch, W, device)}), flush=True)
+        return
 
     wl = W.SCAN_WORKLOADS[args.workload]
     log(f"workload {wl.name}: preparing inputs")
@@ -618,21 +654,9 @@ def main():
 
     if not args.no_secondary:
         sec = {}
-        for name in ("long-bf16", "stack-bf16"):
+        for name in SECONDARY_NAMES:
             log(f"secondary {name}")
-            sec[name] = secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
-        log("secondary lm-bf16-gated")
-        sec["lm-bf16-gated"] = secondary_gated(gl, torch, W, device)
-        log("secondary mlp-lm (paper LM-width adapted MLP, wide maps)")
-        sec["mlp-lm"] = secondary_mlp_lm(gl, torch, device)
-        log("secondary decode-mlp-lm (wide decode states)")
-        sec["decode-mlp-lm"] = secondary_decode_mlp_lm(gl, torch, device)
-        log("secondary decode-f32")
-        sec["decode-f32"] = secondary_decode(gl, torch, W, device)
-        log("secondary decode-f32 with 2048 sequences (state larger than the MALL)")
-        sec["decode-f32-S2048"] = secondary_decode(gl, torch, W, device, S=2048, steps=64)
-        log("secondary decode-f32 gated")
-        sec["decode-f32-gated"] = secondary_decode(gl, torch, W, device, gated=True)
+            sec[name] = run_secondary(name, gl, torch, W, device)
         result["secondary"] = sec
 
     if not args.no_cpu_baseline:
