@@ -169,6 +169,28 @@ def graph_timed(torch, gl, fn, steps, kernels=None):
     return ms, k
 
 
+def copy_bandwidth(torch, device, mib=256, reps=20):
+    """Informational: a plain device copy (torch) of `mib` MiB, read + written,
+    on the same box: the practical streaming rate the HBM-bound kernels are
+    compared with (the roofline peak stays the published 8 TB/s)."""
+    n = mib * 2 ** 20 // 4
+    a = torch.ones(n, device=device)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        b.copy_(a)
+    end.record()
+    torch.cuda.synchronize()
+    gbps = 2 * n * 4 / (start.elapsed_time(end) / reps * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbps
+
+
 def kernel_avgs(gl):
     return {k: (ms / n * 1e3 if n else None, n) for k, (ms, n) in gl.timing_read().items()}
 
@@ -621,6 +643,9 @@ def main():
     roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM, "traffic": traffic, "kernel": dom,
                 "kernel_avg_us": dom_us, "algorithmic_bytes_per_launch": dom_bytes}
+    copy_gbps = copy_bandwidth(torch, device)
+    roofline["copy_GBps_same_box"] = copy_gbps  # informational: 256 MiB torch device copy
+    roofline["frac_of_copy"] = (achieved / 1e9) / copy_gbps
     result = {
         "metric": METRIC,
         "value": tokens / step_s,
