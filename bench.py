@@ -4,8 +4,11 @@
 A step is one pass of the whole hot path over one batch: the forward scan and
 the full backward (gtilde, dX, dG, deta, dW0) of the lm-bf16 workload
 (B=8, H=16, T=2048, d=m=64, bf16 inputs, eta=0.1, chunk 64), inputs already
-resident in HBM.  Two input sets alternate between steps so that the 256 MB
-Infinity Cache cannot carry a step's inputs into the next one.
+resident in HBM.  By default the step is the save-for-backward pair (the
+forward keeps each segment's end state, the backward starts from it); the
+plain pair is reported among the secondaries and by --pair plain.  Two input
+sets alternate between steps so that the 256 MB Infinity Cache cannot carry a
+step's inputs into the next one.
 
 Prints ONE JSON line with the headline (fwd+bwd tokens/s, tokens = B*T per
 step), the roofline of the dominant kernel measured with HIP events recorded
@@ -35,18 +38,23 @@ PEAK_FP32_MFMA = 157.3e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-SECONDARY_NAMES = ("long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
+SECONDARY_NAMES = ("lm-bf16-plain", "long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
                    "decode-f32-S2048", "decode-f32-gated")
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    # The GPU clocks ramp for about 150 steps (~25 ms) of this workload before
-    # settling; the default warm-up covers that twice.
-    ap.add_argument("--warmup", type=int, default=300)
+    # 200 steps are one ~25 ms graph replay: long enough that a clock
+    # excursion during the replay moves the figure by little.
+    ap.add_argument("--steps", type=int, default=200)
+    # The GPU clocks ramp over the first few hundred steps and keep drifting
+    # for about a second; 10000 eager steps (~1.5 s) settle them.
+    ap.add_argument("--warmup", type=int, default=10000)
     ap.add_argument("--workload", default="lm-bf16")
+    ap.add_argument("--pair", default="saved", choices=("plain", "saved"),
+                    help="plain: scan_fwd + scan_bwd; saved: scan_fwd_save + scan_bwd_saved (the forward keeps "
+                         "segment-end states and the backward starts from them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--only", default=None, choices=SECONDARY_NAMES,
@@ -91,13 +99,19 @@ def log(msg):
 class ScanRunner:
     """Preallocated inputs/outputs/workspace for repeated fwd+bwd steps."""
 
-    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0):
+    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False):
         self.gl, self.torch, self.wl = gl, torch, wl
         self.sets = [W.device_scan_inputs(wl, layer0 + i, device, torch=torch) for i in range(nsets)]
         self.shape = gl.make_shape(wl.B, wl.H, wl.T, wl.d, wl.m,
                                    gl.BF16 if wl.dtype == "bf16" else gl.F32, chunk=wl.chunk)
         self.plan = gl.plan(self.shape)
-        self.ws = torch.empty(max(self.plan.workspace_bytes, 256), dtype=torch.uint8, device=device)
+        self.saved = None
+        ws_bytes = self.plan.workspace_bytes
+        if saved:
+            sv_bytes, ws_bytes = gl.saved_bytes(self.shape)
+            self.saved = torch.empty(sv_bytes // 4, dtype=torch.float32, device=device)
+            self.saved_nseg = sv_bytes // (wl.B * wl.H * wl.m * wl.d * 4)
+        self.ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
         f32 = dict(dtype=torch.float32, device=device)
         B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
         self.Y = torch.empty(B, H, T, m, **f32)
@@ -107,6 +121,12 @@ class ScanRunner:
 
     def step(self, i):
         s = self.sets[i % len(self.sets)]
+        if self.saved is not None:
+            self.gl.scan_fwd_save(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
+                                  saved=self.saved, workspace=self.ws)
+            self.gl.scan_bwd_saved(s["W0"], s["X"], s["G"], s["dY"], self.saved, s["eta"], chunk=self.wl.chunk,
+                                   out=self.outs, workspace=self.ws)
+            return
         self.gl.scan_fwd(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
                          workspace=self.ws)
         self.gl.scan_bwd(s["W0"], s["X"], s["G"], s["dY"], s["eta"], chunk=self.wl.chunk,
@@ -323,14 +343,14 @@ def cpu_baseline(W, wl, min_seconds):
                       f"fwd {t_fwd:.1f} s + bwd {t_bwd:.1f} s of float64 numpy on one thread"}
 
 
-def secondary_scan(gl, torch, W, name, steps, warmup, device):
+def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True, nsets=1):
     wl = W.SCAN_WORKLOADS[name]
     if wl.layers == 1:
-        run = ScanRunner(gl, torch, W, wl, 1, device)
+        run = ScanRunner(gl, torch, W, wl, nsets, device, saved=saved)
         fn = run.step
         runs = [run]
     else:
-        runs = [ScanRunner(gl, torch, W, wl, 1, device, layer0=l) for l in range(wl.layers)]
+        runs = [ScanRunner(gl, torch, W, wl, 1, device, layer0=l, saved=saved) for l in range(wl.layers)]
         # Layers share output buffers: the write traffic is identical and 24
         # separate sets would only add allocation.
         for r in runs[1:]:
@@ -551,6 +571,8 @@ def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
 
 
 def run_secondary(name, gl, torch, W, device):
+    if name == "lm-bf16-plain":  # the headline step without the saved segment states
+        return secondary_scan(gl, torch, W, "lm-bf16", 20, 50, device, saved=False, nsets=2)
     if name in ("long-bf16", "stack-bf16"):
         return secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
     if name == "lm-bf16-gated":
@@ -614,7 +636,7 @@ def main():
 
     wl = W.SCAN_WORKLOADS[args.workload]
     log(f"workload {wl.name}: preparing inputs")
-    run = ScanRunner(gl, torch, W, wl, 2, device)
+    run = ScanRunner(gl, torch, W, wl, 2, device, saved=args.pair == "saved")
     plan = run.plan
     work = scan_work(wl, plan)
 
@@ -661,9 +683,13 @@ def main():
         "data": "synthetic: seeded device RNG with the workload's shapes and distributions",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_in": wl.d, "d_out": wl.m,
                    "chunk": wl.chunk, "eta": wl.eta, "prefix": "exclusive",
-                   "step": "scan_fwd + scan_bwd with gtilde, dX, dG, deta, dW0",
-                   "plan": {"fwd": [plan.fwd_chunk, plan.fwd_segment, plan.fwd_nseg],
-                            "bwd": [plan.bwd_chunk, plan.bwd_segment, plan.bwd_nseg]}},
+                   "step": ("scan_fwd_save + scan_bwd_saved" if run.saved is not None else "scan_fwd + scan_bwd")
+                   + " with gtilde, dX, dG, deta, dW0",
+                   "plan": ({"saved_pair_segments": run.saved_nseg,
+                             "saved_state_bytes": run.saved.numel() * 4,
+                             "chunks": [plan.fwd_chunk, plan.bwd_chunk]} if run.saved is not None else
+                            {"fwd": [plan.fwd_chunk, plan.fwd_segment, plan.fwd_nseg],
+                             "bwd": [plan.bwd_chunk, plan.bwd_segment, plan.bwd_nseg]})},
         "roofline": roofline,
         "step_roofline": {"hbm_GBps_algorithmic": work["bytes"] / step_s / 1e9,
                           "frac_hbm_peak": work["bytes"] / step_s / PEAK_HBM,

@@ -159,6 +159,41 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X,
                      float* deta, float* dW0, void* workspace,
                      size_t workspace_bytes, void* stream);
 
+/* Save-for-backward pair.  A training step that runs the forward and then the
+ * backward on the same inputs can let the forward keep the fast weights at the
+ * end of each of its token segments (the prefix sums of Section 3 step 2,
+ * Eq. 3, at the segment boundaries); the backward then starts every segment
+ * from the saved state instead of re-reading X and G to rebuild it, which
+ * removes one of its two streaming passes over the inputs.
+ *
+ * gradlev_scan_saved_bytes: bytes of the saved state (*saved_bytes) and of the
+ *   workspace both calls need (*workspace_bytes) for *s.  Pure host
+ *   computation.  Both calls of a pair take the same shape, the same segment
+ *   hint, and a workspace of at least *workspace_bytes.
+ * gradlev_scan_fwd_save: as gradlev_scan_fwd, and also writes the state to
+ *   saved [B*H][n_seg][m][d] fp32 (W after the last write of each segment,
+ *   row-major; n_seg is private to the plan, only the byte count is public).
+ * gradlev_scan_bwd_saved: as gradlev_scan_bwd, reading the state that
+ *   gradlev_scan_fwd_save wrote for the same W0, X, G and eta; the caller
+ *   keeps that buffer unmodified between the two calls.  Its results equal
+ *   gradlev_scan_bwd's up to float32 rounding order.
+ * saved must be 16-byte aligned device memory of at least the returned size
+ * (GRADLEV_ERR_WORKSPACE otherwise).  Shapes that gradlev_scan_fwd runs in
+ * the parallel form (a width above 128) return GRADLEV_ERR_UNSUPPORTED: that
+ * form has no segment states. */
+int gradlev_scan_saved_bytes(const gradlev_shape* s, size_t* saved_bytes,
+                             size_t* workspace_bytes);
+int gradlev_scan_fwd_save(const gradlev_shape* s, const float* W0, const void* X,
+                          const void* G, const float* eta, float eta_scalar,
+                          float* Y, float* saved, size_t saved_bytes,
+                          void* workspace, size_t workspace_bytes, void* stream);
+int gradlev_scan_bwd_saved(const gradlev_shape* s, const float* W0, const void* X,
+                           const void* G, const float* eta, float eta_scalar,
+                           const void* dY, const float* saved, size_t saved_bytes,
+                           float* gtilde, float* dX, float* dG, float* deta,
+                           float* dW0, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
 /* One deployment step for S sequences x H heads (Section 3, "Training
  * objective", last sentences; Appendix A, last sentence): score with the
  * current weights, then write the true costate.

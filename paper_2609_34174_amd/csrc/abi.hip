@@ -42,6 +42,17 @@ int64_t pick_nseg(int64_t BH, int64_t T, int C, int wgs_per_cu, int64_t hint) {
   return seg_chunks;
 }
 
+// Workspace of a plan: forward segment aggregates; backward aggregates A_k,
+// B_k and the per-sequence dY x^T sums.
+void layout_ws(Plan* out, int64_t BH, size_t md) {
+  out->ws_fwd = out->fwd.nseg > 1 ? round_up((size_t)BH * out->fwd.nseg * md, 256) : 0;
+  const size_t agg_b = out->bwd.nseg > 1 ? round_up((size_t)BH * out->bwd.nseg * md, 256) : 0;
+  out->off_aggA = 0;
+  out->off_aggB = round_up((size_t)BH * out->bwd.nseg * md, 256);
+  out->off_rfin = out->off_aggB + agg_b;
+  out->ws_bwd = out->off_rfin + round_up((size_t)BH * md, 256);
+}
+
 int make_plan(const gradlev_shape* s, Plan* out) {
   if (!s || !out) return GRADLEV_ERR_INVALID;
   if (s->B < 1 || s->H < 1 || s->T < 1 || s->d_in < 1 || s->d_out < 1) return GRADLEV_ERR_INVALID;
@@ -86,12 +97,26 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   out->bwd.nseg = (s->T + out->bwd.seg_len - 1) / out->bwd.seg_len;
   if (out->bwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
 
-  out->ws_fwd = out->fwd.nseg > 1 ? round_up((size_t)BH * out->fwd.nseg * md, 256) : 0;
-  const size_t agg_b = out->bwd.nseg > 1 ? round_up((size_t)BH * out->bwd.nseg * md, 256) : 0;
-  out->off_aggA = 0;
-  out->off_aggB = round_up((size_t)BH * out->bwd.nseg * md, 256);
-  out->off_rfin = out->off_aggB + agg_b;
-  out->ws_bwd = out->off_rfin + round_up((size_t)BH * md, 256);
+  layout_ws(out, BH, md);
+  return GRADLEV_OK;
+}
+
+// The save-for-backward pair: the forward saves the weights at each of its
+// segments' ends and the backward starts its segments from them, so both run
+// on one segmentation: the shorter of the two segment lengths (the backward
+// is the longer pass and wants its parallelism), rounded up to the forward's
+// tile.  The backward tile (32 or 64 tokens) divides the forward's (64 or 128).
+int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
+  const int rc = make_plan(s, out);
+  if (rc != GRADLEV_OK) return rc;
+  const int64_t fc = out->fwd.chunk;
+  const int64_t bs = (out->bwd.seg_len + fc - 1) / fc * fc;
+  const int64_t seg = out->fwd.seg_len < bs ? out->fwd.seg_len : bs;
+  out->fwd.seg_len = out->bwd.seg_len = seg;
+  out->fwd.nseg = out->bwd.nseg = (s->T + seg - 1) / seg;
+  const size_t md = (size_t)s->d_out * s->d_in * sizeof(float);
+  layout_ws(out, s->B * s->H, md);
+  *saved_bytes = (size_t)(s->B * s->H) * out->fwd.nseg * md;
   return GRADLEV_OK;
 }
 
@@ -359,16 +384,16 @@ int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes) {
   return GRADLEV_OK;
 }
 
-int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
-                     const float* eta, float eta_scalar, float* Y, void* workspace,
-                     size_t workspace_bytes, void* stream) {
-  if (wide_shape(s)) {
-    const gradlev_gates none{nullptr, 1.f, nullptr};
-    return gradlev_scan_fwd_gated(s, &none, W0, X, G, eta, eta_scalar, Y, workspace, workspace_bytes, stream);
-  }
-  Plan p;
-  int rc = make_plan(s, &p);
-  if (rc != GRADLEV_OK) return rc;
+}  // extern "C"
+
+namespace gradlev {
+namespace {
+
+// Forward with a validated plan; wend (saved segment-end weights) or null.
+int scan_fwd_planned(const Plan& p, const float* W0, const void* X, const void* G, const float* eta,
+                     float eta_scalar, float* Y, float* wend, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  int rc;
   if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
   if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
     return GRADLEV_ERR_ALIGN;
@@ -382,22 +407,16 @@ int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, con
   f.eta_scalar = eta_scalar;
   f.Y = Y;
   f.agg = static_cast<float*>(workspace);
+  f.wend = wend;
   const hipError_t e = launch_scan_fwd(p.fwd, f, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }
 
-int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
-                     const float* eta, float eta_scalar, const void* dY, float* gtilde,
-                     float* dX, float* dG, float* deta, float* dW0, void* workspace,
-                     size_t workspace_bytes, void* stream) {
-  if (wide_shape(s)) {
-    const gradlev_gates none{nullptr, 1.f, nullptr};
-    return gradlev_scan_bwd_gated(s, &none, W0, X, G, eta, eta_scalar, dY, gtilde, dX, dG, deta, nullptr, dW0,
-                                  workspace, workspace_bytes, stream);
-  }
-  Plan p;
-  int rc = make_plan(s, &p);
-  if (rc != GRADLEV_OK) return rc;
+// Backward with a validated plan; wend (the forward's saved weights) or null.
+int scan_bwd_planned(const Plan& p, const float* W0, const void* X, const void* G, const float* eta,
+                     float eta_scalar, const void* dY, const float* wend, float* gtilde, float* dX, float* dG,
+                     float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc;
   if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
   if (!gtilde && !dX && !dG && !deta && !dW0) return GRADLEV_ERR_INVALID;
   const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dW0};
@@ -421,8 +440,85 @@ int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, con
   b.aggA = reinterpret_cast<float*>(ws + p.off_aggA);
   b.aggB = reinterpret_cast<float*>(ws + p.off_aggB);
   b.rfin = reinterpret_cast<float*>(ws + p.off_rfin);
+  b.wend = wend;
   const hipError_t e = launch_scan_bwd(p.bwd, b, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+}  // namespace
+}  // namespace gradlev
+
+extern "C" {
+
+int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                     const float* eta, float eta_scalar, float* Y, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) {
+    const gradlev_gates none{nullptr, 1.f, nullptr};
+    return gradlev_scan_fwd_gated(s, &none, W0, X, G, eta, eta_scalar, Y, workspace, workspace_bytes, stream);
+  }
+  Plan p;
+  const int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  return scan_fwd_planned(p, W0, X, G, eta, eta_scalar, Y, nullptr, workspace, workspace_bytes, stream);
+}
+
+int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                     const float* eta, float eta_scalar, const void* dY, float* gtilde,
+                     float* dX, float* dG, float* deta, float* dW0, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) {
+    const gradlev_gates none{nullptr, 1.f, nullptr};
+    return gradlev_scan_bwd_gated(s, &none, W0, X, G, eta, eta_scalar, dY, gtilde, dX, dG, deta, nullptr, dW0,
+                                  workspace, workspace_bytes, stream);
+  }
+  Plan p;
+  const int rc = make_plan(s, &p);
+  if (rc != GRADLEV_OK) return rc;
+  return scan_bwd_planned(p, W0, X, G, eta, eta_scalar, dY, nullptr, gtilde, dX, dG, deta, dW0, workspace,
+                          workspace_bytes, stream);
+}
+
+int gradlev_scan_saved_bytes(const gradlev_shape* s, size_t* saved_bytes, size_t* workspace_bytes) {
+  if (!saved_bytes || !workspace_bytes) return GRADLEV_ERR_INVALID;
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  Plan p;
+  size_t sb = 0;
+  const int rc = make_saved_plan(s, &p, &sb);
+  if (rc != GRADLEV_OK) return rc;
+  *saved_bytes = sb;
+  *workspace_bytes = p.ws_fwd > p.ws_bwd ? p.ws_fwd : p.ws_bwd;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_fwd_save(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                          const float* eta, float eta_scalar, float* Y, float* saved, size_t saved_bytes,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  Plan p;
+  size_t need = 0;
+  const int rc = make_saved_plan(s, &p, &need);
+  if (rc != GRADLEV_OK) return rc;
+  if (!saved) return GRADLEV_ERR_INVALID;
+  if (!aligned16(saved)) return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < need) return GRADLEV_ERR_WORKSPACE;
+  return scan_fwd_planned(p, W0, X, G, eta, eta_scalar, Y, saved, workspace, workspace_bytes, stream);
+}
+
+int gradlev_scan_bwd_saved(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                           const float* eta, float eta_scalar, const void* dY, const float* saved,
+                           size_t saved_bytes, float* gtilde, float* dX, float* dG, float* deta, float* dW0,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  Plan p;
+  size_t need = 0;
+  const int rc = make_saved_plan(s, &p, &need);
+  if (rc != GRADLEV_OK) return rc;
+  if (!saved) return GRADLEV_ERR_INVALID;
+  if (!aligned16(saved)) return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < need) return GRADLEV_ERR_WORKSPACE;
+  return scan_bwd_planned(p, W0, X, G, eta, eta_scalar, dY, saved, gtilde, dX, dG, deta, dW0, workspace,
+                          workspace_bytes, stream);
 }
 
 int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes) {

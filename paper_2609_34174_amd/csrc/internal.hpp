@@ -24,7 +24,8 @@ struct FwdPtrs {
   const float* eta;
   float eta_scalar;
   float* Y;
-  float* agg;  // [B*H][nseg][m][d] workspace, or nullptr when nseg == 1
+  float* agg;   // [B*H][nseg][m][d] workspace, or nullptr when nseg == 1
+  float* wend;  // [B*H][nseg][m][d] weights at each segment's end (saved for a backward), or nullptr
 };
 
 struct BwdPtrs {
@@ -42,6 +43,7 @@ struct BwdPtrs {
   float* aggA;   // [B*H][nseg][d][m]: segment write aggregates (transposed)
   float* aggB;   // [B*H][nseg][d][m]: segment dY x^T aggregates (transposed)
   float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
+  const float* wend;  // the forward's saved segment-end weights (same segments), or nullptr
 };
 
 // Gated scans (retention and resets).  Workspace: segment aggregates

@@ -40,6 +40,7 @@ struct BArgs {
   const float* aggA;  // [BH][nseg][d][m]: per-segment write aggregates A_k, transposed
   const float* aggB;  // [BH][nseg][d][m]: per-segment dY x^T aggregates B_k (k >= 1), or null
   float* rfin;        // [BH][m][d]: full-sequence dY x^T (written by segment 0), or null
+  const float* wend;  // [BH][nseg][m][d]: the forward's segment-end weights, or null (then W_0 - sum A)
 };
 
 // Output modes compiled separately so that no accumulator crosses a runtime
@@ -128,13 +129,15 @@ bwd_main_kernel(const BArgs a) {
   // and R = sum_{j>seg} B_j (added from the last segment down).
   f32x4 Wj[IB], Rj[IB];
   if (w < JB) {
-    const float* w0 = a.W0 + (bh % a.H) * M * D;
+    // The segment's end state: saved by the forward, or W_0 minus the
+    // aggregated writes up to and including this segment.
+    const float* w0 = a.wend ? a.wend + (bh * a.nseg + seg) * M * D : a.W0 + (bh % a.H) * M * D;
 #pragma unroll
     for (int ib = 0; ib < IB; ++ib)
 #pragma unroll
       for (int r = 0; r < 4; ++r) Wj[ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c];
     const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
-    for (int64_t j0 = 0; j0 <= seg; j0 += 4) {
+    for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += 4) {
       f32x4 v[4][IB];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
@@ -520,12 +523,22 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   k.aggB = f.aggB;
   // Segment aggregates (writes, and dY x^T when a suffix is needed); each
   // workgroup of the main kernel sums the ones it needs in its prologue.
-  timing_begin(GRADLEV_K_BWD_AGG, s);
-  if (need_sfx)
-    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdAB, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
-  else
-    hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdA, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
-  timing_end(GRADLEV_K_BWD_AGG, s);
+  // With the forward's saved segment-end weights only the dY x^T aggregates
+  // are left to compute (none when the suffix is not needed).
+  if (f.wend) {
+    if (need_sfx) {
+      timing_begin(GRADLEV_K_BWD_AGG, s);
+      hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdB, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+      timing_end(GRADLEV_K_BWD_AGG, s);
+    }
+  } else {
+    timing_begin(GRADLEV_K_BWD_AGG, s);
+    if (need_sfx)
+      hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdAB, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+    else
+      hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdA, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+    timing_end(GRADLEV_K_BWD_AGG, s);
+  }
 
   BArgs b{};
   b.W0 = f.W0;
@@ -546,6 +559,7 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   b.aggA = f.aggA;
   b.aggB = need_sfx ? f.aggB : nullptr;
   b.rfin = f.dW0 ? f.rfin : nullptr;
+  b.wend = f.wend;
   timing_begin(GRADLEV_K_BWD_MAIN, s);
   if (read_only) {
     if (p.inclusive)

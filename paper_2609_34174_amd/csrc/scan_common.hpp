@@ -20,6 +20,7 @@ struct KArgs {
   float* out0;   // fwd: Y
   float* aggA;   // [BH][nseg][m*d] write aggregates A_k (fwd: [m][d]; bwd: transposed [d][m])
   float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates B_k (k >= 1)
+  float* wend;   // fwd, or null: [BH][nseg][m][d] fast weights at each segment's end
 };
 
 // ---------------------------------------------------------------------------
@@ -141,14 +142,17 @@ __device__ __forceinline__ rsrc_t eta_rsrc(const float* eta, int64_t bh, int64_t
 // bf16 products and eta scales the sum once; per-token eta is folded into a
 // hi + lo split operand staged once per chunk.
 // ---------------------------------------------------------------------------
-enum AggMode { kAggFwd = 0, kAggBwdA = 1, kAggBwdAB = 2 };
+// kAggBwdB: the dY x^T aggregates only (segments >= 1), for a backward that
+// starts from the forward's saved segment-end weights and needs no A_k.
+enum AggMode { kAggFwd = 0, kAggBwdA = 1, kAggBwdAB = 2, kAggBwdB = 3 };
 
 template <class OP, int D, int M, int C, int MODE, bool ETAV>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
 agg_kernel(const KArgs a, int64_t nagg) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
-  constexpr bool BWD = MODE == kAggBwdAB;    // also aggregate dY x^T
+  constexpr bool BWD = MODE == kAggBwdAB || MODE == kAggBwdB;  // aggregate dY x^T
+  constexpr bool WA = MODE != kAggBwdB;                          // aggregate the writes
   constexpr bool TRANS = MODE != kAggFwd;    // backward layout
   constexpr bool SPLITV = ETAV && OP::kSplit == 2;
   constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
@@ -161,13 +165,14 @@ agg_kernel(const KArgs a, int64_t nagg) {
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg) || seg >= nagg) return;
+  if (!WA && seg == 0) return;  // B_0 is never needed
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
   const bool with_b = BWD && seg >= 1;
   const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
-  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t G = make_rsrc(WA ? static_cast<const E*>(a.G) + bh * T * M : nullptr, WA ? (uint32_t)(T * M * sizeof(E)) : 0u);
   const rsrc_t Dy = make_rsrc(BWD ? static_cast<const E*>(a.dY) + bh * T * M : nullptr, BWD ? (uint32_t)(T * M * sizeof(E)) : 0u);
 
   f32x4 accA[JB], accB[JB];
@@ -185,9 +190,9 @@ agg_kernel(const KArgs a, int64_t nagg) {
   const rsrc_t Et = eta_rsrc(a.eta, bh, T);
   auto fetch = [&](int k, int64_t t0) {
     const bool ok = t0 < t_end;
-    er[k].load(Et, ok ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    if (WA) er[k].load(Et, ok ? (uint32_t)(t0 * 4) : kOOB, tid, C);
     xr[k].load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
-    gr[k].load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    if (WA) gr[k].load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
     if (with_b) dr[k].load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
 #pragma unroll
@@ -196,11 +201,11 @@ agg_kernel(const KArgs a, int64_t nagg) {
   auto chunk = [&](int k, int64_t t0) {
     const int nvalid = (int)(t_end - t0 < C ? (t_end > t0 ? t_end - t0 : 0) : C);
     __syncthreads();
-    if (ETAV) er[k].stage(et, C, a.eta_scalar, nvalid, 1.f, tid);
+    if (WA && ETAV) er[k].stage(et, C, a.eta_scalar, nvalid, 1.f, tid);
     xr[k].store(Xs, tid);
     if (with_b) dr[k].store(Ds, tid);
-    if (!ETAV) gr[k].store(Gs, tid);
-    if (ETAV) {
+    if (WA && !ETAV) gr[k].store(Gs, tid);
+    if (WA && ETAV) {
       __syncthreads();
       gr[k].store_scaled(Gs, Gl, tid, et);
     }
@@ -210,16 +215,21 @@ agg_kernel(const KArgs a, int64_t nagg) {
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
         // A^T[j][i] += sum_t X[t][j] (eta G)[t][i];  B^T[j][i] += sum_t X[t][j] dY[t][i]
-        const F gh = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
-        F gl = gh;
-        if constexpr (SPLITV) gl = OP::load_t(Gl, M, 32 * kb, 16 * w, lane);
-        F dv = gh;
+        F gh, gl, dv;
+        if constexpr (WA) {
+          gh = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
+          gl = gh;
+          if constexpr (SPLITV) gl = OP::load_t(Gl, M, 32 * kb, 16 * w, lane);
+          dv = gh;
+        }
         if (with_b) dv = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) {
           const F xa = OP::load_t(Xs, D, 32 * kb, 16 * jb, lane);
-          if constexpr (ETAV) accA[jb] = mma_split_b<OP>(accA[jb], xa, gh, gl);
-          else accA[jb] = OP::mma(accA[jb], xa, gh);
+          if constexpr (WA) {
+            if constexpr (ETAV) accA[jb] = mma_split_b<OP>(accA[jb], xa, gh, gl);
+            else accA[jb] = OP::mma(accA[jb], xa, gh);
+          }
           if (with_b) accB[jb] = OP::mma(accB[jb], xa, dv);
         }
       }
@@ -235,7 +245,8 @@ agg_kernel(const KArgs a, int64_t nagg) {
     const float s = ETAV ? 1.f : a.eta_scalar;
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) {
-      if (TRANS) {
+      if constexpr (!WA) {
+      } else if (TRANS) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) a.aggA[base + (int64_t)(16 * jb + 4 * q + r) * M + 16 * w + c] = s * accA[jb][r];
       } else {

@@ -231,6 +231,13 @@ fwd_main_kernel(const KArgs a) {
     chunk(xa, ga, ea, t0);
     chunk(xb, gb, eb, t0 + C);
   }
+  // Saved for a backward: the fast weights after this segment's last write
+  // (row-major [m][d]; lane (c, q) holds W[16w + c][16jb + 4q .. +3]).
+  if (a.wend && w < IB) {
+    float* o = a.wend + (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -310,6 +317,7 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& f, hipStream_t s
   k.out0 = f.Y;
   k.aggA = p.nseg > 1 ? f.agg : nullptr;
   k.aggB = nullptr;
+  k.wend = f.wend;
   if (p.bf16) {
     if (p.chunk == 128) return fwd_by_dims<OpBF16, 128>(p, k, s);
     return fwd_by_dims<OpBF16, 64>(p, k, s);

@@ -132,6 +132,56 @@ def test_bwd_validation_before_launch(L):
     assert bwd_call(s, wsn=1024) == gl.ERR_WORKSPACE
 
 
+@pytest.mark.parametrize("kw", [dict(), dict(B=8, H=16, T=2048), dict(d_in=128, d_out=128, chunk=128),
+                                dict(dtype=gl.F32, d_in=128), dict(T=1), dict(segment=64, T=1000),
+                                dict(B=1, H=1, T=1 << 20)])
+def test_saved_pair_sizes(L, kw):
+    """The saved state is one fp32 [m][d] matrix per sequence and segment, on
+    one segmentation no coarser than the forward's; the workspace covers both
+    calls of the pair."""
+    s = shape(**kw)
+    p = gl.plan(s)
+    sv, ws = gl.saved_bytes(s)
+    md = s.d_in * s.d_out * 4
+    assert sv % (s.B * s.H * md) == 0
+    nseg = sv // (s.B * s.H * md)
+    assert p.fwd_nseg <= nseg <= 16
+    seg = -(-s.T // nseg)
+    assert -(-s.T // (-(-seg // p.fwd_chunk) * p.fwd_chunk)) == nseg  # a whole number of forward tiles
+    agg = s.B * s.H * nseg * md if nseg > 1 else 0
+    assert ws >= agg + s.B * s.H * md
+
+
+def saved_fwd_call(s, saved=FAKE, svn=1 << 40, Y=FAKE):
+    return gl.lib().gradlev_scan_fwd_save(ctypes.byref(s), FAKE, FAKE, FAKE, None, 0.1, Y, saved, svn,
+                                          FAKE, 1 << 40, None)
+
+
+def saved_bwd_call(s, saved=FAKE, svn=1 << 40, outs=(FAKE, FAKE, FAKE, FAKE, FAKE), wsn=1 << 40):
+    return gl.lib().gradlev_scan_bwd_saved(ctypes.byref(s), FAKE, FAKE, FAKE, None, 0.1, FAKE, saved, svn,
+                                           *outs, FAKE, wsn, None)
+
+
+def test_saved_pair_validation_before_launch(L):
+    s = shape()
+    sv, _ = gl.saved_bytes(s)
+    for call in (saved_fwd_call, saved_bwd_call):
+        assert call(s, saved=None) == gl.ERR_INVALID
+        assert call(s, saved=MISALIGNED) == gl.ERR_ALIGN
+        assert call(s, svn=sv - 4) == gl.ERR_WORKSPACE
+        assert call(shape(d_in=32)) == gl.ERR_UNSUPPORTED
+        assert call(shape(B=0)) == gl.ERR_INVALID
+        # Parallel-form widths keep no segment states.
+        assert call(shape(d_in=1024, d_out=128)) == gl.ERR_UNSUPPORTED
+    assert saved_fwd_call(s, Y=None) == gl.ERR_INVALID
+    assert saved_bwd_call(s, outs=(None,) * 5) == gl.ERR_INVALID
+    assert saved_bwd_call(s, wsn=16) == gl.ERR_WORKSPACE
+    n = ctypes.c_size_t(0)
+    assert L.gradlev_scan_saved_bytes(ctypes.byref(shape(d_in=1024)), ctypes.byref(n), ctypes.byref(n)) \
+        == gl.ERR_UNSUPPORTED
+    assert L.gradlev_scan_saved_bytes(ctypes.byref(s), None, ctypes.byref(n)) == gl.ERR_INVALID
+
+
 def test_decode_validation_before_launch(L):
     f = gl.lib().gradlev_decode_step
     assert f(0, 16, 64, 64, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
