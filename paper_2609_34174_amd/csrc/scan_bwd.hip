@@ -137,15 +137,16 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) Wj[ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c];
     const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
-    for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += 4) {
-      f32x4 v[4][IB];
+    constexpr int PU = IB <= 4 ? 4 : 1;  // aggregates summed per batch of loads (register budget)
+    for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += PU) {
+      f32x4 v[PU][IB];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < PU; ++u)
 #pragma unroll
         for (int ib = 0; ib < IB; ++ib)
           v[u][ib] = j0 + u <= seg ? *reinterpret_cast<const f32x4*>(a.aggA + o + (j0 + u) * M * D + 16 * ib) : zero4();
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < PU; ++u)
 #pragma unroll
         for (int ib = 0; ib < IB; ++ib)
           if (j0 + u <= seg) Wj[ib] -= v[u][ib];
@@ -153,15 +154,15 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
     for (int ib = 0; ib < IB; ++ib) Rj[ib] = zero4();
     if (FULL && a.aggB) {
-      for (int64_t j0 = a.nseg - 1; j0 > seg; j0 -= 4) {
-        f32x4 v[4][IB];
+      for (int64_t j0 = a.nseg - 1; j0 > seg; j0 -= PU) {
+        f32x4 v[PU][IB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < PU; ++u)
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib)
             v[u][ib] = j0 - u > seg ? *reinterpret_cast<const f32x4*>(a.aggB + o + (j0 - u) * M * D + 16 * ib) : zero4();
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < PU; ++u)
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib)
             if (j0 - u > seg) Rj[ib] += v[u][ib];
@@ -461,6 +462,370 @@ bwd_main_kernel(const BArgs a) {
   }
 }
 
+// Wave-specialised full backward for square maps (d == m).  Waves [0, JB)
+// own column blocks of W: the un-write, gtilde and dX.  Waves [JB, 2JB) own
+// the same column blocks of R: its publication to LDS, the suffix update, and
+// the row blocks of U (dG, deta).  Each wave keeps half the state of
+// bwd_main_kernel's waves, so twice as many waves share a CU and hide each
+// other's LDS and matrix-core latency.  Same chunk equations, same rounding.
+template <class OP, int D, int M, int C, bool INCL, bool ETAV>
+__global__ void __launch_bounds__(2 * (D / 16) * 64, 128 / D)
+bwd_split_kernel(const BArgs a) {
+  static_assert(D == M, "the wave-specialised backward takes square maps");
+  typedef typename OP::elem E;
+  typedef typename OP::frag F;
+  constexpr int JB = D / 16, IB = M / 16, NW = 2 * JB, NT = NW * 64, TB = C / 16;
+  constexpr bool SPLITV = ETAV && OP::kSplit == 2;
+  __shared__ E Xs[C * D];                  // X[t][j]
+  __shared__ E Gs[C * M];                  // G[t][i]
+  __shared__ E Ds[C * M];                  // dY[t][i]
+  __shared__ E Es[C * C];                  // E[t][s] = eta_s dY_t . g_s (s before t)
+  __shared__ E Vh[ETAV ? C * M : 1];       // (eta G)[t][i] hi (per-token eta)
+  __shared__ E Vl[SPLITV ? C * M : 1];     // (eta G)[t][i] lo
+  __shared__ E Rh[D * M];                  // R^T[j][i] hi
+  __shared__ E Rl[OP::kSplit == 2 ? D * M : 1];  // R^T[j][i] lo
+  constexpr bool SSH = !ETAV && s_shared_fits(OP::kSplit == 2, D, M, C, ETAV);
+  __shared__ E Sh[SSH ? C * C : 1];
+  __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
+  __shared__ float et[C];
+  __shared__ float dpart[IB][C];
+
+  int64_t bh, seg;
+  if (!map_block(a.BH, a.nseg, bh, seg)) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
+  const bool gw = w < JB;          // owner of W's column block wb (else of R's)
+  const int wb = gw ? w : w - JB;
+  const int64_t T = a.T;
+  const int64_t t_begin = seg * a.seg_len;
+  const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
+  const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
+  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t Dy = make_rsrc(static_cast<const E*>(a.dY) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t Og = make_rsrc(a.gtilde ? a.gtilde + bh * T * D : nullptr, a.gtilde ? (uint32_t)(T * D * 4) : 0u);
+  const rsrc_t Ox = make_rsrc(a.dX ? a.dX + bh * T * D : nullptr, a.dX ? (uint32_t)(T * D * 4) : 0u);
+  const rsrc_t Od = make_rsrc(a.dG ? a.dG + bh * T * M : nullptr, a.dG ? (uint32_t)(T * M * 4) : 0u);
+  const rsrc_t Oe = make_rsrc(a.deta ? a.deta + bh * T : nullptr, a.deta ? (uint32_t)(T * 4) : 0u);
+  const int64_t nch = (t_end - t_begin + C - 1) / C;
+
+  // Register staging one chunk ahead (chunks are visited last to first).
+  typedef TileRow<OP, C, D, NT> TX;
+  typedef TileRow<OP, C, M, NT> TM;
+  TX xr;
+  TM gr, dr;
+  EtaReg<ETAV> er;
+  const rsrc_t Et = eta_rsrc(a.eta, bh, T);
+  auto fetch = [&](int64_t n) {
+    const int64_t t0 = t_begin + n * C;
+    er.load(Et, n >= 0 ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    xr.load(X, n >= 0 ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
+    gr.load(G, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    dr.load(Dy, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+  };
+  fetch(nch - 1);
+
+  // St[ib][r] = W (owners of W) or R (owners of R) at [i = 16ib + 4q + r][j = 16wb + c],
+  // at the segment's end: the saved state or W_0 - sum_{k<=seg} A_k, and
+  // R = sum_{k>seg} B_k (added from the last segment down).
+  f32x4 St[IB];
+  constexpr int PU = IB <= 4 ? 4 : 1;  // aggregates summed per batch of loads (register budget)
+  const int64_t ao = bh * a.nseg * M * D + (int64_t)(16 * wb + c) * M + 4 * q;
+  if (gw) {
+    const float* w0 = a.wend ? a.wend + (bh * a.nseg + seg) * M * D : a.W0 + (bh % a.H) * M * D;
+#pragma unroll
+    for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) St[ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * wb + c];
+    for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += PU) {
+      f32x4 v[PU][IB];
+#pragma unroll
+      for (int u = 0; u < PU; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          v[u][ib] = j0 + u <= seg ? *reinterpret_cast<const f32x4*>(a.aggA + ao + (j0 + u) * M * D + 16 * ib) : zero4();
+#pragma unroll
+      for (int u = 0; u < PU; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          if (j0 + u <= seg) St[ib] -= v[u][ib];
+    }
+  } else {
+#pragma unroll
+    for (int ib = 0; ib < IB; ++ib) St[ib] = zero4();
+    for (int64_t j0 = a.nseg - 1; a.aggB && j0 > seg; j0 -= PU) {
+      f32x4 v[PU][IB];
+#pragma unroll
+      for (int u = 0; u < PU; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          v[u][ib] = j0 - u > seg ? *reinterpret_cast<const f32x4*>(a.aggB + ao + (j0 - u) * M * D + 16 * ib) : zero4();
+#pragma unroll
+      for (int u = 0; u < PU; ++u)
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib)
+          if (j0 - u > seg) St[ib] += v[u][ib];
+    }
+  }
+  for (int i = tid; i < C * C; i += NT) Es[i] = (E)0.f;
+  if constexpr (SSH) {
+    for (int i = tid; i < C * C; i += NT) Sh[i] = (E)0.f;
+    if constexpr (OP::kSplit == 2)
+      for (int i = tid; i < C * C; i += NT) Sl[i] = (E)0.f;
+  }
+
+  for (int64_t n = nch - 1; n >= 0; --n) {
+    const int64_t t0 = t_begin + n * C;
+    const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
+    // Lane and thread indices as the loop sees them: kept opaque to the
+    // compiler so that LDS addresses are formed per use instead of being
+    // hoisted out of the loop into dozens of live registers.
+    int ln = lane, td = tid;
+    asm volatile("" : "+v"(ln), "+v"(td));
+    const int c = ln & 15, q = ln >> 4;
+    __syncthreads();
+    er.stage(et, C, a.eta_scalar, nvalid, 1.f, td);
+    xr.store(Xs, td);
+    gr.store(Gs, td);
+    dr.store(Ds, td);
+    __syncthreads();
+    if (ETAV) gr.store_scaled(Vh, Vl, td, et);  // read after the next barrier
+    fetch(n - 1);
+
+    // (1) Intra-chunk tiles E[t][s] and the masked scores, shared through
+    // LDS; the owners of R publish R_n^T (split).
+#pragma unroll
+    for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+      if (idx % NW != w) continue;
+      int tb = 0;
+      while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+      const int sb = idx - tb * (tb + 1) / 2;
+      // acc[r] = g_s . dY_t with s = 16sb + 4q + r, t = 16tb + c.
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < M / 32; ++kb)
+        acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+      const int t = 16 * tb + c;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int s = 16 * sb + 4 * q + r;
+        const bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
+        acc[r] = keep ? acc[r] * et[s] : 0.f;
+      }
+      OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
+    }
+    if constexpr (SSH) {
+#pragma unroll
+      for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
+        if ((idx + NW / 2) % NW != w) continue;
+        int tb = 0;
+        while ((tb + 1) * (tb + 2) / 2 <= idx) ++tb;
+        const int sb = idx - tb * (tb + 1) / 2;
+        f32x4 st = zero4();
+#pragma unroll
+        for (int kb = 0; kb < D / 32; ++kb)
+          st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kb, ln), OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
+        const int t = 16 * tb + c;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int s = 16 * sb + 4 * q + r;
+          if (!(tb > sb || (INCL ? (t >= s) : (t > s)))) st[r] = 0.f;
+        }
+        const int o = lds_off(t, 16 * sb + 4 * q, C);
+        OP::store4_split(Sh + o, Sl + o, st);
+      }
+    }
+    if (!gw) {
+#pragma unroll
+      for (int ib = 0; ib < IB; ++ib) {
+        const int o = lds_off(16 * wb + c, 16 * ib + 4 * q, M);
+        OP::store4_split(Rh + o, Rl + o, St[ib]);
+      }
+    }
+    __syncthreads();
+
+    // X^T rows j of this wave's column block over the chunk's tokens.
+    F xt[C / 32];
+#pragma unroll
+    for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * wb, ln);
+
+    if (gw) {
+      // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
+      if constexpr (ETAV) {
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) {
+            const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, ln);
+            F vl = vh;
+            if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, ln);
+            St[ib] = mma_split_a<OP>(St[ib], vh, vl, xt[kb]);
+          }
+        }
+      } else {
+        f32x4 dw[IB];
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib) dw[ib] = zero4();
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, ln), xt[kb]);
+        }
+        const float e = a.eta_scalar;
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib) St[ib] += e * dw[ib];
+      }
+
+      // (3) gtilde and dX for columns j in [16wb, 16wb+16), all t blocks at once.
+      f32x4 ga[TB], xa2[TB];
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) ga[tb] = xa2[tb] = zero4();
+      // gtilde^T[j][t] += sum_i W[i][j] dY[t][i];  dXw^T[j][s] += sum_i R[i][j] G[s][i]
+#pragma unroll
+      for (int kb = 0; kb < M / 32; ++kb) {
+        F wh, wl;
+        OP::split(cat(St[2 * kb], St[2 * kb + 1]), wh, wl);
+        const F rh = OP::load_n(Rh, M, 16 * wb, 32 * kb, ln);
+        F rl = rh;
+        if constexpr (OP::kSplit == 2) rl = OP::load_n(Rl, M, 16 * wb, 32 * kb, ln);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          ga[tb] = mma_split_a<OP>(ga[tb], wh, wl, OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+          xa2[tb] = mma_split_a<OP>(xa2[tb], rh, rl, OP::load_n(Gs, M, 16 * tb, 32 * kb, ln));
+        }
+        __builtin_amdgcn_sched_barrier(0);  // bound the operands in flight (register budget)
+      }
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) xa2[tb] *= et[16 * tb + c];
+      // Intra-chunk terms: gtilde -= sum_{s<t} X[s][j] E[t][s];  dXw += sum_{t>s} X[t][j] E[t][s]
+#pragma unroll
+      for (int kb = 0; kb < C / 32; ++kb) {
+        const F xq = xt[kb];
+        const F xn = OP::neg(xq);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          if (kb <= tb / 2) ga[tb] = OP::mma(ga[tb], xn, OP::load_n(Es, C, 16 * tb, 32 * kb, ln));
+          if (kb >= tb / 2) xa2[tb] = OP::mma(xa2[tb], xq, OP::load_t(Es, C, 32 * kb, 16 * tb, ln));
+        }
+      }
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        const uint32_t o = (uint32_t)(((t0 + 16 * tb + c) * D + 16 * wb + 4 * q) * 4);
+        if (a.gtilde) buf_store4(Og, o, ga[tb]);
+        if (a.dX) buf_store4(Ox, o, ga[tb] - xa2[tb]);
+      }
+    } else {
+      // (4) U, dG and deta for rows i in [16wb, 16wb+16), all s blocks at once.
+      f32x4 ua[TB];
+#pragma unroll
+      for (int sb = 0; sb < TB; ++sb) ua[sb] = zero4();
+      constexpr bool XCACHE = !SSH && TB * (D / 32) * (int)(sizeof(F) / 4) <= 32;
+      F xc[XCACHE ? TB : 1][XCACHE ? D / 32 : 1];
+      if constexpr (XCACHE) {
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int kb = 0; kb < D / 32; ++kb) xc[tb][kb] = OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
+      }
+      auto xrow = [&](int tb, int kb) -> F {
+        if constexpr (XCACHE) return xc[tb][kb];
+        else return OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
+      };
+      // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
+#pragma unroll
+      for (int kb = 0; kb < D / 32; ++kb) {
+        const F rh = OP::load_t(Rh, M, 32 * kb, 16 * wb, ln);
+        F rl = rh;
+        if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * wb, ln);
+#pragma unroll
+        for (int sb = 0; sb < TB; ++sb) ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, xrow(sb, kb));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (SSH) {
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * wb, ln);
+#pragma unroll
+          for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+            const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, ln);
+            F sl = sh;
+            if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, ln);
+            ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) {
+          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * wb, ln);
+#pragma unroll
+          for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+            f32x8 sv;
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int tb = 2 * kb + hh;
+              f32x4 st = zero4();
+              if (tb >= sb) {
+#pragma unroll
+                for (int kj = 0; kj < D / 32; ++kj) st = OP::mma(st, xrow(tb, kj), xrow(sb, kj));
+                if (tb == sb) {
+#pragma unroll
+                  for (int r = 0; r < 4; ++r) {
+                    const int t = 4 * q + r;
+                    if (!(INCL ? (t >= c) : (t > c))) st[r] = 0.f;
+                  }
+                }
+              }
+#pragma unroll
+              for (int r = 0; r < 4; ++r) sv[4 * hh + r] = st[r];
+            }
+            F sh, sl;
+            OP::split(sv, sh, sl);
+            ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
+          }
+        }
+      }
+#pragma unroll
+      for (int sb = 0; sb < TB; ++sb) {
+        // Lane holds token s = 16sb + c, rows i = 16wb + 4q + r; U = -ua.
+        const int s = 16 * sb + c;
+        const float es = et[s];
+        if (a.dG) buf_store4(Od, (uint32_t)(((t0 + s) * M + 16 * wb + 4 * q) * 4), -es * ua[sb]);
+        if (a.deta) {
+          typedef typename Vec4<E>::type vec4;
+          const vec4 gv = *reinterpret_cast<const vec4*>(Gs + lds_off(s, 16 * wb + 4 * q, M));
+          float p = 0.f;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[sb][r];
+          p += __shfl_xor(p, 16);
+          p += __shfl_xor(p, 32);
+          if (q == 0) dpart[wb][s] = p;
+        }
+      }
+      // (5) Suffix update: R_{n-1} = R_n + dY^T X (exact products).
+#pragma unroll
+      for (int kb = 0; kb < C / 32; ++kb) {
+#pragma unroll
+        for (int ib = 0; ib < IB; ++ib) St[ib] = OP::mma(St[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, ln), xt[kb]);
+      }
+    }
+    if (a.deta) {
+      __syncthreads();
+      const int tt = td < C ? td : 0;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < IB; ++i) s += dpart[i][tt];
+      buf_store1(Oe, td < C ? (uint32_t)((t0 + td) * 4) : kOOB, s);
+    }
+  }
+
+  // Segment 0 ends holding the sum over the whole sequence of dY x^T.
+  if (!gw && a.rfin && seg == 0) {
+    float* o = a.rfin + bh * M * D;
+#pragma unroll
+    for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[(int64_t)(16 * ib + 4 * q + r) * D + 16 * wb + c] = St[ib][r];
+  }
+}
+
 // dW0[h] = sum_b rfin[b, h] in a fixed order.
 static __global__ void __launch_bounds__(256)
 reduce_dw0_kernel(const float* rfin, float* dW0, int64_t B, int64_t H, int64_t md4) {
@@ -567,10 +932,20 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
     else
       hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutRead>), dim3(grid), dim3(NT), 0, s, b);
   } else {
-    if (p.inclusive)
-      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, true, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
-    else
-      hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
+    // 128 x 128 maps: the wave-specialised kernel (twice the waves per CU;
+    // measured 428 -> 343 us per launch at B=2, H=16, T=16384).  Smaller maps
+    // keep the single-role kernel, which two workgroups per CU already feed.
+    if constexpr (D == 128 && M == 128) {
+      if (p.inclusive)
+        hipLaunchKernelGGL((bwd_split_kernel<OP, D, M, C, true, ETAV>), dim3(grid), dim3(2 * NT), 0, s, b);
+      else
+        hipLaunchKernelGGL((bwd_split_kernel<OP, D, M, C, false, ETAV>), dim3(grid), dim3(2 * NT), 0, s, b);
+    } else {
+      if (p.inclusive)
+        hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, true, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
+      else
+        hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutFull>), dim3(grid), dim3(NT), 0, s, b);
+    }
   }
   timing_end(GRADLEV_K_BWD_MAIN, s);
   if (f.dW0) {

@@ -114,6 +114,49 @@ struct Tile4 {
   }
 };
 
+// Chunk tile staging by 4-element row pieces: piece e = tid + i * NT holds
+// row e / (K/4), columns 4 (e % (K/4)) .. +3.  Every thread of a wide
+// workgroup takes a share of the tile (Tile4's 4x4 blocks occupy at most
+// C K / 16 threads), so each holds fewer staging registers; consecutive
+// threads still read consecutive global bytes.
+template <class OP, int C, int K, int NT>
+struct TileRow {
+  typedef typename OP::elem elem;
+  typedef typename Vec4<elem>::type vec4;
+  static constexpr int NCB = K / 4, NE = C * NCB, PER = (NE + NT - 1) / NT;
+  vec4 v[PER];
+
+  __device__ __forceinline__ void load(rsrc_t src, uint32_t off, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = tid + i * NT, row = e / NCB, cb = e % NCB;
+      const uint32_t o = (off == kOOB || e >= NE) ? kOOB : off + (uint32_t)((row * K + 4 * cb) * sizeof(elem));
+      v[i] = buf_load4(src, o, (const elem*)nullptr);
+    }
+  }
+  __device__ __forceinline__ void store(elem* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = tid + i * NT, row = e / NCB, cb = e % NCB;
+      if (e >= NE) continue;
+      *reinterpret_cast<vec4*>(lds + lds_off(row, 4 * cb, K)) = v[i];
+    }
+  }
+  __device__ __forceinline__ void store_scaled(elem* hi, elem* lo, int tid, const float* et) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = tid + i * NT, row = e / NCB, cb = e % NCB;
+      if (e >= NE) continue;
+      const float s = et[row];
+      f32x4 f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) f[j] = (float)v[i][j] * s;
+      const int o = lds_off(row, 4 * cb, K);
+      OP::store4_split(hi + o, lo + o, f);
+    }
+  }
+};
+
 // Step sizes of one chunk, loaded together with the chunk's tiles (thread
 // tid < C holds row tid; per-token values only), then staged into LDS as
 // sign * eta for the valid rows and 0 past them.
