@@ -6,9 +6,12 @@ the full backward (gtilde, dX, dG, deta, dW0) of the lm-bf16 workload
 (B=8, H=16, T=2048, d=m=64, bf16 inputs, eta=0.1, chunk 64), inputs already
 resident in HBM.  By default the step is the save-for-backward pair (the
 forward keeps each segment's end state, the backward starts from it); the
-plain pair is reported among the secondaries and by --pair plain.  Two input
-sets alternate between steps so that the 256 MB Infinity Cache cannot carry a
-step's inputs into the next one.
+plain pair is reported among the secondaries and by --pair plain.  Step i
+runs the forward of input set i mod 8 and the backward of set (i - 2) mod 8:
+every batch still gets one forward and one backward per step, but about
+330 MB of other reads separate a batch's forward from its backward (and about
+1 GB a set's backward from its next forward), so the 256 MB Infinity Cache
+cannot serve them, as in a model where other layers run in between.
 
 Prints ONE JSON line with the headline (fwd+bwd tokens/s, tokens = B*T per
 step), the roofline of the dominant kernel measured with HIP events recorded
@@ -38,7 +41,7 @@ PEAK_FP32_MFMA = 157.3e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-SECONDARY_NAMES = ("lm-bf16-plain", "long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
+SECONDARY_NAMES = ("lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
                    "decode-f32-S2048", "decode-f32-gated")
 
 
@@ -97,10 +100,24 @@ def log(msg):
 
 
 class ScanRunner:
-    """Preallocated inputs/outputs/workspace for repeated fwd+bwd steps."""
+    """Preallocated inputs/outputs/workspace for repeated fwd+bwd steps.
 
-    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False):
+    pipelined: step i runs the forward of input set i and the backward of set
+    i - LAG (sets taken modulo nsets).  The work per step is unchanged (one
+    forward and one backward over one batch), but a batch's backward runs LAG
+    steps after its forward, as in a model where other layers' work separates
+    them.  Scan outputs are streaming stores, so only reads fill the 256 MB
+    Infinity Cache: LAG = 2 puts about 330 MB of other reads (lm-bf16)
+    between a batch's forward and its backward, and eight sets put about 1 GB
+    between a set's backward and its next forward, so neither can be served
+    from that cache."""
+    LAG = 2
+
+    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False, pipelined=False):
         self.gl, self.torch, self.wl = gl, torch, wl
+        if pipelined and nsets <= self.LAG:
+            raise ValueError("a pipelined step needs more input sets than its lag")
+        self.pipelined = pipelined
         self.sets = [W.device_scan_inputs(wl, layer0 + i, device, torch=torch) for i in range(nsets)]
         self.shape = gl.make_shape(wl.B, wl.H, wl.T, wl.d, wl.m,
                                    gl.BF16 if wl.dtype == "bf16" else gl.F32, chunk=wl.chunk)
@@ -109,7 +126,10 @@ class ScanRunner:
         ws_bytes = self.plan.workspace_bytes
         if saved:
             sv_bytes, ws_bytes = gl.saved_bytes(self.shape)
-            self.saved = torch.empty(sv_bytes // 4, dtype=torch.float32, device=device)
+            # One saved-state buffer per set that can be between its forward and backward.
+            self.saved_bufs = [torch.zeros(sv_bytes // 4, dtype=torch.float32, device=device)
+                               for _ in range(nsets if pipelined else 1)]
+            self.saved = self.saved_bufs[0]
             self.saved_nseg = sv_bytes // (wl.B * wl.H * wl.m * wl.d * 4)
         self.ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
         f32 = dict(dtype=torch.float32, device=device)
@@ -119,18 +139,32 @@ class ScanRunner:
                      "dg": torch.empty(B, H, T, m, **f32), "deta": torch.empty(B, H, T, **f32),
                      "dw0": torch.empty(H, m, d, **f32)}
 
-    def step(self, i):
-        s = self.sets[i % len(self.sets)]
+    def fwd(self, k):
+        s = self.sets[k]
         if self.saved is not None:
             self.gl.scan_fwd_save(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
-                                  saved=self.saved, workspace=self.ws)
-            self.gl.scan_bwd_saved(s["W0"], s["X"], s["G"], s["dY"], self.saved, s["eta"], chunk=self.wl.chunk,
-                                   out=self.outs, workspace=self.ws)
-            return
-        self.gl.scan_fwd(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
-                         workspace=self.ws)
-        self.gl.scan_bwd(s["W0"], s["X"], s["G"], s["dY"], s["eta"], chunk=self.wl.chunk,
-                         out=self.outs, workspace=self.ws)
+                                  saved=self.saved_bufs[k % len(self.saved_bufs)], workspace=self.ws)
+        else:
+            self.gl.scan_fwd(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
+                             workspace=self.ws)
+
+    def bwd(self, k):
+        s = self.sets[k]
+        if self.saved is not None:
+            self.gl.scan_bwd_saved(s["W0"], s["X"], s["G"], s["dY"], self.saved_bufs[k % len(self.saved_bufs)],
+                                   s["eta"], chunk=self.wl.chunk, out=self.outs, workspace=self.ws)
+        else:
+            self.gl.scan_bwd(s["W0"], s["X"], s["G"], s["dY"], s["eta"], chunk=self.wl.chunk,
+                             out=self.outs, workspace=self.ws)
+
+    def step(self, i):
+        n = len(self.sets)
+        if self.pipelined:
+            self.fwd(i % n)
+            self.bwd((i - self.LAG) % n)
+        else:
+            self.fwd(i % n)
+            self.bwd(i % n)
 
 
 def timed(torch, fn, steps, warmup):
@@ -343,22 +377,29 @@ def cpu_baseline(W, wl, min_seconds):
                       f"fwd {t_fwd:.1f} s + bwd {t_bwd:.1f} s of float64 numpy on one thread"}
 
 
-def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True, nsets=1):
+def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True):
+    """One workload's fwd+bwd steps as one graph replay.  A single-layer
+    workload runs the pipelined step (eight input sets; see ScanRunner); a
+    layer stack runs every layer's forward, then every layer's backward in
+    reverse order, as a model's training step does."""
     wl = W.SCAN_WORKLOADS[name]
     if wl.layers == 1:
-        run = ScanRunner(gl, torch, W, wl, nsets, device, saved=saved)
+        run = ScanRunner(gl, torch, W, wl, 8, device, saved=saved, pipelined=True)
         fn = run.step
         runs = [run]
     else:
         runs = [ScanRunner(gl, torch, W, wl, 1, device, layer0=l, saved=saved) for l in range(wl.layers)]
         # Layers share output buffers: the write traffic is identical and 24
-        # separate sets would only add allocation.
+        # separate sets would only add allocation.  Inputs and saved states
+        # are per layer.
         for r in runs[1:]:
             r.Y, r.outs, r.ws = runs[0].Y, runs[0].outs, runs[0].ws
 
         def fn(i):
             for r in runs:
-                r.step(0)
+                r.fwd(0)
+            for r in reversed(runs):
+                r.bwd(0)
     for i in range(warmup):
         fn(i)
     ms, k = graph_timed(torch, gl, fn, steps)
@@ -381,16 +422,54 @@ def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True, nsets=
     return res
 
 
-def secondary_gated(gl, torch, W, device, steps=5, warmup=1):
+def secondary_cold(gl, torch, W, device, reps=20):
+    """The headline pair with a cold Infinity Cache: before each call a 512 MiB
+    buffer is read and written (twice the 256 MB cache), then the forward or
+    the backward alone is timed with events on the launching stream.  The
+    flush runs first, so the events bracket GPU work only.  Medians."""
+    wl = W.SCAN_WORKLOADS["lm-bf16"]
+    run = ScanRunner(gl, torch, W, wl, 1, device, saved=True)
+    s = run.sets[0]
+    flush = torch.zeros(512 * 2 ** 20 // 4, dtype=torch.float32, device=device)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    fwd, bwd = [], []
+    for i in range(reps + 3):
+        flush.add_(1.0)
+        ev[0].record()
+        gl.scan_fwd_save(s["W0"], s["X"], s["G"], s["eta"], chunk=wl.chunk, out=run.Y, saved=run.saved,
+                         workspace=run.ws)
+        ev[1].record()
+        flush.add_(1.0)
+        ev[2].record()
+        gl.scan_bwd_saved(s["W0"], s["X"], s["G"], s["dY"], run.saved, s["eta"], chunk=wl.chunk, out=run.outs,
+                          workspace=run.ws)
+        ev[3].record()
+        torch.cuda.synchronize()
+        if i >= 3:
+            fwd.append(ev[0].elapsed_time(ev[1]))
+            bwd.append(ev[2].elapsed_time(ev[3]))
+    fwd.sort()
+    bwd.sort()
+    f, b = fwd[len(fwd) // 2], bwd[len(bwd) // 2]
+    return {"mode": "fwd and bwd each timed alone after a 512 MiB cache flush (eager calls, medians of %d)" % reps,
+            "fwd_ms": f, "bwd_ms": b, "fwd_plus_bwd_ms": f + b, "tokens_per_s": wl.B * wl.T / ((f + b) * 1e-3)}
+
+
+def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2):
     """Gated fwd+bwd (retention, per-token gates, packed-document resets) on the
-    lm-bf16 shape, every gradient including dalpha."""
+    lm-bf16 shape, every gradient including dalpha.  Pipelined like the
+    headline: step i runs the forward of input set i and the backward of set
+    i - lag (modulo nsets), so neither reads its inputs from the Infinity Cache."""
     wl = W.SCAN_WORKLOADS["lm-bf16"]
     B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
-    inp = W.device_scan_inputs(wl, 0, device, torch=torch)
-    a, e = W.gate_tokens(B, H, T, d, wl.seed + 11)
-    alpha = torch.from_numpy(a).to(device)
-    eta = torch.from_numpy(e).to(device)
-    reset = torch.from_numpy(W.reset_flags(B, T, wl.seed + 12, mean_len=512)).to(device)
+    sets = []
+    for k in range(nsets):
+        inp = W.device_scan_inputs(wl, k, device, torch=torch)
+        a, e = W.gate_tokens(B, H, T, d, wl.seed + 11 + 2 * k)
+        inp["alpha"] = torch.from_numpy(a).to(device)
+        inp["eta_t"] = torch.from_numpy(e).to(device)
+        inp["reset"] = torch.from_numpy(W.reset_flags(B, T, wl.seed + 12 + 2 * k, mean_len=512)).to(device)
+        sets.append(inp)
     shape = gl.make_shape(B, H, T, d, m, gl.BF16)
     ws = torch.empty(max(gl.gated_workspace_bytes(shape), 256), dtype=torch.uint8, device=device)
     f32 = dict(dtype=torch.float32, device=device)
@@ -399,11 +478,13 @@ def secondary_gated(gl, torch, W, device, steps=5, warmup=1):
             "dg": torch.empty(B, H, T, m, **f32), "deta": torch.empty(B, H, T, **f32),
             "dalpha": torch.empty(B, H, T, **f32), "dw0": torch.empty(H, m, d, **f32)}
 
-    def fn(_=0):
-        gl.scan_fwd_gated(inp["W0"], inp["X"], inp["G"], eta, alpha, reset, out=Y, workspace=ws)
-        gl.scan_bwd_gated(inp["W0"], inp["X"], inp["G"], inp["dY"], eta, alpha, reset, out=outs, workspace=ws)
-    for _ in range(warmup):
-        fn()
+    def fn(i=0):
+        f, b = sets[i % nsets], sets[(i - lag) % nsets]
+        gl.scan_fwd_gated(f["W0"], f["X"], f["G"], f["eta_t"], f["alpha"], f["reset"], out=Y, workspace=ws)
+        gl.scan_bwd_gated(b["W0"], b["X"], b["G"], b["dY"], b["eta_t"], b["alpha"], b["reset"], out=outs,
+                          workspace=ws)
+    for i in range(warmup):
+        fn(i)
     ms, _ = graph_timed(torch, gl, fn, steps, kernels=[])
     _, k = graph_timed(torch, gl, fn, steps,
                        kernels=["gated_agg", "gated_fwd", "gated_states", "gated_bwd", "bwd_dw0"])
@@ -417,7 +498,7 @@ def secondary_gated(gl, torch, W, device, steps=5, warmup=1):
            "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9, "frac_hbm_peak": nbytes / (ms * 1e-3) / PEAK_HBM,
            "tflops_algorithmic": flops / (ms * 1e-3) / 1e12,
            "kernel_avg_us": {n: round(v[0], 2) for n, v in k.items() if v[0] is not None}}
-    del inp, outs, Y, ws
+    del sets, outs, Y, ws
     torch.cuda.empty_cache()
     return res
 
@@ -571,8 +652,10 @@ def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
 
 
 def run_secondary(name, gl, torch, W, device):
+    if name == "lm-bf16-cold":
+        return secondary_cold(gl, torch, W, device)
     if name == "lm-bf16-plain":  # the headline step without the saved segment states
-        return secondary_scan(gl, torch, W, "lm-bf16", 20, 50, device, saved=False, nsets=2)
+        return secondary_scan(gl, torch, W, "lm-bf16", 200, 500, device, saved=False)
     if name in ("long-bf16", "stack-bf16"):
         return secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
     if name == "lm-bf16-gated":
@@ -636,7 +719,7 @@ def main():
 
     wl = W.SCAN_WORKLOADS[args.workload]
     log(f"workload {wl.name}: preparing inputs")
-    run = ScanRunner(gl, torch, W, wl, 2, device, saved=args.pair == "saved")
+    run = ScanRunner(gl, torch, W, wl, 8, device, saved=args.pair == "saved", pipelined=True)
     plan = run.plan
     work = scan_work(wl, plan)
 
@@ -684,7 +767,7 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_in": wl.d, "d_out": wl.m,
                    "chunk": wl.chunk, "eta": wl.eta, "prefix": "exclusive",
                    "step": ("scan_fwd_save + scan_bwd_saved" if run.saved is not None else "scan_fwd + scan_bwd")
-                   + " with gtilde, dX, dG, deta, dW0",
+                   + " with gtilde, dX, dG, deta, dW0; forward of batch i with backward of batch i-2",
                    "plan": ({"saved_pair_segments": run.saved_nseg,
                              "saved_state_bytes": run.saved.numel() * 4,
                              "chunks": [plan.fwd_chunk, plan.bwd_chunk]} if run.saved is not None else
@@ -696,8 +779,9 @@ def main():
                           "tflops_algorithmic": work["flops"] / step_s / 1e12,
                           "frac_bf16_mfma_peak": work["flops"] / step_s / PEAK_BF16},
         "kernel_avg_us": {n: round(v[0], 3) for n, v in kall.items() if v[0] is not None},
-        "timing": "timed region = one replay of a HIP graph of the K steps (inputs alternate between two "
-                  "sets), after the W eager warmup steps, K eager steps and one untimed replay; roofline kernel "
+        "timing": "timed region = one replay of a HIP graph of the K steps (step i: forward of input set i mod 8, "
+                  "backward of set (i-2) mod 8), after the W eager warmup steps, K eager steps and one untimed "
+                  "replay; roofline kernel "
                   "time from "
                   "HIP events on its launches inside that replay; kernel_avg_us from a second replay with "
                   "every family bracketed",

@@ -104,10 +104,11 @@ bwd_main_kernel(const BArgs a) {
   const int64_t nch = (t_end - t_begin + C - 1) / C;
 
   // Register staging, DEPTH chunks ahead (chunks are visited last to first).
-  // The full backward keeps twice the accumulators of the read-only one and
-  // fp32 tiles take twice the registers: those stage one chunk ahead, which
-  // keeps them free of spills.
-  constexpr int DEPTH = (FULL || OP::kSplit == 1) ? 1 : 2;
+  // Two chunks ahead keep more bytes in flight, which pays once the inputs
+  // come from HBM rather than the Infinity Cache.  fp32 tiles take twice the
+  // registers, and the full backward of maps with a 128-wide side keeps more
+  // accumulators: those stage one chunk ahead, which keeps them free of spills.
+  constexpr int DEPTH = (OP::kSplit == 2 && (!FULL || (D == 64 && M == 64))) ? 2 : 1;
   Tile4<OP, C, D, NT> xa, xb;
   Tile4<OP, C, M, NT> ga, gb, da, db;
   EtaReg<ETAV> ea, eb;
@@ -179,17 +180,23 @@ bwd_main_kernel(const BArgs a) {
   auto chunk = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
     // A step before the segment start (the second of a pair) sees zero
     // tiles, leaves W and R unchanged and stores nothing.
+    // Lane and thread indices as the chunk sees them: opaque to the compiler,
+    // so that LDS addresses are formed per use instead of being hoisted out
+    // of the loop into dozens of live registers.
+    int ln = lane, td = tid;
+    asm volatile("" : "+v"(ln), "+v"(td));
+    const int c = ln & 15, q = ln >> 4;
     const int64_t t0 = t_begin + n * C;
     const bool live = n >= 0;
     const int nvalid = live ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
     const rsrc_t Ogc = live ? Og : none, Oxc = live ? Ox : none, Odc = live ? Od : none, Oec = live ? Oe : none;
     __syncthreads();
-    er.stage(et, C, a.eta_scalar, nvalid, 1.f, tid);
-    xr.store(Xs, tid);
-    gr.store(Gs, tid);
-    dr.store(Ds, tid);
+    er.stage(et, C, a.eta_scalar, nvalid, 1.f, td);
+    xr.store(Xs, td);
+    gr.store(Gs, td);
+    dr.store(Ds, td);
     __syncthreads();
-    if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read after the next barrier
+    if (ETAV) gr.store_scaled(Vh, Vl, td, et);  // read after the next barrier
     fetch(xr, gr, dr, er, n - DEPTH);
 
     // (1) Intra-chunk tiles E[t][s], shared through LDS, and R_n^T (split).
@@ -203,7 +210,7 @@ bwd_main_kernel(const BArgs a) {
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb)
-        acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, lane), OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+        acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
       const int t = 16 * tb + c;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -224,7 +231,7 @@ bwd_main_kernel(const BArgs a) {
         f32x4 st = zero4();
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb)
-          st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+          st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kb, ln), OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
         const int t = 16 * tb + c;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -249,7 +256,7 @@ bwd_main_kernel(const BArgs a) {
     F xt[C / 32];
     if (w < JB) {
 #pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, ln);
     }
 
     // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
@@ -260,9 +267,9 @@ bwd_main_kernel(const BArgs a) {
           const F xq = xt[kb];
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
-            const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, lane);
+            const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, ln);
             F vl = vh;
-            if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, lane);
+            if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, ln);
             Wj[ib] = mma_split_a<OP>(Wj[ib], vh, vl, xq);
           }
         }
@@ -273,7 +280,7 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, lane), xt[kb]);
+          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, ln), xt[kb]);
         }
         const float e = a.eta_scalar;
 #pragma unroll
@@ -293,14 +300,14 @@ bwd_main_kernel(const BArgs a) {
         OP::split(cat(Wj[2 * kb], Wj[2 * kb + 1]), wh, wl);
         F rh, rl;  // this wave's own R^T rows, as published (split) in step (1)
         if (FULL) {
-          rh = OP::load_n(Rh, M, 16 * w, 32 * kb, lane);
+          rh = OP::load_n(Rh, M, 16 * w, 32 * kb, ln);
           rl = rh;
-          if constexpr (OP::kSplit == 2) rl = OP::load_n(Rl, M, 16 * w, 32 * kb, lane);
+          if constexpr (OP::kSplit == 2) rl = OP::load_n(Rl, M, 16 * w, 32 * kb, ln);
         }
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
-          ga[tb] = mma_split_a<OP>(ga[tb], wh, wl, OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
-          if (FULL) xa2[tb] = mma_split_a<OP>(xa2[tb], rh, rl, OP::load_n(Gs, M, 16 * tb, 32 * kb, lane));
+          ga[tb] = mma_split_a<OP>(ga[tb], wh, wl, OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+          if (FULL) xa2[tb] = mma_split_a<OP>(xa2[tb], rh, rl, OP::load_n(Gs, M, 16 * tb, 32 * kb, ln));
         }
       }
       if (FULL) {
@@ -314,8 +321,8 @@ bwd_main_kernel(const BArgs a) {
         const F xn = OP::neg(xq);
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) {
-          if (kb <= tb / 2) ga[tb] = OP::mma(ga[tb], xn, OP::load_n(Es, C, 16 * tb, 32 * kb, lane));
-          if (FULL && kb >= tb / 2) xa2[tb] = OP::mma(xa2[tb], xq, OP::load_t(Es, C, 32 * kb, 16 * tb, lane));
+          if (kb <= tb / 2) ga[tb] = OP::mma(ga[tb], xn, OP::load_n(Es, C, 16 * tb, 32 * kb, ln));
+          if (FULL && kb >= tb / 2) xa2[tb] = OP::mma(xa2[tb], xq, OP::load_t(Es, C, 32 * kb, 16 * tb, ln));
         }
       }
       // Lane holds row t = 16tb + c, columns j = 16w + 4q + r; dX = gtilde - xa2.
@@ -342,18 +349,18 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
           for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-            for (int kb = 0; kb < D / 32; ++kb) xr[tb][kb] = OP::load_n(Xs, D, 16 * tb, 32 * kb, lane);
+            for (int kb = 0; kb < D / 32; ++kb) xr[tb][kb] = OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
         }
         auto xrow = [&](int tb, int kb) -> F {
           if constexpr (XCACHE) return xr[tb][kb];
-          else return OP::load_n(Xs, D, 16 * tb, 32 * kb, lane);
+          else return OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
         };
         // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb) {
-          const F rh = OP::load_t(Rh, M, 32 * kb, 16 * w, lane);
+          const F rh = OP::load_t(Rh, M, 32 * kb, 16 * w, ln);
           F rl = rh;
-          if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * w, lane);
+          if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * w, ln);
 #pragma unroll
           for (int sb = 0; sb < TB; ++sb) ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, xrow(sb, kb));
         }
@@ -362,12 +369,12 @@ bwd_main_kernel(const BArgs a) {
           // row s over k = t is a transposing read of the [t][s] tile.
 #pragma unroll
           for (int kb = 0; kb < C / 32; ++kb) {
-            const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
+            const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, ln);
 #pragma unroll
             for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
-              const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, lane);
+              const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, ln);
               F sl = sh;
-              if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, lane);
+              if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, ln);
               ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
             }
           }
@@ -377,7 +384,7 @@ bwd_main_kernel(const BArgs a) {
         // the tile (rows t, cols s) is directly the operand contracted over t.
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
+          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, ln);
 #pragma unroll
           for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
             f32x8 sv;
@@ -429,16 +436,16 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, lane), xt[kb]);
+          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, ln), xt[kb]);
         }
       }
       if (a.deta) {
         __syncthreads();
-        const int tt = tid < C ? tid : 0;
+        const int tt = td < C ? td : 0;
         float s = 0.f;
 #pragma unroll
         for (int i = 0; i < IB; ++i) s += dpart[i][tt];
-        buf_store1(Oec, tid < C ? (uint32_t)((t0 + tid) * 4) : kOOB, s);
+        buf_store1(Oec, td < C ? (uint32_t)((t0 + td) * 4) : kOOB, s);
       }
     }
   };
