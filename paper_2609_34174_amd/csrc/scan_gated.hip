@@ -552,17 +552,19 @@ states_gated_kernel(const GArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Gated backward.  NW = max(d, m)/16 waves.  Wave w < d/16 owns columns j in
-// [16w, 16w+16) of Lambda (tiles rows i, cols j), of gtilde and of dX; wave
-// w < m/16 owns rows i in [16w, 16w+16) of u and dG.  Chunks run from the
+// Gated backward.  Wave w < d/16 owns columns j in [16w, 16w+16) of Lambda
+// (tiles rows i, cols j), of gtilde and of dX.  The rows i in [16r, 16r+16)
+// of u and dG belong to wave r as well (SPLITW false: max(d, m)/16 waves), or
+// to a wave of their own, w = d/16 + r (SPLITW true: d/16 + m/16 waves, twice
+// as many per CU to hide each other's latency).  Chunks run from the
 // segment's last to its first.
 // ---------------------------------------------------------------------------
-template <class OP, int D, int M, int C>
-__global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
+template <class OP, int D, int M, int C, bool SPLITW>
+__global__ void __launch_bounds__((SPLITW ? D / 16 + M / 16 : cmax(D, M) / 16) * 64)
 bwd_gated_kernel(const GArgs a) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
-  constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
+  constexpr int NW = SPLITW ? D / 16 + M / 16 : cmax(D, M) / 16, NT = NW * 64;
   constexpr int TB = C / 16, JB = D / 16, IB = M / 16;
   constexpr bool SPL = OP::kSplit == 2;
   constexpr int LO = SPL ? 1 : 0;
@@ -652,17 +654,23 @@ bwd_gated_kernel(const GArgs a) {
   };
   fetch(n_last);
   for (int64_t n = n_last; n >= n_first; --n) {
+    // Lane and thread indices as the loop sees them: opaque to the compiler,
+    // so that LDS addresses are formed per use instead of being hoisted out
+    // of the loop into hundreds of live registers.
+    int ln = lane, td = tid;
+    asm volatile("" : "+v"(ln), "+v"(td));
+    const int c = ln & 15, q = ln >> 4;
     const int64_t t0 = n * C;
     const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
     f32x4 dn[IB];
 #pragma unroll
     for (int ib = 0; ib < IB; ++ib) dn[ib] = dnx[ib];
     __syncthreads();
-    ar.stage(al, et, gm, nvalid, tid, C);
-    xr.store(Xs, tid);
-    gr.store(Gs, tid);
-    dr.store(Ds, tid);
-    for (int i = tid; i < NW * C; i += NT) (&dap[0][0])[i] = 0.f;
+    ar.stage(al, et, gm, nvalid, td, C);
+    xr.store(Xs, td);
+    gr.store(Gs, td);
+    dr.store(Ds, td);
+    for (int i = td; i < NW * C; i += NT) (&dap[0][0])[i] = 0.f;
     // Publish Lambda_e^T [j][i] (split) and the partial <Lambda_e, Delta_n>.
     if (w < JB) {
       float t1 = 0.f;
@@ -675,12 +683,12 @@ bwd_gated_kernel(const GArgs a) {
       }
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) t1 += __shfl_xor(t1, o);
-      if (lane == 0) t1p[w] = t1;
+      if (ln == 0) t1p[w] = t1;
     }
     __syncthreads();
-    if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, nullptr, 0.f, lane);
+    if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, nullptr, 0.f, ln);
     __syncthreads();
-    dr.store_scaled(Dph, Dpl, tid, pre);
+    dr.store_scaled(Dph, Dpl, td, pre);
     // Chunk matrices, lower tiles (tb >= sb) spread over the waves.
 #pragma unroll
     for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
@@ -692,10 +700,10 @@ bwd_gated_kernel(const GArgs a) {
       f32x4 gx = zero4(), ed = zero4();
 #pragma unroll
       for (int kb = 0; kb < D / 32; ++kb)
-        gx = OP::mma(gx, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+        gx = OP::mma(gx, OP::load_n(Xs, D, 16 * sb, 32 * kb, ln), OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb)
-        ed = OP::mma(ed, OP::load_n(Gs, M, 16 * sb, 32 * kb, lane), OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+        ed = OP::mma(ed, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
       const f32x4 f = decay4<TB>(al, pin, sinv, mid, sb, tb, q, c);
       const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
       const int t = 16 * tb + c;
@@ -716,7 +724,7 @@ bwd_gated_kernel(const GArgs a) {
     F xt[C / 32];
     if (w < JB) {
 #pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, lane);
+      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, ln);
       // Read side: gtilde = W_0^T dY + pre Delta_n^T dY - (E1 X); write side of dX.
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
@@ -726,7 +734,7 @@ bwd_gated_kernel(const GArgs a) {
         for (int kb = 0; kb < M / 32; ++kb) {
           F dh, dl;
           OP::split(cat(dn[2 * kb], dn[2 * kb + 1]), dh, dl);
-          ad = mma_split_a<OP>(ad, dh, dl, OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+          ad = mma_split_a<OP>(ad, dh, dl, OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
         }
         // c3_t partial: x_t . (Delta_n^T dY_t) over this wave's j.
         float c3 = 0.f;
@@ -737,12 +745,12 @@ bwd_gated_kernel(const GArgs a) {
         f32x4 ag = ad * pre[t];
 #pragma unroll
         for (int kb = 0; kb < M / 32; ++kb)
-          ag = mma_split_a<OP>(ag, w0h[kb], w0l[kb], OP::load_n(Ds, M, 16 * tb, 32 * kb, lane));
+          ag = mma_split_a<OP>(ag, w0h[kb], w0l[kb], OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F eh = OP::load_n(E1h, C, 16 * tb, 32 * kb, lane);
+          const F eh = OP::load_n(E1h, C, 16 * tb, 32 * kb, ln);
           F el = eh;
-          if constexpr (SPL) el = OP::load_n(E1l, C, 16 * tb, 32 * kb, lane);
+          if constexpr (SPL) el = OP::load_n(E1l, C, 16 * tb, 32 * kb, ln);
           ag = mma_split_b<OP>(ag, xt[kb], eh, el);
         }
         const uint32_t off = (uint32_t)(((t0 + t) * D + 16 * w + 4 * q) * 4);
@@ -754,13 +762,13 @@ bwd_gated_kernel(const GArgs a) {
           for (int kb = 0; kb < M / 32; ++kb) {
             F lh, ll;
             OP::split(cat(Lam[2 * kb], Lam[2 * kb + 1]), lh, ll);
-            qs = mma_split_a<OP>(qs, lh, ll, OP::load_n(Gs, M, 16 * tb, 32 * kb, lane));
+            qs = mma_split_a<OP>(qs, lh, ll, OP::load_n(Gs, M, 16 * tb, 32 * kb, ln));
           }
 #pragma unroll
           for (int kb = 0; kb < C / 32; ++kb) {
-            const F ph = OP::load_t(Peh, C, 32 * kb, 16 * tb, lane);
+            const F ph = OP::load_t(Peh, C, 32 * kb, 16 * tb, ln);
             F pl = ph;
-            if constexpr (SPL) pl = OP::load_t(Pel, C, 32 * kb, 16 * tb, lane);
+            if constexpr (SPL) pl = OP::load_t(Pel, C, 32 * kb, 16 * tb, ln);
             qi = mma_split_b<OP>(qi, xt[kb], ph, pl);
           }
           const f32x4 dx = ag - et[t] * (suf[t] * qs + qi);
@@ -768,7 +776,8 @@ bwd_gated_kernel(const GArgs a) {
         }
       }
     }
-    if (w < IB) {
+    if (SPLITW ? (w >= JB && w < JB + IB) : w < IB) {
+      const int rw = SPLITW ? w - JB : w;  // row block of u and dG
       // u_t = -(suf_t Lambda_e x_t + sum_{u>t} F[u][t] (x_u . x_t) dY_u).
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
@@ -776,33 +785,33 @@ bwd_gated_kernel(const GArgs a) {
         f32x4 us = zero4(), ui = zero4();
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb) {
-          const F lh = OP::load_t(LTh, M, 32 * kb, 16 * w, lane);
+          const F lh = OP::load_t(LTh, M, 32 * kb, 16 * rw, ln);
           F ll = lh;
-          if constexpr (SPL) ll = OP::load_t(LTl, M, 32 * kb, 16 * w, lane);
-          us = mma_split_a<OP>(us, lh, ll, OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+          if constexpr (SPL) ll = OP::load_t(LTl, M, 32 * kb, 16 * rw, ln);
+          us = mma_split_a<OP>(us, lh, ll, OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
         }
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F ph = OP::load_t(Pgh, C, 32 * kb, 16 * tb, lane);
+          const F ph = OP::load_t(Pgh, C, 32 * kb, 16 * tb, ln);
           F pl = ph;
-          if constexpr (SPL) pl = OP::load_t(Pgl, C, 32 * kb, 16 * tb, lane);
-          ui = mma_split_b<OP>(ui, OP::load_t(Ds, M, 32 * kb, 16 * w, lane), ph, pl);
+          if constexpr (SPL) pl = OP::load_t(Pgl, C, 32 * kb, 16 * tb, ln);
+          ui = mma_split_b<OP>(ui, OP::load_t(Ds, M, 32 * kb, 16 * rw, ln), ph, pl);
         }
         const f32x4 u = -(suf[t] * us + ui);
         float c2 = 0.f, de = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float gv = (float)Gs[lds_off(t, 16 * w + 4 * q + r, M)];
+          const float gv = (float)Gs[lds_off(t, 16 * rw + 4 * q + r, M)];
           c2 += gv * us[r];
           de += gv * u[r];
         }
         c2 = sum_q(c2);
         de = sum_q(de);
         if (q == 0) {
-          c2p[w][t] = c2;
-          dep[w][t] = de;
+          c2p[rw][t] = c2;
+          dep[rw][t] = de;
         }
-        if (a.dG) buf_store4(Od, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), et[t] * u);
+        if (a.dG) buf_store4(Od, (uint32_t)(((t0 + t) * M + 16 * rw + 4 * q) * 4), et[t] * u);
       }
     }
     if (a.dalpha) {
@@ -817,12 +826,12 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
           if (32 * kb > 16 * tb + 15) break;
-          const F kh = OP::load_n(Kh, C, 16 * ub, 32 * kb, lane);
-          const F fh = OP::load_n(Plh, C, 16 * tb, 32 * kb, lane);
+          const F kh = OP::load_n(Kh, C, 16 * ub, 32 * kb, ln);
+          const F fh = OP::load_n(Plh, C, 16 * tb, 32 * kb, ln);
           z = OP::mma(z, kh, fh);
           if constexpr (SPL) {
-            z = OP::mma(z, OP::load_n(Kl, C, 16 * ub, 32 * kb, lane), fh);
-            z = OP::mma(z, kh, OP::load_n(Pll, C, 16 * tb, 32 * kb, lane));
+            z = OP::mma(z, OP::load_n(Kl, C, 16 * ub, 32 * kb, ln), fh);
+            z = OP::mma(z, kh, OP::load_n(Pll, C, 16 * tb, 32 * kb, ln));
           }
         }
         // z[r] = Z[u = 16ub + 4q + r][t = 16tb + c]
@@ -840,9 +849,9 @@ bwd_gated_kernel(const GArgs a) {
       }
     }
     __syncthreads();
-    if (w == 0) {
+    if (w == NW - 1) {
       // Per-token gate gradients.  Lane t < C.
-      const int t = lane;
+      const int t = ln;
       const bool in = t < C;
       const int tc = in ? t : C - 1;
       float c3 = 0.f, c2 = 0.f, de = 0.f, da = 0.f, t1 = 0.f;
@@ -861,19 +870,19 @@ bwd_gated_kernel(const GArgs a) {
       const float at = in ? al[tc] : 1.f;
       // z_t = alpha_{t-1} z_{t-1} + c2_{t-1}:  affine scan (A, B) upward.
       float A = __shfl_up(at, 1), B = __shfl_up(c2, 1);
-      if (lane == 0) A = 0.f, B = 0.f;
+      if (ln == 0) A = 0.f, B = 0.f;
       // w_t = alpha_{t+1} w_{t+1} + c3_{t+1}: affine scan downward.
       float A2 = __shfl_down(at, 1), B2 = __shfl_down(c3, 1);
-      if (lane == 63) A2 = 0.f, B2 = 0.f;
+      if (ln == 63) A2 = 0.f, B2 = 0.f;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const float pa = __shfl_up(A, o), pb = __shfl_up(B, o);
-        if (lane >= o) {
+        if (ln >= o) {
           B = A * pb + B;
           A = A * pa;
         }
         const float qa = __shfl_down(A2, o), qb = __shfl_down(B2, o);
-        if (lane + o < 64) {
+        if (ln + o < 64) {
           B2 = A2 * qb + B2;
           A2 = A2 * qa;
         }
@@ -894,9 +903,9 @@ bwd_gated_kernel(const GArgs a) {
       for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
         for (int ib = 0; ib < IB; ++ib) {
-          const F ph = OP::load_t(Dph, M, 32 * kb, 16 * ib, lane);
+          const F ph = OP::load_t(Dph, M, 32 * kb, 16 * ib, ln);
           F pl = ph;
-          if constexpr (SPL) pl = OP::load_t(Dpl, M, 32 * kb, 16 * ib, lane);
+          if constexpr (SPL) pl = OP::load_t(Dpl, M, 32 * kb, 16 * ib, ln);
           Lam[ib] = mma_split_a<OP>(Lam[ib], ph, pl, xt[kb]);
         }
       }
@@ -1001,7 +1010,11 @@ static hipError_t bwd_gated_dims_c(const ScanProblem& p, const GArgs& k, float* 
   hipLaunchKernelGGL((states_gated_kernel<OP, D, M, C>), dim3(grid), dim3(NT), 0, s, k);
   timing_end(GRADLEV_K_GATED_STATES, s);
   timing_begin(GRADLEV_K_GATED_BWD, s);
-  hipLaunchKernelGGL((bwd_gated_kernel<OP, D, M, C>), dim3(grid), dim3(NT), 0, s, k);
+  // Separate waves for the row blocks of u where the wider workgroup keeps
+  // its registers (measured on the 64 x 64 bf16 map).
+  constexpr bool SPLITW = OP::kSplit == 2 && D == 64 && M == 64;
+  constexpr int NTB = (SPLITW ? D / 16 + M / 16 : cmax(D, M) / 16) * 64;
+  hipLaunchKernelGGL((bwd_gated_kernel<OP, D, M, C, SPLITW>), dim3(grid), dim3(NTB), 0, s, k);
   timing_end(GRADLEV_K_GATED_BWD, s);
   if (dW0) {
     const int64_t md = (int64_t)M * D;
