@@ -41,8 +41,8 @@ PEAK_FP32_MFMA = 157.3e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-SECONDARY_NAMES = ("lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated", "mlp-lm", "decode-mlp-lm", "decode-f32",
-                   "decode-f32-S2048", "decode-f32-gated")
+SECONDARY_NAMES = ("lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated", "lm-bf16-gated-plain",
+                   "mlp-lm", "decode-mlp-lm", "decode-f32", "decode-f32-S2048", "decode-f32-gated")
 
 
 def parse():
@@ -455,11 +455,13 @@ def secondary_cold(gl, torch, W, device, reps=20):
             "fwd_ms": f, "bwd_ms": b, "fwd_plus_bwd_ms": f + b, "tokens_per_s": wl.B * wl.T / ((f + b) * 1e-3)}
 
 
-def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2):
+def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2, saved=True):
     """Gated fwd+bwd (retention, per-token gates, packed-document resets) on the
     lm-bf16 shape, every gradient including dalpha.  Pipelined like the
     headline: step i runs the forward of input set i and the backward of set
-    i - lag (modulo nsets), so neither reads its inputs from the Infinity Cache."""
+    i - lag (modulo nsets), so neither reads its inputs from the Infinity Cache.
+    saved: the save-for-backward pair (the forward keeps the chunk-start
+    states, one buffer per set); else the plain gated calls."""
     wl = W.SCAN_WORKLOADS["lm-bf16"]
     B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
     sets = []
@@ -471,7 +473,13 @@ def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2):
         inp["reset"] = torch.from_numpy(W.reset_flags(B, T, wl.seed + 12 + 2 * k, mean_len=512)).to(device)
         sets.append(inp)
     shape = gl.make_shape(B, H, T, d, m, gl.BF16)
-    ws = torch.empty(max(gl.gated_workspace_bytes(shape), 256), dtype=torch.uint8, device=device)
+    if saved:
+        sv_bytes, ws_bytes = gl.gated_saved_bytes(shape)
+        for inp in sets:
+            inp["saved"] = torch.zeros(sv_bytes // 4, dtype=torch.float32, device=device)
+    else:
+        ws_bytes = gl.gated_workspace_bytes(shape)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
     f32 = dict(dtype=torch.float32, device=device)
     Y = torch.empty(B, H, T, m, **f32)
     outs = {"gtilde": torch.empty(B, H, T, d, **f32), "dx": torch.empty(B, H, T, d, **f32),
@@ -480,20 +488,27 @@ def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2):
 
     def fn(i=0):
         f, b = sets[i % nsets], sets[(i - lag) % nsets]
-        gl.scan_fwd_gated(f["W0"], f["X"], f["G"], f["eta_t"], f["alpha"], f["reset"], out=Y, workspace=ws)
-        gl.scan_bwd_gated(b["W0"], b["X"], b["G"], b["dY"], b["eta_t"], b["alpha"], b["reset"], out=outs,
-                          workspace=ws)
+        if saved:
+            gl.scan_fwd_gated_save(f["W0"], f["X"], f["G"], f["eta_t"], f["alpha"], f["reset"], out=Y,
+                                   saved=f["saved"], workspace=ws)
+            gl.scan_bwd_gated_saved(b["W0"], b["X"], b["G"], b["dY"], b["saved"], b["eta_t"], b["alpha"],
+                                    b["reset"], out=outs, workspace=ws)
+        else:
+            gl.scan_fwd_gated(f["W0"], f["X"], f["G"], f["eta_t"], f["alpha"], f["reset"], out=Y, workspace=ws)
+            gl.scan_bwd_gated(b["W0"], b["X"], b["G"], b["dY"], b["eta_t"], b["alpha"], b["reset"], out=outs,
+                              workspace=ws)
     for i in range(warmup):
         fn(i)
     ms, _ = graph_timed(torch, gl, fn, steps, kernels=[])
     _, k = graph_timed(torch, gl, fn, steps,
-                       kernels=["gated_agg", "gated_fwd", "gated_states", "gated_bwd", "bwd_dw0"])
+                       kernels=["gated_agg", "gated_fwd", "gated_bwd", "bwd_dw0"] + ([] if saved else ["gated_states"]))
     # Algorithmic bytes: x, g (and dY) in bf16, alpha and eta per token; outputs fp32
     # (y; gtilde, dX, dG, deta, dalpha).  Flops as the unit-retention scan.
     nbytes = B * H * T * (2 * (d + m) + 8 + 4 * m + 2 * (d + 2 * m) + 8 + 4 * (2 * d + m) + 8)
     flops = B * H * T * (flops_fwd(d, m, 64) + flops_bwd(d, m, 32))
     res = {"workload": "lm-bf16 shape, gated: alpha = sigmoid(N(1.5, 0.5^2)), eta = 4/d sigmoid(N(log(0.9/3.1), 0.5^2)) "
                        "per token, documents of geometric length (mean 512) packed per row",
+           "pair": "scan_fwd_gated_save + scan_bwd_gated_saved" if saved else "scan_fwd_gated + scan_bwd_gated",
            "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3),
            "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9, "frac_hbm_peak": nbytes / (ms * 1e-3) / PEAK_HBM,
            "tflops_algorithmic": flops / (ms * 1e-3) / 1e12,
@@ -660,6 +675,8 @@ def run_secondary(name, gl, torch, W, device):
         return secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
     if name == "lm-bf16-gated":
         return secondary_gated(gl, torch, W, device)
+    if name == "lm-bf16-gated-plain":
+        return secondary_gated(gl, torch, W, device, saved=False)
     if name == "mlp-lm":
         return secondary_mlp_lm(gl, torch, device)
     if name == "decode-mlp-lm":

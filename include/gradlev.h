@@ -271,6 +271,43 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates,
                            float* dalpha, float* dW0, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* Gated save-for-backward pair.  With retention the backward needs Delta at
+ * the start of every one of its tiles (Section 3, Eq. 2 with alpha; the
+ * writes cannot be taken back, so they are carried forward), which the plain
+ * gated backward recomputes in a state pass over X and G.  Here the forward
+ * runs on the backward's tile and stores those states as it passes them, and
+ * the backward reads them: no state pass, and no write aggregates, so its
+ * aggregate pass reads X, dY and the gates but not G.
+ *
+ * gradlev_scan_gated_saved_bytes: bytes of the saved states (*saved_bytes:
+ *   B*H * ceil(T / tile) * m * d * 4, tile 64 for bf16 64 x 64 maps, else 32)
+ *   and of the workspace both calls need (*workspace_bytes).  Pure host
+ *   computation.  Both calls of a pair take the same shape, the same
+ *   segment hint, the same gates and a workspace of at least that size.
+ * gradlev_scan_fwd_gated_save: as gradlev_scan_fwd_gated, and also writes
+ *   the states into saved (layout private to the library).
+ * gradlev_scan_bwd_gated_saved: as gradlev_scan_bwd_gated, reading the
+ *   states that gradlev_scan_fwd_gated_save wrote for the same inputs and
+ *   gates; the caller keeps that buffer unmodified in between.  Results equal
+ *   gradlev_scan_bwd_gated's up to float32 rounding order.
+ * saved must be 16-byte aligned device memory of at least the returned size
+ * (GRADLEV_ERR_WORKSPACE otherwise).  Wide shapes return
+ * GRADLEV_ERR_UNSUPPORTED (the parallel form keeps no states). */
+int gradlev_scan_gated_saved_bytes(const gradlev_shape* s, size_t* saved_bytes,
+                                   size_t* workspace_bytes);
+int gradlev_scan_fwd_gated_save(const gradlev_shape* s, const gradlev_gates* gates,
+                                const float* W0, const void* X, const void* G,
+                                const float* eta, float eta_scalar, float* Y,
+                                float* saved, size_t saved_bytes, void* workspace,
+                                size_t workspace_bytes, void* stream);
+int gradlev_scan_bwd_gated_saved(const gradlev_shape* s, const gradlev_gates* gates,
+                                 const float* W0, const void* X, const void* G,
+                                 const float* eta, float eta_scalar, const void* dY,
+                                 const float* saved, size_t saved_bytes,
+                                 float* gtilde, float* dX, float* dG, float* deta,
+                                 float* dalpha, float* dW0, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
 /* Gated deployment step: score with the current weights, then write with
  * centered decay,
  *   y[s,h,:]  = W[s,h] x[s,h,:]            (W[s,h] replaced by W0[h] first if reset[s])

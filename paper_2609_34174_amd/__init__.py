@@ -100,6 +100,12 @@ def lib():
                                              f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_scan_bwd_gated.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
                                              vp, f32p, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_gated_saved_bytes.argtypes = [ctypes.POINTER(Shape), szp, szp]
+        L.gradlev_scan_fwd_gated_save.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
+                                                  f32p, f32p, ctypes.c_size_t, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_bwd_gated_saved.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
+                                                   vp, f32p, ctypes.c_size_t, f32p, f32p, f32p, f32p, f32p, f32p,
+                                                   vp, ctypes.c_size_t, vp]
         L.gradlev_decode_step_gated.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p, f32p,
                                                 ctypes.c_float, f32p, ctypes.c_float, vp, f32p, vp]
         mp = ctypes.POINTER(MlpShape)
@@ -115,6 +121,7 @@ def lib():
                      "gradlev_scan_bwd", "gradlev_scan_saved_bytes", "gradlev_scan_fwd_save",
                      "gradlev_scan_bwd_saved", "gradlev_decode_step", "gradlev_scan_gated_workspace_bytes",
                      "gradlev_scan_fwd_gated", "gradlev_scan_bwd_gated", "gradlev_decode_step_gated",
+                     "gradlev_scan_gated_saved_bytes", "gradlev_scan_fwd_gated_save", "gradlev_scan_bwd_gated_saved",
                      "gradlev_mlp_workspace_bytes", "gradlev_mlp_fwd", "gradlev_mlp_reverse",
                      "gradlev_timing_enable",
                      "gradlev_timing_reset", "gradlev_timing_read"):
@@ -458,6 +465,74 @@ def scan_bwd_gated(W0, X, G, dY, eta=0.1, alpha=1.0, reset=None, *, chunk=0, seg
                                       _ptr(res.get("dw0")), _ptr(ws), wsn, _stream(X.device))
     if rc != OK:
         raise GradLevError(rc, "gradlev_scan_bwd_gated")
+    return res
+
+
+def gated_saved_bytes(shape: Shape):
+    """(saved-state bytes, workspace bytes) of the gated save-for-backward pair."""
+    sv, ws = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    rc = lib().gradlev_scan_gated_saved_bytes(ctypes.byref(shape), ctypes.byref(sv), ctypes.byref(ws))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_gated_saved_bytes")
+    return int(sv.value), int(ws.value)
+
+
+def scan_fwd_gated_save(W0, X, G, eta=0.1, alpha=1.0, reset=None, *, chunk=0, segment=0, out=None, saved=None,
+                        workspace=None):
+    """Gated forward that also keeps the backward's chunk-start states.
+
+    Returns (Y, saved) (see gradlev_scan_fwd_gated_save)."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", chunk, segment)
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    sv_need, ws_need = gated_saved_bytes(s)
+    if out is None:
+        out = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    _check_dev("out", out, torch.float32, (s.B, s.H, s.T, s.d_out))
+    if saved is None:
+        saved = torch.empty(sv_need // 4, dtype=torch.float32, device=X.device)
+    saved, svn = _bytes_of("saved", saved, sv_need)
+    if workspace is None and ws_need:
+        workspace = torch.empty(ws_need, dtype=torch.uint8, device=X.device)
+    ws, wsn = _bytes_of("workspace", workspace, ws_need)
+    rc = lib().gradlev_scan_fwd_gated_save(ctypes.byref(s), ctypes.byref(gt), _ptr(W0), _ptr(X), _ptr(G), _ptr(e),
+                                           es, _ptr(out), _ptr(saved), svn, _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_fwd_gated_save")
+    return out, saved
+
+
+def scan_bwd_gated_saved(W0, X, G, dY, saved, eta=0.1, alpha=1.0, reset=None, *, chunk=0, segment=0,
+                         outputs=GATED_OUTPUTS, out=None, workspace=None):
+    """scan_bwd_gated starting from the states scan_fwd_gated_save kept."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", chunk, segment)
+    _check_dev("dY", dY, X.dtype, (s.B, s.H, s.T, s.d_out))
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    gt = _gates(alpha, reset, s.B, s.H, s.T, X)
+    sv_need, ws_need = gated_saved_bytes(s)
+    shapes = {"gtilde": (s.B, s.H, s.T, s.d_in), "dx": (s.B, s.H, s.T, s.d_in),
+              "dg": (s.B, s.H, s.T, s.d_out), "deta": (s.B, s.H, s.T), "dalpha": (s.B, s.H, s.T),
+              "dw0": (s.H, s.d_out, s.d_in)}
+    res = dict(out or {})
+    for k in outputs:
+        if k not in shapes:
+            raise ValueError(f"unknown output {k!r}")
+        if k not in res:
+            res[k] = torch.empty(shapes[k], dtype=torch.float32, device=X.device)
+        _check_dev(k, res[k], torch.float32, shapes[k])
+    saved, svn = _bytes_of("saved", saved, sv_need)
+    if workspace is None and ws_need:
+        workspace = torch.empty(ws_need, dtype=torch.uint8, device=X.device)
+    ws, wsn = _bytes_of("workspace", workspace, ws_need)
+    rc = lib().gradlev_scan_bwd_gated_saved(ctypes.byref(s), ctypes.byref(gt), _ptr(W0), _ptr(X), _ptr(G),
+                                            _ptr(e), es, _ptr(dY), _ptr(saved), svn, _ptr(res.get("gtilde")),
+                                            _ptr(res.get("dx")), _ptr(res.get("dg")), _ptr(res.get("deta")),
+                                            _ptr(res.get("dalpha")), _ptr(res.get("dw0")), _ptr(ws), wsn,
+                                            _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_bwd_gated_saved")
     return res
 
 

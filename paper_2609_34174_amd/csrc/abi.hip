@@ -222,6 +222,37 @@ int make_gated_plan(const gradlev_shape* s, GatedPlan* out) {
   return GRADLEV_OK;
 }
 
+// The gated save-for-backward pair: the forward runs on the backward's tile
+// and writes Delta at every tile start into the saved buffer, in the order
+// the backward loads it; the backward then needs no state pass and no write
+// aggregates (its workspace ends before the state region).
+int make_gated_saved_plan(const gradlev_shape* s, GatedPlan* out, size_t* saved_bytes) {
+  const int rc = make_gated_plan(s, out);
+  if (rc != GRADLEV_OK) return rc;
+  const int64_t BH = s->B * s->H;
+  const size_t md = (size_t)s->d_out * s->d_in * sizeof(float);
+  const int bf = s->in_dtype == GRADLEV_BF16;
+  out->fwd.chunk = out->bwd.chunk;
+  const int64_t sc = pick_nseg(BH, s->T, out->fwd.chunk, gated_wgs_per_cu(1, bf, (int)s->d_in, (int)s->d_out),
+                               s->segment);
+  out->fwd.seg_len = sc * out->fwd.chunk;
+  out->fwd.nseg = (s->T + out->fwd.seg_len - 1) / out->fwd.seg_len;
+  if (out->fwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
+  const size_t nf = (size_t)BH * out->fwd.nseg;
+  out->ws_fwd = out->fwd.nseg > 1 ? round_up(nf * md, 256) + round_up(nf * 4, 256) : 0;
+  *saved_bytes = (size_t)BH * ((s->T + out->bwd.chunk - 1) / out->bwd.chunk) * md;
+  out->ws_bwd = out->off_S;
+  return GRADLEV_OK;
+}
+
+int gated_fwd_planned(const gradlev_shape* s, const GatedPlan& p, const gradlev_gates* gates, const float* W0,
+                      const void* X, const void* G, const float* eta, float eta_scalar, float* Y, float* states,
+                      void* workspace, size_t workspace_bytes, void* stream);
+int gated_bwd_planned(const GatedPlan& p, const gradlev_gates* gates, const float* W0, const void* X,
+                      const void* G, const float* eta, float eta_scalar, const void* dY, const float* states,
+                      float* gtilde, float* dX, float* dG, float* deta, float* dalpha, float* dW0, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
 int check_gates(const gradlev_gates* g) {
   if (!g) return GRADLEV_ERR_INVALID;
   if (g->alpha && !aligned16(g->alpha)) return GRADLEV_ERR_ALIGN;
@@ -551,9 +582,21 @@ int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
     return launch_wide_fwd(w, f, static_cast<hipStream_t>(stream)) == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
   }
   GatedPlan p;
-  int rc = make_gated_plan(s, &p);
+  const int rc = make_gated_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
-  rc = check_gates(gates);
+  return gated_fwd_planned(s, p, gates, W0, X, G, eta, eta_scalar, Y, nullptr, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace gradlev {
+namespace {
+
+// Gated forward with a validated plan; states (saved chunk-start states) or null.
+int gated_fwd_planned(const gradlev_shape* s, const GatedPlan& p, const gradlev_gates* gates, const float* W0,
+                      const void* X, const void* G, const float* eta, float eta_scalar, float* Y, float* states,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_gates(gates);
   if (rc != GRADLEV_OK) return rc;
   if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
   if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
@@ -577,9 +620,58 @@ int gradlev_scan_fwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
     f.aggA = reinterpret_cast<float*>(ws);
     f.aggD = reinterpret_cast<float*>(ws + round_up(nf * (size_t)s->d_out * s->d_in * sizeof(float), 256));
   }
+  f.states = states;
   const hipError_t e = launch_scan_fwd_gated(p.fwd, f, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }
+
+// Gated backward with a validated plan; states: the saving forward's states,
+// or null (then the workspace's state region, filled by the state pass).
+int gated_bwd_planned(const GatedPlan& p, const gradlev_gates* gates, const float* W0, const void* X,
+                      const void* G, const float* eta, float eta_scalar, const void* dY, const float* states,
+                      float* gtilde, float* dX, float* dG, float* deta, float* dalpha, float* dW0, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  int rc = check_gates(gates);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
+  if (!gtilde && !dX && !dG && !deta && !dalpha && !dW0) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dalpha, dW0};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  rc = check_workspace(workspace, workspace_bytes, p.ws_bwd);
+  if (rc != GRADLEV_OK) return rc;
+  char* ws = static_cast<char*>(workspace);
+  GatedPtrs b{};
+  b.W0 = W0;
+  b.X = X;
+  b.G = G;
+  b.dY = dY;
+  b.eta = eta;
+  b.eta_scalar = eta_scalar;
+  b.eta_mul = 1.f;
+  b.alpha = gates->alpha;
+  b.alpha_scalar = gates->alpha_scalar;
+  b.reset = gates->reset;
+  b.gtilde = gtilde;
+  b.dX = dX;
+  b.dG = dG;
+  b.deta = deta;
+  b.dalpha = dalpha;
+  b.dW0 = dW0;
+  b.aggA = reinterpret_cast<float*>(ws + p.off_A);
+  b.aggB = reinterpret_cast<float*>(ws + p.off_B);
+  b.aggBu = reinterpret_cast<float*>(ws + p.off_Bu);
+  b.aggD = reinterpret_cast<float*>(ws + p.off_D);
+  b.states = states ? const_cast<float*>(states) : reinterpret_cast<float*>(ws + p.off_S);
+  b.saved_states = states != nullptr;
+  const hipError_t e = launch_scan_bwd_gated(p.bwd, b, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+}  // namespace
+}  // namespace gradlev
+
+extern "C" {
 
 int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
                            const void* X, const void* G, const float* eta, float eta_scalar,
@@ -613,42 +705,54 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
     return launch_wide_read(w, f, static_cast<hipStream_t>(stream)) == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
   }
   GatedPlan p;
-  int rc = make_gated_plan(s, &p);
+  const int rc = make_gated_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
-  rc = check_gates(gates);
+  return gated_bwd_planned(p, gates, W0, X, G, eta, eta_scalar, dY, nullptr, gtilde, dX, dG, deta, dalpha, dW0,
+                           workspace, workspace_bytes, stream);
+}
+
+int gradlev_scan_gated_saved_bytes(const gradlev_shape* s, size_t* saved_bytes, size_t* workspace_bytes) {
+  if (!saved_bytes || !workspace_bytes) return GRADLEV_ERR_INVALID;
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  GatedPlan p;
+  size_t sb = 0;
+  const int rc = make_gated_saved_plan(s, &p, &sb);
   if (rc != GRADLEV_OK) return rc;
-  if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
-  if (!gtilde && !dX && !dG && !deta && !dalpha && !dW0) return GRADLEV_ERR_INVALID;
-  const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dalpha, dW0};
-  for (const void* q : ptrs)
-    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
-  rc = check_workspace(workspace, workspace_bytes, p.ws_bwd);
+  *saved_bytes = sb;
+  *workspace_bytes = p.ws_fwd > p.ws_bwd ? p.ws_fwd : p.ws_bwd;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_fwd_gated_save(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
+                                const void* X, const void* G, const float* eta, float eta_scalar, float* Y,
+                                float* saved, size_t saved_bytes, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  GatedPlan p;
+  size_t need = 0;
+  const int rc = make_gated_saved_plan(s, &p, &need);
   if (rc != GRADLEV_OK) return rc;
-  char* ws = static_cast<char*>(workspace);
-  GatedPtrs b{};
-  b.W0 = W0;
-  b.X = X;
-  b.G = G;
-  b.dY = dY;
-  b.eta = eta;
-  b.eta_scalar = eta_scalar;
-  b.eta_mul = 1.f;
-  b.alpha = gates->alpha;
-  b.alpha_scalar = gates->alpha_scalar;
-  b.reset = gates->reset;
-  b.gtilde = gtilde;
-  b.dX = dX;
-  b.dG = dG;
-  b.deta = deta;
-  b.dalpha = dalpha;
-  b.dW0 = dW0;
-  b.aggA = reinterpret_cast<float*>(ws + p.off_A);
-  b.aggB = reinterpret_cast<float*>(ws + p.off_B);
-  b.aggBu = reinterpret_cast<float*>(ws + p.off_Bu);
-  b.aggD = reinterpret_cast<float*>(ws + p.off_D);
-  b.states = reinterpret_cast<float*>(ws + p.off_S);
-  const hipError_t e = launch_scan_bwd_gated(p.bwd, b, static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+  if (!saved) return GRADLEV_ERR_INVALID;
+  if (!aligned16(saved)) return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < need) return GRADLEV_ERR_WORKSPACE;
+  return gated_fwd_planned(s, p, gates, W0, X, G, eta, eta_scalar, Y, saved, workspace, workspace_bytes, stream);
+}
+
+int gradlev_scan_bwd_gated_saved(const gradlev_shape* s, const gradlev_gates* gates, const float* W0,
+                                 const void* X, const void* G, const float* eta, float eta_scalar, const void* dY,
+                                 const float* saved, size_t saved_bytes, float* gtilde, float* dX, float* dG,
+                                 float* deta, float* dalpha, float* dW0, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  if (wide_shape(s)) return s && s->B >= 1 ? GRADLEV_ERR_UNSUPPORTED : GRADLEV_ERR_INVALID;
+  GatedPlan p;
+  size_t need = 0;
+  const int rc = make_gated_saved_plan(s, &p, &need);
+  if (rc != GRADLEV_OK) return rc;
+  if (!saved) return GRADLEV_ERR_INVALID;
+  if (!aligned16(saved)) return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < need) return GRADLEV_ERR_WORKSPACE;
+  return gated_bwd_planned(p, gates, W0, X, G, eta, eta_scalar, dY, saved, gtilde, dX, dG, deta, dalpha, dW0,
+                           workspace, workspace_bytes, stream);
 }
 
 int gradlev_mlp_workspace_bytes(const gradlev_mlp_shape* s, size_t* bytes) {

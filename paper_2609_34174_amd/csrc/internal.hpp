@@ -73,6 +73,7 @@ struct GatedPtrs {
   float* aggBu;   // [B*H][nseg][m][d] (backward)
   float* aggD;    // [B*H][nseg]
   float* states;  // [B*H][ceil(T/chunk)][m*d] (backward), in the backward's register order
+  bool saved_states;  // backward: states were written by a saving forward (no state pass, no A)
 };
 
 struct DecodeGates {

@@ -204,19 +204,25 @@ __device__ __forceinline__ float sum_q(float v) {
 //   A  <- tot A + sum_s eta_s suf_s g_s x_s^T
 //   B  <- B + P sum_u pre_u dY_u x_u^T,   P <- P tot      (P = decay since the segment start)
 //   Bu <- Bu + sum_u dY_u x_u^T
-// All stored row-major [m][d]; D_k = P at the end.
+// All stored row-major [m][d]; D_k = P at the end.  Modes: kGAggFwd (A, D),
+// kGAggBwd (A, B, Bu, D) and kGAggBwdSaved (B, Bu, D: a backward whose
+// chunk-start states the forward saved needs no A, and so no G).
 // ---------------------------------------------------------------------------
-template <class OP, int D, int M, int C, bool BWD>
+enum GAggMode { kGAggFwd = 0, kGAggBwd = 1, kGAggBwdSaved = 2 };
+
+template <class OP, int D, int M, int C, int MODE>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
 agg_gated_kernel(const GArgs a, int64_t nagg) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
+  constexpr bool BWD = MODE != kGAggFwd;  // B, Bu
+  constexpr bool WA = MODE != kGAggBwdSaved;  // A
   constexpr int NW = cmax(D, M) / 16, NT = NW * 64;
   constexpr int JB = D / 16, IB = M / 16;
   constexpr bool SPL = OP::kSplit == 2;
   __shared__ E Xs[C * D];
-  __shared__ E Vh[C * M];
-  __shared__ E Vl[SPL ? C * M : 1];
+  __shared__ E Vh[WA ? C * M : 1];
+  __shared__ E Vl[WA && SPL ? C * M : 1];
   __shared__ E Ds[BWD ? C * M : 1];
   __shared__ E Bh[BWD ? C * M : 1];
   __shared__ E Bl[BWD && SPL ? C * M : 1];
@@ -230,7 +236,7 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
   const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
-  const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
+  const rsrc_t G = make_rsrc(WA ? static_cast<const E*>(a.G) + bh * T * M : nullptr, WA ? (uint32_t)(T * M * sizeof(E)) : 0u);
   const rsrc_t Dy = make_rsrc(BWD ? static_cast<const E*>(a.dY) + bh * T * M : nullptr, BWD ? (uint32_t)(T * M * sizeof(E)) : 0u);
   const GateSrc gs = gate_src(a, bh);
 
@@ -246,7 +252,7 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
     const bool ok = t0 < t_end;
     ar.load(gs, t0, ok, tid, C);
     xr.load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
-    gr.load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    if (WA) gr.load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
     if (BWD) dr.load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
   fetch(t_begin);
@@ -257,10 +263,10 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
     xr.store(Xs, tid);
     if (BWD) dr.store(Ds, tid);
     __syncthreads();
-    if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, vw, 1.f, lane);
+    if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, WA ? vw : nullptr, 1.f, lane);
     __syncthreads();
     if (BWD && tid < C) pw[tid] = P * pre[tid];
-    gr.store_scaled(Vh, Vl, tid, vw);
+    if (WA) gr.store_scaled(Vh, Vl, tid, vw);
     __syncthreads();
     if (BWD) dr.store_scaled(Bh, Bl, tid, pw);
     const float tt = tot;
@@ -271,9 +277,12 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
       for (int jb = 0; jb < JB; ++jb) accA[jb] *= tt;
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
-        const F vh = OP::load_t(Vh, M, 32 * kb, 16 * w, lane);
-        F vl = vh;
-        if constexpr (SPL) vl = OP::load_t(Vl, M, 32 * kb, 16 * w, lane);
+        F vh{}, vl{};
+        if constexpr (WA) {
+          vh = OP::load_t(Vh, M, 32 * kb, 16 * w, lane);
+          vl = vh;
+          if constexpr (SPL) vl = OP::load_t(Vl, M, 32 * kb, 16 * w, lane);
+        }
         F bh2 = vh, bl2 = vh, dv = vh;
         if constexpr (BWD) {
           bh2 = OP::load_t(Bh, M, 32 * kb, 16 * w, lane);
@@ -283,7 +292,7 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) {
           const F xa = OP::load_t(Xs, D, 32 * kb, 16 * jb, lane);
-          accA[jb] = mma_split_b<OP>(accA[jb], xa, vh, vl);
+          if constexpr (WA) accA[jb] = mma_split_b<OP>(accA[jb], xa, vh, vl);
           if constexpr (BWD) {
             accB[jb] = mma_split_b<OP>(accB[jb], xa, bh2, bl2);
             accU[jb] = OP::mma(accU[jb], xa, dv);
@@ -298,7 +307,7 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
     const int64_t base = (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) {
-      *reinterpret_cast<f32x4*>(a.aggA + base + 16 * jb) = accA[jb];
+      if (WA) *reinterpret_cast<f32x4*>(a.aggA + base + 16 * jb) = accA[jb];
       if (BWD) {
         *reinterpret_cast<f32x4*>(a.aggB + base + 16 * jb) = accB[jb];
         *reinterpret_cast<f32x4*>(a.aggBu + base + 16 * jb) = accU[jb];
@@ -389,6 +398,18 @@ fwd_gated_kernel(const GArgs a) {
     __syncthreads();
     if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, vw, -1.f, lane);
     __syncthreads();
+    if (a.states && w < IB) {
+      // Saved for a backward with the same chunk: Delta at this chunk's
+      // start, in the order the backward's lanes load it (tiles of rows
+      // 16ib + 4q' + r', columns 16w' + c', one f32x4 per (w', ib, lane')).
+      // Issued here, before the longest stretch without a barrier, so that
+      // the stores retire under the output computation.
+      float* st = a.states + (bh * a.nchunks + t0 / C) * md + 256 * w + 4 * (16 * (c >> 2)) + (c & 3);
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) st[jb * IB * 256 + 4 * (4 * q + r)] = Dt[jb][r];
+    }
     gr.store_scaled(Vh, Vl, tid, vw);  // -eta_s suf_s g_s, read by the carry after a barrier
     fetch(t0 + C);
     if (w < IB) {
@@ -984,31 +1005,45 @@ static GArgs gargs(const ScanProblem& p, const GatedPtrs& f) {
   return k;
 }
 
-template <class OP, int D, int M>
-static hipError_t fwd_gated_dims(const ScanProblem& p, const GArgs& k, hipStream_t s) {
+template <class OP, int D, int M, int C>
+static hipError_t fwd_gated_dims_c(const ScanProblem& p, const GArgs& k, hipStream_t s) {
   constexpr int NT = cmax(D, M) / 16 * 64;
   const unsigned grid = (unsigned)seg_grid(k.BH, p.nseg);
   if (p.nseg > 1) {
     timing_begin(GRADLEV_K_GATED_AGG, s);
-    hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, 64, false>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
+    hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, C, kGAggFwd>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
     timing_end(GRADLEV_K_GATED_AGG, s);
   }
   timing_begin(GRADLEV_K_GATED_FWD, s);
-  hipLaunchKernelGGL((fwd_gated_kernel<OP, D, M, 64>), dim3(grid), dim3(NT), 0, s, k);
+  hipLaunchKernelGGL((fwd_gated_kernel<OP, D, M, C>), dim3(grid), dim3(NT), 0, s, k);
   timing_end(GRADLEV_K_GATED_FWD, s);
   return hipGetLastError();
 }
 
+// 64-token tiles; a forward that saves chunk-start states for a backward with
+// 32-token tiles runs 32-token tiles itself.
+template <class OP, int D, int M>
+static hipError_t fwd_gated_dims(const ScanProblem& p, const GArgs& k, hipStream_t s) {
+  if (p.chunk == 32) return fwd_gated_dims_c<OP, D, M, 32>(p, k, s);
+  return fwd_gated_dims_c<OP, D, M, 64>(p, k, s);
+}
+
 template <class OP, int D, int M, int C>
-static hipError_t bwd_gated_dims_c(const ScanProblem& p, const GArgs& k, float* dW0, hipStream_t s) {
+static hipError_t bwd_gated_dims_c(const ScanProblem& p, const GArgs& k, float* dW0, bool saved,
+                                   hipStream_t s) {
   constexpr int NT = cmax(D, M) / 16 * 64;
   const unsigned grid = (unsigned)seg_grid(k.BH, p.nseg);
   timing_begin(GRADLEV_K_GATED_AGG, s);
-  hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, C, true>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+  if (saved)
+    hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, C, kGAggBwdSaved>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+  else
+    hipLaunchKernelGGL((agg_gated_kernel<OP, D, M, C, kGAggBwd>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
   timing_end(GRADLEV_K_GATED_AGG, s);
-  timing_begin(GRADLEV_K_GATED_STATES, s);
-  hipLaunchKernelGGL((states_gated_kernel<OP, D, M, C>), dim3(grid), dim3(NT), 0, s, k);
-  timing_end(GRADLEV_K_GATED_STATES, s);
+  if (!saved) {  // the chunk-start states, unless the forward saved them
+    timing_begin(GRADLEV_K_GATED_STATES, s);
+    hipLaunchKernelGGL((states_gated_kernel<OP, D, M, C>), dim3(grid), dim3(NT), 0, s, k);
+    timing_end(GRADLEV_K_GATED_STATES, s);
+  }
   timing_begin(GRADLEV_K_GATED_BWD, s);
   // Separate waves for the row blocks of u where the wider workgroup keeps
   // its registers (measured on the 64 x 64 bf16 map).
@@ -1027,11 +1062,11 @@ static hipError_t bwd_gated_dims_c(const ScanProblem& p, const GArgs& k, float* 
 }
 
 template <class OP, int D, int M>
-static hipError_t bwd_gated_dims(const ScanProblem& p, const GArgs& k, float* dW0, hipStream_t s) {
+static hipError_t bwd_gated_dims(const ScanProblem& p, const GArgs& k, float* dW0, bool saved, hipStream_t s) {
   if constexpr (OP::kSplit == 2 && D == 64 && M == 64) {
-    if (p.chunk == 64) return bwd_gated_dims_c<OP, D, M, 64>(p, k, dW0, s);
+    if (p.chunk == 64) return bwd_gated_dims_c<OP, D, M, 64>(p, k, dW0, saved, s);
   }
-  return bwd_gated_dims_c<OP, D, M, 32>(p, k, dW0, s);
+  return bwd_gated_dims_c<OP, D, M, 32>(p, k, dW0, saved, s);
 }
 
 hipError_t launch_scan_fwd_gated(const ScanProblem& p, const GatedPtrs& f, hipStream_t s) {
@@ -1053,10 +1088,10 @@ hipError_t launch_scan_fwd_gated(const ScanProblem& p, const GatedPtrs& f, hipSt
 hipError_t launch_scan_bwd_gated(const ScanProblem& p, const GatedPtrs& f, hipStream_t s) {
   const GArgs k = gargs(p, f);
 #define GL_DIMS(OPT)                                                                   \
-  if (p.d == 64 && p.m == 64) return bwd_gated_dims<OPT, 64, 64>(p, k, f.dW0, s);     \
-  if (p.d == 64 && p.m == 128) return bwd_gated_dims<OPT, 64, 128>(p, k, f.dW0, s);   \
-  if (p.d == 128 && p.m == 64) return bwd_gated_dims<OPT, 128, 64>(p, k, f.dW0, s);   \
-  if (p.d == 128 && p.m == 128) return bwd_gated_dims<OPT, 128, 128>(p, k, f.dW0, s);
+  if (p.d == 64 && p.m == 64) return bwd_gated_dims<OPT, 64, 64>(p, k, f.dW0, f.saved_states, s);     \
+  if (p.d == 64 && p.m == 128) return bwd_gated_dims<OPT, 64, 128>(p, k, f.dW0, f.saved_states, s);   \
+  if (p.d == 128 && p.m == 64) return bwd_gated_dims<OPT, 128, 64>(p, k, f.dW0, f.saved_states, s);   \
+  if (p.d == 128 && p.m == 128) return bwd_gated_dims<OPT, 128, 128>(p, k, f.dW0, f.saved_states, s);
   if (p.bf16) {
     GL_DIMS(OpBF16)
   } else {

@@ -182,6 +182,35 @@ def test_saved_pair_validation_before_launch(L):
     assert L.gradlev_scan_saved_bytes(ctypes.byref(s), None, ctypes.byref(n)) == gl.ERR_INVALID
 
 
+def test_gated_saved_pair_sizes_and_validation(L):
+    """Saved states: one fp32 m x d matrix per sequence and backward tile (64
+    tokens for bf16 64 x 64 maps, else 32); the backward's workspace needs no
+    state region."""
+    for kw, tile in ((dict(), 64), (dict(dtype=gl.F32), 32), (dict(d_in=128), 32), (dict(T=1), 64)):
+        s = shape(**kw)
+        sv, ws = gl.gated_saved_bytes(s)
+        assert sv == s.B * s.H * -(-s.T // tile) * s.d_in * s.d_out * 4
+        assert ws <= gl.gated_workspace_bytes(s)
+    s = shape()
+    sv, _ = gl.gated_saved_bytes(s)
+    g = gl.Gates()
+    g.alpha, g.alpha_scalar, g.reset = None, 0.9, None
+
+    def fwd(sh=s, saved=FAKE, svn=1 << 40):
+        return L.gradlev_scan_fwd_gated_save(ctypes.byref(sh), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE,
+                                             saved, svn, FAKE, 1 << 40, None)
+
+    def bwd(sh=s, saved=FAKE, svn=1 << 40):
+        return L.gradlev_scan_bwd_gated_saved(ctypes.byref(sh), ctypes.byref(g), FAKE, FAKE, FAKE, None, 0.1, FAKE,
+                                              saved, svn, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
+    for call in (fwd, bwd):
+        assert call(saved=None) == gl.ERR_INVALID
+        assert call(saved=MISALIGNED) == gl.ERR_ALIGN
+        assert call(svn=sv - 4) == gl.ERR_WORKSPACE
+        assert call(sh=shape(prefix="inclusive")) == gl.ERR_UNSUPPORTED
+        assert call(sh=shape(d_in=1024, d_out=128)) == gl.ERR_UNSUPPORTED
+
+
 def test_decode_validation_before_launch(L):
     f = gl.lib().gradlev_decode_step
     assert f(0, 16, 64, 64, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
