@@ -20,6 +20,7 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
   ScanProblem fwd, bwd;
+  int64_t save_len;  // save-for-backward pair: tokens per saved state (the backward's segment)
   size_t ws_fwd, ws_bwd;
   // Offsets (bytes) inside the workspace.
   size_t off_aggA, off_aggB, off_rfin;
@@ -97,26 +98,31 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   out->bwd.nseg = (s->T + out->bwd.seg_len - 1) / out->bwd.seg_len;
   if (out->bwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
 
+  out->save_len = out->bwd.seg_len;
   layout_ws(out, BH, md);
   return GRADLEV_OK;
 }
 
-// The save-for-backward pair: the forward saves the weights at each of its
-// segments' ends and the backward starts its segments from them, so both run
-// on one segmentation: the shorter of the two segment lengths (the backward
-// is the longer pass and wants its parallelism), rounded up to the forward's
-// tile.  The backward tile (32 or 64 tokens) divides the forward's (64 or 128).
+// The save-for-backward pair: the forward saves the weights after each of
+// the backward's segments and the backward starts its segments from them.
+// The backward keeps its own segmentation, rounded up to the forward's tile
+// so that no forward tile straddles a saved boundary (the backward tile, 32
+// or 64 tokens, divides the forward's, 64 or 128); the forward's segments
+// are rounded up to whole backward segments.
 int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
   const int rc = make_plan(s, out);
   if (rc != GRADLEV_OK) return rc;
   const int64_t fc = out->fwd.chunk;
-  const int64_t bs = (out->bwd.seg_len + fc - 1) / fc * fc;
-  const int64_t seg = out->fwd.seg_len < bs ? out->fwd.seg_len : bs;
-  out->fwd.seg_len = out->bwd.seg_len = seg;
-  out->fwd.nseg = out->bwd.nseg = (s->T + seg - 1) / seg;
+  const int64_t sb = (out->bwd.seg_len + fc - 1) / fc * fc;
+  out->bwd.seg_len = sb;
+  out->bwd.nseg = (s->T + sb - 1) / sb;
+  const int64_t sf = (out->fwd.seg_len + sb - 1) / sb * sb;
+  out->fwd.seg_len = sf;
+  out->fwd.nseg = (s->T + sf - 1) / sf;
+  out->save_len = sb;
   const size_t md = (size_t)s->d_out * s->d_in * sizeof(float);
   layout_ws(out, s->B * s->H, md);
-  *saved_bytes = (size_t)(s->B * s->H) * out->fwd.nseg * md;
+  *saved_bytes = (size_t)(s->B * s->H) * out->bwd.nseg * md;
   return GRADLEV_OK;
 }
 
@@ -439,6 +445,8 @@ int scan_fwd_planned(const Plan& p, const float* W0, const void* X, const void* 
   f.Y = Y;
   f.agg = static_cast<float*>(workspace);
   f.wend = wend;
+  f.save_len = p.save_len;
+  f.nsave = p.bwd.nseg;
   const hipError_t e = launch_scan_fwd(p.fwd, f, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }

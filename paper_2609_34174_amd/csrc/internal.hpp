@@ -25,7 +25,8 @@ struct FwdPtrs {
   float eta_scalar;
   float* Y;
   float* agg;   // [B*H][nseg][m][d] workspace, or nullptr when nseg == 1
-  float* wend;  // [B*H][nseg][m][d] weights at each segment's end (saved for a backward), or nullptr
+  float* wend;  // [B*H][nsave][m][d] weights after each save_len-token block (for a backward), or nullptr
+  int64_t save_len, nsave;  // the backward's segment length and count (a multiple of the chunk)
 };
 
 struct BwdPtrs {

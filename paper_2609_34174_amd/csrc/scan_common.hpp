@@ -20,7 +20,8 @@ struct KArgs {
   float* out0;   // fwd: Y
   float* aggA;   // [BH][nseg][m*d] write aggregates A_k (fwd: [m][d]; bwd: transposed [d][m])
   float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates B_k (k >= 1)
-  float* wend;   // fwd, or null: [BH][nseg][m][d] fast weights at each segment's end
+  float* wend;   // fwd, or null: [BH][nsave][m][d] fast weights after each save_len-token block
+  int64_t save_len, nsave;
 };
 
 // ---------------------------------------------------------------------------

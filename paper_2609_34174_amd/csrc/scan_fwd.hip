@@ -224,19 +224,21 @@ fwd_main_kernel(const KArgs a) {
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) Ws[jb] -= e * dw[jb];
       }
+      // Saved for a backward: the fast weights after the last write of each
+      // save_len-token block (and of the sequence), row-major [m][d]; lane
+      // (c, q) holds W[16w + c][16jb + 4q .. +3].
+      const int64_t te = t0 + C < t_end ? t0 + C : t_end;
+      if (a.wend && live && (te % a.save_len == 0 || te == T)) {
+        float* o = a.wend + (bh * a.nsave + (te - 1) / a.save_len) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
+      }
     }
   };
 
   for (int64_t t0 = t_begin; t0 < t_end; t0 += 2 * C) {
     chunk(xa, ga, ea, t0);
     chunk(xb, gb, eb, t0 + C);
-  }
-  // Saved for a backward: the fast weights after this segment's last write
-  // (row-major [m][d]; lane (c, q) holds W[16w + c][16jb + 4q .. +3]).
-  if (a.wend && w < IB) {
-    float* o = a.wend + (bh * a.nseg + seg) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
   }
 }
 
@@ -255,11 +257,17 @@ int fwd_chunk_for(int bf16, int d, int m, int requested) {
   return C;
 }
 
+// Workgroups per CU the forward's segmentation aims at: one.  With inputs
+// streamed from HBM, half as many segments of twice the length measured
+// faster at B=8, H=16, T=2048, d=m=64 (main kernel 40 -> 35 us, aggregate
+// pass 19 -> 17 us): fewer concurrent streams, and a quarter less aggregate
+// reading.
 int fwd_wgs_per_cu(int bf16, int d, int m, int C) {
-  int n = 160 * 1024 / lds_bytes_fwd(bf16, d, m, C, 0);
-  const int waves = cmax(d, m) / 16;
-  if (n * waves > 8) n = 8 / waves;  // two waves per SIMD (register budget)
-  return n < 1 ? 1 : n;
+  (void)bf16;
+  (void)d;
+  (void)m;
+  (void)C;
+  return 1;
 }
 
 template <class OP, int D, int M, int C, bool ETAV>
@@ -318,6 +326,8 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& f, hipStream_t s
   k.aggA = p.nseg > 1 ? f.agg : nullptr;
   k.aggB = nullptr;
   k.wend = f.wend;
+  k.save_len = f.save_len;
+  k.nsave = f.nsave;
   if (p.bf16) {
     if (p.chunk == 128) return fwd_by_dims<OpBF16, 128>(p, k, s);
     return fwd_by_dims<OpBF16, 64>(p, k, s);

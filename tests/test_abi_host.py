@@ -136,18 +136,17 @@ def test_bwd_validation_before_launch(L):
                                 dict(dtype=gl.F32, d_in=128), dict(T=1), dict(segment=64, T=1000),
                                 dict(B=1, H=1, T=1 << 20)])
 def test_saved_pair_sizes(L, kw):
-    """The saved state is one fp32 [m][d] matrix per sequence and segment, on
-    one segmentation no coarser than the forward's; the workspace covers both
-    calls of the pair."""
+    """The saved state is one fp32 [m][d] matrix per sequence and backward
+    segment, the backward's segment rounded up to whole forward tiles; the
+    workspace covers both calls of the pair."""
     s = shape(**kw)
     p = gl.plan(s)
     sv, ws = gl.saved_bytes(s)
     md = s.d_in * s.d_out * 4
     assert sv % (s.B * s.H * md) == 0
     nseg = sv // (s.B * s.H * md)
-    assert p.fwd_nseg <= nseg <= 16
-    seg = -(-s.T // nseg)
-    assert -(-s.T // (-(-seg // p.fwd_chunk) * p.fwd_chunk)) == nseg  # a whole number of forward tiles
+    seg = -(-p.bwd_segment // p.fwd_chunk) * p.fwd_chunk
+    assert nseg == -(-s.T // seg) and 1 <= nseg <= 16
     agg = s.B * s.H * nseg * md if nseg > 1 else 0
     assert ws >= agg + s.B * s.H * md
 

@@ -103,22 +103,28 @@ def test_saved_pair_parity(dtype, prefix, d, m, T, seg):
         check(k, out[k], ref[k], dtype)
 
 
-@pytest.mark.parametrize("dtype,d,m", [("f32", 64, 64), ("bf16", 64, 64), ("bf16", 128, 64), ("f32", 64, 128)])
-def test_saved_states_are_segment_ends(dtype, d, m):
-    """The saved buffer holds W_0 + Delta at each segment's end, [B*H][nseg][m][d]."""
-    T, hint = 700, 256
-    log(f"saved states dtype={dtype} d={d} m={m} T={T} segment={hint}")
-    inp = small_inputs(2, 2, T, d, m, dtype, seed=77 + d + m, eta_kind="token")
-    s = gl.make_shape(B=2, H=2, T=T, d_in=d, d_out=m, dtype=gl.BF16 if dtype == "bf16" else gl.F32,
+@pytest.mark.parametrize("dtype,d,m,B,H,T,hint", [("f32", 64, 64, 2, 2, 700, 256), ("bf16", 64, 64, 2, 2, 700, 256),
+                                                  ("bf16", 128, 64, 2, 2, 700, 256), ("f32", 64, 128, 2, 2, 700, 256),
+                                                  ("bf16", 64, 64, 8, 16, 517, 0)])
+def test_saved_states_are_segment_ends(dtype, d, m, B, H, T, hint):
+    """The saved buffer holds W_0 + Delta after each of the backward's
+    segments, [B*H][nseg][m][d].  The last case has the automatic plan, where
+    the forward's segments span two of the backward's (B*H = 128)."""
+    log(f"saved states dtype={dtype} d={d} m={m} B={B} H={H} T={T} segment={hint}")
+    inp = small_inputs(B, H, T, d, m, dtype, seed=77 + d + m + T, eta_kind="token")
+    s = gl.make_shape(B=B, H=H, T=T, d_in=d, d_out=m, dtype=gl.BF16 if dtype == "bf16" else gl.F32,
                       segment=hint)
-    seg = gl.plan(s).fwd_segment
+    p = gl.plan(s)
+    seg = -(-p.bwd_segment // p.fwd_chunk) * p.fwd_chunk
     nseg = -(-T // seg)
+    if hint == 0:
+        assert p.fwd_segment > seg, (p.fwd_segment, seg)  # the case this test is for
     sv, _ = gl.saved_bytes(s)
-    assert sv == 2 * 2 * nseg * m * d * 4
+    assert sv == B * H * nseg * m * d * 4
     t = dev(inp, dtype)
     _, saved = gl.scan_fwd_save(t["W0"], t["X"], t["G"], t["eta"], segment=hint)
     torch.cuda.synchronize()
-    got = to_host(saved).reshape(2, 2, nseg, m, d)
+    got = to_host(saved).reshape(B, H, nseg, m, d)
     check("w_end", got, oracle_segment_ends(inp, seg), dtype)
 
 
