@@ -671,8 +671,10 @@ def run_secondary(name, gl, torch, W, device):
         return secondary_cold(gl, torch, W, device)
     if name == "lm-bf16-plain":  # the headline step without the saved segment states
         return secondary_scan(gl, torch, W, "lm-bf16", 200, 500, device, saved=False)
-    if name in ("long-bf16", "stack-bf16"):
-        return secondary_scan(gl, torch, W, name, 5 if name == "long-bf16" else 2, 1, device)
+    if name == "long-bf16":
+        return secondary_scan(gl, torch, W, name, 20, 20, device)
+    if name == "stack-bf16":
+        return secondary_scan(gl, torch, W, name, 2, 1, device)
     if name == "lm-bf16-gated":
         return secondary_gated(gl, torch, W, device)
     if name == "lm-bf16-gated-plain":

@@ -107,6 +107,20 @@ def test_chunk_hint_and_segments_change_rounding_only(dtype):
             check(f"{k}", out[k], ref[k], dtype)
 
 
+@pytest.mark.parametrize("prefix,T,seg", [("exclusive", 200, 0), ("inclusive", 333, 128), ("exclusive", 1000, 256),
+                                          ("inclusive", 1000, 0), ("exclusive", 130, 128)])
+def test_128_wide_tiles(prefix, T, seg):
+    """128 x 128 maps with 128-token forward tiles (shared score tiles in
+    LDS), several segments and ragged tails, both read conventions."""
+    log(f"128x128 chunk 128 prefix={prefix} T={T} seg={seg}")
+    inp = small_inputs(2, 3, T, 128, 128, "bf16", seed=T + seg + 5, eta_kind="scalar")
+    assert gl.plan(gl.make_shape(B=2, H=3, T=T, d_in=128, d_out=128, dtype=gl.BF16, chunk=128)).fwd_chunk == 128
+    out = run_gpu(inp, "bf16", prefix, chunk=128, segment=seg)
+    ref = oracle_all(inp, prefix)
+    for k in KEYS:
+        check(k, out[k], ref[k], "bf16")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_sixteen_segments(dtype):
     """The largest carry: 16 segments of 64 tokens, the last one ragged."""
