@@ -40,6 +40,12 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// A compile-time integer passed to a generic lambda (one instantiation per value).
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
 __device__ __forceinline__ f32x8 cat(f32x4 a, f32x4 b) {
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
@@ -226,6 +232,35 @@ __device__ __forceinline__ void buf_store4(rsrc_t r, uint32_t off, f32x4 v) {
 template <int POLICY = kStoreStream>
 __device__ __forceinline__ void buf_store1(rsrc_t r, uint32_t off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, POLICY);
+}
+
+// Whole-line output stores.  An accumulator tile stored as it lies writes 16
+// rows x 64 bytes per instruction; streamed to HBM as half lines, such stores
+// ran at about 70 % of the rate of stores that cover whole 128-byte lines.
+// pair_rows takes two tiles over the same 16 rows and two adjacent 16-column
+// blocks (lane (c, q): row c, columns 4q..4q+3 of each) and swaps halves
+// between lanes c and c ^ 8 with a DPP row rotation by 8 (the bank mask picks
+// the lanes that take the rotated value), so that lane (c, q) holds
+//   a: row c & 7,       columns 16 (c >> 3) + 4q .. +3 of the 32-column pair,
+//   b: row 8 + (c & 7), the same columns,
+// and one store of a (or of b) covers 8 whole rows of 32 fp32.
+template <int BANKS>  // 0x3: lanes c < 8 take the rotated value; 0xC: lanes c >= 8
+__device__ __forceinline__ float dpp_ror8(float old, float src) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                               __builtin_bit_cast(int, src), 0x128, 0xF, BANKS, false));
+}
+__device__ __forceinline__ void pair_rows(f32x4 t0, f32x4 t1, f32x4& a, f32x4& b) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    a[r] = dpp_ror8<0xC>(t0[r], t1[r]);  // lanes c >= 8 take tile 1's row c - 8
+    b[r] = dpp_ror8<0x3>(t1[r], t0[r]);  // lanes c < 8 take tile 0's row c + 8
+  }
+}
+// Byte offset, within a row-major fp32 matrix of `width` columns, of what
+// pair_rows puts in `a` for the tiles at rows [row0, row0 + 16) and columns
+// [col0, col0 + 32); `b` lies 8 rows further.
+__device__ __forceinline__ uint32_t pair_off(int64_t row0, int col0, int width, int c, int q) {
+  return (uint32_t)(((row0 + (c & 7)) * width + col0 + 16 * (c >> 3) + 4 * q) * 4);
 }
 
 }  // namespace gradlev

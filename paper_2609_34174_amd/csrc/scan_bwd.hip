@@ -69,6 +69,15 @@ bwd_main_kernel(const BArgs a) {
   constexpr int TB = C / 16, JB = D / 16, IB = M / 16;
   constexpr bool SPLITV = ETAV && OP::kSplit == 2;
   constexpr bool FULL = OUT == kOutFull;
+  // Paired column blocks (64x64 maps, 64-token chunks): waves 2p and 2p+1
+  // both keep W's column blocks 2p and 2p+1 and split the chunk's token
+  // blocks between them, so that each wave holds adjacent column blocks of
+  // the same rows and writes gtilde, dX and dG as whole 128-byte rows
+  // (pair_rows).  The pair's duplicated un-write costs a few matrix-core
+  // steps; the stores run at the full-line rate.
+  constexpr bool PAIR = D == 64 && M == 64 && C == 64;
+  constexpr int NWB = PAIR ? 2 : 1;   // W column blocks (and U row blocks) per wave
+  constexpr int TBW = PAIR ? 2 : TB;  // token blocks per wave in the output phases
   __shared__ E Xs[C * D];                  // X[t][j]
   __shared__ E Gs[C * M];                  // G[t][i]
   __shared__ E Ds[C * M];                  // dY[t][i]
@@ -84,11 +93,14 @@ bwd_main_kernel(const BArgs a) {
   __shared__ E Sh[SSH ? C * C : 1];
   __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
   __shared__ float et[C];
-  __shared__ float dpart[IB][C];
+  __shared__ float dpart[PAIR ? 2 : IB][C];
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg)) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: block indices stay scalar
+  // Column block of W (and row block of U) e of this wave.
+  auto blk = [&](int e) { return PAIR ? 2 * (w >> 1) + e : w; };
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
@@ -108,7 +120,7 @@ bwd_main_kernel(const BArgs a) {
   // come from HBM rather than the Infinity Cache.  fp32 tiles take twice the
   // registers, and the full backward of maps with a 128-wide side keeps more
   // accumulators: those stage one chunk ahead, which keeps them free of spills.
-  constexpr int DEPTH = (OP::kSplit == 2 && (!FULL || (D == 64 && M == 64))) ? 2 : 1;
+  constexpr int DEPTH = (OP::kSplit == 2 && (!FULL || (D == 64 && M == 64 && !PAIR))) ? 2 : 1;
   Tile4<OP, C, D, NT> xa, xb;
   Tile4<OP, C, M, NT> ga, gb, da, db;
   EtaReg<ETAV> ea, eb;
@@ -125,33 +137,37 @@ bwd_main_kernel(const BArgs a) {
   fetch(xa, ga, da, ea, nch - 1);
   if (DEPTH == 2) fetch(xb, gb, db, eb, nch - 2);
 
-  // Column-block state (wave w < JB): Wj[ib], Rj[ib] hold W/R[i = 16ib + 4q + r][j = 16w + c]
-  // at the segment's end: W_0 - sum_{j<=seg} A_j (subtracted in segment order)
-  // and R = sum_{j>seg} B_j (added from the last segment down).
-  f32x4 Wj[IB], Rj[IB];
+  // Column-block state (wave w < JB): Wj[e][ib] holds W[i = 16ib + 4q + r][j = 16 blk(e) + c]
+  // and Rj[ib] holds R[i][j = 16w + c], at the segment's end: W_0 - sum_{j<=seg} A_j
+  // (subtracted in segment order) and R = sum_{j>seg} B_j (added from the last segment down).
+  f32x4 Wj[NWB][IB], Rj[IB];
+  constexpr int PU = IB <= 4 ? 4 : 1;  // aggregates summed per batch of loads (register budget)
   if (w < JB) {
     // The segment's end state: saved by the forward, or W_0 minus the
     // aggregated writes up to and including this segment.
     const float* w0 = a.wend ? a.wend + (bh * a.nseg + seg) * M * D : a.W0 + (bh % a.H) * M * D;
 #pragma unroll
-    for (int ib = 0; ib < IB; ++ib)
+    for (int e = 0; e < NWB; ++e) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) Wj[ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * w + c];
-    const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
-    constexpr int PU = IB <= 4 ? 4 : 1;  // aggregates summed per batch of loads (register budget)
-    for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += PU) {
-      f32x4 v[PU][IB];
+      for (int ib = 0; ib < IB; ++ib)
 #pragma unroll
-      for (int u = 0; u < PU; ++u)
+        for (int r = 0; r < 4; ++r) Wj[e][ib][r] = w0[(int64_t)(16 * ib + 4 * q + r) * D + 16 * blk(e) + c];
+      const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * blk(e) + c) * M + 4 * q;
+      for (int64_t j0 = 0; !a.wend && j0 <= seg; j0 += PU) {
+        f32x4 v[PU][IB];
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib)
-          v[u][ib] = j0 + u <= seg ? *reinterpret_cast<const f32x4*>(a.aggA + o + (j0 + u) * M * D + 16 * ib) : zero4();
+        for (int u = 0; u < PU; ++u)
 #pragma unroll
-      for (int u = 0; u < PU; ++u)
+          for (int ib = 0; ib < IB; ++ib)
+            v[u][ib] = j0 + u <= seg ? *reinterpret_cast<const f32x4*>(a.aggA + o + (j0 + u) * M * D + 16 * ib) : zero4();
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib)
-          if (j0 + u <= seg) Wj[ib] -= v[u][ib];
+        for (int u = 0; u < PU; ++u)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib)
+            if (j0 + u <= seg) Wj[e][ib] -= v[u][ib];
+      }
     }
+    const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
 #pragma unroll
     for (int ib = 0; ib < IB; ++ib) Rj[ib] = zero4();
     if (FULL && a.aggB) {
@@ -253,10 +269,12 @@ bwd_main_kernel(const BArgs a) {
 
     // X^T rows j of this wave's column block over the chunk's tokens: shared
     // by the un-write, both intra-chunk terms and the suffix update.
-    F xt[C / 32];
+    F xt[NWB][C / 32];
     if (w < JB) {
 #pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, ln);
+      for (int e = 0; e < NWB; ++e)
+#pragma unroll
+        for (int kb = 0; kb < C / 32; ++kb) xt[e][kb] = OP::load_t(Xs, D, 32 * kb, 16 * blk(e), ln);
     }
 
     // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
@@ -264,82 +282,139 @@ bwd_main_kernel(const BArgs a) {
       if constexpr (ETAV) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F xq = xt[kb];
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
             const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, ln);
             F vl = vh;
             if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, ln);
-            Wj[ib] = mma_split_a<OP>(Wj[ib], vh, vl, xq);
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) Wj[e][ib] = mma_split_a<OP>(Wj[e][ib], vh, vl, xt[e][kb]);
           }
         }
       } else {
-        f32x4 dw[IB];
+        f32x4 dw[NWB][IB];
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib) dw[ib] = zero4();
+        for (int e = 0; e < NWB; ++e)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) dw[e][ib] = zero4();
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) dw[ib] = OP::mma(dw[ib], OP::load_t(Gs, M, 32 * kb, 16 * ib, ln), xt[kb]);
-        }
-        const float e = a.eta_scalar;
+          for (int ib = 0; ib < IB; ++ib) {
+            const F gq = OP::load_t(Gs, M, 32 * kb, 16 * ib, ln);
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib) Wj[ib] += e * dw[ib];
+            for (int e = 0; e < NWB; ++e) dw[e][ib] = OP::mma(dw[e][ib], gq, xt[e][kb]);
+          }
+        }
+        const float es = a.eta_scalar;
+#pragma unroll
+        for (int e = 0; e < NWB; ++e)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) Wj[e][ib] += es * dw[e][ib];
       }
     }
 
-    // (3) gtilde and dX for columns j in [16w, 16w+16), all t blocks at once.
+    // Token block hh of this wave in the gtilde/dX phase (tok3) and in the
+    // U/dG phase (tok4).  In a pair, wave 2p + H takes token blocks {2H, 2H+1}
+    // for gtilde/dX and {H, 3-H} for U/dG, which balances the causal
+    // intra-chunk terms; H is a template constant so that those terms'
+    // conditions fold at compile time.
+    auto outputs = [&](auto hc) {
+    constexpr int H = decltype(hc)::value;
+    auto tok3 = [&](int hh) { return PAIR ? 2 * H + hh : hh; };
+    auto tok4 = [&](int hh) { return PAIR ? (hh == 0 ? H : TB - 1 - H) : hh; };
+    // (3) gtilde and dX for columns j of blocks blk(e), token blocks tok3(hh).
     if (w < JB) {
-      f32x4 ga[TB], xa2[TB];
+      f32x4 ga[NWB][TBW], xa2[NWB][TBW];
 #pragma unroll
-      for (int tb = 0; tb < TB; ++tb) ga[tb] = xa2[tb] = zero4();
+      for (int e = 0; e < NWB; ++e)
+#pragma unroll
+        for (int hh = 0; hh < TBW; ++hh) ga[e][hh] = xa2[e][hh] = zero4();
       // gtilde^T[j][t] += sum_i W[i][j] dY[t][i];  dXw^T[j][s] += sum_i R[i][j] G[s][i]
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb) {
-        F wh, wl;
-        OP::split(cat(Wj[2 * kb], Wj[2 * kb + 1]), wh, wl);
-        F rh, rl;  // this wave's own R^T rows, as published (split) in step (1)
-        if (FULL) {
-          rh = OP::load_n(Rh, M, 16 * w, 32 * kb, ln);
-          rl = rh;
-          if constexpr (OP::kSplit == 2) rl = OP::load_n(Rl, M, 16 * w, 32 * kb, ln);
+        F wh[NWB], wl[NWB], rh[NWB], rl[NWB];  // R^T rows as published (split) in step (1)
+#pragma unroll
+        for (int e = 0; e < NWB; ++e) {
+          OP::split(cat(Wj[e][2 * kb], Wj[e][2 * kb + 1]), wh[e], wl[e]);
+          if (FULL) {
+            rh[e] = OP::load_n(Rh, M, 16 * blk(e), 32 * kb, ln);
+            rl[e] = rh[e];
+            if constexpr (OP::kSplit == 2) rl[e] = OP::load_n(Rl, M, 16 * blk(e), 32 * kb, ln);
+          }
         }
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          ga[tb] = mma_split_a<OP>(ga[tb], wh, wl, OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
-          if (FULL) xa2[tb] = mma_split_a<OP>(xa2[tb], rh, rl, OP::load_n(Gs, M, 16 * tb, 32 * kb, ln));
+        for (int hh = 0; hh < TBW; ++hh) {
+          const int tb = tok3(hh);
+          const F dq = OP::load_n(Ds, M, 16 * tb, 32 * kb, ln);
+          F gq;
+          if (FULL) gq = OP::load_n(Gs, M, 16 * tb, 32 * kb, ln);
+#pragma unroll
+          for (int e = 0; e < NWB; ++e) {
+            ga[e][hh] = mma_split_a<OP>(ga[e][hh], wh[e], wl[e], dq);
+            if (FULL) xa2[e][hh] = mma_split_a<OP>(xa2[e][hh], rh[e], rl[e], gq);
+          }
         }
       }
       if (FULL) {
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) xa2[tb] *= et[16 * tb + c];
+        for (int hh = 0; hh < TBW; ++hh) {
+          const float s = et[16 * tok3(hh) + c];
+#pragma unroll
+          for (int e = 0; e < NWB; ++e) xa2[e][hh] *= s;
+        }
       }
       // Intra-chunk terms: gtilde -= sum_{s<t} X[s][j] E[t][s];  dXw += sum_{t>s} X[t][j] E[t][s]
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
-        const F xq = xt[kb];
-        const F xn = OP::neg(xq);
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          if (kb <= tb / 2) ga[tb] = OP::mma(ga[tb], xn, OP::load_n(Es, C, 16 * tb, 32 * kb, ln));
-          if (FULL && kb >= tb / 2) xa2[tb] = OP::mma(xa2[tb], xq, OP::load_t(Es, C, 32 * kb, 16 * tb, ln));
+        for (int hh = 0; hh < TBW; ++hh) {
+          const int tb = tok3(hh);
+          if (kb <= tb / 2) {
+            const F ef = OP::load_n(Es, C, 16 * tb, 32 * kb, ln);
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) ga[e][hh] = OP::mma(ga[e][hh], OP::neg(xt[e][kb]), ef);
+          }
+          if (FULL && kb >= tb / 2) {
+            const F ef = OP::load_t(Es, C, 32 * kb, 16 * tb, ln);
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) xa2[e][hh] = OP::mma(xa2[e][hh], xt[e][kb], ef);
+          }
         }
       }
-      // Lane holds row t = 16tb + c, columns j = 16w + 4q + r; dX = gtilde - xa2.
+      // Lane holds row t = 16 tok3(hh) + c, columns j = 16 blk(e) + 4q + r; dX = gtilde - xa2.
 #pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        const uint32_t o = (uint32_t)(((t0 + 16 * tb + c) * D + 16 * w + 4 * q) * 4);
-        if (a.gtilde) buf_store4(Ogc, o, ga[tb]);
-        if (FULL && a.dX) buf_store4(Oxc, o, ga[tb] - xa2[tb]);
+      for (int hh = 0; hh < TBW; ++hh) {
+        const int tb = tok3(hh);
+        if constexpr (PAIR) {
+          const uint32_t o = pair_off(t0 + 16 * tb, 32 * (w >> 1), D, c, q), o8 = o + 8 * D * 4;
+          f32x4 lo, hi;
+          if (a.gtilde) {
+            pair_rows(ga[0][hh], ga[1][hh], lo, hi);
+            buf_store4(Ogc, o, lo);
+            buf_store4(Ogc, o8, hi);
+          }
+          if (FULL && a.dX) {
+            pair_rows(ga[0][hh] - xa2[0][hh], ga[1][hh] - xa2[1][hh], lo, hi);
+            buf_store4(Oxc, o, lo);
+            buf_store4(Oxc, o8, hi);
+          }
+        } else {
+          const uint32_t o = (uint32_t)(((t0 + 16 * tb + c) * D + 16 * w + 4 * q) * 4);
+          if (a.gtilde) buf_store4(Ogc, o, ga[0][hh]);
+          if (FULL && a.dX) buf_store4(Oxc, o, ga[0][hh] - xa2[0][hh]);
+        }
       }
     }
 
     if constexpr (FULL) {
-      // (4) U, dG and deta for rows i in [16w, 16w+16), all s blocks at once.
+      // (4) U, dG and deta for rows i of blocks blk(e), token blocks tok4(hh).
       if (w < IB) {
-        f32x4 ua[TB];
+        f32x4 ua[NWB][TBW];
 #pragma unroll
-        for (int sb = 0; sb < TB; ++sb) ua[sb] = zero4();
+        for (int e = 0; e < NWB; ++e)
+#pragma unroll
+          for (int hh = 0; hh < TBW; ++hh) ua[e][hh] = zero4();
         // Row fragments of X (rows t over j) serve both the R term and, when
         // the scores are not shared, the intra-chunk scores; they are then read
         // once when they fit the register budget (32 VGPRs), else per use.
@@ -358,24 +433,37 @@ bwd_main_kernel(const BArgs a) {
         // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb) {
-          const F rh = OP::load_t(Rh, M, 32 * kb, 16 * w, ln);
-          F rl = rh;
-          if constexpr (OP::kSplit == 2) rl = OP::load_t(Rl, M, 32 * kb, 16 * w, ln);
+          F rh[NWB], rl[NWB];
 #pragma unroll
-          for (int sb = 0; sb < TB; ++sb) ua[sb] = mma_split_a<OP>(ua[sb], rh, rl, xrow(sb, kb));
+          for (int e = 0; e < NWB; ++e) {
+            rh[e] = OP::load_t(Rh, M, 32 * kb, 16 * blk(e), ln);
+            rl[e] = rh[e];
+            if constexpr (OP::kSplit == 2) rl[e] = OP::load_t(Rl, M, 32 * kb, 16 * blk(e), ln);
+          }
+#pragma unroll
+          for (int hh = 0; hh < TBW; ++hh) {
+            const F xq = xrow(tok4(hh), kb);
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) ua[e][hh] = mma_split_a<OP>(ua[e][hh], rh[e], rl[e], xq);
+          }
         }
         if constexpr (SSH) {
           // Intra-chunk term from the shared split scores: the operand for
           // row s over k = t is a transposing read of the [t][s] tile.
 #pragma unroll
           for (int kb = 0; kb < C / 32; ++kb) {
-            const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, ln);
+            F dq[NWB];
 #pragma unroll
-            for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+            for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, M, 32 * kb, 16 * blk(e), ln);
+#pragma unroll
+            for (int hh = 0; hh < TBW; ++hh) {
+              const int sb = tok4(hh);
+              if (sb > 2 * kb + 1) continue;
               const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, ln);
               F sl = sh;
               if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, ln);
-              ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
+#pragma unroll
+              for (int e = 0; e < NWB; ++e) ua[e][hh] = mma_split_b<OP>(ua[e][hh], dq[e], sh, sl);
             }
           }
         } else {
@@ -384,13 +472,17 @@ bwd_main_kernel(const BArgs a) {
         // the tile (rows t, cols s) is directly the operand contracted over t.
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F dq = OP::load_t(Ds, M, 32 * kb, 16 * w, ln);
+          F dq[NWB];
 #pragma unroll
-          for (int sb = 0; sb <= 2 * kb + 1 && sb < TB; ++sb) {
+          for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, M, 32 * kb, 16 * blk(e), ln);
+#pragma unroll
+          for (int hh = 0; hh < TBW; ++hh) {
+            const int sb = tok4(hh);
+            if (sb > 2 * kb + 1) continue;
             f32x8 sv;
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-              const int tb = 2 * kb + hh;
+            for (int h2 = 0; h2 < 2; ++h2) {
+              const int tb = 2 * kb + h2;
               f32x4 st = zero4();
               if (tb >= sb) {
 #pragma unroll
@@ -404,47 +496,71 @@ bwd_main_kernel(const BArgs a) {
                 }
               }
 #pragma unroll
-              for (int r = 0; r < 4; ++r) sv[4 * hh + r] = st[r];
+              for (int r = 0; r < 4; ++r) sv[4 * h2 + r] = st[r];
             }
             F sh, sl;
             OP::split(sv, sh, sl);
-            ua[sb] = mma_split_b<OP>(ua[sb], dq, sh, sl);
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) ua[e][hh] = mma_split_b<OP>(ua[e][hh], dq[e], sh, sl);
           }
         }
         }
 #pragma unroll
-        for (int sb = 0; sb < TB; ++sb) {
-          // Lane holds token s = 16sb + c, rows i = 16w + 4q + r; U = -ua.
+        for (int hh = 0; hh < TBW; ++hh) {
+          // Lane holds token s = 16 tok4(hh) + c, rows i = 16 blk(e) + 4q + r; U = -ua.
+          const int sb = tok4(hh);
           const int s = 16 * sb + c;
           const float es = et[s];
-          if (a.dG) buf_store4(Odc, (uint32_t)(((t0 + s) * M + 16 * w + 4 * q) * 4), -es * ua[sb]);
+          if (a.dG) {
+            if constexpr (PAIR) {
+              const uint32_t o = pair_off(t0 + 16 * sb, 32 * (w >> 1), M, c, q);
+              f32x4 lo, hi;
+              pair_rows(-es * ua[0][hh], -es * ua[1][hh], lo, hi);
+              buf_store4(Odc, o, lo);
+              buf_store4(Odc, o + 8 * M * 4, hi);
+            } else {
+              buf_store4(Odc, (uint32_t)(((t0 + s) * M + 16 * w + 4 * q) * 4), -es * ua[0][hh]);
+            }
+          }
           if (a.deta) {
             typedef typename Vec4<E>::type vec4;
-            const vec4 gv = *reinterpret_cast<const vec4*>(Gs + lds_off(s, 16 * w + 4 * q, M));
             float p = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[sb][r];
+            for (int e = 0; e < NWB; ++e) {
+              const vec4 gv = *reinterpret_cast<const vec4*>(Gs + lds_off(s, 16 * blk(e) + 4 * q, M));
+#pragma unroll
+              for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[e][hh][r];
+            }
             p += __shfl_xor(p, 16);
             p += __shfl_xor(p, 32);
-            if (q == 0) dpart[w][s] = p;
+            if (q == 0) dpart[PAIR ? (w >> 1) : w][s] = p;
           }
         }
       }
 
+    }
+    if constexpr (FULL) {
       // (5) Suffix update: R_{n-1} = R_n + dY^T X (exact products).
       if (w < JB) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib) Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, ln), xt[kb]);
+          for (int ib = 0; ib < IB; ++ib)
+            Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, ln), xt[PAIR ? H : 0][kb]);
         }
       }
+    }
+    };
+    if (PAIR && (w & 1)) outputs(IntC<1>{});
+    else outputs(IntC<0>{});
+
+    if constexpr (FULL) {
       if (a.deta) {
         __syncthreads();
         const int tt = td < C ? td : 0;
         float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < IB; ++i) s += dpart[i][tt];
+        for (int i = 0; i < (PAIR ? 2 : IB); ++i) s += dpart[i][tt];
         buf_store1(Oec, td < C ? (uint32_t)((t0 + td) * 4) : kOOB, s);
       }
     }
