@@ -239,8 +239,14 @@ agg_kernel(const KArgs a, int64_t nagg) {
     if (WA) gr[k].load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
     if (with_b) dr[k].load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
+  // Issued in slot order (the scheduler would otherwise hoist the later
+  // slots' loads above the first's, and the loop's first wait, which must
+  // hold for both entries into the loop, would then drain every load).
 #pragma unroll
-  for (int k = 0; k < DEPTH; ++k) fetch(k, t_begin + k * C);
+  for (int k = 0; k < DEPTH; ++k) {
+    fetch(k, t_begin + k * C);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
   auto chunk = [&](int k, int64_t t0) {
     const int nvalid = (int)(t_end - t0 < C ? (t_end > t0 ? t_end - t0 : 0) : C);
