@@ -179,6 +179,22 @@ def test_backward_is_deterministic():
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
 
 
+@pytest.mark.parametrize("d,m,chunk,seg,eta_kind", [(64, 64, 128, 256, "token"), (64, 64, 64, 128, "token"),
+                                                    (64, 64, 0, 0, "scalar"), (128, 128, 0, 256, "token"),
+                                                    (64, 128, 0, 0, "token"), (128, 64, 128, 0, "scalar")])
+def test_repeated_calls_are_bitwise_identical(d, m, chunk, seg, eta_kind):
+    """Every tile variant (64- and 128-token forward tiles, register and LDS
+    score tiles, paired and wave-specialised backward tiles) reduces in a
+    fixed order, so repeated calls agree bitwise; a race between waves would
+    show here as run-to-run differences."""
+    log(f"repeat d={d} m={m} chunk={chunk} seg={seg} eta={eta_kind}")
+    inp = small_inputs(2, 3, 700, d, m, "bf16", seed=d + m + seg, eta_kind=eta_kind)
+    runs = [run_gpu(inp, "bf16", "exclusive", chunk=chunk, segment=seg) for _ in range(3)]
+    for r in runs[1:]:
+        for k in KEYS:
+            np.testing.assert_array_equal(r[k], runs[0][k], err_msg=k)
+
+
 # ---------------------------------------------------------------------------
 # Workload configurations at full size
 # ---------------------------------------------------------------------------
