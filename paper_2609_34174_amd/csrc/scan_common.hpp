@@ -223,11 +223,15 @@ agg_kernel(const KArgs a, int64_t nagg) {
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) accA[jb] = accB[jb] = zero4();
 
-  // The pass streams its inputs and does little arithmetic per byte, so its
-  // rate is set by the bytes in flight: chunks are staged DEPTH ahead.  Every
-  // group runs all DEPTH chunk steps (a step past the segment end sees zero
-  // tiles and adds nothing), which keeps the memory operations branch-free.
-  constexpr int DEPTH = 4;
+  // The pass streams its inputs and does little arithmetic per byte; chunks
+  // are staged DEPTH ahead.  Two measured best from HBM at B=8, H=16,
+  // T=2048, d=m=64 (forward pass 16.4 -> 15.4 us, backward 18.5 -> 16.5 us
+  // against four; one, three, six and eight were slower, and so were two
+  // groups of waves per workgroup): more loads in flight per CU only add
+  // concurrent streams.  Every group runs all DEPTH chunk steps (a step past
+  // the segment end sees zero tiles and adds nothing), which keeps the memory
+  // operations branch-free.
+  constexpr int DEPTH = 2;
   Tile4<OP, C, D, NT> xr[DEPTH];
   Tile4<OP, C, M, NT> gr[DEPTH], dr[DEPTH];
   EtaReg<ETAV> er[DEPTH];
