@@ -345,10 +345,17 @@ fwd_gated_kernel(const GArgs a) {
   __shared__ E Vl[SPL ? C * M : 1];
   __shared__ __attribute__((aligned(16))) float al[C], et[C], pre[C], suf[C], pin[C], sinv[C], vw[C];
   __shared__ float mid[16], tot;
+  // Y staged through LDS for whole-row stores (16-row x 64-byte tile stores
+  // stream to HBM at a fraction of the full-line rate); fp32 [C][M + 4], the
+  // pad staggering the owners' tile writes over the banks.
+  constexpr int YP = M + 4;
+  constexpr bool YSTG = OP::kSplit == 2 && D == 64 && M == 64 && C == 64 && NT == C * M / 16;
+  __shared__ __attribute__((aligned(16))) float Ys[YSTG ? C * YP : 4];
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg)) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 15, q = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: block indices stay scalar
   const int64_t h = bh % a.H;
   const int64_t T = a.T;
   const int64_t md = (int64_t)M * D;
@@ -464,10 +471,21 @@ fwd_gated_kernel(const GArgs a) {
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
         const int t = 16 * tb + c;
-        buf_store4(Y, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), acc[tb]);
+        if constexpr (YSTG) *reinterpret_cast<f32x4*>(Ys + t * YP + 16 * w + 4 * q) = acc[tb];
+        else buf_store4(Y, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), acc[tb]);
       }
     }
     __syncthreads();
+    if constexpr (YSTG) {
+      // Whole rows: thread tid stores 16 bytes of row tid / (M/4), so each
+      // wave writes four 256-byte rows (rows past T are dropped).  Ys is
+      // rewritten only after the next chunk's third barrier.
+#pragma unroll
+      for (int i = 0; i < C * M / 4 / NT; ++i) {
+        const int e = tid + i * NT, r = e / (M / 4), c4 = 4 * (e % (M / 4));
+        buf_store4(Y, (uint32_t)(((t0 + r) * M + c4) * 4), *reinterpret_cast<const f32x4*>(Ys + r * YP + c4));
+      }
+    }
     if (w < IB) {
       // Carry: Delta^T <- tot Delta^T + X^T V.
       const float tt = tot;
