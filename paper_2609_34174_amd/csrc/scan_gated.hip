@@ -245,32 +245,38 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
   for (int jb = 0; jb < JB; ++jb) accA[jb] = accB[jb] = accU[jb] = zero4();
   float P = 1.f;
 
-  Tile4<OP, C, D, NT> xr;
-  Tile4<OP, C, M, NT> gr, dr;
-  GateReg ar;
-  auto fetch = [&](int64_t t0) {
+  // Chunks staged two ahead in two register slots; every pass runs both
+  // slots' steps (a step past the segment end sees zero tiles, unit decay
+  // and zero step sizes, so it changes nothing), which keeps the memory
+  // operations branch-free.
+  Tile4<OP, C, D, NT> xr[2];
+  Tile4<OP, C, M, NT> gr[2], dr[2];
+  GateReg ar[2];
+  auto fetch = [&](int k, int64_t t0) {
     const bool ok = t0 < t_end;
-    ar.load(gs, t0, ok, tid, C);
-    xr.load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
-    if (WA) gr.load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
-    if (BWD) dr.load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    ar[k].load(gs, t0, ok, tid, C);
+    xr[k].load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
+    if (WA) gr[k].load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
+    if (BWD) dr[k].load(Dy, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
-  fetch(t_begin);
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += C) {
-    const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
+  fetch(0, t_begin);
+  __builtin_amdgcn_sched_barrier(0);  // slot order (the loop's first wait holds on entry too)
+  fetch(1, t_begin + C);
+  auto chunk = [&](int k, int64_t t0) {
+    const int nvalid = t0 < t_end ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
     __syncthreads();
-    ar.stage(al, et, nullptr, nvalid, tid, C);
-    xr.store(Xs, tid);
-    if (BWD) dr.store(Ds, tid);
+    ar[k].stage(al, et, nullptr, nvalid, tid, C);
+    xr[k].store(Xs, tid);
+    if (BWD) dr[k].store(Ds, tid);
     __syncthreads();
     if (w == 0) gate_scan<C>(al, et, pre, suf, pin, sinv, mid, &tot, WA ? vw : nullptr, 1.f, lane);
     __syncthreads();
     if (BWD && tid < C) pw[tid] = P * pre[tid];
-    if (WA) gr.store_scaled(Vh, Vl, tid, vw);
+    if (WA) gr[k].store_scaled(Vh, Vl, tid, vw);
     __syncthreads();
-    if (BWD) dr.store_scaled(Bh, Bl, tid, pw);
+    if (BWD) dr[k].store_scaled(Bh, Bl, tid, pw);
     const float tt = tot;
-    fetch(t0 + C);
+    fetch(k, t0 + 2 * C);
     __syncthreads();
     if (w < IB) {
 #pragma unroll
@@ -301,6 +307,10 @@ agg_gated_kernel(const GArgs a, int64_t nagg) {
       }
     }
     P *= tt;
+  };
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += 2 * C) {
+    chunk(0, t0);
+    chunk(1, t0 + C);
   }
   if (w < IB) {
     // acc[jb] holds A^T[j = 16jb + 4q + r][i = 16w + c]; stored as A[i][j].
