@@ -414,7 +414,7 @@ def token_outputs(W_read, R, x, g, eta_t, dy):
             "deta": g @ u}
 
 
-def decode_step(W, x, g, eta, alpha=None, W0=None):
+def decode_step(W, x, g, eta, alpha=None, W0=None, reset=None):
     """One deployment step for every (sequence, head): score, then write.
 
     W [S,H,m,d], x [S,H,d], g [S,H,m], eta scalar or [S,H].
@@ -422,8 +422,20 @@ def decode_step(W, x, g, eta, alpha=None, W0=None):
     W_next = W - eta g x^T, or, with retentions alpha (scalar or [S,H]) and
     the slow weights W0 [H,m,d], the centered decay of Eq. 2:
     W_next = W0 + alpha (W - W0) - eta g x^T.
+
+    reset [S] (0/1, optional, needs W0): a flagged sequence starts a new
+    document at this step.  Its read excludes every earlier write (the scan
+    reads of the appendix on forward and transpose reads; Eq. 2 holds within
+    each reset segment), so the state is replaced by W0 before the read.
     """
     W, x, g = _as_array(W), _as_array(x), _as_array(g)
+    if reset is not None:
+        if W0 is None:
+            raise ValueError("a reset needs the slow weights W0")
+        r = np.asarray(reset)
+        if r.shape != W.shape[:1]:
+            raise ValueError(f"reset must be [S]={W.shape[:1]}, got {r.shape}")
+        W = np.where((r != 0)[:, None, None, None], np.broadcast_to(_as_array(W0), W.shape), W)
     e = _as_array(eta)
     if e.ndim == 0:
         e = np.broadcast_to(e, W.shape[:2])
@@ -438,3 +450,61 @@ def decode_step(W, x, g, eta, alpha=None, W0=None):
         a = np.broadcast_to(a, W.shape[:2])
     W0b = np.broadcast_to(_as_array(W0), W.shape)
     return y, W0b + a[:, :, None, None] * (W - W0b) - write
+
+
+def scan_reads(W0, X, G, eta, A=None, Bq=None, alpha=None, reset=None):
+    """The forward and transpose scan reads as explicit causal sums.
+
+    The appendix on forward and transpose scan reads writes both reads of the
+    exclusive scan out from the expanded form of Eq. 2 (Eq. 16):
+
+        Delta_t a_t   = - sum_{i<t} eta_i (prod_{j=i+1}^{t-1} alpha_j) g_i (x_i . a_t)
+        Delta_t^T b_t = - sum_{i<t} eta_i (prod_{j=i+1}^{t-1} alpha_j) x_i (g_i . b_t)
+
+    where each read excludes the current write and every write before the
+    most recent document or context reset.  This function evaluates those
+    sums directly: a coefficient matrix K[t, i] = -eta_i prod(alpha) for the
+    writes a read sees (i < t, no reset in i+1..t) and zero otherwise, then
+    y_t = W_0 a_t + sum_i K[t, i] (x_i . a_t) g_i and
+    gtilde_t = W_0^T b_t + sum_i K[t, i] (g_i . b_t) x_i with matrix
+    products.  It is the same quantity the sequential sweeps produce, summed
+    in another order, and costs O(T^2) per sequence, which is cheaper than
+    the sweeps when the maps are wide.
+
+    A [B,H,T,d] forward queries (default X), Bq [B,H,T,m] transpose queries
+    (optional); eta and alpha scalars or [B,H,T] (alpha None means one);
+    reset [B,T] 0/1 flags, 1 = the token starts a new document.
+    Returns dict(y [B,H,T,m], and gtilde [B,H,T,d] when Bq is given).
+    """
+    W0, X, G = _as_array(W0), _as_array(X), _as_array(G)
+    B, H, T, d = X.shape
+    m = G.shape[-1]
+    A = X if A is None else _as_array(A)
+    e = _eta_array(eta, B, H, T)
+    a = np.ones((B, H, T)) if alpha is None else _eta_array(alpha, B, H, T)
+    doc = np.zeros((B, T), np.int64)
+    if reset is not None:
+        r = np.asarray(reset)
+        if r.shape != (B, T):
+            raise ValueError(f"reset must be [B,T]={B,T}, got {r.shape}")
+        doc = np.cumsum(r != 0, axis=1)
+    y = np.zeros((B, H, T, m))
+    gt = None if Bq is None else np.zeros((B, H, T, d))
+    if Bq is not None:
+        Bq = _as_array(Bq)
+    for b in range(B):
+        sees = (doc[b][:, None] == doc[b][None, :]) & np.tri(T, T, -1, dtype=bool)
+        for h in range(H):
+            K = np.zeros((T, T))
+            for i in range(T - 1):
+                # prod_{j=i+1}^{t-1} alpha_j for t = i+1 .. T-1 (empty product first)
+                K[i + 1:, i] = -e[b, h, i] * np.cumprod(np.concatenate(([1.0], a[b, h, i + 1:T - 1])))
+            K = np.where(sees, K, 0.0)
+            x, g = X[b, h], G[b, h]
+            y[b, h] = A[b, h] @ W0[h].T + (K * (A[b, h] @ x.T)) @ g
+            if Bq is not None:
+                gt[b, h] = Bq[b, h] @ W0[h] + (K * (Bq[b, h] @ g.T)) @ x
+    out = {"y": y}
+    if Bq is not None:
+        out["gtilde"] = gt
+    return out

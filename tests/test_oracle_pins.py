@@ -531,6 +531,125 @@ def test_reset_equals_separate_segments(with_alpha):
     np.testing.assert_allclose(out["dw0"], np.einsum("bhtm,bhtd->hmd", dY, X), rtol=1e-13)
 
 
+def test_hand_example_reset(golden_dir):
+    """The hand example with a document starting at token 2: the scan, the
+    explicit scan reads and decode all read W_0 there."""
+    with open(os.path.join(golden_dir, "hand_T3_d2.json")) as f:
+        gd = json.load(f)
+    W0 = np.array(gd["W0"], float)[None]
+    X = np.array(gd["X"], float)[None, None]
+    G = np.array(gd["G"], float)[None, None]
+    dY = np.array(gd["dY"], float)[None, None]
+    r = np.array([[1, 0, 1]], np.uint8)
+    exp = gd["reset_at_2"]
+    np.testing.assert_array_equal(orc.scan_fwd(W0, X, G, gd["eta"], reset=r)[0, 0], np.array(exp["y"], float))
+    np.testing.assert_array_equal(orc.scan_bwd(W0, X, G, gd["eta"], dY, reset=r)["gtilde"][0, 0],
+                                  np.array(exp["gtilde"], float))
+    reads = orc.scan_reads(W0, X, G, gd["eta"], Bq=dY, reset=r)
+    np.testing.assert_array_equal(reads["y"][0, 0], np.array(exp["y"], float))
+    np.testing.assert_array_equal(reads["gtilde"][0, 0], np.array(exp["gtilde"], float))
+    W = np.array(gd["W0"], float)[None, None]
+    for t in range(3):
+        y, W = orc.decode_step(W, X[:, :, t], G[:, :, t], gd["eta"], W0=W0, reset=r[:, t])
+        np.testing.assert_array_equal(y[0, 0], np.array(exp["y"][t], float))
+    np.testing.assert_array_equal(W[0, 0], np.array(exp["decode_final_W"], float))
+
+
+@pytest.mark.parametrize("with_alpha", [False, True])
+def test_decode_with_resets_equals_scan(with_alpha):
+    """T decode steps whose reset flags mark document starts reproduce the
+    scan with the same flags, and end at the closed-form state: W_0 minus the
+    writes of the last document, each discounted by the retentions after it."""
+    rng = np.random.default_rng(56)
+    S, H, T, d, m = 4, 2, 13, 5, 3
+    W0 = rng.standard_normal((H, m, d))
+    X = rng.standard_normal((S, H, T, d))
+    G = rng.standard_normal((S, H, T, m))
+    e = rng.uniform(0.1, 0.4, size=(S, H, T))
+    a = rng.uniform(0.0, 1.0, size=(S, H, T)) if with_alpha else None
+    r = (rng.uniform(size=(S, T)) < 0.25).astype(np.uint8)
+    r[0] = 0
+    r[1, 5] = r[2, 0] = r[2, T - 1] = 1
+    Y = orc.scan_fwd(W0, X, G, e, alpha=a, reset=r)
+    W = np.broadcast_to(W0, (S, H, m, d)).copy()
+    for t in range(T):
+        y, W = orc.decode_step(W, X[:, :, t], G[:, :, t], e[:, :, t],
+                               alpha=None if a is None else a[:, :, t], W0=W0, reset=r[:, t])
+        np.testing.assert_allclose(y, Y[:, :, t], rtol=0, atol=1e-12)
+    for s in range(S):
+        starts = np.nonzero(r[s])[0]
+        lo = int(starts[-1]) if len(starts) else 0
+        for h in range(H):
+            final = W0[h].copy()
+            for i in range(lo, T):
+                f = 1.0 if a is None else np.prod(a[s, h, i + 1:T])
+                final -= e[s, h, i] * f * np.outer(G[s, h, i], X[s, h, i])
+            np.testing.assert_allclose(W[s, h], final, rtol=0, atol=1e-12)
+
+
+def test_decode_reset_forgets_the_history():
+    """After a reset the decode trajectory is that of a fresh state W_0: the
+    steps before the reset have no effect on any later output."""
+    rng = np.random.default_rng(57)
+    S, H, T, d, m, cut = 2, 3, 9, 4, 4, 4
+    W0 = rng.standard_normal((H, m, d))
+    X = rng.standard_normal((S, H, T, d))
+    G = rng.standard_normal((S, H, T, m))
+    e, a = rng.uniform(0.1, 0.4, size=(S, H, T)), rng.uniform(0.5, 1.0, size=(S, H, T))
+    W = rng.standard_normal((S, H, m, d))           # arbitrary history
+    Wf = np.broadcast_to(W0, (S, H, m, d)).copy()   # fresh start at the cut
+    flag = np.ones(S, np.uint8)
+    for t in range(T):
+        y, W = orc.decode_step(W, X[:, :, t], G[:, :, t], e[:, :, t], a[:, :, t], W0,
+                               reset=flag if t == cut else None)
+        if t >= cut:
+            yf, Wf = orc.decode_step(Wf, X[:, :, t], G[:, :, t], e[:, :, t], a[:, :, t], W0)
+            np.testing.assert_allclose(y, yf, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(W, Wf, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("alpha_kind", ["none", "uniform", "zeros"])
+def test_scan_reads_equal_the_sweeps(alpha_kind):
+    """The explicit causal sums of the scan-read equation equal the sequential
+    learner's reads, forward and transpose, with retentions and resets."""
+    B, H, T, d, m = 3, 2, 23, 4, 6
+    W0, X, G, e, dY = rand_problem(B, H, T, d, m, seed=58)
+    a = None
+    if alpha_kind == "uniform":
+        a = rand_alpha(B, H, T, 59)
+    elif alpha_kind == "zeros":
+        a = rand_alpha(B, H, T, 60)
+        a[:, :, ::5] = 0.0
+    r = np.zeros((B, T), np.uint8)
+    r[0, 7] = r[1, 0] = r[1, 1] = r[2, 22] = r[2, 10] = 1
+    reads = orc.scan_reads(W0, X, G, e, Bq=dY, alpha=a, reset=r)
+    assert rel_err(reads["y"], orc.scan_fwd(W0, X, G, e, alpha=a, reset=r)) < 1e-12
+    assert rel_err(reads["gtilde"], orc.scan_bwd(W0, X, G, e, dY, alpha=a, reset=r)["gtilde"]) < 1e-12
+
+
+def test_scan_reads_equal_the_expanded_sum():
+    """Retention without resets: the explicit sums equal Eq. 2 expanded with
+    explicit products (a triple loop written independently above)."""
+    W0, X, G, e, _ = rand_problem(2, 2, 9, 4, 3, seed=61)
+    a = rand_alpha(2, 2, 9, 62)
+    ref = closed_form_retention(W0, X, G, e, a, orc.EXCLUSIVE)
+    assert rel_err(orc.scan_reads(W0, X, G, e, alpha=a)["y"], ref) < 1e-12
+
+
+def test_scan_reads_with_other_queries():
+    """Forward queries other than the inputs: (W_0 + Delta_t) a_t is linear in
+    a_t, so querying with basis vectors recovers each W_t column by column."""
+    B, H, T, d, m = 1, 1, 6, 3, 2
+    W0, X, G, e, _ = rand_problem(B, H, T, d, m, seed=63)
+    for k in range(d):
+        A = np.zeros((B, H, T, d))
+        A[..., k] = 1.0
+        col = orc.scan_reads(W0, X, G, e, A=A)["y"][0, 0]
+        for t in range(T):
+            Wt = W0[0] - sum(e[0, 0, i] * np.outer(G[0, 0, i], X[0, 0, i]) for i in range(t))
+            np.testing.assert_allclose(col[t], Wt[:, k], rtol=0, atol=1e-13)
+
+
 def test_retention_dw0_is_plain_product():
     W0, X, G, e, dY = rand_problem(3, 2, 9, 4, 5, seed=54)
     out = orc.scan_bwd(W0, X, G, e, dY, alpha=rand_alpha(3, 2, 9, 55))
