@@ -155,9 +155,7 @@ def test_gated_decode(d, m, alpha_kind, with_reset):
                                  to_dev(eta, "f32", torch),
                                  to_dev(al, "f32", torch) if alpha_kind == "state" else float(al),
                                  None if rs is None else torch.from_numpy(rs).to("cuda"))
-        if rs is not None:
-            Wr = np.where(rs[:, None, None, None] != 0, np.broadcast_to(W0, Wr.shape), Wr)
-        yr, Wr = orc.decode_step(Wr, x, g, eta, alpha=al, W0=W0)
+        yr, Wr = orc.decode_step(Wr, x, g, eta, alpha=al, W0=W0, reset=rs)
         check("y", to_host(y), yr, "f32")
     check("W", to_host(Wd), Wr, "f32")
 
