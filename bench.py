@@ -1,23 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the GradLev scan library on one MI355X.
 
-A step is one pass of the whole hot path over one batch: the forward scan and
-the full backward (gtilde, dX, dG, deta, dW0) of the lm-bf16 workload
-(B=8, H=16, T=2048, d=m=64, bf16 inputs, eta=0.1, chunk 64), inputs already
-resident in HBM.  By default the step is the save-for-backward pair (the
-forward keeps each segment's end state, the backward starts from it); the
-plain pair is reported among the secondaries and by --pair plain.  Step i
-runs the forward of input set i mod 8 and the backward of set (i - 2) mod 8:
-every batch still gets one forward and one backward per step, but about
-330 MB of other reads separate a batch's forward from its backward (and about
-1 GB a set's backward from its next forward), so the 256 MB Infinity Cache
-cannot serve them, as in a model where other layers run in between.
+A step is one pass of the whole hot path over one batch.  The headline
+workload is the largest single-GPU configuration, stack-bf16: 24 independent
+layers, each B=4, H=32, T=4096, d=m=64, bf16 inputs, eta=0.1, chunk 64, with
+inputs resident in HBM (4.8 GB of X, G and dY).  A step runs every layer's
+forward scan in layer order, then every layer's full backward (gtilde, dX,
+dG, deta, dW0) in reverse layer order, as a model's training step does.  By
+default each layer runs the save-for-backward pair (the forward keeps each
+backward segment's start state, the backward starts from it); --pair plain
+times the plain calls.  `value` is model tokens (B*T) per second through the
+whole stack.
 
-Prints ONE JSON line with the headline (fwd+bwd tokens/s, tokens = B*T per
-step), the roofline of the dominant kernel measured with HIP events recorded
-around its launches inside the timed region, the float64 oracle timed on the
-host, and secondary measurements of the other workloads (long-context scan,
-24-layer stack, decode).
+Prints ONE JSON line with the headline, the roofline of the dominant kernel
+(the backward main scan) measured with HIP events recorded around its launches
+inside the timed region, the float64 oracle timed on the host (one thread and
+the host's cores), and secondary measurements of the other workloads
+(lm-bf16, long-context scan, gated scans, LM-width MLP, decode).
 """
 
 from __future__ import annotations
@@ -41,20 +40,25 @@ PEAK_FP32_MFMA = 157.3e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-SECONDARY_NAMES = ("lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated", "lm-bf16-gated-plain",
-                   "mlp-lm", "decode-mlp-lm", "decode-f32", "decode-f32-S2048", "decode-f32-gated")
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma.json")
+
+
+SECONDARY_NAMES = ("lm-bf16", "lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated",
+                   "lm-bf16-gated-plain", "mlp-lm", "decode-mlp-lm", "decode-f32", "decode-f32-S2048",
+                   "decode-f32-gated")
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    # 200 steps are one ~25 ms graph replay: long enough that a clock
-    # excursion during the replay moves the figure by little.
-    ap.add_argument("--steps", type=int, default=200)
-    # The GPU clocks ramp over the first few hundred steps and keep drifting
-    # for about a second; 10000 eager steps (~1.5 s) settle them.
-    ap.add_argument("--warmup", type=int, default=10000)
-    ap.add_argument("--workload", default="lm-bf16")
+    # 30 steps of the 24-layer stack are one ~0.2 s graph replay.
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=10)
+    # The GPU clocks ramp over the first ~25 ms of continuous work and keep
+    # drifting for about a second; before the W warm-up steps, untimed steps
+    # run until this many seconds have passed.
+    ap.add_argument("--settle-seconds", type=float, default=1.5)
+    ap.add_argument("--workload", default="stack-bf16", choices=("stack-bf16", "lm-bf16", "long-bf16"))
     ap.add_argument("--pair", default="saved", choices=("plain", "saved"),
                     help="plain: scan_fwd + scan_bwd; saved: scan_fwd_save + scan_bwd_saved (the forward keeps "
                          "segment-end states and the backward starts from them)")
@@ -62,14 +66,21 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--only", default=None, choices=SECONDARY_NAMES,
                     help="run only this secondary workload (after the warm-up) and print its JSON; for profiling")
-    ap.add_argument("--cpu-sample-seconds", type=float, default=12.0,
-                    help="minimum host time spent timing the float64 oracle")
+    ap.add_argument("--cpu-sample-seconds", type=float, default=8.0,
+                    help="minimum host time spent timing the float64 oracle (per leg: one thread, then all cores)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes 5 times (for scaling "
                          "rocprofv3 FETCH_SIZE/WRITE_SIZE to bytes) and exit")
-    ap.add_argument("--ingest-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+    ap.add_argument("--ingest-traffic", nargs=5,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV", "WORKLOAD"),
                     help="only turn four rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE and WRITE_SIZE "
-                         "of a bench run and of a --copy-calibration 256 run) into profiles/traffic.json and exit")
+                         "of a bench run of WORKLOAD and of a --copy-calibration 256 run) into profiles/traffic.json "
+                         "and exit")
+    ap.add_argument("--ingest-mfma", nargs="+", metavar="CSV",
+                    help="only turn rocprofv3 --pmc counter_collection.csv files (SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "GRBM_GUI_ACTIVE, SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_BUSY_CYCLES, SQ_INSTS_VALU, SQ_INSTS_MFMA, "
+                         "SQ_LDS_BANK_CONFLICT, SQ_LDS_IDX_ACTIVE; any split over runs) into profiles/mfma.json "
+                         "and exit")
     return ap.parse_args()
 
 
@@ -113,7 +124,7 @@ class ScanRunner:
     from that cache."""
     LAG = 2
 
-    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False, pipelined=False):
+    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False, pipelined=False, share=None):
         self.gl, self.torch, self.wl = gl, torch, wl
         if pipelined and nsets <= self.LAG:
             raise ValueError("a pipelined step needs more input sets than its lag")
@@ -131,6 +142,12 @@ class ScanRunner:
                                for _ in range(nsets if pipelined else 1)]
             self.saved = self.saved_bufs[0]
             self.saved_nseg = sv_bytes // (wl.B * wl.H * wl.m * wl.d * 4)
+        if share is not None:
+            # Layers of a stack share outputs and workspace: the write traffic
+            # is identical, and separate buffers would only add allocation.
+            # Inputs and saved states stay per layer.
+            self.ws, self.Y, self.outs = share.ws, share.Y, share.outs
+            return
         self.ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=device)
         f32 = dict(dtype=torch.float32, device=device)
         B, H, T, d, m = wl.B, wl.H, wl.T, wl.d, wl.m
@@ -165,6 +182,40 @@ class ScanRunner:
         else:
             self.fwd(i % n)
             self.bwd(i % n)
+
+
+class StackRunner:
+    """A stack of independent layers: a step runs every layer's forward in
+    layer order, then every layer's backward in reverse layer order, as a
+    model's training step does.  Each layer has its own inputs (and saved
+    states); outputs and workspace are shared."""
+
+    def __init__(self, gl, torch, W, wl, device, saved=False):
+        first = ScanRunner(gl, torch, W, wl, 1, device, 0, saved=saved)
+        self.runs = [first] + [ScanRunner(gl, torch, W, wl, 1, device, l, saved=saved, share=first)
+                               for l in range(1, wl.layers)]
+        self.plan, self.saved = first.plan, first.saved
+        self.saved_nseg = getattr(first, "saved_nseg", None)
+
+    def step(self, i=0):
+        for r in self.runs:
+            r.fwd(0)
+        for r in reversed(self.runs):
+            r.bwd(0)
+
+
+def settle(torch, fn, seconds):
+    """Untimed steps until `seconds` have passed (the clocks ramp over the
+    first ~25 ms of continuous work and drift for about a second after).
+    Returns the number of steps run."""
+    n, t0 = 0, time.perf_counter()
+    while True:
+        for _ in range(4):
+            fn(n)
+            n += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= seconds:
+            return n
 
 
 def timed(torch, fn, steps, warmup):
@@ -260,14 +311,15 @@ def scan_work(wl, plan):
     }
 
 
-def load_traffic(kernel):
-    """HBM bytes per launch from committed rocprofv3 --pmc runs, if still current."""
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 --pmc runs, if they were
+    taken on this workload and the kernel sources have not changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f).get(kernel)
     except (OSError, ValueError):
         return None
-    if not rec:
+    if not rec or rec.get("workload") != workload:
         return None
     import hashlib
     h = hashlib.sha256()
@@ -286,7 +338,7 @@ TRAFFIC_KERNELS = {"bwd_main": "bwd_main_kernel", "fwd_main": "fwd_main_kernel"}
 CALIBRATION_MIB = 256
 
 
-def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv):
+def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, workload):
     """HBM bytes per launch of the main kernels from rocprofv3 --pmc runs.
 
     FETCH_SIZE and WRITE_SIZE are read in KiB per dispatch and scaled by what
@@ -316,17 +368,19 @@ def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv):
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     out = {"calibration": {"copy_mib": CALIBRATION_MIB, "bytes_per_unit": cal}}
+    # Instantiations of one family differ by shape; the headline workload's is
+    # the one launched most often in a run of that workload.
     for fam, pat in TRAFFIC_KERNELS.items():
         fk = [k for k in fetch if pat in k]
         wk = [k for k in write if pat in k]
         if not fk or not wk:
             continue
-        # the lm-bf16 kernel is the instantiation launched most often in the bench run
         fk = max(fk, key=lambda k: len(fetch[k]))
         wk = max(wk, key=lambda k: len(write[k]))
         fb = statistics.median(fetch[fk]) * cal["FETCH_SIZE"]
         wb = statistics.median(write[wk]) * cal["WRITE_SIZE"]
-        out[fam] = {"kernel": fk.split("(")[0], "read_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb,
+        out[fam] = {"kernel": fk.split("(")[0], "workload": workload, "read_bytes": fb, "write_bytes": wb,
+                    "bytes_per_launch": fb + wb,
                     "sources": TRAFFIC_SOURCES, "source_sha256": h.hexdigest()}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
@@ -334,47 +388,170 @@ def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv):
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(W, wl, min_seconds):
-    """The float64 oracle, as it stands, on the workload's first batch rows.
+MFMA_KERNELS = {"bwd_main": "bwd_main_kernel", "fwd_main": "fwd_main_kernel", "bwd_split": "bwd_split_kernel",
+                "gated_bwd": "bwd_gated_kernel", "gated_fwd": "fwd_gated_kernel", "wide_out": "wide_out_kernel",
+                "wide_score": "wide_score_kernel"}
+MFMA_SOURCES = TRAFFIC_SOURCES + ["paper_2609_34174_amd/csrc/scan_gated.hip", "paper_2609_34174_amd/csrc/scan_wide.hip",
+                                  "paper_2609_34174_amd/csrc/mlp.hip"]
+NUM_XCC, NUM_SIMD = 8, 1024  # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
-    Starts from one batch row and doubles until one fwd+bwd pass takes at least
-    min_seconds / 4, then repeats that pass until min_seconds have elapsed.
+
+def ingest_mfma(paths):
+    """MFMA and LDS utilisation per kernel from rocprofv3 --pmc runs.
+
+    Counters are read per dispatch as rocprofv3 sums them over their
+    dimensions: GRBM_GUI_ACTIVE over the 8 XCDs (so a kernel's busy clock is
+    that sum / 8), SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs, the SQ
+    instruction counts over the shader engines.  Per kernel (every
+    instantiation whose name matches, medians over its dispatches):
+      mfma_busy   = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024)
+      bf16_flops  = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 (issued, per dispatch)
+      valu_per_mfma = SQ_INSTS_VALU / SQ_INSTS_MFMA (SQ_INSTS_VALU counts MFMAs too)
+      lds_conflict = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE
     """
+    import csv
+    import hashlib
+    import statistics
+    vals = {}
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                k = r["Kernel_Name"].split("(")[0].replace("void ", "")
+                d = vals.setdefault(k, {}).setdefault(r["Counter_Name"], {})
+                key = (path, r["Dispatch_Id"])
+                d[key] = d.get(key, 0.0) + float(r["Counter_Value"])
+    h = hashlib.sha256()
+    for rel in MFMA_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    out = {"sources": MFMA_SOURCES, "source_sha256": h.hexdigest(), "kernels": {}}
+    for kname, cs in vals.items():
+        med = {c: statistics.median(v.values()) for c, v in cs.items() if v}
+        rec = {"dispatches": max(len(v) for v in cs.values()), "counters_median": med}
+        gui = med.get("GRBM_GUI_ACTIVE")
+        if gui and "SQ_VALU_MFMA_BUSY_CYCLES" in med:
+            rec["mfma_busy"] = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui / NUM_XCC * NUM_SIMD)
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med:
+            rec["bf16_flops_issued"] = med["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        if med.get("SQ_INSTS_MFMA"):
+            rec["mfma_insts"] = med["SQ_INSTS_MFMA"]
+            if "SQ_INSTS_VALU" in med:
+                rec["valu_per_mfma"] = (med["SQ_INSTS_VALU"] - med["SQ_INSTS_MFMA"]) / med["SQ_INSTS_MFMA"]
+        if med.get("SQ_LDS_IDX_ACTIVE"):
+            rec["lds_conflict"] = med.get("SQ_LDS_BANK_CONFLICT", 0.0) / med["SQ_LDS_IDX_ACTIVE"]
+            if gui:
+                rec["lds_active"] = med["SQ_LDS_IDX_ACTIVE"] / (gui / NUM_XCC * NUM_SIMD / 4)
+        out["kernels"][kname] = rec
+    with open(MFMA_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
+
+
+def load_mfma(family):
+    """MFMA counters of one kernel family from profiles/mfma.json, if the
+    kernel sources still match; the instantiation with the most dispatches."""
     try:
-        from threadpoolctl import threadpool_limits
-    except ImportError:  # pragma: no cover
-        threadpool_limits = None
+        with open(MFMA_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    import hashlib
+    h = hashlib.sha256()
+    for rel in rec.get("sources", []):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("source_sha256"):
+        return None
+    cands = {k: v for k, v in rec["kernels"].items() if MFMA_KERNELS[family] in k and "mfma_busy" in v}
+    if not cands:
+        return None
+    k = max(cands, key=lambda k_: cands[k_]["dispatches"])
+    v = cands[k]
+    return {"kernel": k, "mfma_busy": v["mfma_busy"], "valu_per_mfma": v.get("valu_per_mfma"),
+            "lds_conflict": v.get("lds_conflict"), "source": "profiles/mfma.json (rocprofv3 --pmc)"}
+
+
+def _oracle_worker(name, layer, min_seconds, barrier, results):
+    """One host process of the CPU baseline: draws one batch row of a layer of
+    a scan workload, waits for every worker to be ready, then runs the float64
+    oracle's forward and backward over that row until min_seconds have passed.
+    Sends (tokens, t_start, t_end) with wall-clock times."""
     from oracle import gradlev_oracle as orc
-    ctx = threadpool_limits(limits=1) if threadpool_limits else None
-    if ctx:
-        ctx.__enter__()
+    from paper_2609_34174_amd import workloads as W
+    wl = W.SCAN_WORKLOADS[name]
+    inp = W.scan_inputs(wl, layer, B=1)
+    barrier.wait()
+    t0 = time.time()
+    reps = 0
+    while True:
+        orc.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"])
+        orc.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["eta"], inp["dY"])
+        reps += 1
+        if time.time() - t0 >= min_seconds:
+            break
+    results.put((reps * wl.T, t0, time.time()))
+
+
+def _oracle_leg(name, workers, min_seconds):
+    """Runs `workers` oracle processes side by side (spawned, one BLAS thread
+    each) and returns (row tokens processed, wall seconds from the common
+    start to the last finish)."""
+    import multiprocessing as mp
+    ctx = mp.get_context("spawn")
+    barrier, results = ctx.Barrier(workers), ctx.Queue()
+    keys = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
+    saved = {k: os.environ.get(k) for k in keys}
+    os.environ.update({k: "1" for k in keys})  # for the children only; restored below
     try:
-        batch, reps, t_fwd, t_bwd = 1, 0, 0.0, 0.0
-        while True:
-            inp = W.scan_inputs(wl, B=batch)
-            t0 = time.perf_counter()
-            orc.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"])
-            t1 = time.perf_counter()
-            orc.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["eta"], inp["dY"])
-            t2 = time.perf_counter()
-            if t2 - t0 >= min_seconds / 4 or batch >= wl.B:
-                break
-            batch *= 2
-        t_fwd, t_bwd, reps = t1 - t0, t2 - t1, 1
-        while t_fwd + t_bwd < min_seconds:
-            t0 = time.perf_counter()
-            orc.scan_fwd(inp["W0"], inp["X"], inp["G"], inp["eta"])
-            t1 = time.perf_counter()
-            orc.scan_bwd(inp["W0"], inp["X"], inp["G"], inp["eta"], inp["dY"])
-            t2 = time.perf_counter()
-            t_fwd, t_bwd, reps = t_fwd + t1 - t0, t_bwd + t2 - t1, reps + 1
+        procs = [ctx.Process(target=_oracle_worker, args=(name, i, min_seconds, barrier, results))
+                 for i in range(workers)]
+        for p_ in procs:
+            p_.start()
     finally:
-        if ctx:
-            ctx.__exit__(None, None, None)
-    tokens = reps * batch * wl.T
-    return {"value": tokens / (t_fwd + t_bwd), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{wl.name} rows B={batch} (H={wl.H}, T={wl.T}, d=m={wl.d}) x {reps} passes; "
-                      f"fwd {t_fwd:.1f} s + bwd {t_bwd:.1f} s of float64 numpy on one thread"}
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    out = [results.get(timeout=600) for _ in range(workers)]
+    for p_ in procs:
+        p_.join()
+        if p_.exitcode != 0:
+            raise RuntimeError(f"oracle worker exited with {p_.exitcode}")
+    tokens = sum(o[0] for o in out)
+    return tokens, max(o[2] for o in out) - min(o[1] for o in out)
+
+
+def cpu_cores():
+    """Cores this process may use: the affinity mask, capped by
+    OMP_NUM_THREADS when the host sets it (a shared host's CPU share)."""
+    n = len(os.sched_getaffinity(0))
+    try:
+        n = min(n, int(os.environ.get("OMP_NUM_THREADS", n)))
+    except ValueError:
+        pass
+    return max(n, 1)
+
+
+def cpu_baseline(wl, min_seconds):
+    """The float64 oracle, as it stands, on the host: one process with one
+    thread, then one process per core side by side, each on its own batch row
+    (B=1, all heads, the full sequence) of a different layer of the workload.
+    Rates are converted to the metric's unit: model tokens per second through
+    all of the workload's layers, forward plus backward."""
+    L = wl.layers
+    n = cpu_cores()
+    t1, s1 = _oracle_leg(wl.name, 1, min_seconds)
+    tn, sn = _oracle_leg(wl.name, n, min_seconds)
+    row = f"rows of B=1, H={wl.H}, T={wl.T}, d=m={wl.d} ({wl.name} distributions)"
+    return {"value": tn / sn / L, "unit": "tokens/s", "cores": n, "kind": "oracle",
+            "sample": f"{n} processes, one BLAS thread each, each running the float64 oracle's forward and "
+                      f"backward over its own row: {tn} row tokens through one layer in {sn:.1f} s wall; "
+                      f"scaled to tokens through all {L} layers",
+            "nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "single_thread": {"value": t1 / s1 / L, "unit": "tokens/s", "cores": 1,
+                              "sample": f"one process, one thread: {t1} row tokens through one layer in "
+                                        f"{s1:.1f} s; {row}; scaled to all {L} layers"}}
 
 
 def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True):
@@ -388,18 +565,8 @@ def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True):
         fn = run.step
         runs = [run]
     else:
-        runs = [ScanRunner(gl, torch, W, wl, 1, device, layer0=l, saved=saved) for l in range(wl.layers)]
-        # Layers share output buffers: the write traffic is identical and 24
-        # separate sets would only add allocation.  Inputs and saved states
-        # are per layer.
-        for r in runs[1:]:
-            r.Y, r.outs, r.ws = runs[0].Y, runs[0].outs, runs[0].ws
-
-        def fn(i):
-            for r in runs:
-                r.fwd(0)
-            for r in reversed(runs):
-                r.bwd(0)
+        stack = StackRunner(gl, torch, W, wl, device, saved=saved)
+        fn, runs = stack.step, stack.runs
     for i in range(warmup):
         fn(i)
     ms, k = graph_timed(torch, gl, fn, steps)
@@ -667,6 +834,8 @@ def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
 
 
 def run_secondary(name, gl, torch, W, device):
+    if name == "lm-bf16":  # the single-layer configuration, pipelined save-for-backward pair
+        return secondary_scan(gl, torch, W, "lm-bf16", 200, 500, device)
     if name == "lm-bf16-cold":
         return secondary_cold(gl, torch, W, device)
     if name == "lm-bf16-plain":  # the headline step without the saved segment states
@@ -674,7 +843,7 @@ def run_secondary(name, gl, torch, W, device):
     if name == "long-bf16":
         return secondary_scan(gl, torch, W, name, 20, 20, device)
     if name == "stack-bf16":
-        return secondary_scan(gl, torch, W, name, 2, 1, device)
+        return secondary_scan(gl, torch, W, name, 20, 10, device)
     if name == "lm-bf16-gated":
         return secondary_gated(gl, torch, W, device)
     if name == "lm-bf16-gated-plain":
@@ -696,6 +865,9 @@ def main():
     args = parse()
     if args.ingest_traffic:
         ingest_traffic(*args.ingest_traffic)
+        return
+    if args.ingest_mfma:
+        ingest_mfma(args.ingest_mfma)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -724,12 +896,10 @@ def main():
         return
     gl.lib()
     if args.only:
-        # Profiling aid: the headline workload warms the clocks, then one
+        # Profiling aid: the lm-bf16 step settles the clocks, then one
         # secondary runs alone.
-        wl = W.SCAN_WORKLOADS["lm-bf16"]
-        run = ScanRunner(gl, torch, W, wl, 1, device)
-        for i in range(args.warmup):
-            run.step(i)
+        run = ScanRunner(gl, torch, W, W.SCAN_WORKLOADS["lm-bf16"], 1, device)
+        settle(torch, run.step, args.settle_seconds)
         del run
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
@@ -737,14 +907,23 @@ def main():
         return
 
     wl = W.SCAN_WORKLOADS[args.workload]
-    log(f"workload {wl.name}: preparing inputs")
-    run = ScanRunner(gl, torch, W, wl, 8, device, saved=args.pair == "saved", pipelined=True)
+    L = wl.layers
+    log(f"workload {wl.name}: preparing inputs ({L} layer(s))")
+    saved = args.pair == "saved"
+    if L > 1:
+        run = StackRunner(gl, torch, W, wl, device, saved=saved)
+        step_desc = (f"all {L} layers' forward scans in layer order, then all {L} backward scans in reverse order")
+    else:
+        run = ScanRunner(gl, torch, W, wl, 8, device, saved=saved, pipelined=True)
+        step_desc = "forward of input set i mod 8 with the backward of set (i-2) mod 8"
     plan = run.plan
     work = scan_work(wl, plan)
 
     # Dominant kernel: the chunked backward scan.
     dom = "bwd_main"
-    log(f"warmup {args.warmup} steps, then {args.steps} timed steps (one HIP graph replay)")
+    n_settle = settle(torch, run.step, args.settle_seconds)
+    log(f"settled the clocks with {n_settle} untimed steps; warmup {args.warmup} steps, then {args.steps} timed "
+        f"steps (one HIP graph replay)")
     for i in range(args.warmup):
         run.step(i)
     torch.cuda.synchronize()
@@ -757,22 +936,25 @@ def main():
     log("kernels (us): " + ", ".join(f"{n}={v[0]:.1f}" for n, v in kall.items() if v[0]))
 
     step_s = ms * 1e-3
-    tokens = wl.B * wl.T
     es = 2 if wl.dtype == "bf16" else 4
     th = wl.B * wl.H * wl.T
     dom_us = k[dom][0]
     dom_bytes = th * bytes_bwd(wl.d, wl.m, es)
     achieved = dom_bytes / (dom_us * 1e-6)
-    traffic = load_traffic(dom)
+    traffic = load_traffic(dom, wl.name)
     roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM, "traffic": traffic, "kernel": dom,
-                "kernel_avg_us": dom_us, "algorithmic_bytes_per_launch": dom_bytes}
+                "kernel_avg_us": dom_us, "algorithmic_bytes_per_launch": dom_bytes,
+                "launches_timed": k[dom][1]}
+    mf = load_mfma(dom)
+    if mf:
+        roofline["mfma_busy_frac"] = mf["mfma_busy"]  # rocprofv3 counters of this kernel (profiles/mfma.json)
     copy_gbps = copy_bandwidth(torch, device)
     roofline["copy_GBps_same_box"] = copy_gbps  # informational: 256 MiB torch device copy
     roofline["frac_of_copy"] = (achieved / 1e9) / copy_gbps
     result = {
         "metric": METRIC,
-        "value": tokens / step_s,
+        "value": wl.B * wl.T / step_s,
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -783,39 +965,49 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic: seeded device RNG with the workload's shapes and distributions",
-        "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_in": wl.d, "d_out": wl.m,
-                   "chunk": wl.chunk, "eta": wl.eta, "prefix": "exclusive",
-                   "step": ("scan_fwd_save + scan_bwd_saved" if run.saved is not None else "scan_fwd + scan_bwd")
-                   + " with gtilde, dX, dG, deta, dW0; forward of batch i with backward of batch i-2",
+        "config": {"workload": wl.name, "layers": L, "B": wl.B, "H": wl.H, "T": wl.T, "d_in": wl.d,
+                   "d_out": wl.m, "chunk": wl.chunk, "eta": wl.eta, "prefix": "exclusive",
+                   "step": ("scan_fwd_save + scan_bwd_saved" if saved else "scan_fwd + scan_bwd")
+                   + " with gtilde, dX, dG, deta, dW0 per layer; " + step_desc,
+                   "tokens": "value = model tokens (B*T) per second through the whole step",
                    "plan": ({"saved_pair_segments": run.saved_nseg,
-                             "saved_state_bytes": run.saved.numel() * 4,
-                             "chunks": [plan.fwd_chunk, plan.bwd_chunk]} if run.saved is not None else
+                             "saved_state_bytes_per_layer": run.saved.numel() * 4,
+                             "chunks": [plan.fwd_chunk, plan.bwd_chunk]} if saved else
                             {"fwd": [plan.fwd_chunk, plan.fwd_segment, plan.fwd_nseg],
                              "bwd": [plan.bwd_chunk, plan.bwd_segment, plan.bwd_nseg]})},
         "roofline": roofline,
-        "step_roofline": {"hbm_GBps_algorithmic": work["bytes"] / step_s / 1e9,
-                          "frac_hbm_peak": work["bytes"] / step_s / PEAK_HBM,
-                          "tflops_algorithmic": work["flops"] / step_s / 1e12,
-                          "frac_bf16_mfma_peak": work["flops"] / step_s / PEAK_BF16},
+        "step_roofline": {"hbm_GBps_algorithmic": L * work["bytes"] / step_s / 1e9,
+                          "frac_hbm_peak": L * work["bytes"] / step_s / PEAK_HBM,
+                          "tflops_algorithmic": L * work["flops"] / step_s / 1e12,
+                          "frac_bf16_mfma_peak": L * work["flops"] / step_s / PEAK_BF16,
+                          "layer_tokens_per_s": L * wl.B * wl.T / step_s},
         "kernel_avg_us": {n: round(v[0], 3) for n, v in kall.items() if v[0] is not None},
-        "timing": "timed region = one replay of a HIP graph of the K steps (step i: forward of input set i mod 8, "
-                  "backward of set (i-2) mod 8), after the W eager warmup steps, K eager steps and one untimed "
-                  "replay; roofline kernel "
-                  "time from "
-                  "HIP events on its launches inside that replay; kernel_avg_us from a second replay with "
-                  "every family bracketed",
+        "timing": f"{n_settle} untimed clock-settling steps ({args.settle_seconds} s), the W warm-up steps, K "
+                  "eager steps and one untimed replay, then the timed region = one replay of a HIP graph of the K "
+                  "steps; roofline kernel time from HIP events on its launches inside that replay; kernel_avg_us "
+                  "from a second replay with every family bracketed",
     }
+    if mf:
+        result["mfma_util"] = {"kernel": dom, "busy_frac_measured": mf["mfma_busy"],
+                               "valu_insts_per_mfma": mf["valu_per_mfma"], "lds_bank_conflict_frac": mf["lds_conflict"],
+                               "algorithmic_frac_of_bf16_peak": L * work["flops"] / step_s / PEAK_BF16,
+                               "source": mf["source"]}
+    del run
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
     if not args.no_secondary:
         sec = {}
         for name in SECONDARY_NAMES:
+            if name == wl.name:
+                continue
             log(f"secondary {name}")
             sec[name] = run_secondary(name, gl, torch, W, device)
         result["secondary"] = sec
 
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host")
-        result["cpu_baseline"] = cpu_baseline(W, wl, args.cpu_sample_seconds)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seconds)
 
     print(json.dumps(result), flush=True)
 

@@ -74,7 +74,9 @@ enum {
  *             parallel and are joined by an fp32 carry of their aggregated
  *             writes; like `chunk` it changes the rounding order only.  At
  *             most 16 segments per sequence: a hint giving more is
- *             GRADLEV_ERR_UNSUPPORTED (the default never does).
+ *             GRADLEV_ERR_UNSUPPORTED (the default never does), and so is
+ *             a plan whose grid, 8 * n_seg * ceil(B*H / 8) workgroups of up
+ *             to 1024 work-items, would reach 2^32 work-items.
  *   in_dtype  GRADLEV_F32 or GRADLEV_BF16
  *   prefix    GRADLEV_EXCLUSIVE or GRADLEV_INCLUSIVE */
 /* Wide maps.  When d_in or d_out is above 128 (both multiples of 128, at most
@@ -205,10 +207,11 @@ int gradlev_scan_bwd_saved(const gradlev_shape* s, const float* W0, const void* 
  *   x    [S, H, d_in]  fp32        g [S, H, d_out] fp32
  *   eta  [S, H] fp32 or NULL (then eta_scalar)
  *   y    [S, H, d_out] fp32 output
- * Supported: d_in in {16, 32, 64, 128, 256} with d_out in [1, 1024], or wide
- * states, d_in in {512, 1024, 2048, 4096, 8192} with d_out in [1, 65536] and
- * d_in * d_out * 4 < 2^31 (the paper's LM-width MLP maps are 1024 -> 4096 and
- * 4096 -> 1024).
+ * Supported: d_in in {16, 32, 64, 128, 256} with d_out in [1, 1024] and
+ * S * H < 2^24, or wide states, d_in in {512, 1024, 2048, 4096, 8192} with
+ * d_out in [1, 65536] and d_in * d_out * 4 < 2^31 (the paper's LM-width MLP
+ * maps are 1024 -> 4096 and 4096 -> 1024).  Larger calls would exceed the
+ * 2^32 work-items of one launch and return GRADLEV_ERR_UNSUPPORTED.
  * Exclusive only: deployment needs y before the costate g exists. */
 int gradlev_decode_step(int64_t S, int64_t H, int64_t d_in, int64_t d_out,
                         float* W, const float* x, const float* g,
@@ -386,7 +389,10 @@ int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates,
  * gradlev_timing_read waits for the recorded events and returns, for one
  * family, the summed duration in milliseconds and the number of launches
  * since the last reset.  Not thread-safe: use from one host thread.  At most
- * 65536 launches per family are kept between resets.
+ * 65536 launches per family are kept between reads: past that, an eager
+ * launch first waits for the recorded events and folds them into the sum,
+ * while a launch under stream capture (whose events have not run yet) is
+ * simply not timed.
  * Families: */
 enum {
   GRADLEV_K_FWD_AGG = 0,   /* per-segment write aggregates (forward)      */

@@ -18,6 +18,14 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// The scan kernels run a 1-D grid of 8 * nseg * ceil(BH / 8) workgroups of
+// at most 1024 work-items (the widest, 16-wave kernels); the grid's
+// work-item count must stay below 2^32.
+constexpr int64_t kMaxBlockThreads = 1024;
+bool grid_fits(int64_t BH, int64_t nseg) {
+  return 8 * nseg * ((BH + 7) / 8) <= ((int64_t(1) << 32) - 1) / kMaxBlockThreads;
+}
+
 struct Plan {
   ScanProblem fwd, bwd;
   int64_t save_len;  // save-for-backward pair: tokens per saved state (the backward's segment)
@@ -97,6 +105,7 @@ int make_plan(const gradlev_shape* s, Plan* out) {
   out->bwd.seg_len = sc * out->bwd.chunk;
   out->bwd.nseg = (s->T + out->bwd.seg_len - 1) / out->bwd.seg_len;
   if (out->bwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
+  if (!grid_fits(BH, out->fwd.nseg) || !grid_fits(BH, out->bwd.nseg)) return GRADLEV_ERR_UNSUPPORTED;
 
   out->save_len = out->bwd.seg_len;
   layout_ws(out, BH, md);
@@ -119,6 +128,7 @@ int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
   const int64_t sf = (out->fwd.seg_len + sb - 1) / sb * sb;
   out->fwd.seg_len = sf;
   out->fwd.nseg = (s->T + sf - 1) / sf;
+  if (!grid_fits(s->B * s->H, out->bwd.nseg)) return GRADLEV_ERR_UNSUPPORTED;
   out->save_len = sb;
   const size_t md = (size_t)s->d_out * s->d_in * sizeof(float);
   layout_ws(out, s->B * s->H, md);
@@ -210,7 +220,7 @@ int make_gated_plan(const gradlev_shape* s, GatedPlan* out) {
     const int64_t sc = pick_nseg(BH, s->T, q.chunk, gated_wgs_per_cu(k == 0, bf, d, m), s->segment);
     q.seg_len = sc * q.chunk;
     q.nseg = (s->T + q.seg_len - 1) / q.seg_len;
-    if (q.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
+    if (q.nseg > 16 || !grid_fits(BH, q.nseg)) return GRADLEV_ERR_UNSUPPORTED;
   }
   // The backward addresses one sequence's chunk-start states with 32-bit
   // buffer offsets: ceil(T / chunk) * m * d * 4 < 2^31.
@@ -243,7 +253,7 @@ int make_gated_saved_plan(const gradlev_shape* s, GatedPlan* out, size_t* saved_
                                s->segment);
   out->fwd.seg_len = sc * out->fwd.chunk;
   out->fwd.nseg = (s->T + out->fwd.seg_len - 1) / out->fwd.seg_len;
-  if (out->fwd.nseg > 16) return GRADLEV_ERR_UNSUPPORTED;
+  if (out->fwd.nseg > 16 || !grid_fits(BH, out->fwd.nseg)) return GRADLEV_ERR_UNSUPPORTED;
   const size_t nf = (size_t)BH * out->fwd.nseg;
   out->ws_fwd = out->fwd.nseg > 1 ? round_up(nf * md, 256) + round_up(nf * 4, 256) : 0;
   *saved_bytes = (size_t)BH * ((s->T + out->bwd.chunk - 1) / out->bwd.chunk) * md;
@@ -346,7 +356,9 @@ GatedPtrs gated_ptrs(const GatedPlan& p, const gradlev_gates* g, const float* W0
 // S * H * ceil(d_out / rows per workgroup) workgroups within 2^31 work-items).
 bool decode_shape_ok(int64_t S, int64_t H, int64_t d_in, int64_t d_out) {
   if (S > kMaxElems / H || S * H > 0x7fffffff) return false;
-  if (d_in == 16 || d_in == 32 || d_in == 64 || d_in == 128 || d_in == 256) return d_out <= 1024;
+  // One 256-work-item workgroup per state: S * H * 256 work-items < 2^32.
+  if (d_in == 16 || d_in == 32 || d_in == 64 || d_in == 128 || d_in == 256)
+    return d_out <= 1024 && S * H < (int64_t(1) << 24);
   if (d_in != 512 && d_in != 1024 && d_in != 2048 && d_in != 4096 && d_in != 8192) return false;
   if (d_out > 65536 || d_in * d_out * 4 >= (int64_t(1) << 31)) return false;
   const int64_t nch = d_in / 256, rows = 4 * (nch >= 16 ? 1 : 16 / nch);

@@ -150,7 +150,13 @@ static hipError_t launch_decode_wide(int64_t S, int64_t H, int d, int m, float* 
   const int U = nch >= 16 ? 1 : 16 / nch;
   const int64_t bps = (m + 4 * U - 1) / (4 * U);
   const dim3 grid((unsigned)(S * H * bps)), block(256);
-#define GL_DECODE_W(N)                                                                                    if (gt)                                                                                                   hipLaunchKernelGGL((decode_wide_kernel<N, true>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs, bps);   else                                                                                                      hipLaunchKernelGGL((decode_wide_kernel<N, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs, bps);
+#define GL_DECODE_W(N)                                                                             \
+  if (gt)                                                                                          \
+    hipLaunchKernelGGL((decode_wide_kernel<N, true>), grid, block, 0, s, W, x, g, eta, eta_scalar, \
+                       y, m, W0, H, al, as, rs, bps);                                              \
+  else                                                                                             \
+    hipLaunchKernelGGL((decode_wide_kernel<N, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, \
+                       y, m, W0, H, al, as, rs, bps);
   switch (nch) {
     case 2: GL_DECODE_W(2) break;
     case 4: GL_DECODE_W(4) break;

@@ -37,7 +37,14 @@ void fold(Family& f) {
 void timing_begin(int family, hipStream_t s) {
   if (family < 0 || family >= GRADLEV_K_COUNT || !(g_mask & (1u << family))) return;
   Family& f = g_fam[family];
-  if (f.used == kMaxPairs) fold(f);
+  if (f.used == kMaxPairs) {
+    // Under stream capture the recorded events are graph nodes that have not
+    // run yet: waiting on them would never return (or invalidate the
+    // capture), so recording stops at the cap instead of folding.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;
+    fold(f);
+  }
   if (f.used == f.start.size()) {
     hipEvent_t a, b;
     if (hipEventCreate(&a) != hipSuccess) return;

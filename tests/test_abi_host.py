@@ -361,3 +361,42 @@ def test_decode_shapes(L, d_in, d_out, ok):
     rc = L.gradlev_decode_step(ctypes.c_int64(2), ctypes.c_int64(1), ctypes.c_int64(d_in), ctypes.c_int64(d_out),
                                FAKE, FAKE, FAKE, None, ctypes.c_float(0.1), MISALIGNED, None)
     assert rc == (gl.ERR_ALIGN if ok else gl.ERR_UNSUPPORTED)
+
+
+@pytest.mark.parametrize("B,H,T,seg,ok", [
+    # 16 segments of 64 tokens: 8 * 16 * ceil(BH / 8) workgroups of up to 1024 work-items
+    (1 << 18, 1, 1024, 64, False), ((1 << 18) - 8, 1, 1024, 64, True),
+    # default plans at T = 1: one segment, 8 * ceil(BH / 8) workgroups
+    ((1 << 22) - 8, 1, 1, 0, True), (1 << 22, 1, 1, 0, False), (1 << 12, (1 << 10) - 1, 1, 0, True),
+    (1 << 12, 1 << 10, 1, 0, False)])
+def test_plan_rejects_grids_past_the_work_item_limit(L, B, H, T, seg, ok):
+    """A plan whose grid would reach 2^32 work-items is refused on the host
+    (the widest scan kernels run 1024 work-items per workgroup)."""
+    s = shape(B=B, H=H, T=T, segment=seg)
+    rc, p = plan_rc(s)
+    assert rc == (gl.OK if ok else gl.ERR_UNSUPPORTED)
+    if ok:
+        for n in (p.fwd_nseg, p.bwd_nseg):
+            assert 8 * n * -(-(B * H) // 8) * 1024 < 2 ** 32
+    sz, ws = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    rc2 = L.gradlev_scan_saved_bytes(ctypes.byref(s), ctypes.byref(sz), ctypes.byref(ws))
+    assert (rc2 == gl.OK) == ok
+    rc3 = L.gradlev_scan_gated_workspace_bytes(ctypes.byref(s), ctypes.byref(ws))
+    assert (rc3 == gl.OK) == ok
+
+
+@pytest.mark.parametrize("S,H,ok", [((1 << 24) - 1, 1, True), (1 << 24, 1, False), (1 << 12, 1 << 12, False),
+                                    (1 << 12, (1 << 12) - 1, True)])
+def test_decode_rejects_grids_past_the_work_item_limit(L, S, H, ok):
+    """Decode at 64-wide states runs one 256-work-item workgroup per state:
+    S * H states must stay below 2^24 (fake pointers; an accepted shape is seen
+    through the alignment error of a misaligned y)."""
+    for fn in ("plain", "gated"):
+        if fn == "plain":
+            rc = L.gradlev_decode_step(ctypes.c_int64(S), ctypes.c_int64(H), ctypes.c_int64(64), ctypes.c_int64(64),
+                                       FAKE, FAKE, FAKE, None, ctypes.c_float(0.1), MISALIGNED, None)
+        else:
+            rc = L.gradlev_decode_step_gated(ctypes.c_int64(S), ctypes.c_int64(H), ctypes.c_int64(64),
+                                             ctypes.c_int64(64), FAKE, FAKE, FAKE, FAKE, None, ctypes.c_float(0.1),
+                                             None, ctypes.c_float(1.0), None, MISALIGNED, None)
+        assert rc == (gl.ERR_ALIGN if ok else gl.ERR_UNSUPPORTED), fn
