@@ -76,8 +76,9 @@ def parse():
                     help="only turn four rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE and WRITE_SIZE "
                          "of a bench run of WORKLOAD and of a --copy-calibration 256 run) into profiles/traffic.json "
                          "and exit")
-    ap.add_argument("--ingest-mfma", nargs="+", metavar="CSV",
-                    help="only turn rocprofv3 --pmc counter_collection.csv files (SQ_VALU_MFMA_BUSY_CYCLES, "
+    ap.add_argument("--ingest-mfma", nargs="+", metavar="WORKLOAD_OR_CSV",
+                    help="only turn rocprofv3 --pmc counter_collection.csv files of one workload's run, given "
+                         "after its name (SQ_VALU_MFMA_BUSY_CYCLES, "
                          "GRBM_GUI_ACTIVE, SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_BUSY_CYCLES, SQ_INSTS_VALU, SQ_INSTS_MFMA, "
                          "SQ_LDS_BANK_CONFLICT, SQ_LDS_IDX_ACTIVE; any split over runs) into profiles/mfma.json "
                          "and exit")
@@ -319,7 +320,7 @@ def load_traffic(kernel, workload):
             rec = json.load(f).get(kernel)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("workload") != workload:
+    if not rec or rec.get("workload") != workload or rec.get("plan") != plan_key(workload):
         return None
     import hashlib
     h = hashlib.sha256()
@@ -331,9 +332,22 @@ def load_traffic(kernel, workload):
     return rec.get("bytes_per_launch")
 
 
-TRAFFIC_SOURCES = ["include/gradlev.h"] + [f"paper_2609_34174_amd/csrc/{n}" for n in (
-    "abi.hip", "decode.hip", "device_common.hpp", "internal.hpp", "scan_bwd.hip", "scan_common.hpp",
-    "scan_fwd.hip", "timing.hip")]
+# Counters stay valid while the kernels' sources and the workload's plan (its
+# tiles and segments, which the library's host code chooses) are unchanged.
+TRAFFIC_SOURCES = [f"paper_2609_34174_amd/csrc/{n}" for n in (
+    "device_common.hpp", "internal.hpp", "scan_bwd.hip", "scan_common.hpp", "scan_fwd.hip")]
+
+
+def plan_key(workload):
+    """The library's plan of a scan workload's save-for-backward pair, as a
+    list: [fwd chunk, segment, segments, bwd chunk, segment, segments, saved
+    bytes].  Pure host computation (no GPU needed)."""
+    import paper_2609_34174_amd as gl
+    from paper_2609_34174_amd import workloads as W
+    wl = W.SCAN_WORKLOADS[workload]
+    s = gl.make_shape(wl.B, wl.H, wl.T, wl.d, wl.m, gl.BF16 if wl.dtype == "bf16" else gl.F32, chunk=wl.chunk)
+    p = gl.plan(s)
+    return [p.fwd_chunk, p.fwd_segment, p.fwd_nseg, p.bwd_chunk, p.bwd_segment, p.bwd_nseg, gl.saved_bytes(s)[0]]
 TRAFFIC_KERNELS = {"bwd_main": "bwd_main_kernel", "fwd_main": "fwd_main_kernel"}
 CALIBRATION_MIB = 256
 
@@ -379,8 +393,8 @@ def ingest_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, workload)
         wk = max(wk, key=lambda k: len(write[k]))
         fb = statistics.median(fetch[fk]) * cal["FETCH_SIZE"]
         wb = statistics.median(write[wk]) * cal["WRITE_SIZE"]
-        out[fam] = {"kernel": fk.split("(")[0], "workload": workload, "read_bytes": fb, "write_bytes": wb,
-                    "bytes_per_launch": fb + wb,
+        out[fam] = {"kernel": fk.split("(")[0], "workload": workload, "plan": plan_key(workload),
+                    "read_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb,
                     "sources": TRAFFIC_SOURCES, "source_sha256": h.hexdigest()}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
@@ -393,63 +407,86 @@ MFMA_KERNELS = {"bwd_main": "bwd_main_kernel", "fwd_main": "fwd_main_kernel", "b
                 "wide_score": "wide_score_kernel"}
 MFMA_SOURCES = TRAFFIC_SOURCES + ["paper_2609_34174_amd/csrc/scan_gated.hip", "paper_2609_34174_amd/csrc/scan_wide.hip",
                                   "paper_2609_34174_amd/csrc/mlp.hip"]
+SCAN_LABELS = ("stack-bf16", "lm-bf16", "long-bf16")  # mfma.json labels that are scan workloads with a plan
 NUM_XCC, NUM_SIMD = 8, 1024  # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
 
-def ingest_mfma(paths):
-    """MFMA and LDS utilisation per kernel from rocprofv3 --pmc runs.
+def ingest_mfma(label, paths):
+    """MFMA and LDS utilisation per kernel from rocprofv3 --pmc runs of one
+    workload (label), stored in profiles/mfma.json under that label.
 
-    Counters are read per dispatch as rocprofv3 sums them over their
-    dimensions: GRBM_GUI_ACTIVE over the 8 XCDs (so a kernel's busy clock is
-    that sum / 8), SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs, the SQ
-    instruction counts over the shader engines.  Per kernel (every
-    instantiation whose name matches, medians over its dispatches):
-      mfma_busy   = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024)
-      bf16_flops  = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 (issued, per dispatch)
-      valu_per_mfma = SQ_INSTS_VALU / SQ_INSTS_MFMA (SQ_INSTS_VALU counts MFMAs too)
-      lds_conflict = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE
+    rocprofv3 reports each counter per dispatch summed over its dimensions:
+    GRBM_GUI_ACTIVE over the 8 XCDs (a kernel's busy clock is that sum / 8),
+    SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs, the SQ instruction counts
+    over the shader engines.  Ratios are formed per dispatch, then the median
+    is taken over the dispatches of one kernel at one grid size:
+      mfma_busy     = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024)
+      bf16_flops    = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 (issued per dispatch)
+      valu_per_mfma = (SQ_INSTS_VALU - SQ_INSTS_MFMA) / SQ_INSTS_MFMA
+      lds_conflict  = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE
+      lds_active    = SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE / 8 * 256)
     """
     import csv
     import hashlib
     import statistics
-    vals = {}
+    disp = {}
     for path in paths:
         with open(path) as f:
             for r in csv.DictReader(f):
-                k = r["Kernel_Name"].split("(")[0].replace("void ", "")
-                d = vals.setdefault(k, {}).setdefault(r["Counter_Name"], {})
-                key = (path, r["Dispatch_Id"])
-                d[key] = d.get(key, 0.0) + float(r["Counter_Value"])
+                d = disp.setdefault((path, r["Dispatch_Id"]), {
+                    "kernel": r["Kernel_Name"].split("(")[0].replace("void ", ""),
+                    "grid": int(r["Grid_Size"]), "c": {}})
+                d["c"][r["Counter_Name"]] = d["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    groups = {}
+    for d in disp.values():
+        c, m = d["c"], {}
+        gui = c.get("GRBM_GUI_ACTIVE")
+        if gui and "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+            m["mfma_busy"] = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui / NUM_XCC * NUM_SIMD)
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c:
+            m["bf16_flops_issued"] = c["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        if c.get("SQ_INSTS_MFMA") and "SQ_INSTS_VALU" in c:
+            m["valu_per_mfma"] = (c["SQ_INSTS_VALU"] - c["SQ_INSTS_MFMA"]) / c["SQ_INSTS_MFMA"]
+        if c.get("SQ_LDS_IDX_ACTIVE"):
+            m["lds_conflict"] = c.get("SQ_LDS_BANK_CONFLICT", 0.0) / c["SQ_LDS_IDX_ACTIVE"]
+            if gui:
+                m["lds_active"] = c["SQ_LDS_IDX_ACTIVE"] / (gui / NUM_XCC * NUM_SIMD / 4)
+        if gui:
+            m["gui_cycles"] = gui / NUM_XCC
+        g = groups.setdefault((d["kernel"], d["grid"]), {})
+        for k, v in m.items():
+            g.setdefault(k, []).append(v)
     h = hashlib.sha256()
     for rel in MFMA_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
-    out = {"sources": MFMA_SOURCES, "source_sha256": h.hexdigest(), "kernels": {}}
-    for kname, cs in vals.items():
-        med = {c: statistics.median(v.values()) for c, v in cs.items() if v}
-        rec = {"dispatches": max(len(v) for v in cs.values()), "counters_median": med}
-        gui = med.get("GRBM_GUI_ACTIVE")
-        if gui and "SQ_VALU_MFMA_BUSY_CYCLES" in med:
-            rec["mfma_busy"] = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui / NUM_XCC * NUM_SIMD)
-        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med:
-            rec["bf16_flops_issued"] = med["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
-        if med.get("SQ_INSTS_MFMA"):
-            rec["mfma_insts"] = med["SQ_INSTS_MFMA"]
-            if "SQ_INSTS_VALU" in med:
-                rec["valu_per_mfma"] = (med["SQ_INSTS_VALU"] - med["SQ_INSTS_MFMA"]) / med["SQ_INSTS_MFMA"]
-        if med.get("SQ_LDS_IDX_ACTIVE"):
-            rec["lds_conflict"] = med.get("SQ_LDS_BANK_CONFLICT", 0.0) / med["SQ_LDS_IDX_ACTIVE"]
-            if gui:
-                rec["lds_active"] = med["SQ_LDS_IDX_ACTIVE"] / (gui / NUM_XCC * NUM_SIMD / 4)
-        out["kernels"][kname] = rec
+    try:
+        with open(MFMA_FILE) as f:
+            out = json.load(f)
+    except (OSError, ValueError):
+        out = {}
+    if out.get("source_sha256") != h.hexdigest():
+        out = {}  # counters of older kernel sources are dropped
+    out.update({"sources": MFMA_SOURCES, "source_sha256": h.hexdigest()})
+    recs = []
+    for (kname, grid), g in sorted(groups.items()):
+        if "gradlev" not in kname:
+            continue  # the input generators' and torch's own kernels
+        rec = {"kernel": kname, "grid": grid, "dispatches": max(len(v) for v in g.values())}
+        rec.update({k: statistics.median(v) for k, v in g.items()})
+        recs.append(rec)
+    out.setdefault("workloads", {})[label] = recs
+    if label in SCAN_LABELS:
+        out.setdefault("plans", {})[label] = plan_key(label)
     with open(MFMA_FILE, "w") as f:
         json.dump(out, f, indent=1)
-    print(json.dumps(out, indent=1))
+    return recs
 
 
-def load_mfma(family):
-    """MFMA counters of one kernel family from profiles/mfma.json, if the
-    kernel sources still match; the instantiation with the most dispatches."""
+def load_mfma(family, workload):
+    """MFMA counters of one kernel family in one workload's run from
+    profiles/mfma.json, if the kernel sources still match: the
+    (instantiation, grid) with the most dispatches."""
     try:
         with open(MFMA_FILE) as f:
             rec = json.load(f)
@@ -462,12 +499,14 @@ def load_mfma(family):
             h.update(f.read())
     if h.hexdigest() != rec.get("source_sha256"):
         return None
-    cands = {k: v for k, v in rec["kernels"].items() if MFMA_KERNELS[family] in k and "mfma_busy" in v}
+    if workload in SCAN_LABELS and rec.get("plans", {}).get(workload) != plan_key(workload):
+        return None
+    cands = [r for r in rec.get("workloads", {}).get(workload, [])
+             if MFMA_KERNELS[family] in r["kernel"] and "mfma_busy" in r]
     if not cands:
         return None
-    k = max(cands, key=lambda k_: cands[k_]["dispatches"])
-    v = cands[k]
-    return {"kernel": k, "mfma_busy": v["mfma_busy"], "valu_per_mfma": v.get("valu_per_mfma"),
+    v = max(cands, key=lambda r: r["dispatches"])
+    return {"kernel": v["kernel"], "mfma_busy": v["mfma_busy"], "valu_per_mfma": v.get("valu_per_mfma"),
             "lds_conflict": v.get("lds_conflict"), "source": "profiles/mfma.json (rocprofv3 --pmc)"}
 
 
@@ -867,7 +906,8 @@ def main():
         ingest_traffic(*args.ingest_traffic)
         return
     if args.ingest_mfma:
-        ingest_mfma(args.ingest_mfma)
+        for r in ingest_mfma(args.ingest_mfma[0], args.ingest_mfma[1:]):
+            print(json.dumps(r))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -946,7 +986,7 @@ def main():
                 "frac": achieved / PEAK_HBM, "traffic": traffic, "kernel": dom,
                 "kernel_avg_us": dom_us, "algorithmic_bytes_per_launch": dom_bytes,
                 "launches_timed": k[dom][1]}
-    mf = load_mfma(dom)
+    mf = load_mfma(dom, wl.name)
     if mf:
         roofline["mfma_busy_frac"] = mf["mfma_busy"]  # rocprofv3 counters of this kernel (profiles/mfma.json)
     copy_gbps = copy_bandwidth(torch, device)
