@@ -57,7 +57,9 @@ enum {
   GRADLEV_ERR_UNSUPPORTED = -2, /* valid but outside the compiled shapes */
   GRADLEV_ERR_ALIGN = -3,       /* a pointer is not 16-byte aligned */
   GRADLEV_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required */
-  GRADLEV_ERR_HIP = -5          /* a HIP launch failed */
+  GRADLEV_ERR_HIP = -5,         /* a HIP launch failed */
+  GRADLEV_ERR_SCRATCH = -6      /* gradlev_scan_fwd_static: the call needs more scratch
+                                   than GRADLEV_STATIC_SCRATCH_BYTES */
 };
 
 /* Problem description for the scans.
@@ -132,6 +134,29 @@ int gradlev_scan_workspace_bytes(const gradlev_shape* s, size_t* bytes);
 int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X,
                      const void* G, const float* eta, float eta_scalar, float* Y,
                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Forward scan that allocates nothing and takes no workspace, for callers
+ * that cannot allocate device memory or pass one: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, results and kernels as gradlev_scan_fwd; the scratch that
+ * gradlev_scan_fwd takes from its workspace argument (segment aggregates, or
+ * the wide maps' gate prefixes and score tiles) comes instead from a static
+ * device array of GRADLEV_STATIC_SCRATCH_BYTES that the library keeps on
+ * each GPU it runs on until the process ends.
+ *   - The array of the CURRENT device (hipGetDevice) is used; `stream` must
+ *     belong to that device.  Its address is looked up once per device, on
+ *     that device's first call.
+ *   - Calls whose workspace (gradlev_scan_workspace_bytes) exceeds the array
+ *     return GRADLEV_ERR_SCRATCH before any HIP call.
+ *   - Every call on one GPU shares that GPU's array, and each call leaves its
+ *     contents behind (nothing in it needs to start at zero).  Calls that can
+ *     overlap on one GPU - on different streams, or from several host threads
+ *     without ordering - race on it: order them on one stream or synchronise
+ *     between them. */
+#define GRADLEV_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int gradlev_scan_fwd_static(const gradlev_shape* s, const float* W0, const void* X,
+                            const void* G, const float* eta, float eta_scalar, float* Y,
+                            void* stream);
 
 /* Backward of the forward scan for an upstream gradient dY = dL/dY.
  *

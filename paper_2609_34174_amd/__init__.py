@@ -25,7 +25,8 @@ LIB_PATH = os.path.join(_PKG, "_lib", "libgradlev.so")
 
 F32, BF16 = 0, 1
 EXCLUSIVE, INCLUSIVE = 0, 1
-OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4, -5
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_HIP, ERR_SCRATCH = 0, -1, -2, -3, -4, -5, -6
+STATIC_SCRATCH_BYTES = 64 << 20  # GRADLEV_STATIC_SCRATCH_BYTES
 
 _PREFIX = {"exclusive": EXCLUSIVE, "inclusive": INCLUSIVE}
 
@@ -83,6 +84,8 @@ def lib():
         L.gradlev_scan_workspace_bytes.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(ctypes.c_size_t)]
         L.gradlev_scan_fwd.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
                                        f32p, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_fwd_static.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
+                                              f32p, vp]
         L.gradlev_scan_bwd.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
                                        vp, f32p, f32p, f32p, f32p, f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_decode_step.argtypes = [i64, i64, i64, i64, f32p, f32p, f32p, f32p,
@@ -117,7 +120,7 @@ def lib():
         L.gradlev_timing_enable.argtypes = [ctypes.c_int]
         L.gradlev_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]
-        for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd",
+        for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd", "gradlev_scan_fwd_static",
                      "gradlev_scan_bwd", "gradlev_scan_saved_bytes", "gradlev_scan_fwd_save",
                      "gradlev_scan_bwd_saved", "gradlev_decode_step", "gradlev_scan_gated_workspace_bytes",
                      "gradlev_scan_fwd_gated", "gradlev_scan_bwd_gated", "gradlev_decode_step_gated",
@@ -251,6 +254,24 @@ def scan_fwd(W0, X, G, eta=0.1, *, prefix="exclusive", chunk=0, segment=0, out=N
                                 _ptr(ws), wsn, _stream(X.device))
     if rc != OK:
         raise GradLevError(rc, "gradlev_scan_fwd")
+    return out
+
+
+def scan_fwd_static(W0, X, G, eta=0.1, *, prefix="exclusive", chunk=0, segment=0, out=None):
+    """Forward scan with no workspace: the library's static per-device scratch
+    holds what scan_fwd keeps in its workspace (see gradlev_scan_fwd_static;
+    calls that may overlap on one GPU race on that scratch)."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, prefix, chunk, segment)
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    if out is None:
+        out = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    _check_dev("out", out, torch.float32, (s.B, s.H, s.T, s.d_out))
+    with torch.cuda.device(X.device):
+        rc = lib().gradlev_scan_fwd_static(ctypes.byref(s), _ptr(W0), _ptr(X), _ptr(G), _ptr(e), es, _ptr(out),
+                                           _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_fwd_static")
     return out
 
 

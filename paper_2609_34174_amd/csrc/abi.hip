@@ -5,8 +5,16 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/gradlev.h"
 #include "internal.hpp"
+
+// Device scratch of gradlev_scan_fwd_static: one copy per GPU, at its own
+// address on each.  Host code never uses this name as an address (on the host
+// it is only a stand-in for the symbol); it uses the pointer that
+// static_scratch() looks up per device.
+static __device__ __align__(256) unsigned char scratch[GRADLEV_STATIC_SCRATCH_BYTES];
 
 namespace gradlev {
 namespace {
@@ -372,6 +380,25 @@ int check_workspace(void* ws, size_t have, size_t need) {
   return GRADLEV_OK;
 }
 
+// Device address of `scratch` on the current device, looked up once per
+// device with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return GRADLEV_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GRADLEV_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GRADLEV_OK;
+}
+
 }  // namespace
 }  // namespace gradlev
 
@@ -389,6 +416,7 @@ const char* gradlev_error_string(int code) {
     case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
     case GRADLEV_ERR_HIP: return "HIP launch failed";
+    case GRADLEV_ERR_SCRATCH: return "the call needs more device scratch than GRADLEV_STATIC_SCRATCH_BYTES (use gradlev_scan_fwd with a workspace)";
     default: return "unknown status code";
   }
 }
@@ -512,6 +540,23 @@ int gradlev_scan_fwd(const gradlev_shape* s, const float* W0, const void* X, con
   const int rc = make_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
   return scan_fwd_planned(p, W0, X, G, eta, eta_scalar, Y, nullptr, workspace, workspace_bytes, stream);
+}
+
+int gradlev_scan_fwd_static(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                            const float* eta, float eta_scalar, float* Y, void* stream) {
+  // Host validation first (the same checks gradlev_scan_fwd makes), then the
+  // scratch lookup, the only HIP call before the launches.
+  size_t need = 0;
+  const int rc = gradlev_scan_workspace_bytes(s, &need);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !Y) return GRADLEV_ERR_INVALID;
+  if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || (eta && !aligned16(eta)))
+    return GRADLEV_ERR_ALIGN;
+  if (need > GRADLEV_STATIC_SCRATCH_BYTES) return GRADLEV_ERR_SCRATCH;
+  void* ws = nullptr;
+  const int rs = static_scratch(&ws);
+  if (rs != GRADLEV_OK) return rs;
+  return gradlev_scan_fwd(s, W0, X, G, eta, eta_scalar, Y, ws, GRADLEV_STATIC_SCRATCH_BYTES, stream);
 }
 
 int gradlev_scan_bwd(const gradlev_shape* s, const float* W0, const void* X, const void* G,

@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_error_strings(L):
-    for code in (0, -1, -2, -3, -4, -5, 7):
+    for code in (0, -1, -2, -3, -4, -5, -6, 7):
         assert isinstance(gl.error_string(code), str) and gl.error_string(code)
     assert gl.error_string(0) == "success"
 
@@ -400,3 +400,28 @@ def test_decode_rejects_grids_past_the_work_item_limit(L, S, H, ok):
                                              ctypes.c_int64(64), FAKE, FAKE, FAKE, FAKE, None, ctypes.c_float(0.1),
                                              None, ctypes.c_float(1.0), None, MISALIGNED, None)
         assert rc == (gl.ERR_ALIGN if ok else gl.ERR_UNSUPPORTED), fn
+
+
+def test_static_forward_validation_before_any_hip_call(L):
+    """gradlev_scan_fwd_static checks its arguments, and that the call's
+    workspace fits the static scratch, on the host before any HIP call (here
+    there is no GPU: an accepted call would fail in the scratch lookup)."""
+    f = L.gradlev_scan_fwd_static
+    s = shape()
+    assert f(ctypes.byref(s), None, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, None, 0.1, None, None) == gl.ERR_INVALID
+    assert f(ctypes.byref(s), FAKE, MISALIGNED, FAKE, None, 0.1, FAKE, None) == gl.ERR_ALIGN
+    assert f(ctypes.byref(s), FAKE, FAKE, FAKE, MISALIGNED, 0.1, FAKE, None) == gl.ERR_ALIGN
+    assert f(ctypes.byref(shape(d_in=32)), FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_UNSUPPORTED
+    assert f(None, FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_INVALID
+    # A forward whose segment aggregates exceed the 64 MiB scratch.
+    big = shape(B=64, H=64, T=1 << 14, segment=1024, d_in=128, d_out=128)
+    assert gl.workspace_bytes(big) > gl.STATIC_SCRATCH_BYTES
+    assert f(ctypes.byref(big), FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_SCRATCH
+    # The wide maps' score matrix counts too: 8 sequences of 4096 tokens.
+    wide = shape(B=8, H=1, T=4096, d_in=1024, d_out=4096)
+    assert gl.workspace_bytes(wide) > gl.STATIC_SCRATCH_BYTES
+    assert f(ctypes.byref(wide), FAKE, FAKE, FAKE, None, 0.1, FAKE, None) == gl.ERR_SCRATCH
+    assert "GRADLEV_STATIC_SCRATCH_BYTES" in gl.error_string(gl.ERR_SCRATCH)
+    m = re.search(r"#define GRADLEV_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == gl.STATIC_SCRATCH_BYTES
