@@ -90,10 +90,13 @@ enum {
  * rounding.  Limits: exclusive reads only, T <= 16384 (the workspace holds
  * the causal B*H*T*T score matrix: gradlev_scan_workspace_bytes), chunk and
  * segment hints are ignored (the plan reports one chunk of T rounded up to
- * 128).  The backward returns gtilde, deta and dW0 - the gradients that remain
- * when writes are detached (Appendix E); dX, dG and dalpha give
- * GRADLEV_ERR_UNSUPPORTED.  Calls are deterministic: every reduction,
- * including the split of long score contractions, runs in a fixed order. */
+ * 128).  The backward returns every output of the narrow scans: gtilde and
+ * the write side of dX (S_read and its transpose, S_read = F c (dY G^T),
+ * contracted with X), dG (the transpose of the forward's scores contracted
+ * with dY), deta and dalpha (masked column sums over the pairs of reads and
+ * writes; dalpha through Z = K F^T with K = c (dY G^T) o (X X^T)) and dW0.
+ * Calls are deterministic: every reduction, including the split of long score
+ * contractions, runs in a fixed order. */
 typedef struct gradlev_shape {
   int64_t B, H, T, d_in, d_out;
   int64_t chunk;

@@ -412,7 +412,7 @@ const char* gradlev_error_string(int code) {
   switch (code) {
     case GRADLEV_OK: return "success";
     case GRADLEV_ERR_INVALID: return "invalid argument (null pointer, non-positive size or unknown enum)";
-    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out 64 or 128, or multiples of 128 up to 8192 with T <= 16384 and exclusive reads for wide maps; chunk 0/64/128, segment a multiple of 64 giving at most 16 segments; gated scans read exclusively; the wide backward returns gtilde, deta and dW0 only)";
+    case GRADLEV_ERR_UNSUPPORTED: return "unsupported shape (d_in/d_out 64 or 128, or multiples of 128 up to 8192 with T <= 16384 and exclusive reads for wide maps; chunk 0/64/128, segment a multiple of 64 giving at most 16 segments; gated scans read exclusively)";
     case GRADLEV_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case GRADLEV_ERR_WORKSPACE: return "workspace missing or too small";
     case GRADLEV_ERR_HIP: return "HIP launch failed";
@@ -744,10 +744,8 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
                            float* dalpha, float* dW0, void* workspace, size_t workspace_bytes,
                            void* stream) {
   if (wide_shape(s)) {
-    // Wide maps return the transpose read (the grounded target), the
-    // write-strength gradient and dW0: the gradients that remain when writes
-    // are detached (Appendix E).  The write-side dX, dG and dalpha are not
-    // built for wide maps.
+    // Wide maps: the parallel form's backward (transpose read, write-side
+    // terms, gate gradients and dW0), each output when requested.
     WideProblem w;
     int rc = make_wide(s, &w);
     if (rc != GRADLEV_OK) return rc;
@@ -755,8 +753,7 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
     if (rc != GRADLEV_OK) return rc;
     if (!W0 || !X || !G || !dY) return GRADLEV_ERR_INVALID;
     if (!gtilde && !dX && !dG && !deta && !dalpha && !dW0) return GRADLEV_ERR_INVALID;
-    if (dX || dG || dalpha) return GRADLEV_ERR_UNSUPPORTED;
-    const void* ptrs[] = {W0, X, G, dY, eta, gtilde, deta, dW0};
+    const void* ptrs[] = {W0, X, G, dY, eta, gtilde, dX, dG, deta, dalpha, dW0};
     for (const void* q : ptrs)
       if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
     rc = check_workspace(workspace, workspace_bytes, wide_workspace_bytes(w));
@@ -765,7 +762,10 @@ int gradlev_scan_bwd_gated(const gradlev_shape* s, const gradlev_gates* gates, c
     WidePtrs f = wide_ptrs(gates, W0, X, G, eta, eta_scalar, 1.f, workspace);
     f.dY = dY;
     f.gtilde = gtilde;
+    f.dX = dX;
+    f.dG = dG;
     f.deta = deta;
+    f.dalpha = dalpha;
     f.dW0 = dW0;
     return launch_wide_read(w, f, static_cast<hipStream_t>(stream)) == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
   }

@@ -124,14 +124,17 @@ struct WidePtrs {
   const uint8_t* reset;
   float* Y;
   float* gtilde;
+  float* dX;
+  float* dG;
   float* deta;
+  float* dalpha;
   float* dW0;
   void* ws;  // wide_workspace_bytes
 };
 
 size_t wide_workspace_bytes(const WideProblem& p);
 hipError_t launch_wide_fwd(const WideProblem& p, const WidePtrs& a, hipStream_t s);
-// Backward of a wide map: gtilde, deta and dW0 (each when non-null).
+// Backward of a wide map: gtilde, dX, dG, deta, dalpha and dW0 (each when non-null).
 hipError_t launch_wide_read(const WideProblem& p, const WidePtrs& a, hipStream_t s);
 
 // Optional event timing around each kernel launch (see gradlev_timing_*).

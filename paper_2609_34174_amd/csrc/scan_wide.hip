@@ -375,6 +375,9 @@ struct WDetaArgs {
   float* dpart;
   float* deta;
   const uint8_t* reset;
+  const float* cw;  // c_s = -eta_s, for Km
+  float* Km;        // [BH][Tp][Tp] or null: K[t][s] = c_s (dY_t . g_s)(x_t . x_s), s < t (lower tiles)
+  float* Fm;        // [BH][Tp][Tp] or null: F[t][s], s < t (lower tiles)
 };
 
 template <class OP, int FMODE>
@@ -455,13 +458,23 @@ static __global__ void __launch_bounds__(256) wide_deta_kernel(const WDetaArgs a
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t s = s0 + 16 * i + 4 * q;
+      f32x4 kv, fv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float f = (s + r < t && t < a.T) ? 1.f : 0.f;
+        const bool live = s + r < t && t < a.T;
+        float f = live ? 1.f : 0.f;
         const int zs = FMODE >= 1 ? zc[s + r] : 0;
         if (FMODE >= 1 && (zs >> 1) != (zt >> 1)) f = 0.f;
         if (FMODE == 2 && f != 0.f) f = ((zs ^ zt) & 1 ? -1.f : 1.f) * expf(at + (float)(ref - lc[s + r]));
-        col[i][r] += f * acc[0][i][j][r] * acc[1][i][j][r];
+        const float k = acc[0][i][j][r] * acc[1][i][j][r];
+        col[i][r] += f * k;
+        fv[r] = f;
+        kv[r] = live ? a.cw[bh * a.Tp + s + r] * k : 0.f;
+      }
+      if (a.Km) {
+        const int64_t o = (bh * a.Tp + t) * a.Tp + s;
+        *reinterpret_cast<f32x4*>(a.Km + o) = kv;
+        *reinterpret_cast<f32x4*>(a.Fm + o) = fv;
       }
     }
   }
@@ -484,9 +497,10 @@ static __global__ void __launch_bounds__(256) wide_deta_kernel(const WDetaArgs a
   }
 }
 
-// deta[bh][s] = -(sum of the partial column sums of the row halves at or
-// below s's block, in order), 0 for a token whose write a reset overrides.
-static __global__ void __launch_bounds__(256) wide_deta_reduce(const WDetaArgs a) {
+// out[bh][s] = sign * (sum of the partial column sums of the row halves at
+// or below s's block, in order), 0 for a token whose gates a reset overrides
+// (deta: sign -1; dalpha: sign +1).
+static __global__ void __launch_bounds__(256) wide_colsum_reduce(const WDetaArgs a, float* out, float sign) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= a.BH * a.T) return;
   const int64_t bh = i / a.T, s = i % a.T, b = bh / a.H;
@@ -495,7 +509,121 @@ static __global__ void __launch_bounds__(256) wide_deta_reduce(const WDetaArgs a
   float v = 0.f;
   for (int64_t h = 2 * (s / 128); h < nh; ++h) v += p[h * a.Tp];
   const bool cut = a.reset && s + 1 < a.T && a.reset[b * a.T + s + 1];
-  a.deta[bh * a.T + s] = cut ? 0.f : -v;
+  out[bh * a.T + s] = cut ? 0.f : sign * v;
+}
+
+// ---------------------------------------------------------------------------
+// Retention gradient (Appendix E keeps gate derivatives):
+//   dalpha_t = <Lambda_{t+1}, Delta_t>_F
+//            = sum_{u>t} F[u][t] Z[u][t],   Z[u][t] = sum_{s<t} F[t][s] K[u][s],
+// with K[u][s] = c_s (dY_u . g_s)(x_u . x_s) and F the retention products:
+// a pair of reads u and write s straddling t contributes through both decays
+// on either side of t (the product is never divided by alpha_t, so zero
+// retentions and resets stay exact).  Z = K F^T is a dense fp32 contraction
+// over s (MFMA 16x16x4 f32) of the K and F tiles that wide_deta_kernel
+// stored; tile (u block tb, t block sb) contracts s over [0, 128 (sb + 1)),
+// where F[t][.] is nonzero, and its masked column sums over u go to the same
+// partial layout as deta's.
+// ---------------------------------------------------------------------------
+template <int FMODE>
+static __global__ void __launch_bounds__(256) wide_dalpha_kernel(const WDetaArgs a) {
+  typedef OpF32 OP;
+  typedef OP::frag F;
+  constexpr int BT = 128, BK = 64, NT = 256;
+  __shared__ __attribute__((aligned(16))) float Ps[BT * BK];  // F rows t
+  __shared__ __attribute__((aligned(16))) float Qs[BT * BK];  // K rows u
+
+  const int64_t Kp = a.Tp / BT, per_seq = Kp * (Kp + 1) / 2;
+  const int64_t bh = blockIdx.x / per_seq;
+  int64_t tb, sb;
+  tri_tile(blockIdx.x % per_seq, tb, sb);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wt = w >> 1, ws = w & 1;
+  const int c = lane & 15, q = lane >> 4;
+
+  f32x4 acc[4][4];  // [t block][u block]: D[t][u] = F_t . K_u = Z[u][t]
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
+  {
+    const size_t plane = (size_t)a.Tp * a.Tp;
+    const rsrc_t Qr = make_rsrc(a.Km + bh * plane, (uint32_t)(plane * 4));
+    const rsrc_t Kr = make_rsrc(a.Fm + bh * plane, (uint32_t)(plane * 4));
+    const uint32_t stride = (uint32_t)(a.Tp * 4);
+    const uint32_t qoff = (uint32_t)(BT * tb) * stride, koff = (uint32_t)(BT * sb) * stride;
+    GTile<float, BT, BK, NT> qt, kt;
+    const int64_t nk = 2 * (sb + 1);
+    qt.load(Qr, qoff, stride, 0, tid);
+    kt.load(Kr, koff, stride, 0, tid);
+    for (int64_t k = 0; k < nk; ++k) {
+      __syncthreads();
+      qt.store(Qs, tid);
+      kt.store(Ps, tid);
+      __syncthreads();
+      const bool more = k + 1 < nk;
+      qt.load(Qr, more ? qoff : kOOB, stride, (uint32_t)((k + 1) * BK * 4), tid);
+      kt.load(Kr, more ? koff : kOOB, stride, (uint32_t)((k + 1) * BK * 4), tid);
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 32) {
+        F qf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = OP::mma(acc[i][j], pf, qf[j]);
+        }
+      }
+    }
+  }
+
+  // Lane (c, q) of block (i, j): t = s0 + 16 i + 4 q + r (the gradient's
+  // token), u = t0 + 16 j + c (the read).
+  const int64_t s0 = BT * sb + 64 * ws, t0 = BT * tb + 64 * wt;
+  const int* zc = a.zc + bh * a.Tp;
+  const double* lc = a.lc + bh * a.Tp;
+  const double ref = FMODE == 2 ? lc[s0 + 63] : 0.0;
+  float col[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) col[i][r] = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t u = t0 + 16 * j + c;
+    int zu = 0;
+    float au = 0.f;
+    if (FMODE >= 1 && u >= 1) zu = zc[u - 1];
+    if (FMODE == 2 && u >= 1) au = (float)(lc[u - 1] - ref);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t t = s0 + 16 * i + 4 * q;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float f = (t + r < u && u < a.T) ? 1.f : 0.f;
+        const int zt = FMODE >= 1 ? zc[t + r] : 0;
+        if (FMODE >= 1 && (zt >> 1) != (zu >> 1)) f = 0.f;
+        if (FMODE == 2 && f != 0.f) f = ((zt ^ zu) & 1 ? -1.f : 1.f) * expf(au + (float)(ref - lc[t + r]));
+        col[i][r] += f * acc[i][j][r];
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = col[i][r];
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 16);
+      col[i][r] = v;
+    }
+  if (c == 0) {
+    float* out = a.dpart + ((bh * 2 * (a.Tp / BT)) + 2 * tb + wt) * a.Tp;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<f32x4*>(out + s0 + 16 * i + 4 * q) = f32x4{col[i][0], col[i][1], col[i][2], col[i][3]};
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -590,10 +718,17 @@ struct WOutArgs {
   const void* Sl;
   const void* V;
   float* out;
+  const float* addend;  // anti-causal mode: added before the store (may be out itself), or null
   int64_t wq, wout, BH, H, T, Tp;
 };
 
-template <class OP, bool TRANS, int BN>
+// MODE 0 (causal): OUT[t] = Q_t P0 + sum_{s<t} S[t][s] V[s], the forward and
+// the transpose read.  MODE 1 (anti-causal, no W_0 phase): OUT[t] =
+// addend[t] + sum_{s>t} S[s][t] V[s], the write-side gradients: with the
+// forward's scores and V = dY it is dG, with the read's scores and V = X the
+// write side of dX (the transposed contraction of the same score matrix, read
+// from its stored lower triangle with transposing LDS reads).
+template <class OP, bool TRANS, int BN, int MODE>
 static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) {
   typedef typename OP::elem E;
   typedef typename OP::frag F;
@@ -615,7 +750,7 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
 
   const int64_t nTB = a.Tp / BM, nNB = a.wout / BN;
   const int64_t L = blockIdx.x, per_row = a.BH * nNB;
-  const int64_t tb = nTB - 1 - L / per_row;
+  const int64_t tb = MODE == 0 ? nTB - 1 - L / per_row : L / per_row;  // heaviest row tiles first
   const int64_t bh = (L % per_row) / nNB, nb = L % nNB;
   const int64_t h = bh % a.H;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, kh = w >> 2, wt = (w >> 1) & 1, wn = w & 1;
@@ -636,7 +771,7 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
   // offset beyond the buffer (zeros, no branch), so the outstanding-load
   // counts stay exact across the barriers.
   // Phase 1: acc += W_0-term over k in [0, wq).
-  {
+  if constexpr (MODE == 0) {
     const rsrc_t Qr = make_rsrc(static_cast<const E*>(a.Q) + bh * a.T * a.wq, (uint32_t)(a.T * a.wq * es));
     const int64_t md = a.wq * a.wout;
     const rsrc_t Wr = make_rsrc(a.W0 + h * md, (uint32_t)(md * 4));
@@ -698,23 +833,29 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
     }
   }
 
-  // Phase 2: acc += S V over s in [0, 128 (tb + 1)).
+  // Phase 2: acc += S V over s in [0, 128 (tb + 1)) (causal), or
+  // S^T V over s in [128 tb, Tp) (anti-causal: tiles of rows s, columns t).
   {
     const rsrc_t Shr = make_rsrc(static_cast<const E*>(a.Sh) + bh * a.Tp * a.Tp, (uint32_t)(a.Tp * a.Tp * es));
     const rsrc_t Slr = make_rsrc(SPLIT ? static_cast<const E*>(a.Sl) + bh * a.Tp * a.Tp : nullptr,
                                  SPLIT ? (uint32_t)(a.Tp * a.Tp * es) : 0u);
     const rsrc_t Vr = make_rsrc(static_cast<const E*>(a.V) + bh * a.T * a.wout, (uint32_t)(a.T * a.wout * es));
     const uint32_t sstride = (uint32_t)(a.Tp * es), vstride = (uint32_t)(a.wout * es);
+    typedef GTile<E, MODE == 0 ? BM : BK, MODE == 0 ? BK : BM, NT> ST;
     struct Set {
-      GTile<E, BM, BK, NT> sh, sl;
+      ST sh, sl;
       GTile<E, BK, BN, NT> vt;
     } st[2];
-    const int64_t n2 = 2 * (tb + 1);
+    const int64_t n2 = MODE == 0 ? 2 * (tb + 1) : 2 * (nTB - tb);
+    const int64_t sbeg = MODE == 0 ? 0 : t0;
     auto fetch = [&](Set& x, int64_t k) {
       const bool ok = k < n2;
-      const int64_t s0 = k * BK;
-      x.sh.load(Shr, ok ? (uint32_t)(t0 * sstride) : kOOB, sstride, (uint32_t)(s0 * es), tid);
-      if constexpr (SPLIT) x.sl.load(Slr, ok ? (uint32_t)(t0 * sstride) : kOOB, sstride, (uint32_t)(s0 * es), tid);
+      const int64_t s0 = sbeg + k * BK;
+      // causal: rows t [t0, +128), columns s; anti-causal: rows s [s0, +64), columns t
+      const uint32_t rows = MODE == 0 ? (uint32_t)(t0 * sstride) : (uint32_t)(s0 * sstride);
+      const uint32_t col = MODE == 0 ? (uint32_t)(s0 * es) : (uint32_t)(t0 * es);
+      x.sh.load(Shr, ok ? rows : kOOB, sstride, col, tid);
+      if constexpr (SPLIT) x.sl.load(Slr, ok ? rows : kOOB, sstride, col, tid);
       x.vt.load(Vr, ok ? (uint32_t)(s0 * vstride) : kOOB, vstride, (uint32_t)(n0 * es), tid);
     };
     auto step = [&](Set& x, int64_t k) {
@@ -729,8 +870,13 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
       F sfh[4], sfl[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        sfh[j] = OP::load_n(Shs, BK, 64 * wt + 16 * j, kk, lane);
-        sfl[j] = SPLIT ? OP::load_n(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
+        if constexpr (MODE == 0) {
+          sfh[j] = OP::load_n(Shs, BK, 64 * wt + 16 * j, kk, lane);
+          sfl[j] = SPLIT ? OP::load_n(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
+        } else {
+          sfh[j] = OP::load_t(Shs, BM, kk, 64 * wt + 16 * j, lane);
+          sfl[j] = SPLIT ? OP::load_t(Sls, BM, kk, 64 * wt + 16 * j, lane) : sfh[j];
+        }
       }
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
@@ -766,13 +912,17 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
 
   // Lane (c, q) of block (i, j): n = n0 + BN/2 wn + 16 i + 4 q + r, t = t0 + 64 wt + 16 j + c.
   const rsrc_t Or = make_rsrc(a.out + bh * a.T * a.wout, (uint32_t)(a.T * a.wout * 4));
+  const rsrc_t Ar = make_rsrc(MODE == 1 && a.addend ? a.addend + bh * a.T * a.wout : nullptr,
+                              MODE == 1 && a.addend ? (uint32_t)(a.T * a.wout * 4) : 0u);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t t = t0 + 64 * wt + 16 * j + c;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int64_t n = n0 + BN / 2 * wn + 16 * i + 4 * q;
-      buf_store4(Or, (uint32_t)((t * a.wout + n) * 4), acc[i][j]);
+      const uint32_t o = (uint32_t)((t * a.wout + n) * 4);
+      if constexpr (MODE == 1) acc[i][j] += buf_load4(Ar, o, (const float*)nullptr);
+      buf_store4(Or, o, acc[i][j]);
     }
   }
 }
@@ -793,14 +943,15 @@ static int wide_score_splits(int64_t BH, int64_t Tp, int64_t w) {
 size_t wide_workspace_bytes(const WideProblem& p) {
   const size_t BH = (size_t)(p.B * p.H), Tp = (size_t)p.Tp;
   const size_t gates = BH * Tp * (4 + 4 + 8);
-  const size_t S = BH * Tp * Tp * 4;  // bf16 hi + lo, or fp32
+  const size_t S = BH * Tp * Tp * 4;  // bf16 hi + lo, or fp32; also the fp32 K tiles of dalpha
   const int kd = wide_score_splits((int64_t)BH, (int64_t)Tp, p.d), km = wide_score_splits((int64_t)BH, (int64_t)Tp, p.m);
   const int ks = kd > km ? kd : km;  // the forward contracts over d, the read over m
   const size_t part = ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0;
   const size_t planes = p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0;  // W_0 hi + lo
-  const size_t dpart = BH * 2 * (Tp / 128) * Tp * 4;               // deta partial column sums
+  const size_t dpart = BH * 2 * (Tp / 128) * Tp * 4;               // partial column sums (deta, dalpha)
+  const size_t fm = BH * Tp * Tp * 4;                              // dalpha: fp32 F tiles
   return (gates + 255) / 256 * 256 + (S + 255) / 256 * 256 + (part + 255) / 256 * 256 + (planes + 255) / 256 * 256 +
-         dpart;
+         (dpart + 255) / 256 * 256 + fm;
 }
 
 namespace {
@@ -815,6 +966,8 @@ struct WideWs {
   bf16* Wh;
   bf16* Wl;
   float* dpart;
+  float* Km;  // the score region, reused once the scores are no longer needed
+  float* Fm;
 };
 
 WideWs wide_ws(const WideProblem& p, void* ws) {
@@ -827,6 +980,7 @@ WideWs wide_ws(const WideProblem& p, void* ws) {
   char* s = w + (BH * Tp * 16 + 255) / 256 * 256;
   o.Sh = s;
   o.Sl = s + BH * Tp * Tp * 2;  // bf16 only
+  o.Km = reinterpret_cast<float*>(s);
   char* pt = s + (BH * Tp * Tp * 4 + 255) / 256 * 256;
   o.part = reinterpret_cast<float*>(pt);
   const int kd = wide_score_splits((int64_t)BH, (int64_t)Tp, p.d), km = wide_score_splits((int64_t)BH, (int64_t)Tp, p.m);
@@ -834,25 +988,29 @@ WideWs wide_ws(const WideProblem& p, void* ws) {
   char* wp = pt + ((ks > 1 ? (size_t)ks * BH * Tp * Tp * 4 : 0) + 255) / 256 * 256;
   o.Wh = reinterpret_cast<bf16*>(wp);
   o.Wl = reinterpret_cast<bf16*>(wp + (size_t)p.H * p.m * p.d * 2);
-  o.dpart = reinterpret_cast<float*>(wp + ((p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0) + 255) / 256 * 256);
+  char* dp = wp + ((p.bf16 ? (size_t)p.H * p.m * p.d * 4 : 0) + 255) / 256 * 256;
+  o.dpart = reinterpret_cast<float*>(dp);
+  o.Fm = reinterpret_cast<float*>(dp + (BH * 2 * (Tp / 128) * Tp * 4 + 255) / 256 * 256);
   return o;
 }
 
 template <class OP>
-hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, hipStream_t s) {
-  const int64_t BH = p.B * p.H;
-  const WideWs ws = wide_ws(p, f.ws);
+void wide_gates(const WideProblem& p, const WidePtrs& f, const WideWs& ws, hipStream_t s) {
   WGateArgs g{f.eta, f.eta_scalar, f.eta_mul, f.alpha, f.alpha_scalar, f.reset, p.H, p.T, p.Tp, ws.cw, ws.zc, ws.lc};
-  timing_begin(GRADLEV_K_WIDE_SCORE, s);
-  hipLaunchKernelGGL(wide_gate_kernel, dim3((unsigned)BH), dim3(256), 0, s, g);
+  hipLaunchKernelGGL(wide_gate_kernel, dim3((unsigned)(p.B * p.H)), dim3(256), 0, s, g);
+}
 
-  // forward: Q = K = X over d; read: Q = dY over m, K = G.
+// Causal score matrix S[t][s] = F[t][s] c_s (Q_t . K_s) over width w into the
+// score region (lower-triangle 128 x 128 tiles).
+template <class OP>
+void wide_scores(const WideProblem& p, const WideWs& ws, const void* Q, const void* K, int64_t w, hipStream_t s) {
+  const int64_t BH = p.B * p.H;
   WScoreArgs sa{};
-  sa.Q = read ? f.dY : f.X;
-  sa.K = read ? f.G : f.X;
+  sa.Q = Q;
+  sa.K = K;
   sa.T = p.T;
   sa.Tp = p.Tp;
-  sa.w = read ? p.m : p.d;
+  sa.w = w;
   sa.BH = BH;
   sa.cw = ws.cw;
   sa.zc = ws.zc;
@@ -871,37 +1029,64 @@ hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, hipStrea
     else if (p.fmode == 1) hipLaunchKernelGGL((wide_score_finish<OP, 1>), dim3(16 * tiles), dim3(256), 0, s, sa);
     else hipLaunchKernelGGL((wide_score_finish<OP, 2>), dim3(16 * tiles), dim3(256), 0, s, sa);
   }
-  timing_end(GRADLEV_K_WIDE_SCORE, s);
+}
 
+// Output tiles of MODE 0 (W_0 term read as W_0^T when !trans, W_0 when
+// trans, plus the causal S V) or MODE 1 (anti-causal S^T V plus addend).
+template <class OP>
+void wide_out(const WideProblem& p, const WidePtrs& f, const WideWs& ws, int mode, bool trans, const void* Q,
+              int64_t wq, const void* V, int64_t wout, float* out, const float* addend, hipStream_t s) {
+  const int64_t BH = p.B * p.H;
   WOutArgs oa{};
-  oa.Q = sa.Q;
+  oa.Q = Q;
   oa.W0 = f.W0;
-  if (OP::kSplit == 2) {
-    const int64_t n4 = p.H * (int64_t)p.m * p.d / 4;
-    const unsigned g = (unsigned)(n4 / 256 < 4096 ? (n4 + 255) / 256 : 4096);
-    hipLaunchKernelGGL(wide_split_w0, dim3(g), dim3(256), 0, s, f.W0, ws.Wh, ws.Wl, n4);
-    oa.Wh = ws.Wh;
-    oa.Wl = ws.Wl;
-  }
+  oa.Wh = ws.Wh;
+  oa.Wl = ws.Wl;
   oa.Sh = ws.Sh;
-  oa.Sl = sa.Sl;
-  oa.V = read ? f.X : f.G;
-  oa.out = read ? f.gtilde : f.Y;
-  oa.wq = sa.w;
-  oa.wout = read ? p.d : p.m;
+  oa.Sl = OP::kSplit == 2 ? ws.Sl : ws.Sh;
+  oa.V = V;
+  oa.out = out;
+  oa.addend = addend;
+  oa.wq = wq;
+  oa.wout = wout;
   oa.BH = BH;
   oa.H = p.H;
   oa.T = p.T;
   oa.Tp = p.Tp;
   // 128-wide column tiles unless that leaves fewer than two tiles per compute unit.
-  const int64_t t128 = BH * (p.Tp / 128) * (oa.wout / 128);
+  const int64_t t128 = BH * (p.Tp / 128) * (wout / 128);
   const bool narrow = t128 < 2 * 256;
-  const unsigned ogrid = (unsigned)(narrow ? 2 * t128 : t128);
+  const unsigned g = (unsigned)(narrow ? 2 * t128 : t128);
+  if (mode == 1) {
+    if (narrow) hipLaunchKernelGGL((wide_out_kernel<OP, false, 64, 1>), dim3(g), dim3(512), 0, s, oa);
+    else hipLaunchKernelGGL((wide_out_kernel<OP, false, 128, 1>), dim3(g), dim3(512), 0, s, oa);
+  } else if (trans && narrow) hipLaunchKernelGGL((wide_out_kernel<OP, true, 64, 0>), dim3(g), dim3(512), 0, s, oa);
+  else if (trans) hipLaunchKernelGGL((wide_out_kernel<OP, true, 128, 0>), dim3(g), dim3(512), 0, s, oa);
+  else if (narrow) hipLaunchKernelGGL((wide_out_kernel<OP, false, 64, 0>), dim3(g), dim3(512), 0, s, oa);
+  else hipLaunchKernelGGL((wide_out_kernel<OP, false, 128, 0>), dim3(g), dim3(512), 0, s, oa);
+}
+
+template <class OP>
+void wide_split(const WideProblem& p, const WidePtrs& f, const WideWs& ws, hipStream_t s) {
+  if (OP::kSplit != 2) return;
+  const int64_t n4 = p.H * (int64_t)p.m * p.d / 4;
+  const unsigned g = (unsigned)(n4 / 256 < 4096 ? (n4 + 255) / 256 : 4096);
+  hipLaunchKernelGGL(wide_split_w0, dim3(g), dim3(256), 0, s, f.W0, ws.Wh, ws.Wl, n4);
+}
+
+// Forward (read = false: Q = K = X, V = G) or transpose read (read = true:
+// Q = dY, K = G, V = X) into `out`.
+template <class OP>
+hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, float* out, hipStream_t s) {
+  const WideWs ws = wide_ws(p, f.ws);
+  timing_begin(GRADLEV_K_WIDE_SCORE, s);
+  wide_gates<OP>(p, f, ws, s);
+  wide_scores<OP>(p, ws, read ? f.dY : f.X, read ? f.G : f.X, read ? p.m : p.d, s);
+  timing_end(GRADLEV_K_WIDE_SCORE, s);
+  wide_split<OP>(p, f, ws, s);
   timing_begin(GRADLEV_K_WIDE_OUT, s);
-  if (read && narrow) hipLaunchKernelGGL((wide_out_kernel<OP, true, 64>), dim3(ogrid), dim3(512), 0, s, oa);
-  else if (read) hipLaunchKernelGGL((wide_out_kernel<OP, true, 128>), dim3(ogrid), dim3(512), 0, s, oa);
-  else if (narrow) hipLaunchKernelGGL((wide_out_kernel<OP, false, 64>), dim3(ogrid), dim3(512), 0, s, oa);
-  else hipLaunchKernelGGL((wide_out_kernel<OP, false, 128>), dim3(ogrid), dim3(512), 0, s, oa);
+  wide_out<OP>(p, f, ws, 0, read, read ? f.dY : f.X, read ? p.m : p.d, read ? f.X : f.G, read ? p.d : p.m, out,
+               nullptr, s);
   timing_end(GRADLEV_K_WIDE_OUT, s);
   return hipGetLastError();
 }
@@ -909,31 +1094,59 @@ hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, hipStrea
 }  // namespace
 
 hipError_t launch_wide_fwd(const WideProblem& p, const WidePtrs& f, hipStream_t s) {
-  return p.bf16 ? wide_run<OpBF16>(p, f, false, s) : wide_run<OpF32>(p, f, false, s);
+  return p.bf16 ? wide_run<OpBF16>(p, f, false, f.Y, s) : wide_run<OpF32>(p, f, false, f.Y, s);
 }
 
-// The backward of a wide map: the transpose read (gtilde), the write-strength
-// gradient (deta) and dW0, each when requested.
+// The backward of a wide map, each output when requested:
+//   gtilde = dY W_0 + S_read X        (causal; S_read = F c (dY G^T))
+//   dX     = gtilde + S_read^T X      (anti-causal, write side)
+//   dG     = S_fwd^T dY               (anti-causal; S_fwd = F c (X X^T))
+//   deta, dalpha: masked column sums of the pair terms (wide_deta_kernel,
+//   wide_dalpha_kernel); dW0 = sum_b dY^T X.
 template <class OP>
 static hipError_t wide_bwd(const WideProblem& p, const WidePtrs& f, hipStream_t s) {
   const int64_t BH = p.B * p.H;
   const WideWs ws = wide_ws(p, f.ws);
-  if (f.gtilde) {
-    const hipError_t e = wide_run<OP>(p, f, true, s);
+  const bool need_gates = f.gtilde || f.dX || f.dG || f.deta || f.dalpha;
+  if (f.gtilde || f.dX) {
+    // The read lands in gtilde, or directly in dX when only dX is requested.
+    float* g = f.gtilde ? f.gtilde : f.dX;
+    const hipError_t e = wide_run<OP>(p, f, true, g, s);
     if (e != hipSuccess) return e;
-  } else if (f.deta) {
-    WGateArgs g{f.eta, f.eta_scalar, f.eta_mul, f.alpha, f.alpha_scalar, f.reset, p.H, p.T, p.Tp, ws.cw, ws.zc, ws.lc};
-    hipLaunchKernelGGL(wide_gate_kernel, dim3((unsigned)BH), dim3(256), 0, s, g);
+    if (f.dX) {
+      timing_begin(GRADLEV_K_WIDE_OUT, s);
+      wide_out<OP>(p, f, ws, 1, false, nullptr, 0, f.X, p.d, f.dX, g, s);
+      timing_end(GRADLEV_K_WIDE_OUT, s);
+    }
+  } else if (need_gates) {
+    wide_gates<OP>(p, f, ws, s);
   }
-  if (f.deta) {
-    WDetaArgs da{f.X, f.G, f.dY, p.T, p.Tp, p.d, p.m, BH, p.H, ws.zc, ws.lc, ws.dpart, f.deta, f.reset};
+  if (f.dG) {
+    timing_begin(GRADLEV_K_WIDE_SCORE, s);
+    wide_scores<OP>(p, ws, f.X, f.X, p.d, s);
+    timing_end(GRADLEV_K_WIDE_SCORE, s);
+    timing_begin(GRADLEV_K_WIDE_OUT, s);
+    wide_out<OP>(p, f, ws, 1, false, nullptr, 0, f.dY, p.m, f.dG, nullptr, s);
+    timing_end(GRADLEV_K_WIDE_OUT, s);
+  }
+  if (f.deta || f.dalpha) {
+    // The K and F tiles of dalpha take the score region, free from here on.
+    WDetaArgs da{f.X, f.G, f.dY, p.T, p.Tp, p.d, p.m, BH, p.H, ws.zc, ws.lc, ws.dpart, f.deta, f.reset,
+                 ws.cw, f.dalpha ? ws.Km : nullptr, f.dalpha ? ws.Fm : nullptr};
     const int64_t Kp = p.Tp / 128;
     const unsigned grid = (unsigned)(BH * Kp * (Kp + 1) / 2);
+    const unsigned rgrid = (unsigned)((BH * p.T + 255) / 256);
     timing_begin(GRADLEV_K_WIDE_SCORE, s);
     if (p.fmode == 0) hipLaunchKernelGGL((wide_deta_kernel<OP, 0>), dim3(grid), dim3(256), 0, s, da);
     else if (p.fmode == 1) hipLaunchKernelGGL((wide_deta_kernel<OP, 1>), dim3(grid), dim3(256), 0, s, da);
     else hipLaunchKernelGGL((wide_deta_kernel<OP, 2>), dim3(grid), dim3(256), 0, s, da);
-    hipLaunchKernelGGL(wide_deta_reduce, dim3((unsigned)((BH * p.T + 255) / 256)), dim3(256), 0, s, da);
+    if (f.deta) hipLaunchKernelGGL(wide_colsum_reduce, dim3(rgrid), dim3(256), 0, s, da, f.deta, -1.f);
+    if (f.dalpha) {
+      if (p.fmode == 0) hipLaunchKernelGGL((wide_dalpha_kernel<0>), dim3(grid), dim3(256), 0, s, da);
+      else if (p.fmode == 1) hipLaunchKernelGGL((wide_dalpha_kernel<1>), dim3(grid), dim3(256), 0, s, da);
+      else hipLaunchKernelGGL((wide_dalpha_kernel<2>), dim3(grid), dim3(256), 0, s, da);
+      hipLaunchKernelGGL(wide_colsum_reduce, dim3(rgrid), dim3(256), 0, s, da, f.dalpha, 1.f);
+    }
     timing_end(GRADLEV_K_WIDE_SCORE, s);
   }
   if (f.dW0) {

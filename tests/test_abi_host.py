@@ -309,17 +309,17 @@ def test_wide_plan_is_one_chunk(L):
     # gate prefixes (16 B per padded token), the causal score matrix (4 B per
     # pair), with 72 triangle tiles for 256 compute units the fp32 partials
     # of a 4-way split of the score contraction, and the bf16 hi + lo planes
-    # of W_0, and the write-strength gradient's partial column sums (two row
-    # halves per 128-token block)
+    # of W_0, the gate gradients' partial column sums (two row halves per
+    # 128-token block) and the retention gradient's fp32 F tiles (4 B per pair)
     BH, Tp = 2, 1024
     gates = (BH * Tp * 16 + 255) // 256 * 256
     planes = 1024 * 4096 * 4
     dpart = BH * 2 * (Tp // 128) * Tp * 4
-    assert p.workspace_bytes == gates + BH * Tp * Tp * 4 + 4 * BH * Tp * Tp * 4 + planes + dpart
+    assert p.workspace_bytes == gates + BH * Tp * Tp * 4 + 4 * BH * Tp * Tp * 4 + planes + dpart + BH * Tp * Tp * 4
     # many sequences fill the chip without splitting
     _, p2 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096))
     assert p2.workspace_bytes == ((64 * Tp * 16 + 255) // 256 * 256 + 64 * Tp * Tp * 4 + 4 * planes
-                                  + 64 * 2 * (Tp // 128) * Tp * 4)
+                                  + 64 * 2 * (Tp // 128) * Tp * 4 + 64 * Tp * Tp * 4)
     # fp32 operands need no planes
     _, p3 = plan_rc(shape(B=16, H=4, T=1000, d_in=1024, d_out=4096, dtype=gl.F32))
     assert p3.workspace_bytes == p2.workspace_bytes - 4 * planes
@@ -339,16 +339,24 @@ def test_wide_plan_rejects(L, bad, code):
     assert rc == code
 
 
-def test_wide_backward_refuses_unbuilt_outputs_before_launch(L):
+def test_wide_backward_validation_before_launch(L):
+    """Every backward output is accepted for wide maps; its alignment and the
+    workspace are checked before any launch."""
     s = shape(B=1, H=1, T=100, d_in=256, d_out=128)
     g = gl.Gates()
     g.alpha, g.alpha_scalar, g.reset = None, 1.0, None
     args = [ctypes.byref(s), ctypes.byref(g)] + [FAKE] * 4 + [ctypes.c_float(0.1), FAKE]
     # gtilde, dX, dG, deta, dalpha, dW0, ws, bytes, stream
-    rc = L.gradlev_scan_bwd_gated(*args, FAKE, FAKE, None, None, None, None, FAKE, ctypes.c_size_t(1 << 30), None)
-    assert rc == gl.ERR_UNSUPPORTED
-    rc = L.gradlev_scan_bwd_gated(*args, FAKE, None, None, None, None, None, FAKE, ctypes.c_size_t(16), None)
-    assert rc == gl.ERR_WORKSPACE
+    for k in range(6):
+        outs = [None] * 6
+        outs[k] = MISALIGNED
+        rc = L.gradlev_scan_bwd_gated(*args, *outs, FAKE, ctypes.c_size_t(1 << 30), None)
+        assert rc == gl.ERR_ALIGN, k
+        outs[k] = FAKE
+        rc = L.gradlev_scan_bwd_gated(*args, *outs, FAKE, ctypes.c_size_t(16), None)
+        assert rc == gl.ERR_WORKSPACE, k
+    rc = L.gradlev_scan_bwd_gated(*args, *([None] * 6), FAKE, ctypes.c_size_t(1 << 30), None)
+    assert rc == gl.ERR_INVALID
 
 
 @pytest.mark.parametrize("d_in,d_out,ok", [(512, 4096, True), (1024, 4096, True), (4096, 1024, True),

@@ -2,8 +2,8 @@
 
 The HIP path runs through the C ABI (gated and unit-retention entry points,
 the two-map MLP); the float64 oracle (the sequential learner of Section 3,
-Eq. 2 general form) checks the forward outputs and the transpose read
-gtilde.  Small cases compare every element, with ragged tails (T not a
+Eq. 2 general form) checks the forward outputs and every backward output
+(gtilde, dX, dG, deta, dalpha, dW0).  Small cases compare every element, with ragged tails (T not a
 multiple of the 128-token tile), T = 1, and the three retention modes the
 kernels distinguish (none, resets only, general retention with exact zeros
 and negative values).  The paper's adapted MLP at its LM width
@@ -86,9 +86,10 @@ CASES = [
 ]
 
 
-# The wide backward's outputs: the transpose read, the write-strength
-# gradient and dW0 (what remains when writes are detached).
-WIDE_BWD = ("gtilde", "deta", "dw0")
+# Every backward output of the wide path (unit-retention entry points have
+# no dalpha).
+WIDE_BWD = ("gtilde", "dx", "dg", "deta", "dalpha", "dw0")
+UNIT_BWD = ("gtilde", "dx", "dg", "deta", "dw0")
 
 
 @pytest.mark.parametrize("dtype,d,m,T,ak,ek,rs", CASES)
@@ -114,23 +115,28 @@ def test_wide_unit_entry_points(dtype):
     inp = inputs(3, 1, 270, 128, 256, dtype, seed=11, alpha_kind="1", eta_kind="token", with_reset=False)
     W0, X, G, dY, e, _, _ = dev_inputs(inp, dtype)
     y = gl.scan_fwd(W0, X, G, e)
-    out = gl.scan_bwd(W0, X, G, dY, e, outputs=WIDE_BWD)
+    out = gl.scan_bwd(W0, X, G, dY, e, outputs=UNIT_BWD)
     torch.cuda.synchronize()
     args = (inp["W0"], inp["X"], inp["G"], inp["eta"])
     check("y", to_host(y), orc.scan_fwd(*args), dtype)
     ref = orc.scan_bwd(*args, inp["dY"])
-    for k in WIDE_BWD:
+    for k in UNIT_BWD:
         check(k, to_host(out[k]), ref[k], dtype)
 
 
-def test_wide_rejects_unbuilt_outputs():
-    """The wide backward refuses the write-side outputs (dX, dG, dalpha)."""
-    inp = inputs(1, 1, 64, 256, 128, "bf16", seed=5, alpha_kind="1", eta_kind="scalar", with_reset=False)
-    W0, X, G, dY, e, _, _ = dev_inputs(inp, "bf16")
-    for outs in (("gtilde", "dx"), ("dg",), ("deta", "dalpha")):
-        with pytest.raises(gl.GradLevError) as ex:
-            gl.scan_bwd_gated(W0, X, G, dY, e, 0.9, outputs=outs)
-        assert ex.value.code == gl.ERR_UNSUPPORTED
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_wide_output_subsets_are_bitwise_identical(dtype):
+    """Each backward output requested alone (or in a subset) equals the same
+    output of the full call bitwise: dX alone lands the read in dX itself,
+    dalpha alone runs the gate pass without deta's reduction."""
+    inp = inputs(2, 1, 333, 256, 128, dtype, seed=5, alpha_kind="family", eta_kind="token", with_reset=True)
+    W0, X, G, dY, e, a, r = dev_inputs(inp, dtype)
+    full = {k: to_host(v) for k, v in gl.scan_bwd_gated(W0, X, G, dY, e, a, r, outputs=WIDE_BWD).items()}
+    for subset in (("dx",), ("dg",), ("dalpha",), ("deta", "dalpha"), ("gtilde", "dg"), ("dw0",)):
+        log(f"  subset {subset}")
+        part = gl.scan_bwd_gated(W0, X, G, dY, e, a, r, outputs=subset)
+        for k in subset:
+            np.testing.assert_array_equal(to_host(part[k]), full[k], err_msg=str(subset))
 
 
 @pytest.mark.timeout(600)
@@ -224,11 +230,12 @@ def test_lm_width_training_gradients_sampled():
     dv = lambda a, dt="bf16": to_dev(a, dt, torch)  # noqa: E731
     args = (dv(W0, "f32"), dv(X), dv(G))
     y = gl.scan_fwd_gated(*args, dv(eta, "f32"), 1.0, torch.from_numpy(rs).to("cuda"))
-    out = gl.scan_bwd_gated(*args, dv(dY), dv(eta, "f32"), 1.0, torch.from_numpy(rs).to("cuda"), outputs=WIDE_BWD)
+    out = gl.scan_bwd_gated(*args, dv(dY), dv(eta, "f32"), 1.0, torch.from_numpy(rs).to("cuda"), outputs=UNIT_BWD)
     torch.cuda.synchronize()
     yh, gth, deh, dwh = to_host(y), to_host(out["gtilde"]), to_host(out["deta"]), to_host(out["dw0"])
+    dxh, dgh = to_host(out["dx"]), to_host(out["dg"])
     picks = sorted({0, 1, 127, 128, 500, 1022, 1023, *rng.integers(0, T, 5).tolist()})
-    got = {k: [] for k in ("y", "gtilde", "deta")}
+    got = {k: [] for k in ("y", "gtilde", "dx", "dg", "deta")}
     ref = {k: [] for k in got}
     for b in range(B):
         starts = np.nonzero(rs[b])[0].tolist() + [T]
@@ -241,6 +248,7 @@ def test_lm_width_training_gradients_sampled():
             # a token whose write the next document's reset drops has deta = 0
             de = 0.0 if hi == t + 1 and t + 1 < T else r["deta"]
             for k, g_, r_ in (("y", yh[b, 0, t], r["y"]), ("gtilde", gth[b, 0, t], r["gtilde"]),
+                              ("dx", dxh[b, 0, t], r["dx"]), ("dg", dgh[b, 0, t], r["dg"]),
                               ("deta", deh[b, 0, t], de)):
                 got[k].append(g_)
                 ref[k].append(r_)
