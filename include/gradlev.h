@@ -401,12 +401,25 @@ int gradlev_mlp_fwd(const gradlev_mlp_shape* s, const gradlev_gates* gates,
  *   gY [B,H,T,d_out] in_dtype.
  *   gZ [B,H,T,hidden] fp32 out: g_z~
  *   gX [B,H,T,d_in]   fp32 out or NULL: g_x~ (the hidden target is stored in
- *                     in_dtype before it queries the first scan) */
+ *                     in_dtype before it queries the first scan)
+ * Training gradients of L = sum_t <gY_t, y_t> with the writes detached, as
+ * the paper trains (Appendix E: costates and write inputs detached; gate and
+ * read derivatives remain), each fp32 out or NULL:
+ *   dMu   [B,H,T]          dL/dmu_t = deta_1 / d_in + deta_2 / hidden, where
+ *                          deta_k is map k's write-strength gradient for its
+ *                          own upstream costate (gY for the second map, the
+ *                          hidden target g_z~ for the first); for a scalar mu
+ *                          its gradient is the sum over tokens
+ *   dAlpha [B,H,T]         dL/dalpha_t, the two maps' retention gradients added
+ *   dW1_0 [H,hidden,d_in]  sum_b sum_t g_z~ x^T (overwritten)
+ *   dW2_0 [H,d_out,hidden] sum_b sum_t gY h^T (overwritten)
+ * The first map's outputs use the in_dtype copy of g_z~, as gX does. */
 int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates,
                         const float* W1_0, const float* W2_0, const void* X,
                         const void* Gz, const void* Gy, const float* mu, float mu_scalar,
                         const float* Z, const void* Hid, const void* gY, float* gZ,
-                        float* gX, void* workspace, size_t workspace_bytes, void* stream);
+                        float* gX, float* dMu, float* dAlpha, float* dW1_0, float* dW2_0,
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Kernel timing for benchmarks and tracing.  While a family's bit is set in
  * the mask given to gradlev_timing_enable (bit f = family f; 0 turns timing

@@ -357,12 +357,22 @@ def mlp_fwd(W10, W20, X, Gz, Gy, alpha, mu, kind="tanh", hidden_bf16=False, rese
 
 
 def mlp_reverse(W10, W20, X, Gz, Gy, alpha, mu, gy, kind="tanh", hidden_bf16=False,
-                slow_transpose=False, reset=None):
+                slow_transpose=False, reset=None, target_bf16=False):
     """Reconstructed costates of Appendix A (Eq. for the reverse targets):
     g_z = sigma'(z_hat) * (W2_0 + Delta2_hat_t)^T g_y, a transpose read of the
     second scan queried by the output costate g_y [B, H, T, o], and the input
     costate g_x = (W1_0 + Delta1_hat_t)^T g_z.  slow_transpose keeps only W2_0
-    (the control of Section 5.1).  Returns dict(z, h, gh, gz, gx).
+    (the control of Section 5.1).  target_bf16 rounds g_z to bfloat16 before
+    it queries the first scan (the storage of a bf16 pipeline).
+
+    Also returns the training gradients of L = sum_t <g_y, y_hat_t> with the
+    writes detached (Appendix E: costates and write inputs are detached; gate
+    and read derivatives remain): the slow weights, dw20 = sum g_y h^T and
+    dw10 = sum g_z x^T; the shared write strength, dmu = deta_1 / d + deta_2 / m
+    (eta_1 = mu / d, eta_2 = mu / m, per token); and, with retentions, the
+    shared retention, dalpha = dalpha_1 + dalpha_2 - each scan's gate gradient
+    for its own upstream costate (g_y for the second, g_z for the first).
+    Returns dict(z, h, gh, gz, gx, dmu, dw10, dw20[, dalpha]).
     """
     f = mlp_fwd(W10, W20, X, Gz, Gy, alpha, mu, kind, hidden_bf16, reset)
     X = _as_array(X)
@@ -371,13 +381,18 @@ def mlp_reverse(W10, W20, X, Gz, Gy, alpha, mu, gy, kind="tanh", hidden_bf16=Fal
     e1 = _as_array(mu) / d
     e2 = _as_array(mu) / m
     gy = _as_array(gy)
+    r2 = scan_bwd(W20, f["h"], Gy, e2, gy, alpha=alpha, reset=reset)
     if slow_transpose:
         gh = np.einsum("hom,bhto->bhtm", _as_array(W20), gy)
     else:
-        gh = scan_bwd(W20, f["h"], Gy, e2, gy, alpha=alpha, reset=reset)["gtilde"]
+        gh = r2["gtilde"]
     gz = act_grad(f["z"], kind) * gh
-    gx = scan_bwd(W10, X, Gz, e1, gz, alpha=alpha, reset=reset)["gtilde"]
-    return {"z": f["z"], "h": f["h"], "gh": gh, "gz": gz, "gx": gx}
+    r1 = scan_bwd(W10, X, Gz, e1, round_bf16(gz) if target_bf16 else gz, alpha=alpha, reset=reset)
+    out = {"z": f["z"], "h": f["h"], "gh": gh, "gz": gz, "gx": r1["gtilde"],
+           "dmu": r1["deta"] / d + r2["deta"] / m, "dw10": r1["dw0"], "dw20": r2["dw0"]}
+    if alpha is not None:
+        out["dalpha"] = r1["dalpha"] + r2["dalpha"]
+    return out
 
 
 def outer_sum(A, Bm, w, lo, hi):
@@ -488,14 +503,15 @@ def scan_reads(W0, X, G, eta, A=None, Bq=None, alpha=None, reset=None):
         if r.shape != (B, T):
             raise ValueError(f"reset must be [B,T]={B,T}, got {r.shape}")
         doc = np.cumsum(r != 0, axis=1)
-    y = np.zeros((B, H, T, m))
-    gt = None if Bq is None else np.zeros((B, H, T, d))
     if Bq is not None:
         Bq = _as_array(Bq)
+    dt = np.result_type(W0, X, G, A, e, a, 0.0 if Bq is None else Bq)
+    y = np.zeros((B, H, T, m), dt)
+    gt = None if Bq is None else np.zeros((B, H, T, d), dt)
     for b in range(B):
         sees = (doc[b][:, None] == doc[b][None, :]) & np.tri(T, T, -1, dtype=bool)
         for h in range(H):
-            K = np.zeros((T, T))
+            K = np.zeros((T, T), dt)
             for i in range(T - 1):
                 # prod_{j=i+1}^{t-1} alpha_j for t = i+1 .. T-1 (empty product first)
                 K[i + 1:, i] = -e[b, h, i] * np.cumprod(np.concatenate(([1.0], a[b, h, i + 1:T - 1])))

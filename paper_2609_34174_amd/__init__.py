@@ -116,7 +116,8 @@ def lib():
         L.gradlev_mlp_fwd.argtypes = [mp, gp, f32p, f32p, vp, vp, vp, f32p, ctypes.c_float,
                                       f32p, vp, f32p, vp, ctypes.c_size_t, vp]
         L.gradlev_mlp_reverse.argtypes = [mp, gp, f32p, f32p, vp, vp, vp, f32p, ctypes.c_float,
-                                          f32p, vp, vp, f32p, f32p, vp, ctypes.c_size_t, vp]
+                                          f32p, vp, vp, f32p, f32p, f32p, f32p, f32p, f32p, vp,
+                                          ctypes.c_size_t, vp]
         L.gradlev_timing_enable.argtypes = [ctypes.c_int]
         L.gradlev_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]
@@ -646,9 +647,15 @@ def mlp_fwd(W10, W20, X, Gz, Gy, mu=0.9, alpha=1.0, reset=None, *, act="tanh", s
     return Z, Hid, Y
 
 
+MLP_GRADS = ("dmu", "dalpha", "dw10", "dw20")
+
+
 def mlp_reverse(W10, W20, X, Gz, Gy, Z, Hid, gY, mu=0.9, alpha=1.0, reset=None, *, act="tanh",
-                with_gx=True, segment=0, workspace=None):
-    """Reverse targets of the MLP: returns (gZ, gX or None), fp32."""
+                with_gx=True, grads=(), segment=0, workspace=None):
+    """Reverse targets of the MLP: returns (gZ, gX or None), fp32; with
+    ``grads`` (any of "dmu" [B,H,T], "dalpha" [B,H,T], "dw10" [H,hidden,d_in],
+    "dw20" [H,d_out,hidden]) returns (gZ, gX, dict of those training
+    gradients) - see gradlev_mlp_reverse."""
     torch = _torch()
     s = _mlp_shape(W10, W20, X, Gz, Gy, act, segment)
     _check_dev("Z", Z, torch.float32, (s.B, s.H, s.T, s.hidden))
@@ -658,13 +665,21 @@ def mlp_reverse(W10, W20, X, Gz, Gy, Z, Hid, gY, mu=0.9, alpha=1.0, reset=None, 
     gt = _gates(alpha, reset, s.B, s.H, s.T, X)
     gZ = torch.empty(s.B, s.H, s.T, s.hidden, dtype=torch.float32, device=X.device)
     gX = torch.empty(s.B, s.H, s.T, s.d_in, dtype=torch.float32, device=X.device) if with_gx else None
+    shapes = {"dmu": (s.B, s.H, s.T), "dalpha": (s.B, s.H, s.T), "dw10": (s.H, s.hidden, s.d_in),
+              "dw20": (s.H, s.d_out, s.hidden)}
+    g = {}
+    for k in grads:
+        if k not in shapes:
+            raise ValueError(f"unknown gradient {k!r}")
+        g[k] = torch.empty(shapes[k], dtype=torch.float32, device=X.device)
     ws, wsn = _mlp_ws(s, X.device, workspace)
     rc = lib().gradlev_mlp_reverse(ctypes.byref(s), ctypes.byref(gt), _ptr(W10), _ptr(W20), _ptr(X), _ptr(Gz),
                                    _ptr(Gy), _ptr(m), ms, _ptr(Z), _ptr(Hid), _ptr(gY), _ptr(gZ), _ptr(gX),
-                                   _ptr(ws), wsn, _stream(X.device))
+                                   _ptr(g.get("dmu")), _ptr(g.get("dalpha")), _ptr(g.get("dw10")),
+                                   _ptr(g.get("dw20")), _ptr(ws), wsn, _stream(X.device))
     if rc != OK:
         raise GradLevError(rc, "gradlev_mlp_reverse")
-    return gZ, gX
+    return (gZ, gX, g) if grads else (gZ, gX)
 
 
 # ---------------------------------------------------------------------------

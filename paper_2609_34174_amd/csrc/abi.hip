@@ -297,7 +297,8 @@ struct MlpPlan {
   bool wide1, wide2;  // the scan runs the wide-map kernels (w1, w2) instead
   WideProblem w1, w2;
   size_t scan_ws;  // the larger of the two scans' workspaces (they run in turn)
-  size_t off_q;    // in_dtype copy of the hidden target (reverse with gX)
+  size_t off_q;    // in_dtype copy of the hidden target (queries the first scan)
+  size_t off_g;    // the first scan's deta and dalpha, the second's deta ([B*H*T] fp32 each)
   size_t total;
 };
 
@@ -326,7 +327,8 @@ int make_mlp_plan(const gradlev_mlp_shape* m, MlpPlan* out) {
   out->scan_ws = round_up(w, 256);
   out->off_q = out->scan_ws;
   const size_t es = m->in_dtype == GRADLEV_BF16 ? 2 : 4;
-  out->total = out->off_q + round_up((size_t)(m->B * m->H * m->T * m->hidden) * es, 256);
+  out->off_g = out->off_q + round_up((size_t)(m->B * m->H * m->T * m->hidden) * es, 256);
+  out->total = out->off_g + 3 * round_up((size_t)(m->B * m->H * m->T) * 4, 256);
   return GRADLEV_OK;
 }
 
@@ -875,49 +877,74 @@ int gradlev_mlp_fwd(const gradlev_mlp_shape* s, const gradlev_gates* gates, cons
 int gradlev_mlp_reverse(const gradlev_mlp_shape* s, const gradlev_gates* gates, const float* W1_0,
                         const float* W2_0, const void* X, const void* Gz, const void* Gy, const float* mu,
                         float mu_scalar, const float* Z, const void* Hid, const void* gY, float* gZ,
-                        float* gX, void* workspace, size_t workspace_bytes, void* stream) {
+                        float* gX, float* dMu, float* dAlpha, float* dW1_0, float* dW2_0, void* workspace,
+                        size_t workspace_bytes, void* stream) {
   MlpPlan p;
   int rc = make_mlp_plan(s, &p);
   if (rc != GRADLEV_OK) return rc;
   rc = check_gates(gates);
   if (rc != GRADLEV_OK) return rc;
   if (!W1_0 || !W2_0 || !X || !Gz || !Gy || !Z || !Hid || !gY || !gZ) return GRADLEV_ERR_INVALID;
-  const void* ptrs[] = {W1_0, W2_0, X, Gz, Gy, mu, Z, Hid, gY, gZ, gX};
+  const void* ptrs[] = {W1_0, W2_0, X, Gz, Gy, mu, Z, Hid, gY, gZ, gX, dMu, dAlpha, dW1_0, dW2_0};
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
   rc = check_workspace(workspace, workspace_bytes, p.total);
   if (rc != GRADLEV_OK) return rc;
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t BH = s->B * s->H;
-  // Transpose read of the second scan: g_h = (W2_0 + Delta2_t)^T gY, written into gZ.
+  const int64_t BH = s->B * s->H, n = BH * s->T;
+  char* ws = static_cast<char*>(workspace);
+  const size_t gstride = round_up((size_t)n * 4, 256);
+  float* de1 = reinterpret_cast<float*>(ws + p.off_g);
+  float* de2 = reinterpret_cast<float*>(ws + p.off_g + gstride);
+  float* da1 = reinterpret_cast<float*>(ws + p.off_g + 2 * gstride);
+  // The second scan with the output costate: its transpose read g_h (written
+  // into gZ), and with the training gradients its deta, dalpha and dW0.
   const int fm = wide_fmode(gates);
   if (p.wide2) {
     WidePtrs b2 = wide_ptrs(gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace);
     b2.dY = gY;
     b2.gtilde = gZ;
+    b2.deta = dMu ? de2 : nullptr;
+    b2.dalpha = dAlpha;
+    b2.dW0 = dW2_0;
     p.w2.fmode = fm;
     if (launch_wide_read(p.w2, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
   } else {
     GatedPtrs b2 = gated_ptrs(p.p2, gates, W2_0, Hid, Gy, mu, mu_scalar, 1.f / (float)s->hidden, workspace, true, BH);
     b2.dY = gY;
     b2.gtilde = gZ;
+    b2.deta = dMu ? de2 : nullptr;
+    b2.dalpha = dAlpha;
+    b2.dW0 = dW2_0;
     if (launch_scan_bwd_gated(p.p2.bwd, b2, st) != hipSuccess) return GRADLEV_ERR_HIP;
   }
-  void* q = gX ? static_cast<void*>(static_cast<char*>(workspace) + p.off_q) : nullptr;
+  // g_z = sigma'(z) g_h, and its in_dtype copy for the first scan's queries.
+  const bool first = gX || dMu || dAlpha || dW1_0;
+  void* q = first ? static_cast<void*>(ws + p.off_q) : nullptr;
   if (launch_act_bwd(s->in_dtype == GRADLEV_BF16, Z, gZ, q, BH * s->T * s->hidden, s->act, st) != hipSuccess)
     return GRADLEV_ERR_HIP;
-  if (gX && p.wide1) {
+  if (first && p.wide1) {
     WidePtrs b1 = wide_ptrs(gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace);
     b1.dY = q;
     b1.gtilde = gX;
+    b1.deta = dMu ? de1 : nullptr;
+    b1.dalpha = dAlpha ? da1 : nullptr;
+    b1.dW0 = dW1_0;
     p.w1.fmode = fm;
     if (launch_wide_read(p.w1, b1, st) != hipSuccess) return GRADLEV_ERR_HIP;
-  } else if (gX) {
+  } else if (first) {
     GatedPtrs b1 = gated_ptrs(p.p1, gates, W1_0, X, Gz, mu, mu_scalar, 1.f / (float)s->d_in, workspace, true, BH);
     b1.dY = q;
     b1.gtilde = gX;
+    b1.deta = dMu ? de1 : nullptr;
+    b1.dalpha = dAlpha ? da1 : nullptr;
+    b1.dW0 = dW1_0;
     if (launch_scan_bwd_gated(p.p1.bwd, b1, st) != hipSuccess) return GRADLEV_ERR_HIP;
   }
+  if ((dMu || dAlpha) &&
+      launch_mlp_gate_grads(de1, de2, 1.f / (float)s->d_in, 1.f / (float)s->hidden, dMu, da1, dAlpha, n, st) !=
+          hipSuccess)
+    return GRADLEV_ERR_HIP;
   return GRADLEV_OK;
 }
 

@@ -87,6 +87,8 @@ struct DecodeGates {
 // Two-map MLP elementwise stages (n values, a multiple of 4).
 hipError_t launch_act_fwd(int bf16, const float* Z, void* H, int64_t n, int kind, hipStream_t s);
 hipError_t launch_act_bwd(int bf16, const float* Z, float* G, void* Gq, int64_t n, int kind, hipStream_t s);
+hipError_t launch_mlp_gate_grads(const float* de1, const float* de2, float s1, float s2, float* dmu,
+                                 const float* da1, float* dalpha, int64_t n, hipStream_t s);
 
 int gated_fwd_chunk(int bf16, int d, int m);
 int gated_bwd_chunk(int bf16, int d, int m);

@@ -1,8 +1,9 @@
 // Elementwise stages of the two-map online MLP (Appendix A): the hidden
-// activation between the two scans, h = sigma(z), and the reverse target of
-// the hidden layer, g_z = sigma'(z) * g_h.  Both are pure streams (a few
-// flops per 8-16 bytes), so each thread handles 4 consecutive values with
-// 16-byte accesses in a grid-stride loop.
+// activation between the two scans, h = sigma(z), the reverse target of the
+// hidden layer, g_z = sigma'(z) * g_h, and the combination of the two scans'
+// gate gradients into those of the shared gates.  All are pure streams (a few
+// flops per 8-16 bytes); the activation stages handle 4 consecutive values
+// per thread with 16-byte accesses in a grid-stride loop.
 #include "../../include/gradlev.h"
 #include "device_common.hpp"
 #include "internal.hpp"
@@ -73,6 +74,27 @@ act_bwd_kernel(const float* __restrict__ Z, float* __restrict__ G, E* __restrict
 static unsigned act_grid(int64_t n4) {
   const int64_t b = (n4 + 255) / 256;
   return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
+}
+
+// The shared gates' gradients from the two scans' (Appendix A: both maps use
+// the write strength mu, with eta_1 = mu / d_in and eta_2 = mu / hidden, and
+// the same retention):  dmu = deta_1 / d_in + deta_2 / hidden,
+// dalpha += dalpha_1 (dalpha already holds the second scan's).
+__global__ void __launch_bounds__(256)
+mlp_gate_grads_kernel(const float* __restrict__ de1, const float* __restrict__ de2, float s1, float s2,
+                      float* __restrict__ dmu, const float* __restrict__ da1, float* __restrict__ dalpha, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    if (dmu) dmu[i] = de1[i] * s1 + de2[i] * s2;
+    if (dalpha) dalpha[i] += da1[i];
+  }
+}
+
+hipError_t launch_mlp_gate_grads(const float* de1, const float* de2, float s1, float s2, float* dmu,
+                                 const float* da1, float* dalpha, int64_t n, hipStream_t s) {
+  const int64_t b = (n + 255) / 256;
+  hipLaunchKernelGGL(mlp_gate_grads_kernel, dim3((unsigned)(b < 4096 ? b : 4096)), dim3(256), 0, s, de1, de2, s1, s2,
+                     dmu, da1, dalpha, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_act_fwd(int is_bf16, const float* Z, void* H, int64_t n, int kind, hipStream_t s) {

@@ -293,8 +293,18 @@ def test_mlp_validation_before_launch(L):
     bad[11] = 16                       # workspace too small
     assert fwd(ctypes.byref(ms()), ctypes.byref(g), *bad) == gl.ERR_WORKSPACE
     rev = L.gradlev_mlp_reverse
-    rargs = [FAKE] * 5 + [None, 0.9, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None]
+    # W1_0, W2_0, X, Gz, Gy, mu, mu_scalar, Z, Hid, gY, gZ, gX, dMu, dAlpha, dW1_0, dW2_0, ws, bytes, stream
+    rargs = [FAKE] * 5 + [None, 0.9, FAKE, FAKE, FAKE, None, None, None, None, None, None, FAKE, 1 << 40, None]
     assert rev(ctypes.byref(ms()), ctypes.byref(g), *rargs) == gl.ERR_INVALID   # gZ missing
+    for k in range(12, 16):                                                   # each gradient output misaligned
+        bad = list(rargs)
+        bad[10] = FAKE
+        bad[k] = MISALIGNED
+        assert rev(ctypes.byref(ms()), ctypes.byref(g), *bad) == gl.ERR_ALIGN, k
+    ok = list(rargs)
+    ok[10] = ok[12] = ok[13] = ok[14] = ok[15] = FAKE
+    ok[17] = 16                                                               # workspace too small
+    assert rev(ctypes.byref(ms()), ctypes.byref(g), *ok) == gl.ERR_WORKSPACE
 
 
 # ---------------------------------------------------------------------------

@@ -2,7 +2,8 @@
 
 Forward: z_hat (first gated scan), h_hat = sigma(z_hat) stored in the input
 dtype, y_hat (second gated scan).  Reverse: g_z = sigma'(z_hat) times the
-transpose read of the second scan, and g_x through the first.  A further case
+transpose read of the second scan, g_x through the first, and the training
+gradients of the shared gates and the slow weights (writes detached).  A further case
 feeds the serial learner's exact costates (fp32) and checks that the GPU
 scans reproduce serial test-time training, as the paper's FP64 experiment
 does on the CPU.
@@ -59,23 +60,41 @@ def test_mlp_parity(dtype, act, d, hid, o, seg):
     args = (dev(W10, "f32"), dev(W20, "f32"), dev(X), dev(Gz), dev(Gy))
     mud, ald, rsd = dev(mu, "f32"), dev(al, "f32"), torch.from_numpy(rs).to("cuda")
     Z, Hid, Y = gl.mlp_fwd(*args, mud, ald, rsd, act=act, segment=seg)
-    gZ, gX = gl.mlp_reverse(*args, Z, Hid, dev(gY), mud, ald, rsd, act=act, segment=seg)
+    gZ, gX, gr = gl.mlp_reverse(*args, Z, Hid, dev(gY), mud, ald, rsd, act=act, segment=seg, grads=gl.MLP_GRADS)
     torch.cuda.synchronize()
     kw = dict(kind=act, hidden_bf16=dtype == "bf16", reset=rs)
     f = orc.mlp_fwd(W10, W20, X, Gz, Gy, al, mu, **kw)
-    r = orc.mlp_reverse(W10, W20, X, Gz, Gy, al, mu, gY, **kw)
+    # The hidden target meets the first scan in bf16 when the pipeline is bf16
+    # (as the library stores it); the oracle rounds its own fp64 target alike.
+    r = orc.mlp_reverse(W10, W20, X, Gz, Gy, al, mu, gY, target_bf16=dtype == "bf16", **kw)
     check("z", to_host(Z), f["z"], dtype)
     check("h", to_host(Hid), f["h"], dtype)
     check("y", to_host(Y), f["y"], dtype)
     check("gz", to_host(gZ), r["gz"], dtype)
-    if dtype == "f32":
-        check("gx", to_host(gX), r["gx"], dtype)
-    else:
-        # The hidden target meets the first scan in bf16 (as the library
-        # stores it); the oracle rounds its own fp64 target the same way.
-        gzq = orc.round_bf16(r["gz"])
-        gx_ref = orc.scan_bwd(W10, X, Gz, mu / d, gzq, alpha=al, reset=rs)["gtilde"]
-        check("gx", to_host(gX), gx_ref, dtype)
+    check("gx", to_host(gX), r["gx"], dtype)
+    for k in gl.MLP_GRADS:
+        check(k, to_host(gr[k]), r[k], dtype)
+
+
+def test_mlp_gradient_subsets_are_bitwise_identical():
+    """Each MLP training gradient requested alone equals the full call's."""
+    rng = np.random.default_rng(12)
+    B, H, T, d, hid, o = 2, 1, 150, 64, 128, 64
+    W10 = (rng.standard_normal((H, hid, d)) * d ** -0.5).astype(np.float32)
+    W20 = (rng.standard_normal((H, o, hid)) * hid ** -0.5).astype(np.float32)
+    X, Gz, Gy, gY = (q(rng.standard_normal((B, H, T, w)) * sc, "bf16")
+                     for w, sc in ((d, 1.0), (hid, 0.3), (o, 0.3), (o, 1.0)))
+    al, mu = W.gate_tokens(B, H, T, d, 13)
+    dev = lambda a, dt="bf16": to_dev(a, dt, torch)  # noqa: E731
+    args = (dev(W10, "f32"), dev(W20, "f32"), dev(X), dev(Gz), dev(Gy))
+    mud, ald = dev(mu * d, "f32"), dev(al, "f32")
+    Z, Hid, _ = gl.mlp_fwd(*args, mud, ald, act="gelu_tanh")
+    gz0, gx0, full = gl.mlp_reverse(*args, Z, Hid, dev(gY), mud, ald, act="gelu_tanh", grads=gl.MLP_GRADS)
+    gz1, _ = gl.mlp_reverse(*args, Z, Hid, dev(gY), mud, ald, act="gelu_tanh", with_gx=False)
+    np.testing.assert_array_equal(to_host(gz1), to_host(gz0))
+    for k in gl.MLP_GRADS:
+        _, _, part = gl.mlp_reverse(*args, Z, Hid, dev(gY), mud, ald, act="gelu_tanh", with_gx=False, grads=(k,))
+        np.testing.assert_array_equal(to_host(part[k]), to_host(full[k]), err_msg=k)
 
 
 def test_mlp_scans_reproduce_serial_ttt():

@@ -723,6 +723,55 @@ def test_mlp_with_unit_gates_is_two_scans():
                                rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("with_alpha", [False, True])
+def test_mlp_training_gradients_complex_step(with_alpha):
+    """The MLP's gate and slow-weight gradients with the writes detached
+    (Appendix E) against complex-step derivatives of
+    L = sum_t <g_y, y_t>, y_t = (W2_0 + Delta2_t) h_t, h = sigma(z_hat), where
+    Delta2 takes its write inputs from a fixed copy of h (the detached
+    writes) and z_hat is the first scan; resets included.  y is evaluated with
+    the explicit scan reads (reads of h, writes of the fixed copy)."""
+    rng = np.random.default_rng(64)
+    B, H, T, d, m, o = 2, 1, 9, 3, 4, 2
+    W10 = rng.standard_normal((H, m, d)) * 0.5
+    W20 = rng.standard_normal((H, o, m)) * 0.5
+    X, Gz, Gy = rng.standard_normal((B, H, T, d)), rng.standard_normal((B, H, T, m)), rng.standard_normal((B, H, T, o))
+    gy = rng.standard_normal((B, H, T, o))
+    mu = rng.uniform(0.3, 1.5, (B, H, T))
+    al = rng.uniform(0.3, 1.0, (B, H, T)) if with_alpha else None
+    rs = np.zeros((B, T), np.uint8)
+    rs[1, 4] = 1
+    hbar = orc.act(orc.scan_fwd(W10, X, Gz, mu / d, alpha=al, reset=rs), "tanh")
+
+    def loss(W10_, W20_, mu_, al_):
+        z = orc.scan_fwd(W10_, X, Gz, mu_ / d, alpha=al_, reset=rs)
+        y = orc.scan_reads(W20_, hbar, Gy, mu_ / m, A=orc.act(z, "tanh"), alpha=al_, reset=rs)["y"]
+        return np.sum(y * gy)
+
+    r = orc.mlp_reverse(W10, W20, X, Gz, Gy, al, mu, gy, kind="tanh", reset=rs)
+    h_ = 1e-30
+    params = {"W10": W10, "W20": W20, "mu": mu, "al": al}
+
+    def cs(name):
+        base = params[name]
+        g = np.zeros(base.shape)
+        for i in np.ndindex(base.shape):
+            p_ = dict(params)
+            v = base.astype(complex)
+            v[i] += 1j * h_
+            p_[name] = v
+            g[i] = np.imag(loss(p_["W10"], p_["W20"], p_["mu"], p_["al"])) / h_
+        return g
+
+    assert rel_err(r["dw10"], cs("W10")) < 1e-12
+    assert rel_err(r["dw20"], cs("W20")) < 1e-12
+    assert rel_err(r["dmu"], cs("mu")) < 1e-12
+    if with_alpha:
+        assert rel_err(r["dalpha"], cs("al")) < 1e-12
+    else:
+        assert "dalpha" not in r
+
+
 @pytest.mark.parametrize("kind", orc.ACTS)
 def test_activation_derivatives(kind):
     z = np.linspace(-4, 4, 41)
