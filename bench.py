@@ -43,7 +43,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 MFMA_FILE = os.path.join(ROOT, "profiles", "mfma.json")
 
 
-SECONDARY_NAMES = ("lm-bf16", "lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated",
+SECONDARY_NAMES = ("lm-bf16", "lm-bf16-reset", "lm-bf16-plain", "lm-bf16-cold", "long-bf16", "stack-bf16", "lm-bf16-gated",
                    "lm-bf16-gated-plain", "mlp-lm", "decode-mlp-lm", "decode-f32", "decode-f32-S2048",
                    "decode-f32-gated")
 
@@ -125,19 +125,27 @@ class ScanRunner:
     from that cache."""
     LAG = 2
 
-    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False, pipelined=False, share=None):
+    def __init__(self, gl, torch, W, wl, nsets, device, layer0=0, saved=False, pipelined=False, share=None,
+                 reset_mean=0):
         self.gl, self.torch, self.wl = gl, torch, wl
         if pipelined and nsets <= self.LAG:
             raise ValueError("a pipelined step needs more input sets than its lag")
         self.pipelined = pipelined
         self.sets = [W.device_scan_inputs(wl, layer0 + i, device, torch=torch) for i in range(nsets)]
+        # reset_mean > 0: the reset pair (unit retention, packed documents of
+        # geometric length with that mean; one flag set per input set).
+        self.resets = reset_mean > 0
+        if self.resets:
+            for i, st in enumerate(self.sets):
+                st["reset"] = torch.from_numpy(W.reset_flags(wl.B, wl.T, wl.seed + 12 + 2 * (layer0 + i),
+                                                             mean_len=reset_mean)).to(device)
         self.shape = gl.make_shape(wl.B, wl.H, wl.T, wl.d, wl.m,
                                    gl.BF16 if wl.dtype == "bf16" else gl.F32, chunk=wl.chunk)
         self.plan = gl.plan(self.shape)
         self.saved = None
         ws_bytes = self.plan.workspace_bytes
         if saved:
-            sv_bytes, ws_bytes = gl.saved_bytes(self.shape)
+            sv_bytes, ws_bytes = (gl.reset_saved_bytes if self.resets else gl.saved_bytes)(self.shape)
             # One saved-state buffer per set that can be between its forward and backward.
             self.saved_bufs = [torch.zeros(sv_bytes // 4, dtype=torch.float32, device=device)
                                for _ in range(nsets if pipelined else 1)]
@@ -159,7 +167,10 @@ class ScanRunner:
 
     def fwd(self, k):
         s = self.sets[k]
-        if self.saved is not None:
+        if self.resets:
+            self.gl.scan_fwd_reset_save(s["W0"], s["X"], s["G"], s["eta"], s["reset"], out=self.Y,
+                                        saved=self.saved_bufs[k % len(self.saved_bufs)], workspace=self.ws)
+        elif self.saved is not None:
             self.gl.scan_fwd_save(s["W0"], s["X"], s["G"], s["eta"], chunk=self.wl.chunk, out=self.Y,
                                   saved=self.saved_bufs[k % len(self.saved_bufs)], workspace=self.ws)
         else:
@@ -168,7 +179,10 @@ class ScanRunner:
 
     def bwd(self, k):
         s = self.sets[k]
-        if self.saved is not None:
+        if self.resets:
+            self.gl.scan_bwd_reset_saved(s["W0"], s["X"], s["G"], s["dY"], self.saved_bufs[k % len(self.saved_bufs)],
+                                         s["eta"], s["reset"], out=self.outs, workspace=self.ws)
+        elif self.saved is not None:
             self.gl.scan_bwd_saved(s["W0"], s["X"], s["G"], s["dY"], self.saved_bufs[k % len(self.saved_bufs)],
                                    s["eta"], chunk=self.wl.chunk, out=self.outs, workspace=self.ws)
         else:
@@ -593,14 +607,14 @@ def cpu_baseline(wl, min_seconds):
                                         f"{s1:.1f} s; {row}; scaled to all {L} layers"}}
 
 
-def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True):
+def secondary_scan(gl, torch, W, name, steps, warmup, device, saved=True, reset_mean=0):
     """One workload's fwd+bwd steps as one graph replay.  A single-layer
     workload runs the pipelined step (eight input sets; see ScanRunner); a
     layer stack runs every layer's forward, then every layer's backward in
     reverse order, as a model's training step does."""
     wl = W.SCAN_WORKLOADS[name]
     if wl.layers == 1:
-        run = ScanRunner(gl, torch, W, wl, 8, device, saved=saved, pipelined=True)
+        run = ScanRunner(gl, torch, W, wl, 8, device, saved=saved, pipelined=True, reset_mean=reset_mean)
         fn = run.step
         runs = [run]
     else:
@@ -875,6 +889,11 @@ def secondary_decode(gl, torch, W, device, S=None, steps=None, gated=False):
 def run_secondary(name, gl, torch, W, device):
     if name == "lm-bf16":  # the single-layer configuration, pipelined save-for-backward pair
         return secondary_scan(gl, torch, W, "lm-bf16", 200, 500, device)
+    if name == "lm-bf16-reset":  # unit retention with packed documents (mean 512): the reset pair
+        r = secondary_scan(gl, torch, W, "lm-bf16", 200, 500, device, reset_mean=512)
+        r["workload"] = ("lm-bf16 shape, unit retention, documents of geometric length (mean 512) packed per row; "
+                         "scan_fwd_reset_save + scan_bwd_reset_saved with every output, pipelined as lm-bf16")
+        return r
     if name == "lm-bf16-cold":
         return secondary_cold(gl, torch, W, device)
     if name == "lm-bf16-plain":  # the headline step without the saved segment states

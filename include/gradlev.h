@@ -224,6 +224,43 @@ int gradlev_scan_bwd_saved(const gradlev_shape* s, const float* W0, const void* 
                            float* dW0, void* workspace, size_t workspace_bytes,
                            void* stream);
 
+/* Save-for-backward pair with document resets, at unit retention (the
+ * paper's LM configuration: retention one, fast state reset at document and
+ * packed-row boundaries; Section 3, Eq. 2 holds within each reset segment;
+ * Appendix E).  A reset flag at token t starts a new document: t reads W_0
+ * plus the writes of its own document, and the backward's suffix of a token
+ * ends before the next document.  Results are those of the gated scans with
+ * alpha = 1 and the same flags (the tokens a reset overrides have dG = 0,
+ * deta = 0 and no write-side dX), computed by the unit-retention kernels:
+ * within a 64-token chunk a reset becomes masks (scores pair tokens of one
+ * document, rows after the chunk's first reset read W_0, only its last
+ * document's writes and reads cross the chunk boundary), and the forward
+ * stores the fast weights at the start of each chunk that holds a reset,
+ * where the backward cannot take writes back.
+ *   reset  [B, T] uint8 (0 or 1, shared by the heads of a batch row), or NULL
+ *          (no document starts); a flag at t = 0 changes nothing.
+ * Supported: d_in = d_out = 64, exclusive reads (GRADLEV_ERR_UNSUPPORTED
+ * otherwise; other widths use the gated pair).  The chunk hint is ignored
+ * (both directions use 64-token tiles); segment hints as for the plain pair.
+ * gradlev_scan_reset_saved_bytes: bytes of the saved state (segment-end
+ *   weights plus room for a state at every chunk start) and of the workspace
+ *   both calls need.  Other arguments, ownership and the saved buffer's
+ *   rules as in gradlev_scan_fwd_save / gradlev_scan_bwd_saved (dW0 is the
+ *   full sum_b sum_t dY_t X_t^T: every read sees W_0). */
+int gradlev_scan_reset_saved_bytes(const gradlev_shape* s, size_t* saved_bytes,
+                                   size_t* workspace_bytes);
+int gradlev_scan_fwd_reset_save(const gradlev_shape* s, const float* W0, const void* X,
+                                const void* G, const float* eta, float eta_scalar,
+                                const uint8_t* reset, float* Y, float* saved,
+                                size_t saved_bytes, void* workspace, size_t workspace_bytes,
+                                void* stream);
+int gradlev_scan_bwd_reset_saved(const gradlev_shape* s, const float* W0, const void* X,
+                                 const void* G, const float* eta, float eta_scalar,
+                                 const void* dY, const uint8_t* reset, const float* saved,
+                                 size_t saved_bytes, float* gtilde, float* dX, float* dG,
+                                 float* deta, float* dW0, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
 /* One deployment step for S sequences x H heads (Section 3, "Training
  * objective", last sentences; Appendix A, last sentence): score with the
  * current weights, then write the true costate.

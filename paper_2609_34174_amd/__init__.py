@@ -97,6 +97,12 @@ def lib():
         L.gradlev_scan_bwd_saved.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
                                              vp, f32p, ctypes.c_size_t, f32p, f32p, f32p, f32p, f32p,
                                              vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_reset_saved_bytes.argtypes = [ctypes.POINTER(Shape), szp, szp]
+        L.gradlev_scan_fwd_reset_save.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float, vp,
+                                                  f32p, f32p, ctypes.c_size_t, vp, ctypes.c_size_t, vp]
+        L.gradlev_scan_bwd_reset_saved.argtypes = [ctypes.POINTER(Shape), f32p, vp, vp, f32p, ctypes.c_float,
+                                                   vp, vp, f32p, ctypes.c_size_t, f32p, f32p, f32p, f32p, f32p,
+                                                   vp, ctypes.c_size_t, vp]
         gp = ctypes.POINTER(Gates)
         L.gradlev_scan_gated_workspace_bytes.argtypes = [ctypes.POINTER(Shape), ctypes.POINTER(ctypes.c_size_t)]
         L.gradlev_scan_fwd_gated.argtypes = [ctypes.POINTER(Shape), gp, f32p, vp, vp, f32p, ctypes.c_float,
@@ -124,6 +130,7 @@ def lib():
         for name in ("gradlev_scan_plan", "gradlev_scan_workspace_bytes", "gradlev_scan_fwd", "gradlev_scan_fwd_static",
                      "gradlev_scan_bwd", "gradlev_scan_saved_bytes", "gradlev_scan_fwd_save",
                      "gradlev_scan_bwd_saved", "gradlev_decode_step", "gradlev_scan_gated_workspace_bytes",
+                     "gradlev_scan_reset_saved_bytes", "gradlev_scan_fwd_reset_save", "gradlev_scan_bwd_reset_saved",
                      "gradlev_scan_fwd_gated", "gradlev_scan_bwd_gated", "gradlev_decode_step_gated",
                      "gradlev_scan_gated_saved_bytes", "gradlev_scan_fwd_gated_save", "gradlev_scan_bwd_gated_saved",
                      "gradlev_mlp_workspace_bytes", "gradlev_mlp_fwd", "gradlev_mlp_reverse",
@@ -376,6 +383,81 @@ def scan_bwd_saved(W0, X, G, dY, saved, eta=0.1, *, prefix="exclusive", chunk=0,
         raise GradLevError(rc, "gradlev_scan_bwd_saved")
     return res
 
+
+
+def reset_saved_bytes(shape: Shape):
+    """(saved-state bytes, workspace bytes) of the reset pair."""
+    sv, ws = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    rc = lib().gradlev_scan_reset_saved_bytes(ctypes.byref(shape), ctypes.byref(sv), ctypes.byref(ws))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_reset_saved_bytes")
+    return int(sv.value), int(ws.value)
+
+
+def _reset_arg(reset, B, T, X):
+    torch = _torch()
+    if reset is None:
+        return None
+    _check_dev("reset", reset, torch.uint8, (B, T))
+    if reset.device != X.device:
+        raise ValueError("reset must be on the same device as X")
+    return reset
+
+
+def scan_fwd_reset_save(W0, X, G, eta=0.1, reset=None, *, segment=0, out=None, saved=None, workspace=None):
+    """Forward of the reset pair (unit retention, document starts reset [B,T]
+    uint8); returns (Y, saved) for scan_bwd_reset_saved."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", 0, segment)
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    r = _reset_arg(reset, s.B, s.T, X)
+    sv_need, ws_need = reset_saved_bytes(s)
+    if out is None:
+        out = torch.empty(s.B, s.H, s.T, s.d_out, dtype=torch.float32, device=X.device)
+    _check_dev("out", out, torch.float32, (s.B, s.H, s.T, s.d_out))
+    if saved is None:
+        saved = torch.empty(sv_need // 4, dtype=torch.float32, device=X.device)
+    saved, svn = _bytes_of("saved", saved, sv_need)
+    if workspace is None and ws_need:
+        workspace = torch.empty(ws_need, dtype=torch.uint8, device=X.device)
+    ws, wsn = _bytes_of("workspace", workspace, ws_need)
+    rc = lib().gradlev_scan_fwd_reset_save(ctypes.byref(s), _ptr(W0), _ptr(X), _ptr(G), _ptr(e), es, _ptr(r),
+                                           _ptr(out), _ptr(saved), svn, _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_fwd_reset_save")
+    return out, saved
+
+
+def scan_bwd_reset_saved(W0, X, G, dY, saved, eta=0.1, reset=None, *, segment=0, outputs=BWD_OUTPUTS, out=None,
+                         workspace=None):
+    """Backward of the reset pair from the state scan_fwd_reset_save kept
+    (same inputs, flags and segment hint); returns the dict of scan_bwd."""
+    torch = _torch()
+    s = _scan_shape(W0, X, G, "exclusive", 0, segment)
+    _check_dev("dY", dY, X.dtype, (s.B, s.H, s.T, s.d_out))
+    e, es = _eta_args(eta, s.B, s.H, s.T, X)
+    r = _reset_arg(reset, s.B, s.T, X)
+    sv_need, ws_need = reset_saved_bytes(s)
+    saved, svn = _bytes_of("saved", saved, sv_need)
+    shapes = {"gtilde": (s.B, s.H, s.T, s.d_in), "dx": (s.B, s.H, s.T, s.d_in),
+              "dg": (s.B, s.H, s.T, s.d_out), "deta": (s.B, s.H, s.T), "dw0": (s.H, s.d_out, s.d_in)}
+    res = dict(out or {})
+    for k in outputs:
+        if k not in shapes:
+            raise ValueError(f"unknown output {k!r}")
+        if k not in res:
+            res[k] = torch.empty(shapes[k], dtype=torch.float32, device=X.device)
+        _check_dev(k, res[k], torch.float32, shapes[k])
+    if workspace is None and ws_need:
+        workspace = torch.empty(ws_need, dtype=torch.uint8, device=X.device)
+    ws, wsn = _bytes_of("workspace", workspace, ws_need)
+    rc = lib().gradlev_scan_bwd_reset_saved(ctypes.byref(s), _ptr(W0), _ptr(X), _ptr(G), _ptr(e), es, _ptr(dY),
+                                            _ptr(r), _ptr(saved), svn, _ptr(res.get("gtilde")), _ptr(res.get("dx")),
+                                            _ptr(res.get("dg")), _ptr(res.get("deta")), _ptr(res.get("dw0")),
+                                            _ptr(ws), wsn, _stream(X.device))
+    if rc != OK:
+        raise GradLevError(rc, "gradlev_scan_bwd_reset_saved")
+    return res
 
 def decode_step(W, x, g, eta=0.1, *, out=None):
     """One deployment step: returns y = W x and updates W <- W - eta g x^T in place."""

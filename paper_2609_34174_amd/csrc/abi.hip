@@ -144,6 +144,43 @@ int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
   return GRADLEV_OK;
 }
 
+// The save-for-backward pair with document resets at unit retention: the
+// saved plan at 64-token tiles for both directions (the backward restarts its
+// un-write at the forward's chunk-start states, so the two share the tile).
+// Saved: segment-end weights [BH][nseg_b][m][d], then the chunk-start states
+// [BH][ceil(T/64)][m][d] (written only for chunks that hold a reset).
+// Workspace: forward aggregates [BH][nseg_f][m][d]; backward pre-reset and
+// full dY x^T aggregates [BH][nseg_b][d][m] each.
+struct ResetPlan {
+  Plan p;
+  size_t off_cstate, saved_bytes;
+  size_t off_aggF, ws;
+};
+
+int make_reset_plan(const gradlev_shape* s, ResetPlan* out) {
+  if (!s) return GRADLEV_ERR_INVALID;
+  if (s->B < 1 || s->H < 1 || s->T < 1 || s->d_in < 1 || s->d_out < 1) return GRADLEV_ERR_INVALID;
+  if (s->d_in != 64 || s->d_out != 64 || s->prefix != GRADLEV_EXCLUSIVE) return GRADLEV_ERR_UNSUPPORTED;
+  gradlev_shape s64 = *s;
+  s64.chunk = 64;
+  size_t sv = 0;
+  const int rc = make_saved_plan(&s64, &out->p, &sv);
+  if (rc != GRADLEV_OK) return rc;
+  if (out->p.fwd.chunk != 64 || out->p.bwd.chunk != 64) return GRADLEV_ERR_UNSUPPORTED;
+  const int64_t BH = s->B * s->H;
+  const size_t md = (size_t)64 * 64 * sizeof(float);
+  // One sequence's chunk-start states stay under 2 GiB (32-bit offsets).
+  const int64_t nch = (s->T + 63) / 64;
+  if (nch > ((int64_t(1) << 31) - 1) / (int64_t)md) return GRADLEV_ERR_UNSUPPORTED;
+  out->off_cstate = round_up(sv, 256);
+  out->saved_bytes = out->off_cstate + (size_t)BH * nch * md;
+  const size_t agg_f = out->p.fwd.nseg > 1 ? round_up((size_t)BH * out->p.fwd.nseg * md, 256) : 0;
+  const size_t agg_b = round_up((size_t)BH * out->p.bwd.nseg * md, 256);
+  out->off_aggF = agg_b;
+  out->ws = agg_f > 2 * agg_b ? agg_f : 2 * agg_b;
+  return GRADLEV_OK;
+}
+
 // Wide maps: widths that are multiples of 128 with one of them above 128 run
 // the parallel form (scan_wide.hip).  Its workspace holds the gate prefixes
 // and the causal score matrix, B*H*Tp*Tp*4 bytes, so the sequence length is
@@ -617,6 +654,85 @@ int gradlev_scan_bwd_saved(const gradlev_shape* s, const float* W0, const void* 
   if (saved_bytes < need) return GRADLEV_ERR_WORKSPACE;
   return scan_bwd_planned(p, W0, X, G, eta, eta_scalar, dY, saved, gtilde, dX, dG, deta, dW0, workspace,
                           workspace_bytes, stream);
+}
+
+int gradlev_scan_reset_saved_bytes(const gradlev_shape* s, size_t* saved_bytes, size_t* workspace_bytes) {
+  if (!saved_bytes || !workspace_bytes) return GRADLEV_ERR_INVALID;
+  ResetPlan r;
+  const int rc = make_reset_plan(s, &r);
+  if (rc != GRADLEV_OK) return rc;
+  *saved_bytes = r.saved_bytes;
+  *workspace_bytes = r.ws;
+  return GRADLEV_OK;
+}
+
+int gradlev_scan_fwd_reset_save(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                                const float* eta, float eta_scalar, const uint8_t* reset, float* Y, float* saved,
+                                size_t saved_bytes, void* workspace, size_t workspace_bytes, void* stream) {
+  ResetPlan r;
+  int rc = make_reset_plan(s, &r);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !Y || !saved) return GRADLEV_ERR_INVALID;
+  if (!aligned16(W0) || !aligned16(X) || !aligned16(G) || !aligned16(Y) || !aligned16(saved) ||
+      (eta && !aligned16(eta)))
+    return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < r.saved_bytes) return GRADLEV_ERR_WORKSPACE;
+  rc = check_workspace(workspace, workspace_bytes, r.ws);
+  if (rc != GRADLEV_OK) return rc;
+  FwdPtrs f{};
+  f.W0 = W0;
+  f.X = X;
+  f.G = G;
+  f.eta = eta;
+  f.eta_scalar = eta_scalar;
+  f.Y = Y;
+  f.agg = static_cast<float*>(workspace);
+  f.wend = saved;
+  f.save_len = r.p.save_len;
+  f.nsave = r.p.bwd.nseg;
+  f.reset = reset;
+  f.cstate = reinterpret_cast<float*>(reinterpret_cast<char*>(saved) + r.off_cstate);
+  f.resets = true;
+  const hipError_t e = launch_scan_fwd(r.p.fwd, f, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
+}
+
+int gradlev_scan_bwd_reset_saved(const gradlev_shape* s, const float* W0, const void* X, const void* G,
+                                 const float* eta, float eta_scalar, const void* dY, const uint8_t* reset,
+                                 const float* saved, size_t saved_bytes, float* gtilde, float* dX, float* dG,
+                                 float* deta, float* dW0, void* workspace, size_t workspace_bytes, void* stream) {
+  ResetPlan r;
+  int rc = make_reset_plan(s, &r);
+  if (rc != GRADLEV_OK) return rc;
+  if (!W0 || !X || !G || !dY || !saved) return GRADLEV_ERR_INVALID;
+  if (!gtilde && !dX && !dG && !deta && !dW0) return GRADLEV_ERR_INVALID;
+  const void* ptrs[] = {W0, X, G, dY, eta, saved, gtilde, dX, dG, deta, dW0};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GRADLEV_ERR_ALIGN;
+  if (saved_bytes < r.saved_bytes) return GRADLEV_ERR_WORKSPACE;
+  rc = check_workspace(workspace, workspace_bytes, r.ws);
+  if (rc != GRADLEV_OK) return rc;
+  char* ws = static_cast<char*>(workspace);
+  BwdPtrs b{};
+  b.W0 = W0;
+  b.X = X;
+  b.G = G;
+  b.eta = eta;
+  b.eta_scalar = eta_scalar;
+  b.dY = dY;
+  b.gtilde = gtilde;
+  b.dX = dX;
+  b.dG = dG;
+  b.deta = deta;
+  b.dW0 = dW0;
+  b.aggB = reinterpret_cast<float*>(ws);
+  b.aggF = reinterpret_cast<float*>(ws + r.off_aggF);
+  b.wend = saved;
+  b.reset = reset;
+  b.cstate = reinterpret_cast<const float*>(reinterpret_cast<const char*>(saved) + r.off_cstate);
+  b.resets = true;
+  const hipError_t e = launch_scan_bwd(r.p.bwd, b, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }
 
 int gradlev_scan_gated_workspace_bytes(const gradlev_shape* s, size_t* bytes) {

@@ -27,6 +27,9 @@ struct FwdPtrs {
   float* agg;   // [B*H][nseg][m][d] workspace, or nullptr when nseg == 1
   float* wend;  // [B*H][nsave][m][d] weights after each save_len-token block (for a backward), or nullptr
   int64_t save_len, nsave;  // the backward's segment length and count (a multiple of the chunk)
+  const uint8_t* reset;     // [B][T] document starts (unit retention with resets), or nullptr
+  float* cstate;            // with resets: [B*H][ceil(T/64)][m][d] chunk-start states of reset chunks
+  bool resets;              // run the reset kernels (reset may still be nullptr: no document starts)
 };
 
 struct BwdPtrs {
@@ -45,6 +48,10 @@ struct BwdPtrs {
   float* aggB;   // [B*H][nseg][d][m]: segment dY x^T aggregates (transposed)
   float* rfin;  // [B*H][m][d]: full-sequence sum of dY x^T per sequence
   const float* wend;  // the forward's saved segment-end weights (same segments), or nullptr
+  const uint8_t* reset;  // document starts, with `resets`
+  const float* cstate;   // the forward's chunk-start states of reset chunks, with `resets`
+  float* aggF;           // with resets: [B*H][nseg][d][m] full dY x^T per segment (for dW0)
+  bool resets;
 };
 
 // Gated scans (retention and resets).  Workspace: segment aggregates

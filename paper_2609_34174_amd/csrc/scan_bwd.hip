@@ -41,6 +41,8 @@ struct BArgs {
   const float* aggB;  // [BH][nseg][d][m]: per-segment dY x^T aggregates B_k (k >= 1), or null
   float* rfin;        // [BH][m][d]: full-sequence dY x^T (written by segment 0), or null
   const float* wend;  // [BH][nseg][m][d]: the forward's segment-end weights, or null (then W_0 - sum A)
+  const uint8_t* reset;  // [B][T] document starts (RST kernels)
+  const float* cstate;   // [BH][ceil(T/C)][m][d]: chunk-start states of the chunks holding a reset
 };
 
 // Output modes compiled separately so that no accumulator crosses a runtime
@@ -60,7 +62,14 @@ static constexpr bool s_shared_fits(bool bf16, int d, int m, int C, bool etav) {
   return lds_bytes_bwd(bf16, d, m, C, etav) + (bf16 ? 2 : 1) * C * C * (bf16 ? 2 : 4) <= 160 * 1024;
 }
 
-template <class OP, int D, int M, int C, bool INCL, bool ETAV, int OUT>
+// RST (document resets at unit retention, with the forward's saved states;
+// exclusive reads, 64 x 64 maps, 64-token chunks): intra-chunk tiles pair
+// tokens of one document; a chunk holding a reset takes its start state from
+// cstate (writes before a reset cannot be taken back), its rows at or after
+// the first reset read W_0, only its last document's tokens see the suffix
+// R_n, and the suffix passed to the previous chunk keeps the tokens before
+// the first reset only.
+template <class OP, int D, int M, int C, bool INCL, bool ETAV, int OUT, bool RST = false>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64, 128 / cmax(D, M))
 bwd_main_kernel(const BArgs a) {
   typedef typename OP::elem E;
@@ -94,6 +103,8 @@ bwd_main_kernel(const BArgs a) {
   __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
   __shared__ float et[C];
   __shared__ float dpart[PAIR ? 2 : IB][C];
+  static_assert(!RST || (C == 64 && D == 64 && M == 64 && !INCL), "resets: exclusive 64 x 64 maps, 64-token chunks");
+  __shared__ int red[1];
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg)) return;
@@ -124,18 +135,31 @@ bwd_main_kernel(const BArgs a) {
   Tile4<OP, C, D, NT> xa, xb;
   Tile4<OP, C, M, NT> ga, gb, da, db;
   EtaReg<ETAV> ea, eb;
+  RstReg<RST> ra, rb;
   const rsrc_t Et = eta_rsrc(a.eta, bh, T);
+  const rsrc_t Rrow = reset_rsrc(RST ? a.reset : nullptr, bh / a.H, T);
   typedef Tile4<OP, C, D, NT> TX;
   typedef Tile4<OP, C, M, NT> TM;
-  auto fetch = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
+  auto fetch = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, RstReg<RST>& rr, int64_t n) {
     const int64_t t0 = t_begin + n * C;
     er.load(Et, n >= 0 ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    rr.load(Rrow, t0, n >= 0, tid, C);
     xr.load(X, n >= 0 ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
     gr.load(G, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
     dr.load(Dy, n >= 0 ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
-  fetch(xa, ga, da, ea, nch - 1);
-  if (DEPTH == 2) fetch(xb, gb, db, eb, nch - 2);
+  // With resets the suffix at the segment end holds the dY x^T of the tokens
+  // up to the next document start: none if it is t_end itself, else the
+  // (pre-reset) aggregates up to that document start's segment.
+  fetch(xa, ga, da, ea, ra, nch - 1);
+  if (DEPTH == 2) fetch(xb, gb, db, eb, rb, nch - 2);
+  int64_t j_last = a.nseg - 1;
+  bool no_sfx = false;
+  if constexpr (RST) {
+    const int64_t fr = first_reset_in<NT>(Rrow, t_end, T, tid, red);
+    if (fr == t_end) no_sfx = true;
+    else if (fr > 0) j_last = fr / a.seg_len;
+  }
 
   // Column-block state (wave w < JB): Wj[e][ib] holds W[i = 16ib + 4q + r][j = 16 blk(e) + c]
   // and Rj[ib] holds R[i][j = 16w + c], at the segment's end: W_0 - sum_{j<=seg} A_j
@@ -170,8 +194,8 @@ bwd_main_kernel(const BArgs a) {
     const int64_t o = bh * a.nseg * M * D + (int64_t)(16 * w + c) * M + 4 * q;
 #pragma unroll
     for (int ib = 0; ib < IB; ++ib) Rj[ib] = zero4();
-    if (FULL && a.aggB) {
-      for (int64_t j0 = a.nseg - 1; j0 > seg; j0 -= PU) {
+    if (FULL && a.aggB && !no_sfx) {
+      for (int64_t j0 = j_last; j0 > seg; j0 -= PU) {
         f32x4 v[PU][IB];
 #pragma unroll
         for (int u = 0; u < PU; ++u)
@@ -193,7 +217,7 @@ bwd_main_kernel(const BArgs a) {
       for (int i = tid; i < C * C; i += NT) Sl[i] = (E)0.f;
   }
 
-  auto chunk = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, int64_t n) {
+  auto chunk = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, RstReg<RST>& rr, int64_t n) {
     // A step before the segment start (the second of a pair) sees zero
     // tiles, leaves W and R unchanged and stores nothing.
     // Lane and thread indices as the chunk sees them: opaque to the compiler,
@@ -212,8 +236,30 @@ bwd_main_kernel(const BArgs a) {
     gr.store(Gs, td);
     dr.store(Ds, td);
     __syncthreads();
+    // Reset masks of this chunk (fr = C, lr = -1 without a reset).
+    const uint64_t dm = rr.mask();
+    const int fr = first_flag(dm), lr = last_flag(dm);
+    const bool has = RST && lr >= 0 && live;
     if (ETAV) gr.store_scaled(Vh, Vl, td, et);  // read after the next barrier
-    fetch(xr, gr, dr, er, n - DEPTH);
+    fetch(xr, gr, dr, er, rr, n - DEPTH);
+    // The chunk's compute, compiled with the reset masks (HAS) for the chunks
+    // that hold a reset and without them for the others.
+    auto compute = [&](auto hc) {
+    constexpr bool HAS = decltype(hc)::value;
+    // A chunk holding a reset starts from the forward's saved state, not from
+    // the un-write: loaded here into the state registers (unused until the
+    // un-write step), so the loads overlap the score-tile phase.
+    if constexpr (HAS) {
+      if (w < JB) {
+        const float* cs = a.cstate + (bh * ((T + C - 1) / C) + t0 / C) * M * D;
+#pragma unroll
+        for (int e = 0; e < NWB; ++e)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) Wj[e][ib][r] = cs[(int64_t)(16 * ib + 4 * q + r) * D + 16 * blk(e) + c];
+      }
+    }
 
     // (1) Intra-chunk tiles E[t][s], shared through LDS, and R_n^T (split).
 #pragma unroll
@@ -231,7 +277,8 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int s = 16 * sb + 4 * q + r;
-        const bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
+        bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
+        if constexpr (HAS) keep = keep && same_doc(dm, s, t);
         acc[r] = keep ? acc[r] * et[s] : 0.f;
       }
       OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
@@ -252,7 +299,9 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int s = 16 * sb + 4 * q + r;
-          if (!(tb > sb || (INCL ? (t >= s) : (t > s)))) st[r] = 0.f;
+          bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
+          if constexpr (HAS) keep = keep && same_doc(dm, s, t);
+          if (!keep) st[r] = 0.f;
         }
         const int o = lds_off(t, 16 * sb + 4 * q, C);
         OP::store4_split(Sh + o, Sl + o, st);
@@ -277,8 +326,9 @@ bwd_main_kernel(const BArgs a) {
         for (int kb = 0; kb < C / 32; ++kb) xt[e][kb] = OP::load_t(Xs, D, 32 * kb, 16 * blk(e), ln);
     }
 
-    // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X.
-    if (w < JB) {
+    // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X (a chunk holding a
+    // reset already holds W_n, loaded above).
+    if (!HAS && w < JB) {
       if constexpr (ETAV) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
@@ -346,13 +396,41 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
         for (int hh = 0; hh < TBW; ++hh) {
           const int tb = tok3(hh);
-          const F dq = OP::load_n(Ds, M, 16 * tb, 32 * kb, ln);
+          F dq = OP::load_n(Ds, M, 16 * tb, 32 * kb, ln);
           F gq;
           if (FULL) gq = OP::load_n(Gs, M, 16 * tb, 32 * kb, ln);
+          if constexpr (HAS) {
+            dq = keep_row<OP>(dq, 16 * tb + c < fr);  // rows after the first reset read W_0 (below)
+            if (FULL) gq = keep_row<OP>(gq, 16 * tb + c >= lr);  // only the last document sees R_n
+          }
 #pragma unroll
           for (int e = 0; e < NWB; ++e) {
             ga[e][hh] = mma_split_a<OP>(ga[e][hh], wh[e], wl[e], dq);
             if (FULL) xa2[e][hh] = mma_split_a<OP>(xa2[e][hh], rh[e], rl[e], gq);
+          }
+        }
+      }
+      if constexpr (HAS) {
+        {
+          const float* w0 = a.W0 + (bh % a.H) * M * D;
+#pragma unroll
+          for (int kb = 0; kb < M / 32; ++kb) {
+            F wh[NWB], wl[NWB];
+#pragma unroll
+            for (int e = 0; e < NWB; ++e) {
+              f32x8 v;
+#pragma unroll
+              for (int r = 0; r < 8; ++r)
+                v[r] = w0[(int64_t)(32 * kb + 16 * (r >> 2) + 4 * q + (r & 3)) * D + 16 * blk(e) + c];
+              OP::split(v, wh[e], wl[e]);
+            }
+#pragma unroll
+            for (int hh = 0; hh < TBW; ++hh) {
+              const int tb = tok3(hh);
+              const F dq = keep_row<OP>(OP::load_n(Ds, M, 16 * tb, 32 * kb, ln), 16 * tb + c >= fr);
+#pragma unroll
+              for (int e = 0; e < NWB; ++e) ga[e][hh] = mma_split_a<OP>(ga[e][hh], wh[e], wl[e], dq);
+            }
           }
         }
       }
@@ -442,7 +520,8 @@ bwd_main_kernel(const BArgs a) {
           }
 #pragma unroll
           for (int hh = 0; hh < TBW; ++hh) {
-            const F xq = xrow(tok4(hh), kb);
+            F xq = xrow(tok4(hh), kb);
+            if constexpr (HAS) xq = keep_row<OP>(xq, 16 * tok4(hh) + c >= lr);  // only the last document sees R_n
 #pragma unroll
             for (int e = 0; e < NWB; ++e) ua[e][hh] = mma_split_a<OP>(ua[e][hh], rh[e], rl[e], xq);
           }
@@ -494,6 +573,11 @@ bwd_main_kernel(const BArgs a) {
                     if (!(INCL ? (t >= c) : (t > c))) st[r] = 0.f;
                   }
                 }
+                if constexpr (HAS) {
+#pragma unroll
+                  for (int r = 0; r < 4; ++r)
+                    if (!same_doc(dm, 16 * tb + 4 * q + r, 16 * sb + c)) st[r] = 0.f;
+                }
               }
 #pragma unroll
               for (int r = 0; r < 4; ++r) sv[4 * h2 + r] = st[r];
@@ -542,11 +626,19 @@ bwd_main_kernel(const BArgs a) {
     if constexpr (FULL) {
       // (5) Suffix update: R_{n-1} = R_n + dY^T X (exact products).
       if (w < JB) {
+        // With a reset the previous chunk's document ends at the first reset:
+        // the suffix restarts from the tokens before it.
+        if (HAS)
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib) Rj[ib] = zero4();
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
-          for (int ib = 0; ib < IB; ++ib)
-            Rj[ib] = OP::mma(Rj[ib], OP::load_t(Ds, M, 32 * kb, 16 * ib, ln), xt[PAIR ? H : 0][kb]);
+          for (int ib = 0; ib < IB; ++ib) {
+            F dsf = OP::load_t(Ds, M, 32 * kb, 16 * ib, ln);
+            if constexpr (HAS) dsf = mask_k<OP>(dsf, 32 * kb, q, 0, fr);
+            Rj[ib] = OP::mma(Rj[ib], dsf, xt[PAIR ? H : 0][kb]);
+          }
         }
       }
     }
@@ -564,15 +656,18 @@ bwd_main_kernel(const BArgs a) {
         buf_store1(Oec, td < C ? (uint32_t)((t0 + td) * 4) : kOOB, s);
       }
     }
+      };
+    if (RST && has) compute(IntC<RST ? 1 : 0>{});
+    else compute(IntC<0>{});
   };
 
   if constexpr (DEPTH == 2) {
     for (int64_t n = nch - 1; n >= 0; n -= 2) {
-      chunk(xa, ga, da, ea, n);
-      chunk(xb, gb, db, eb, n - 1);
+      chunk(xa, ga, da, ea, ra, n);
+      chunk(xb, gb, db, eb, rb, n - 1);
     }
   } else {
-    for (int64_t n = nch - 1; n >= 0; --n) chunk(xa, ga, da, ea, n);
+    for (int64_t n = nch - 1; n >= 0; --n) chunk(xa, ga, da, ea, ra, n);
   }
 
   // Segment 0 ends holding the sum over the whole sequence of dY x^T.
@@ -960,6 +1055,41 @@ reduce_dw0_kernel(const float* rfin, float* dW0, int64_t B, int64_t H, int64_t m
   reinterpret_cast<f32x4*>(dW0)[h * md4 + e] = s;
 }
 
+// With resets: dW0[h][i][j] = sum_b sum_k aggF[b, h, k][j][i] (the full
+// dY x^T of every segment, transposed), in a fixed order.  Four threads per
+// (h, j, 4 consecutive i) each sum a quarter of the (b, k) terms, eight
+// 16-byte reads in flight, and the quarters are added in order through LDS.
+static __global__ void __launch_bounds__(256)
+reduce_dw0_segs_kernel(const float* aggF, float* dW0, int64_t B, int64_t H, int64_t nseg, int D, int M) {
+  __shared__ f32x4 part[4][64];
+  const int M4 = M / 4;
+  const int64_t g = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const int quarter = threadIdx.x >> 6;
+  const bool ok = g < H * (int64_t)D * M4;
+  const int64_t h = ok ? g / ((int64_t)D * M4) : 0, j = g / M4 % D, i = 4 * (g % M4);
+  const int64_t n = B * nseg, md = (int64_t)M * D, per = (n + 3) / 4;
+  const int64_t k0 = quarter * per, k1 = k0 + per < n ? k0 + per : n;
+  const float* p = aggF + j * M + i;
+  f32x4 s = zero4();
+  for (int64_t u0 = k0; ok && u0 < k1; u0 += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t k = u0 + u, b = k / nseg, sg = k % nseg;
+      v[u] = k < k1 ? *reinterpret_cast<const f32x4*>(p + ((b * H + h) * nseg + sg) * md) : zero4();
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  part[quarter][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (quarter == 0 && ok) {
+    const f32x4 t = ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dW0[(h * M + i + r) * D + j] = t[r];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
@@ -1009,6 +1139,58 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   k.nseg = p.nseg;
   k.aggA = f.aggA;
   k.aggB = f.aggB;
+  k.reset = f.reset;
+  k.aggF = f.aggF;
+  if (f.resets) {
+    // Document resets at unit retention (the saved pair; exclusive 64 x 64
+    // maps, 64-token chunks): pre-reset suffix aggregates and full per-segment
+    // sums for dW0, then the reset kernel.
+    if constexpr (D == 64 && M == 64 && C == 64) {
+      if (p.inclusive || !f.wend || !f.cstate) return hipErrorInvalidValue;
+      if (!read_only) {
+        timing_begin(GRADLEV_K_BWD_AGG, s);
+        hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggBwdB, ETAV, true>), dim3(grid), dim3(NT), 0, s, k, p.nseg);
+        timing_end(GRADLEV_K_BWD_AGG, s);
+      }
+      BArgs b{};
+      b.W0 = f.W0;
+      b.X = f.X;
+      b.G = f.G;
+      b.dY = f.dY;
+      b.eta = f.eta;
+      b.eta_scalar = f.eta_scalar;
+      b.BH = BH;
+      b.H = p.H;
+      b.T = p.T;
+      b.seg_len = p.seg_len;
+      b.nseg = p.nseg;
+      b.gtilde = f.gtilde;
+      b.dX = f.dX;
+      b.dG = f.dG;
+      b.deta = f.deta;
+      b.aggB = need_sfx ? f.aggB : nullptr;
+      b.rfin = nullptr;
+      b.wend = f.wend;
+      b.reset = f.reset;
+      b.cstate = f.cstate;
+      timing_begin(GRADLEV_K_BWD_MAIN, s);
+      if (read_only)
+        hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutRead, true>), dim3(grid), dim3(NT), 0, s, b);
+      else
+        hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutFull, true>), dim3(grid), dim3(NT), 0, s, b);
+      timing_end(GRADLEV_K_BWD_MAIN, s);
+      if (f.dW0) {
+        const int64_t n = p.H * (int64_t)D * M / 4;
+        timing_begin(GRADLEV_K_BWD_DW0, s);
+        hipLaunchKernelGGL(reduce_dw0_segs_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, s, f.aggF, f.dW0,
+                           p.B, p.H, p.nseg, D, M);
+        timing_end(GRADLEV_K_BWD_DW0, s);
+      }
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   // Segment aggregates (writes, and dY x^T when a suffix is needed); each
   // workgroup of the main kernel sums the ones it needs in its prologue.
   // With the forward's saved segment-end weights only the dY x^T aggregates

@@ -22,6 +22,14 @@ struct KArgs {
   float* aggB;   // bwd: [BH][nseg][d][m] transposed dY x^T aggregates B_k (k >= 1)
   float* wend;   // fwd, or null: [BH][nsave][m][d] fast weights after each save_len-token block
   int64_t save_len, nsave;
+  // Document resets (unit retention): reset [B][T] uint8, 1 where a document
+  // starts.  cstate [BH][ceil(T/C)][m][d]: the forward stores the state at the
+  // start of every chunk holding a reset there.  aggF [BH][nseg][d][m]: the
+  // backward's full dY x^T per segment (for dW0; aggB then holds the part
+  // before the segment's first reset).
+  const uint8_t* reset;
+  float* cstate;
+  float* aggF;
 };
 
 // ---------------------------------------------------------------------------
@@ -178,6 +186,125 @@ __device__ __forceinline__ rsrc_t eta_rsrc(const float* eta, int64_t bh, int64_t
 }
 
 // ---------------------------------------------------------------------------
+// Document resets at unit retention.  A reset at token t (t > 0) starts a new
+// document: t's read sees W_0 plus the writes of its own document only
+// (Section 3: Eq. 2 holds within each reset segment).  Within one chunk of
+// C = 64 tokens this is a set of masks, all taken from the chunk's 64-bit
+// flag mask m (bit p: a document starts at chunk position p):
+//   same_doc(s, t)  no flag in (min, max] of the two positions
+//   fr              first flagged position (C if none): rows p < fr read the
+//                   carried state, rows p >= fr read W_0 (and their document)
+//   lr              last flagged position (-1 if none): only writes at
+//                   p >= lr reach the next chunk, which starts from W_0.
+// Every wave loads the chunk's flags (lane p: position p, with the chunk's
+// tiles; a buffer load, so past the sequence end it reads 0) and forms m with
+// a ballot, so no wave waits for another.  A flag at t = 0 has no earlier
+// write to drop and is ignored.
+// ---------------------------------------------------------------------------
+template <bool RST>
+struct RstReg {
+  int v;
+  __device__ __forceinline__ void load(rsrc_t row, int64_t t0, bool ok, int tid, int C) {
+    v = 0;
+    if constexpr (RST) {
+      const int lane = tid & 63;
+      const int64_t t = t0 + lane;
+      v = __builtin_amdgcn_raw_buffer_load_b8(row, (ok && lane < C && t > 0) ? (int)t : (int)kOOB, 0, 0);
+    }
+  }
+  // The chunk's flag mask (wave-uniform).
+  __device__ __forceinline__ uint64_t mask() const {
+    if constexpr (RST) return __ballot(v != 0);
+    return 0;
+  }
+};
+
+__device__ __forceinline__ rsrc_t reset_rsrc(const uint8_t* reset, int64_t b, int64_t T) {
+  return make_rsrc(reset ? reset + b * T : nullptr, reset ? (uint32_t)T : 0u);
+}
+
+// Positions s and t (0..63) of one chunk lie in the same document.
+__device__ __forceinline__ bool same_doc(uint64_t m, int s, int t) {
+  const int lo = s < t ? s : t, hi = s < t ? t : s;
+  const uint64_t upto_hi = hi >= 63 ? ~0ull : ((2ull << hi) - 1);
+  const uint64_t upto_lo = (2ull << lo) - 1;
+  return (m & upto_hi & ~upto_lo) == 0;
+}
+__device__ __forceinline__ int first_flag(uint64_t m) { return m ? __builtin_ctzll(m) : 64; }
+__device__ __forceinline__ int last_flag(uint64_t m) { return m ? 63 - __builtin_clzll(m) : -1; }
+
+// A fragment with the elements whose k (k0 + slot_k(e, q)) lies outside
+// [lo, hi) set to zero: for operands read with k along the tile rows.
+template <class OP>
+__device__ __forceinline__ typename OP::frag mask_k(typename OP::frag f, int k0, int q, int lo, int hi) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int k = k0 + slot_k(e, q);
+    if (k < lo || k >= hi) f[e] = (typename OP::elem)0.f;
+  }
+  return f;
+}
+// A row fragment (row = row0 + lane % 16) kept or zeroed as a whole.
+template <class OP>
+__device__ __forceinline__ typename OP::frag keep_row(typename OP::frag f, bool keep) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (!keep) f[e] = (typename OP::elem)0.f;
+  return f;
+}
+
+// Last document start in (lo, hi], or the first in [lo, hi) (-1 if none;
+// t = 0 never counts), over one sequence's reset flags, by the whole
+// workgroup: blocks of 16 NT tokens (16 independent byte loads per thread,
+// each through the row's resource, so nothing past the row is read) from the
+// end nearest the segment, stopping at the first block that holds a reset.
+// Every thread returns the same value.
+template <int NT>
+__device__ __forceinline__ int64_t last_reset_in(rsrc_t row, int64_t lo, int64_t hi, int tid, int* red) {
+  constexpr int SPAN = 16 * NT;
+  for (int64_t top = hi; top > lo; top -= SPAN) {
+    int best = -1;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int64_t t = top - (int64_t)u * NT - tid;
+      const bool in = t > lo && t >= 1;
+      const int f = __builtin_amdgcn_raw_buffer_load_b8(row, in ? (int)t : (int)kOOB, 0, 0);
+      if (in && f && (int)t > best) best = (int)t;
+    }
+    __syncthreads();
+    if (tid == 0) red[0] = -1;
+    __syncthreads();
+    if (best >= 0) atomicMax(red, best);
+    __syncthreads();
+    const int r = red[0];
+    if (r >= 0) return r;
+  }
+  return -1;
+}
+template <int NT>
+__device__ __forceinline__ int64_t first_reset_in(rsrc_t row, int64_t lo, int64_t hi, int tid, int* red) {
+  constexpr int SPAN = 16 * NT;
+  for (int64_t base = lo; base < hi; base += SPAN) {
+    int best = 0x7fffffff;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int64_t t = base + (int64_t)u * NT + tid;
+      const bool in = t < hi && t >= 1;
+      const int f = __builtin_amdgcn_raw_buffer_load_b8(row, in ? (int)t : (int)kOOB, 0, 0);
+      if (in && f && (int)t < best) best = (int)t;
+    }
+    __syncthreads();
+    if (tid == 0) red[0] = 0x7fffffff;
+    __syncthreads();
+    if (best != 0x7fffffff) atomicMin(red, best);
+    __syncthreads();
+    const int r = red[0];
+    if (r != 0x7fffffff) return r;
+  }
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
 // Segment aggregates: A_k = sum_{t in seg k} eta_t g_t x_t^T (fp32) and, for
 // the backward (mode kAggBwdAB), B_k = sum_{t in seg k} dY_t x_t^T for k >= 1.
 // Forward: A row-major [m][d].  Backward: A and B transposed [d][m] (its waves
@@ -190,7 +317,12 @@ __device__ __forceinline__ rsrc_t eta_rsrc(const float* eta, int64_t bh, int64_t
 // starts from the forward's saved segment-end weights and needs no A_k.
 enum AggMode { kAggFwd = 0, kAggBwdA = 1, kAggBwdAB = 2, kAggBwdB = 3 };
 
-template <class OP, int D, int M, int C, int MODE, bool ETAV>
+// With document resets (RST, modes kAggFwd and kAggBwdB): the forward's A_k
+// keeps only the writes at or after the segment's last reset (the ones that
+// reach the next segment); the backward's B_k keeps the tokens before the
+// segment's first reset (the ones a read in an earlier segment's document
+// sees), and aggF takes the full sum of every segment for dW0.
+template <class OP, int D, int M, int C, int MODE, bool ETAV, bool RST = false>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64)
 agg_kernel(const KArgs a, int64_t nagg) {
   typedef typename OP::elem E;
@@ -206,22 +338,27 @@ agg_kernel(const KArgs a, int64_t nagg) {
   __shared__ E Gl[SPLITV ? C * M : 1];    // eta G lo
   __shared__ E Ds[BWD ? C * M : 1];
   __shared__ float et[C];
+  __shared__ int red[1];
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg) || seg >= nagg) return;
-  if (!WA && seg == 0) return;  // B_0 is never needed
+  if (!WA && !RST && seg == 0) return;  // B_0 is never needed (with resets, its full sum is)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, c = lane & 15, q = lane >> 4;
   const int64_t T = a.T;
   const int64_t t_begin = seg * a.seg_len;
   const int64_t t_end = t_begin + a.seg_len < T ? t_begin + a.seg_len : T;
-  const bool with_b = BWD && seg >= 1;
+  const bool with_b = BWD && (seg >= 1 || RST);
+
   const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
   const rsrc_t G = make_rsrc(WA ? static_cast<const E*>(a.G) + bh * T * M : nullptr, WA ? (uint32_t)(T * M * sizeof(E)) : 0u);
   const rsrc_t Dy = make_rsrc(BWD ? static_cast<const E*>(a.dY) + bh * T * M : nullptr, BWD ? (uint32_t)(T * M * sizeof(E)) : 0u);
 
-  f32x4 accA[JB], accB[JB];
+  f32x4 accA[JB], accB[JB], accF[RST && BWD ? JB : 1];
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) accA[jb] = accB[jb] = zero4();
+  if constexpr (RST && BWD)
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) accF[jb] = zero4();
 
   // The pass streams its inputs and does little arithmetic per byte; chunks
   // are staged DEPTH ahead.  Two measured best from HBM at B=8, H=16,
@@ -251,6 +388,18 @@ agg_kernel(const KArgs a, int64_t nagg) {
     fetch(k, t_begin + k * C);
     __builtin_amdgcn_sched_barrier(0);
   }
+  // Segment-local reset bounds: writes kept from wlo on, dY x^T pre-reset part below bhi.
+  int64_t wlo = t_begin, bhi = t_end;
+  if constexpr (RST) {
+    const rsrc_t rrow = reset_rsrc(a.reset, bh / a.H, T);
+    if constexpr (WA) {
+      const int64_t lr = last_reset_in<NT>(rrow, t_begin - 1, t_end - 1, threadIdx.x, red);
+      if (lr >= 0) wlo = lr;
+    } else {
+      const int64_t fr = first_reset_in<NT>(rrow, t_begin, t_end, threadIdx.x, red);
+      if (fr >= 0) bhi = fr;
+    }
+  }
 
   auto chunk = [&](int k, int64_t t0) {
     const int nvalid = (int)(t_end - t0 < C ? (t_end > t0 ? t_end - t0 : 0) : C);
@@ -269,14 +418,21 @@ agg_kernel(const KArgs a, int64_t nagg) {
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
         // A^T[j][i] += sum_t X[t][j] (eta G)[t][i];  B^T[j][i] += sum_t X[t][j] dY[t][i]
-        F gh, gl, dv;
+        F gh{}, gl{}, dv{}, dp{};
         if constexpr (WA) {
           gh = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
           gl = gh;
           if constexpr (SPLITV) gl = OP::load_t(Gl, M, 32 * kb, 16 * w, lane);
+          if constexpr (RST) {
+            gh = mask_k<OP>(gh, 32 * kb, q, (int)(wlo - t0 > -1 ? (wlo - t0 < C ? wlo - t0 : C) : 0), C);
+            gl = mask_k<OP>(gl, 32 * kb, q, (int)(wlo - t0 > -1 ? (wlo - t0 < C ? wlo - t0 : C) : 0), C);
+          }
           dv = gh;
         }
         if (with_b) dv = OP::load_t(Ds, M, 32 * kb, 16 * w, lane);
+        dp = dv;
+        if constexpr (RST && BWD)
+          dp = mask_k<OP>(dv, 32 * kb, q, 0, (int)(bhi - t0 < C ? (bhi - t0 > 0 ? bhi - t0 : 0) : C));
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) {
           const F xa = OP::load_t(Xs, D, 32 * kb, 16 * jb, lane);
@@ -284,7 +440,8 @@ agg_kernel(const KArgs a, int64_t nagg) {
             if constexpr (ETAV) accA[jb] = mma_split_b<OP>(accA[jb], xa, gh, gl);
             else accA[jb] = OP::mma(accA[jb], xa, gh);
           }
-          if (with_b) accB[jb] = OP::mma(accB[jb], xa, dv);
+          if (with_b) accB[jb] = OP::mma(accB[jb], xa, dp);
+          if constexpr (RST && BWD) accF[jb] = OP::mma(accF[jb], xa, dv);
         }
       }
     }
@@ -309,6 +466,10 @@ agg_kernel(const KArgs a, int64_t nagg) {
       if (with_b) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) a.aggB[base + (int64_t)(16 * jb + 4 * q + r) * M + 16 * w + c] = accB[jb][r];
+      }
+      if constexpr (RST && BWD) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) a.aggF[base + (int64_t)(16 * jb + 4 * q + r) * M + 16 * w + c] = accF[jb][r];
       }
     }
   }

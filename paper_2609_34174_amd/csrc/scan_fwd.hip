@@ -28,7 +28,13 @@ namespace gradlev {
 // tiles of W^T (rows j, cols i) and produces the matching columns of Y for
 // every token of the chunk.
 // ---------------------------------------------------------------------------
-template <class OP, int D, int M, int C, bool INCL, bool ETAV>
+// RST (document resets, unit retention; exclusive reads, 64-token chunks):
+// the chunk masks of scan_common.hpp.  Scores pair tokens of one document
+// only; rows at or after the chunk's first reset read W_0 (a second state
+// pass against W_0, in the chunks that hold a reset); the carry keeps the
+// writes of the chunk's last document and restarts from W_0.  The state at
+// the start of each such chunk is stored for the backward (cstate).
+template <class OP, int D, int M, int C, bool INCL, bool ETAV, bool RST = false>
 __global__ void __launch_bounds__(cmax(D, M) / 16 * 64, 128 / cmax(D, M))
 fwd_main_kernel(const KArgs a) {
   typedef typename OP::elem E;
@@ -45,6 +51,9 @@ fwd_main_kernel(const KArgs a) {
   __shared__ E Vh[ETAV ? C * M : 1];      // -(eta G)[t][i] hi (per-token eta)
   __shared__ E Vl[SPLITV ? C * M : 1];    // -(eta G)[t][i] lo
   __shared__ __attribute__((aligned(16))) float et[C];
+  static_assert(!RST || (C == 64 && !INCL), "resets: exclusive reads, 64-token chunks");
+  __shared__ int red[1];
+  __shared__ int didw[RST ? NW : 1][64];  // per wave: document index of each chunk position (reset chunks)
 
   int64_t bh, seg;
   if (!map_block(a.BH, a.nseg, bh, seg)) return;
@@ -62,26 +71,44 @@ fwd_main_kernel(const KArgs a) {
   Tile4<OP, C, D, NT> xa, xb;
   Tile4<OP, C, M, NT> ga, gb;
   EtaReg<ETAV> ea, eb;
+  RstReg<RST> ra, rb;
   const rsrc_t Et = eta_rsrc(a.eta, bh, T);
-  auto fetch = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, int64_t t0) {
+  const rsrc_t Rrow = reset_rsrc(RST ? a.reset : nullptr, bh / a.H, T);
+  auto fetch = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, RstReg<RST>& rr,
+                   int64_t t0) {
     const bool ok = t0 < t_end;
     er.load(Et, ok ? (uint32_t)(t0 * 4) : kOOB, tid, C);
+    rr.load(Rrow, t0, ok, tid, C);
     xr.load(X, ok ? (uint32_t)(t0 * D * sizeof(E)) : kOOB, tid);
     gr.load(G, ok ? (uint32_t)(t0 * M * sizeof(E)) : kOOB, tid);
   };
-  fetch(xa, ga, ea, t_begin);
-  fetch(xb, gb, eb, t_begin + C);
+  // With resets the segment starts from the state after the last document
+  // start at or before t_begin: W_0 if that is t_begin itself, else W_0 minus
+  // the (post-reset) aggregates from that document's segment on.
+  fetch(xa, ga, ea, ra, t_begin);
+  fetch(xb, gb, eb, rb, t_begin + C);
+  int64_t j_first = 0;
+  bool from_w0 = false;
+  if constexpr (RST) {
+    const int64_t lr = last_reset_in<NT>(Rrow, 0, t_begin, tid, red);
+    if (lr == t_begin) from_w0 = true;
+    else if (lr > 0) j_first = lr / a.seg_len;
+  }
 
   // State tiles: Ws[jb] holds W[i = 16w + c][j = 16jb + 4q + r] = W^T tile (rows j, cols i).
   // The segment starts from W_0 - sum_{j<seg} A_j (the aggregate pass's sums),
   // subtracted in segment order, four segments' loads in flight at a time.
   f32x4 Ws[JB];
+  f32x4 W0r[RST ? JB : 1];  // with resets, this wave's rows of W_0 stay in registers
   if (w < IB) {
     const int64_t o = (int64_t)(16 * w + c) * D + 4 * q;
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) Ws[jb] = *reinterpret_cast<const f32x4*>(a.W0 + h * M * D + o + 16 * jb);
+    if constexpr (RST)
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) W0r[jb] = Ws[jb];
     const float* ag = a.aggA + bh * a.nseg * M * D + o;
-    for (int64_t j0 = 0; j0 < seg; j0 += 4) {
+    for (int64_t j0 = j_first; !from_w0 && j0 < seg; j0 += 4) {
       f32x4 v[4][JB];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
@@ -98,7 +125,8 @@ fwd_main_kernel(const KArgs a) {
   if constexpr (!RS)
     for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
 
-  auto chunk = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, int64_t t0) {
+  auto chunk = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, RstReg<RST>& rr,
+                   int64_t t0) {
     // A step past the segment end (the second of a pair) sees zero tiles,
     // leaves the state unchanged and stores nothing.
     const bool live = t0 < t_end;
@@ -109,8 +137,18 @@ fwd_main_kernel(const KArgs a) {
     xr.store(Xs, tid);
     gr.store(Gs, tid);
     __syncthreads();
+    // Reset masks of this chunk (fr = C, lr = -1 without a reset).
+    const uint64_t dm = rr.mask();
+    const int fr = first_flag(dm), lr = last_flag(dm);
+    const bool has = RST && lr >= 0 && live;
     if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read by the carry, after a barrier
-    fetch(xr, gr, er, t0 + 2 * C);
+    fetch(xr, gr, er, rr, t0 + 2 * C);
+    // The chunk's compute, compiled with the reset masks (HAS) for the chunks
+    // that hold a reset and without them for the others.
+    auto compute = [&](auto hc) {
+    constexpr bool HAS = decltype(hc)::value;
+    // Each wave writes its own table (in-order LDS within a wave: no barrier).
+    if constexpr (HAS) didw[w][lane] = __builtin_popcountll(lane == 63 ? dm : dm & ((2ull << lane) - 1));
 
     // Intra-chunk scores, lower-triangular tiles (tb >= sb) shared by all waves.
     if constexpr (!RS) {
@@ -130,7 +168,8 @@ fwd_main_kernel(const KArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int s = 16 * sb + 4 * q + r;
-          const bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
+          bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
+          if constexpr (HAS) keep = keep && didw[w][s] == didw[w][t];
           v[r] = keep ? acc[r] * et[s] : 0.f;
         }
         OP::store4(Pl + lds_off(t, 16 * sb + 4 * q, C), v);
@@ -147,8 +186,25 @@ fwd_main_kernel(const KArgs a) {
         F wh, wl;
         OP::split(cat(Ws[2 * kb], Ws[2 * kb + 1]), wh, wl);
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
-          acc[tb] = mma_split_a<OP>(acc[tb], wh, wl, OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
+        for (int tb = 0; tb < TB; ++tb) {
+          F xf = OP::load_n(Xs, D, 16 * tb, 32 * kb, lane);
+          if constexpr (HAS) xf = keep_row<OP>(xf, 16 * tb + c < fr);
+          acc[tb] = mma_split_a<OP>(acc[tb], wh, wl, xf);
+        }
+      }
+      if constexpr (HAS) {
+        {
+          // Rows of the documents that start in this chunk read W_0.
+#pragma unroll
+          for (int kb = 0; kb < D / 32; ++kb) {
+            F wh, wl;
+            OP::split(cat(W0r[2 * kb], W0r[2 * kb + 1]), wh, wl);
+#pragma unroll
+            for (int tb = 0; tb < TB; ++tb)
+              acc[tb] = mma_split_a<OP>(acc[tb], wh, wl,
+                                        keep_row<OP>(OP::load_n(Xs, D, 16 * tb, 32 * kb, lane), 16 * tb + c >= fr));
+          }
+        }
       }
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) {
@@ -171,7 +227,8 @@ fwd_main_kernel(const KArgs a) {
                 const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                  const bool keep = sb < tb || (INCL ? (4 * q + r <= c) : (4 * q + r < c));
+                  bool keep = sb < tb || (INCL ? (4 * q + r <= c) : (4 * q + r < c));
+                  if constexpr (HAS) keep = keep && didw[w][16 * sb + 4 * q + r] == didw[w][16 * tb + c];
                   st[r] = keep ? st[r] * es[r] : 0.f;
                 }
               }
@@ -197,14 +254,32 @@ fwd_main_kernel(const KArgs a) {
     // no barrier has passed since (the shared-score path had one).
     if constexpr (RS && ETAV) __syncthreads();
     if (w < IB) {
+      // With resets: the state at this chunk's start, for the backward, and
+      // a carry that restarts from W_0 with the last document's writes.
+      if constexpr (HAS) {
+        {
+          if (a.cstate) {
+            float* o = a.cstate + (bh * ((T + C - 1) / C) + t0 / C) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
+#pragma unroll
+            for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
+          }
+#pragma unroll
+          for (int jb = 0; jb < JB; ++jb) Ws[jb] = W0r[jb];
+        }
+      }
+      const int klo = HAS ? lr : 0;  // writes before the last reset do not reach the next chunk
       // Carry to the next chunk (also after the last one, where it is unused).
       if constexpr (ETAV) {
         // W^T[j][i] += sum_t X[t][j] (-eta G)[t][i], eta folded into the split operand.
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F vh = OP::load_t(Vh, M, 32 * kb, 16 * w, lane);
+          F vh = OP::load_t(Vh, M, 32 * kb, 16 * w, lane);
           F vl = vh;
           if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * w, lane);
+          if constexpr (HAS) {
+            vh = mask_k<OP>(vh, 32 * kb, q, klo, C);
+            vl = mask_k<OP>(vl, 32 * kb, q, klo, C);
+          }
 #pragma unroll
           for (int jb = 0; jb < JB; ++jb)
             Ws[jb] = mma_split_b<OP>(Ws[jb], OP::load_t(Xs, D, 32 * kb, 16 * jb, lane), vh, vl);
@@ -216,7 +291,8 @@ fwd_main_kernel(const KArgs a) {
         for (int jb = 0; jb < JB; ++jb) dw[jb] = zero4();
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F gq = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
+          F gq = OP::load_t(Gs, M, 32 * kb, 16 * w, lane);
+          if constexpr (HAS) gq = mask_k<OP>(gq, 32 * kb, q, klo, C);
 #pragma unroll
           for (int jb = 0; jb < JB; ++jb) dw[jb] = OP::mma(dw[jb], OP::load_t(Xs, D, 32 * kb, 16 * jb, lane), gq);
         }
@@ -234,11 +310,14 @@ fwd_main_kernel(const KArgs a) {
         for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
       }
     }
+      };
+    if (RST && has) compute(IntC<RST ? 1 : 0>{});
+    else compute(IntC<0>{});
   };
 
   for (int64_t t0 = t_begin; t0 < t_end; t0 += 2 * C) {
-    chunk(xa, ga, ea, t0);
-    chunk(xb, gb, eb, t0 + C);
+    chunk(xa, ga, ea, ra, t0);
+    chunk(xb, gb, eb, rb, t0 + C);
   }
 }
 
@@ -271,9 +350,26 @@ int fwd_wgs_per_cu(int bf16, int d, int m, int C) {
 }
 
 template <class OP, int D, int M, int C, bool ETAV>
-static hipError_t fwd_dispatch2(const ScanProblem& p, const KArgs& k, hipStream_t s) {
+static hipError_t fwd_dispatch2(const ScanProblem& p, const KArgs& k, bool resets, hipStream_t s) {
   constexpr int NT = cmax(D, M) / 16 * 64;
   const unsigned grid = (unsigned)seg_grid(k.BH, p.nseg);
+  if (resets) {
+    // Document resets at unit retention: exclusive 64 x 64 maps, 64-token chunks.
+    if constexpr (D == 64 && M == 64 && C == 64) {
+      if (p.inclusive) return hipErrorInvalidValue;
+      if (p.nseg > 1) {
+        timing_begin(GRADLEV_K_FWD_AGG, s);
+        hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggFwd, ETAV, true>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
+        timing_end(GRADLEV_K_FWD_AGG, s);
+      }
+      timing_begin(GRADLEV_K_FWD_MAIN, s);
+      hipLaunchKernelGGL((fwd_main_kernel<OP, D, M, C, false, ETAV, true>), dim3(grid), dim3(NT), 0, s, k);
+      timing_end(GRADLEV_K_FWD_MAIN, s);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   if (p.nseg > 1) {
     timing_begin(GRADLEV_K_FWD_AGG, s);
     hipLaunchKernelGGL((agg_kernel<OP, D, M, C, kAggFwd, ETAV>), dim3(grid), dim3(NT), 0, s, k, p.nseg - 1);
@@ -289,23 +385,23 @@ static hipError_t fwd_dispatch2(const ScanProblem& p, const KArgs& k, hipStream_
 }
 
 template <class OP, int D, int M, int C>
-static hipError_t fwd_dispatch(const ScanProblem& p, const KArgs& k, hipStream_t s) {
+static hipError_t fwd_dispatch(const ScanProblem& p, const KArgs& k, bool resets, hipStream_t s) {
   constexpr int bf = OP::kSplit == 2 ? 1 : 0;
   if (k.eta) {
     // The per-token split operands need two more tiles of LDS; where they do
     // not fit at this tile length the chunk drops to 64 (same segments).
-    if constexpr (lds_bytes_fwd(bf, D, M, C, 1) <= 160 * 1024) return fwd_dispatch2<OP, D, M, C, true>(p, k, s);
-    else return fwd_dispatch2<OP, D, M, 64, true>(p, k, s);
+    if constexpr (lds_bytes_fwd(bf, D, M, C, 1) <= 160 * 1024) return fwd_dispatch2<OP, D, M, C, true>(p, k, resets, s);
+    else return fwd_dispatch2<OP, D, M, 64, true>(p, k, resets, s);
   }
-  return fwd_dispatch2<OP, D, M, C, false>(p, k, s);
+  return fwd_dispatch2<OP, D, M, C, false>(p, k, resets, s);
 }
 
 template <class OP, int C>
-static hipError_t fwd_by_dims(const ScanProblem& p, const KArgs& k, hipStream_t s) {
-  if (p.d == 64 && p.m == 64) return fwd_dispatch<OP, 64, 64, C>(p, k, s);
-  if (p.d == 64 && p.m == 128) return fwd_dispatch<OP, 64, 128, C>(p, k, s);
-  if (p.d == 128 && p.m == 64) return fwd_dispatch<OP, 128, 64, C>(p, k, s);
-  if (p.d == 128 && p.m == 128) return fwd_dispatch<OP, 128, 128, C>(p, k, s);
+static hipError_t fwd_by_dims(const ScanProblem& p, const KArgs& k, bool resets, hipStream_t s) {
+  if (p.d == 64 && p.m == 64) return fwd_dispatch<OP, 64, 64, C>(p, k, resets, s);
+  if (p.d == 64 && p.m == 128) return fwd_dispatch<OP, 64, 128, C>(p, k, resets, s);
+  if (p.d == 128 && p.m == 64) return fwd_dispatch<OP, 128, 64, C>(p, k, resets, s);
+  if (p.d == 128 && p.m == 128) return fwd_dispatch<OP, 128, 128, C>(p, k, resets, s);
   return hipErrorInvalidValue;
 }
 
@@ -328,11 +424,14 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& f, hipStream_t s
   k.wend = f.wend;
   k.save_len = f.save_len;
   k.nsave = f.nsave;
+  k.reset = f.reset;
+  k.cstate = f.cstate;
+  if (f.resets && p.chunk != 64) return hipErrorInvalidValue;
   if (p.bf16) {
-    if (p.chunk == 128) return fwd_by_dims<OpBF16, 128>(p, k, s);
-    return fwd_by_dims<OpBF16, 64>(p, k, s);
+    if (p.chunk == 128) return fwd_by_dims<OpBF16, 128>(p, k, f.resets, s);
+    return fwd_by_dims<OpBF16, 64>(p, k, f.resets, s);
   }
-  return fwd_by_dims<OpF32, 64>(p, k, s);
+  return fwd_by_dims<OpF32, 64>(p, k, f.resets, s);
 }
 
 }  // namespace gradlev
