@@ -443,3 +443,39 @@ def test_static_forward_validation_before_any_hip_call(L):
     assert "GRADLEV_STATIC_SCRATCH_BYTES" in gl.error_string(gl.ERR_SCRATCH)
     m = re.search(r"#define GRADLEV_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
     assert m and int(m.group(1)) << int(m.group(2)) == gl.STATIC_SCRATCH_BYTES
+
+
+def test_reset_pair_sizes_and_validation(L):
+    """The reset pair (unit retention with document resets) takes 64 x 64
+    exclusive maps; its saved buffer holds the segment-end weights and room for
+    a state at every 64-token chunk start; arguments are checked before any
+    launch."""
+    s = shape(B=2, H=4, T=1000)
+    sv, ws = gl.reset_saved_bytes(s)
+    sv_plain, _ = gl.saved_bytes(shape(B=2, H=4, T=1000, chunk=64))
+    md = 64 * 64 * 4
+    assert sv >= sv_plain + 2 * 4 * -(-1000 // 64) * md
+    for bad, code in ((dict(d_in=128), gl.ERR_UNSUPPORTED), (dict(d_out=128), gl.ERR_UNSUPPORTED),
+                      (dict(prefix="inclusive"), gl.ERR_UNSUPPORTED), (dict(T=0), gl.ERR_INVALID)):
+        a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+        assert L.gradlev_scan_reset_saved_bytes(ctypes.byref(shape(**bad)), ctypes.byref(a), ctypes.byref(b)) == code
+    fwd, bwd = L.gradlev_scan_fwd_reset_save, L.gradlev_scan_bwd_reset_saved
+    # W0, X, G, eta, eta_scalar, reset, Y, saved, saved_bytes, ws, ws_bytes, stream
+    fa = [FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, FAKE, sv, FAKE, ws, None]
+    for k, v, code in ((0, None, gl.ERR_INVALID), (6, None, gl.ERR_INVALID), (7, None, gl.ERR_INVALID),
+                       (1, MISALIGNED, gl.ERR_ALIGN), (3, MISALIGNED, gl.ERR_ALIGN), (8, sv - 4, gl.ERR_WORKSPACE),
+                       (10, 16, gl.ERR_WORKSPACE)):
+        bad = list(fa)
+        bad[k] = v
+        assert fwd(ctypes.byref(s), *bad) == code, k
+    # W0, X, G, eta, eta_scalar, dY, reset, saved, saved_bytes, gtilde, dX, dG, deta, dW0, ws, ws_bytes, stream
+    ba = [FAKE, FAKE, FAKE, None, 0.1, FAKE, FAKE, FAKE, sv, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None]
+    for k, v, code in ((5, None, gl.ERR_INVALID), (7, None, gl.ERR_INVALID), (12, MISALIGNED, gl.ERR_ALIGN),
+                       (8, 16, gl.ERR_WORKSPACE), (15, 16, gl.ERR_WORKSPACE)):
+        bad = list(ba)
+        bad[k] = v
+        assert bwd(ctypes.byref(s), *bad) == code, k
+    none = list(ba)
+    for k in range(9, 14):
+        none[k] = None
+    assert bwd(ctypes.byref(s), *none) == gl.ERR_INVALID   # no output requested
