@@ -87,7 +87,7 @@ static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g
     float a, e;
     gate_at(g, bh, b, t, a, e);
     z = zc_step(z, a);
-    if (a != 0.f) l += log(fabs((double)a));
+    if (a != 0.f && fabsf(a) != 1.f) l += log(fabs((double)a));  // log 1 = 0 exactly
   }
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -122,7 +122,7 @@ static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g
     float a, e;
     gate_at(g, bh, b, t, a, e);
     z = zc_step(z, a);
-    if (a != 0.f) l += log(fabs((double)a));
+    if (a != 0.f && fabsf(a) != 1.f) l += log(fabs((double)a));
     g.zc[bh * g.Tp + t] = z;
     g.lc[bh * g.Tp + t] = l;
     g.cw[bh * g.Tp + t] = -e;
@@ -259,7 +259,9 @@ static __global__ void __launch_bounds__(256) wide_score_kernel(const WScoreArgs
   tri_tile(tile % per_seq, tb, sb);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wt = w >> 1, ws = w & 1;
   const int c = lane & 15, q = lane >> 4;
-  const int64_t wk = a.w / a.KS, kbeg = ks * wk;
+  // this range's 64-wide steps of the contraction (ranges differ by at most one step)
+  const int64_t nsteps = a.w / 64, kb = nsteps * ks / a.KS, ke = nsteps * (ks + 1) / a.KS;
+  const int64_t kbeg = 64 * kb;
 
   f32x4 acc[4][4];  // [s block][t block]: D[s][t] = K_s . Q_t
 #pragma unroll
@@ -273,12 +275,12 @@ static __global__ void __launch_bounds__(256) wide_score_kernel(const WScoreArgs
     const rsrc_t Kr = make_rsrc(static_cast<const E*>(a.K) + bh * a.T * a.w, (uint32_t)(a.T * a.w * es));
     const uint32_t stride = (uint32_t)(a.w * es);
     const uint32_t qoff = (uint32_t)(BT * tb * stride), koff = (uint32_t)(BT * sb * stride);
-    // Two-deep register pipeline as in wide_out_kernel (the step count
-    // wk / 64 is even: the split rule keeps every range a multiple of 128).
+    // Two-deep register pipeline as in wide_out_kernel; an odd step count
+    // ends with one step of zeros (its fetch lies past the range).
     struct Set {
       GTile<E, BT, BK, NT> qt, kt;
     } st[2];
-    const int64_t nk = wk / BK;
+    const int64_t nk = ke - kb;
     auto fetch = [&](Set& x, int64_t k) {
       const bool ok = k < nk;
       const uint32_t col = (uint32_t)((kbeg + k * BK) * es);
@@ -306,6 +308,9 @@ static __global__ void __launch_bounds__(256) wide_score_kernel(const WScoreArgs
       }
     };
     fetch(st[0], 0);
+    // Issue order is the loop's: the first wait of every step counts only
+    // the other set's loads, on entry too.
+    __builtin_amdgcn_sched_barrier(0);
     fetch(st[1], 1);
     for (int64_t k = 0; k < nk; k += 2) {
       step(st[0], k);
@@ -826,6 +831,9 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
       }
     };
     fetch(st[0], 0);
+    // Issue order is the loop's: the first wait of every step counts only
+    // the other set's loads, on entry too.
+    __builtin_amdgcn_sched_barrier(0);
     fetch(st[1], 1);
     for (int64_t k = 0; k < n1; k += 2) {
       step(st[0], k);
@@ -886,6 +894,9 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
       }
     };
     fetch(st[0], 0);
+    // Issue order is the loop's: the first wait of every step counts only
+    // the other set's loads, on entry too.
+    __builtin_amdgcn_sched_barrier(0);
     fetch(st[1], 1);
     for (int64_t k = 0; k < n2; k += 2) {
       step(st[0], k);
@@ -930,13 +941,12 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-// Splits of the score contraction: enough workgroups for two per compute
-// unit, at most 4 ranges, each at least 256 wide and a whole number of the
-// kernel's 64-wide steps.
+// Splits of the score contraction: at most 4 ranges of at least four
+// 64-wide steps each, no more than 512 workgroups (two per compute unit).
 static int wide_score_splits(int64_t BH, int64_t Tp, int64_t w) {
   const int64_t tiles = BH * (Tp / 128) * (Tp / 128 + 1) / 2;
   int ks = 1;
-  while (ks < 4 && tiles * ks < 2 * 256 && w / (2 * ks) >= 256 && w % (2 * ks * 64) == 0) ks *= 2;
+  while (ks < 4 && tiles * (ks + 1) <= 2 * 256 && w / 64 / (ks + 1) >= 4) ++ks;
   return ks;
 }
 
