@@ -148,7 +148,7 @@ int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
 // saved plan at 64-token tiles for both directions (the backward restarts its
 // un-write at the forward's chunk-start states, so the two share the tile).
 // Saved: segment-end weights [BH][nseg_b][m][d], then the chunk-start states
-// [BH][ceil(T/64)][m][d] (written only for chunks that hold a reset).
+// [BH][ceil(T/64)][d][m], transposed (written only for chunks that hold a reset).
 // Workspace: forward aggregates [BH][nseg_f][m][d]; backward pre-reset and
 // full dY x^T aggregates [BH][nseg_b][d][m] each.
 struct ResetPlan {

@@ -28,7 +28,7 @@ struct FwdPtrs {
   float* wend;  // [B*H][nsave][m][d] weights after each save_len-token block (for a backward), or nullptr
   int64_t save_len, nsave;  // the backward's segment length and count (a multiple of the chunk)
   const uint8_t* reset;     // [B][T] document starts (unit retention with resets), or nullptr
-  float* cstate;            // with resets: [B*H][ceil(T/64)][m][d] chunk-start states of reset chunks
+  float* cstate;            // with resets: [B*H][ceil(T/64)][d][m] chunk-start states of reset chunks, transposed
   bool resets;              // run the reset kernels (reset may still be nullptr: no document starts)
 };
 

@@ -42,7 +42,7 @@ struct BArgs {
   float* rfin;        // [BH][m][d]: full-sequence dY x^T (written by segment 0), or null
   const float* wend;  // [BH][nseg][m][d]: the forward's segment-end weights, or null (then W_0 - sum A)
   const uint8_t* reset;  // [B][T] document starts (RST kernels)
-  const float* cstate;   // [BH][ceil(T/C)][m][d]: chunk-start states of the chunks holding a reset
+  const float* cstate;   // [BH][ceil(T/C)][d][m]: chunk-start states of the chunks holding a reset, transposed
 };
 
 // Output modes compiled separately so that no accumulator crosses a runtime
@@ -256,8 +256,7 @@ bwd_main_kernel(const BArgs a) {
         for (int e = 0; e < NWB; ++e)
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) Wj[e][ib][r] = cs[(int64_t)(16 * ib + 4 * q + r) * D + 16 * blk(e) + c];
+            Wj[e][ib] = *reinterpret_cast<const f32x4*>(cs + (int64_t)(16 * blk(e) + c) * M + 16 * ib + 4 * q);
       }
     }
 

@@ -66,6 +66,10 @@ fwd_main_kernel(const KArgs a) {
   const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
   const rsrc_t Y = make_rsrc(a.out0 + bh * T * M, (uint32_t)(T * M * 4));
   const rsrc_t none = make_rsrc(nullptr, 0u);  // every access out of range
+  // With resets: this sequence's chunk-start states (under 2 GiB, checked by the host).
+  const int64_t nchs = (T + C - 1) / C;
+  const rsrc_t Cst = make_rsrc(RST && a.cstate ? a.cstate + bh * nchs * M * D : nullptr,
+                               RST && a.cstate ? (uint32_t)(nchs * M * D * 4) : 0u);
 
   // Register staging, two chunks ahead.
   Tile4<OP, C, D, NT> xa, xb;
@@ -142,6 +146,18 @@ fwd_main_kernel(const KArgs a) {
     const int fr = first_flag(dm), lr = last_flag(dm);
     const bool has = RST && lr >= 0 && live;
     if (ETAV) gr.store_scaled(Vh, Vl, tid, et);  // read by the carry, after a barrier
+    // The state at the start of a chunk holding a reset, kept for the
+    // backward: stored transposed, [d][m], so that the backward's lanes read
+    // it 16 bytes at a time, and before the next chunks' loads, so that
+    // waiting for those does not wait for these stores as well.
+    // Streamed like the outputs: no dirty lines left in the L2 at the end.
+    if (RST && has && a.cstate && w < IB) {
+      const uint32_t o = (uint32_t)(((t0 / C) * M * D + 16 * w + c) * 4);
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) buf_store1(Cst, o + (uint32_t)((16 * jb + 4 * q + r) * M * 4), Ws[jb][r]);
+    }
     fetch(xr, gr, er, rr, t0 + 2 * C);
     // The chunk's compute, compiled with the reset masks (HAS) for the chunks
     // that hold a reset and without them for the others.
@@ -254,18 +270,10 @@ fwd_main_kernel(const KArgs a) {
     // no barrier has passed since (the shared-score path had one).
     if constexpr (RS && ETAV) __syncthreads();
     if (w < IB) {
-      // With resets: the state at this chunk's start, for the backward, and
-      // a carry that restarts from W_0 with the last document's writes.
+      // With resets: a carry that restarts from W_0 with the last document's writes.
       if constexpr (HAS) {
-        {
-          if (a.cstate) {
-            float* o = a.cstate + (bh * ((T + C - 1) / C) + t0 / C) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
 #pragma unroll
-            for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
-          }
-#pragma unroll
-          for (int jb = 0; jb < JB; ++jb) Ws[jb] = W0r[jb];
-        }
+        for (int jb = 0; jb < JB; ++jb) Ws[jb] = W0r[jb];
       }
       const int klo = HAS ? lr : 0;  // writes before the last reset do not reach the next chunk
       // Carry to the next chunk (also after the last one, where it is unused).
