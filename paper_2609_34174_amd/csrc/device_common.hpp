@@ -34,6 +34,20 @@ namespace gradlev {
 typedef __bf16 bf16;
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values as bf16 hi + lo pairs (v ~= hi + lo): hi rounds each value
+// to bf16 (one packed conversion for the pair), its fp32 value is the packed
+// word's upper or lower half moved into place, and lo rounds the exact
+// remainder v - hi.  The same values as converting each element on its own,
+// with one conversion per pair for each of hi and lo.
+__device__ __forceinline__ void split2(float v0, float v1, bf16x2& hi, bf16x2& lo) {
+  hi = __builtin_convertvector((f32x2){v0, v1}, bf16x2);
+  const uint32_t hb = __builtin_bit_cast(uint32_t, hi);
+  const float h0 = __builtin_bit_cast(float, hb << 16), h1 = __builtin_bit_cast(float, hb & 0xffff0000u);
+  lo = __builtin_convertvector((f32x2){v0 - h0, v1 - h1}, bf16x2);
+}
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
@@ -113,10 +127,13 @@ struct OpBF16 {
   // v ~= hi + lo, both bf16 (about 16 significant bits in total).
   __device__ static __forceinline__ void split(f32x8 v, frag& hi, frag& lo) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16 h = (bf16)v[e];
-      hi[e] = h;
-      lo[e] = (bf16)(v[e] - (float)h);
+    for (int e = 0; e < 8; e += 2) {
+      bf16x2 h, l;
+      split2(v[e], v[e + 1], h, l);
+      hi[e] = h[0];
+      hi[e + 1] = h[1];
+      lo[e] = l[0];
+      lo[e + 1] = l[1];
     }
   }
   // Store 4 consecutive elements (one chunk, 8 bytes).
@@ -129,9 +146,13 @@ struct OpBF16 {
   __device__ static __forceinline__ void store4_split(elem* hi, elem* lo, f32x4 v) {
     bf16x4 h, l;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      h[r] = (bf16)v[r];
-      l[r] = (bf16)(v[r] - (float)h[r]);
+    for (int r = 0; r < 4; r += 2) {
+      bf16x2 h2, l2;
+      split2(v[r], v[r + 1], h2, l2);
+      h[r] = h2[0];
+      h[r + 1] = h2[1];
+      l[r] = l2[0];
+      l[r + 1] = l2[1];
     }
     *reinterpret_cast<bf16x4*>(hi) = h;
     *reinterpret_cast<bf16x4*>(lo) = l;

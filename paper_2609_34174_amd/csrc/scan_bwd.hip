@@ -101,7 +101,7 @@ bwd_main_kernel(const BArgs a) {
   constexpr bool SSH = FULL && !ETAV && s_shared_fits(OP::kSplit == 2, D, M, C, ETAV);
   __shared__ E Sh[SSH ? C * C : 1];
   __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
-  __shared__ float et[C];
+  __shared__ __attribute__((aligned(16))) float et[C];
   __shared__ float dpart[PAIR ? 2 : IB][C];
   static_assert(!RST || (C == 64 && D == 64 && M == 64 && !INCL), "resets: exclusive 64 x 64 maps, 64-token chunks");
   __shared__ int red[1];
@@ -273,12 +273,14 @@ bwd_main_kernel(const BArgs a) {
       for (int kb = 0; kb < M / 32; ++kb)
         acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
       const int t = 16 * tb + c;
+      // eta of the four s of this lane, read unconditionally (a select, not a branch per element).
+      const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int s = 16 * sb + 4 * q + r;
         bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
         if constexpr (HAS) keep = keep && same_doc(dm, s, t);
-        acc[r] = keep ? acc[r] * et[s] : 0.f;
+        acc[r] = keep ? acc[r] * es[r] : 0.f;
       }
       OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
     }
@@ -704,7 +706,7 @@ bwd_split_kernel(const BArgs a) {
   constexpr bool SSH = !ETAV && s_shared_fits(OP::kSplit == 2, D, M, C, ETAV);
   __shared__ E Sh[SSH ? C * C : 1];
   __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
-  __shared__ float et[C];
+  __shared__ __attribute__((aligned(16))) float et[C];
   __shared__ float dpart[IB][C];
 
   int64_t bh, seg;
@@ -821,11 +823,12 @@ bwd_split_kernel(const BArgs a) {
       for (int kb = 0; kb < M / 32; ++kb)
         acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
       const int t = 16 * tb + c;
+      const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int s = 16 * sb + 4 * q + r;
         const bool keep = tb > sb || (INCL ? (t >= s) : (t > s));
-        acc[r] = keep ? acc[r] * et[s] : 0.f;
+        acc[r] = keep ? acc[r] * es[r] : 0.f;
       }
       OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
     }

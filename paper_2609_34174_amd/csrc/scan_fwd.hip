@@ -180,13 +180,14 @@ fwd_main_kernel(const KArgs a) {
           acc = OP::mma(acc, OP::load_n(Xs, D, 16 * sb, 32 * kb, lane), OP::load_n(Xs, D, 16 * tb, 32 * kb, lane));
         // acc[r] = x_s . x_t with s = 16sb + 4q + r, t = 16tb + c; et holds -eta.
         const int t = 16 * tb + c;
+        const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
         f32x4 v;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int s = 16 * sb + 4 * q + r;
           bool keep = sb < tb || (INCL ? (s <= t) : (s < t));
           if constexpr (HAS) keep = keep && didw[w][s] == didw[w][t];
-          v[r] = keep ? acc[r] * et[s] : 0.f;
+          v[r] = keep ? acc[r] * es[r] : 0.f;
         }
         OP::store4(Pl + lds_off(t, 16 * sb + 4 * q, C), v);
       }
