@@ -56,7 +56,7 @@ static constexpr int lds_bytes_bwd(int bf16, int d, int m, int C, int etav) {
   const int es = bf16 ? 2 : 4;
   const int v = etav ? (bf16 ? 2 : 1) * C * m : 0;
   const int r = (bf16 ? 2 : 1) * d * m;
-  return es * (C * d + 2 * C * m + C * C + v + r) + 4 * C + 4 * (m / 16) * C;
+  return es * (C * d + 2 * C * m + C * C + v + r) + 4 * C + 4 * 4 * (m / 16) * C;  // last: deta partials, at most
 }
 static constexpr bool s_shared_fits(bool bf16, int d, int m, int C, bool etav) {
   return lds_bytes_bwd(bf16, d, m, C, etav) + (bf16 ? 2 : 1) * C * C * (bf16 ? 2 : 4) <= 160 * 1024;
@@ -102,7 +102,7 @@ bwd_main_kernel(const BArgs a) {
   __shared__ E Sh[SSH ? C * C : 1];
   __shared__ E Sl[SSH && OP::kSplit == 2 ? C * C : 1];
   __shared__ __attribute__((aligned(16))) float et[C];
-  __shared__ float dpart[PAIR ? 2 : IB][C];
+  __shared__ float dpart[PAIR ? 2 : IB][4][C];  // deta partial sums per wave (pair) and lane group
   static_assert(!RST || (C == 64 && D == 64 && M == 64 && !INCL), "resets: exclusive 64 x 64 maps, 64-token chunks");
   __shared__ int red[1];
 
@@ -616,9 +616,9 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
               for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[e][hh][r];
             }
-            p += __shfl_xor(p, 16);
-            p += __shfl_xor(p, 32);
-            if (q == 0) dpart[PAIR ? (w >> 1) : w][s] = p;
+            // The four lane groups' partial sums are added after the barrier
+            // below (no cross-lane shuffles here).
+            dpart[PAIR ? (w >> 1) : w][q][s] = p;
           }
         }
       }
@@ -653,7 +653,8 @@ bwd_main_kernel(const BArgs a) {
         const int tt = td < C ? td : 0;
         float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < (PAIR ? 2 : IB); ++i) s += dpart[i][tt];
+        for (int i = 0; i < (PAIR ? 2 : IB); ++i)
+          s += (dpart[i][0][tt] + dpart[i][1][tt]) + (dpart[i][2][tt] + dpart[i][3][tt]);
         buf_store1(Oec, td < C ? (uint32_t)((t0 + td) * 4) : kOOB, s);
       }
     }
