@@ -106,6 +106,18 @@ struct OpBF16 {
     const bf16x4 b = *reinterpret_cast<const bf16x4*>(base + lds_off(r, k + 16, K));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
   }
+  // load_n with reads the compiler keeps apart (volatile): it would otherwise
+  // pair the first halves of two fragments into one two-address read and
+  // then move each fragment's halves together.  Pays in the wide-map kernels
+  // (LM-width MLP step -2.5 %); in the narrow scans the extra read
+  // instructions and the fixed read order cost more than the moves saved.
+  __device__ static __forceinline__ frag load_n_sep(const elem* base, int K, int row0, int k0, int lane) {
+    const int r = row0 + (lane & 15), k = k0 + 4 * (lane >> 4);
+    typedef const volatile __attribute__((address_space(3))) bf16x4 lds_v4;
+    const bf16x4 a = *(lds_v4*)(base + lds_off(r, k, K));
+    const bf16x4 b = *(lds_v4*)(base + lds_off(r, k + 16, K));
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
   __device__ static __forceinline__ frag load_t(const elem* base, int K, int k0, int n0, int lane) {
     const int c = lane & 15, r = k0 + 4 * (lane >> 4) + (c >> 2), n = n0 + 4 * (c & 3);
     const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + lds_off(r, n, K)));
@@ -174,6 +186,9 @@ struct OpF32 {
     const f32x4 a = *reinterpret_cast<const f32x4*>(base + lds_off(r, k, K));
     const f32x4 b = *reinterpret_cast<const f32x4*>(base + lds_off(r, k + 16, K));
     return cat(a, b);
+  }
+  __device__ static __forceinline__ frag load_n_sep(const elem* base, int K, int row0, int k0, int lane) {
+    return load_n(base, K, row0, k0, lane);
   }
   __device__ static __forceinline__ frag load_t(const elem* base, int K, int k0, int n0, int lane) {
     const int c = lane & 15, q = lane >> 4;

@@ -298,10 +298,10 @@ static __global__ void __launch_bounds__(256) wide_score_kernel(const WScoreArgs
       for (int kk = 0; kk < BK; kk += 32) {
         F qf[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n_sep(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
+          const F pf = OP::load_n_sep(Ps, BK, 64 * ws + 16 * i, kk, lane);
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[i][j] = OP::mma(acc[i][j], pf, qf[j]);
         }
@@ -432,10 +432,10 @@ static __global__ void __launch_bounds__(256) wide_deta_kernel(const WDetaArgs a
       for (int kk = 0; kk < BK; kk += 32) {
         F qf[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n_sep(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
+          const F pf = OP::load_n_sep(Ps, BK, 64 * ws + 16 * i, kk, lane);
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[z][i][j] = OP::mma(acc[z][i][j], pf, qf[j]);
         }
@@ -572,10 +572,10 @@ static __global__ void __launch_bounds__(256) wide_dalpha_kernel(const WDetaArgs
       for (int kk = 0; kk < BK; kk += 32) {
         F qf[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+        for (int j = 0; j < 4; ++j) qf[j] = OP::load_n_sep(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const F pf = OP::load_n(Ps, BK, 64 * ws + 16 * i, kk, lane);
+          const F pf = OP::load_n_sep(Ps, BK, 64 * ws + 16 * i, kk, lane);
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[i][j] = OP::mma(acc[i][j], pf, qf[j]);
         }
@@ -815,7 +815,7 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
       const int kk = 32 * kh;
       F qf[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) qf[j] = OP::load_n(Qs, BK, 64 * wt + 16 * j, kk, lane);
+      for (int j = 0; j < 4; ++j) qf[j] = OP::load_n_sep(Qs, BK, 64 * wt + 16 * j, kk, lane);
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
         F ph, pl;
@@ -823,8 +823,8 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
           ph = OP::load_t(Ph, BN, kk, BN / 2 * wn + 16 * i, lane);
           pl = SPLIT ? OP::load_t(Pl, BN, kk, BN / 2 * wn + 16 * i, lane) : ph;
         } else {
-          ph = OP::load_n(Ph, BK, BN / 2 * wn + 16 * i, kk, lane);
-          pl = SPLIT ? OP::load_n(Pl, BK, BN / 2 * wn + 16 * i, kk, lane) : ph;
+          ph = OP::load_n_sep(Ph, BK, BN / 2 * wn + 16 * i, kk, lane);
+          pl = SPLIT ? OP::load_n_sep(Pl, BK, BN / 2 * wn + 16 * i, kk, lane) : ph;
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mma_split_a<OP>(acc[i][j], ph, pl, qf[j]);
@@ -879,8 +879,8 @@ static __global__ void __launch_bounds__(512) wide_out_kernel(const WOutArgs a) 
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if constexpr (MODE == 0) {
-          sfh[j] = OP::load_n(Shs, BK, 64 * wt + 16 * j, kk, lane);
-          sfl[j] = SPLIT ? OP::load_n(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
+          sfh[j] = OP::load_n_sep(Shs, BK, 64 * wt + 16 * j, kk, lane);
+          sfl[j] = SPLIT ? OP::load_n_sep(Sls, BK, 64 * wt + 16 * j, kk, lane) : sfh[j];
         } else {
           sfh[j] = OP::load_t(Shs, BM, kk, 64 * wt + 16 * j, lane);
           sfl[j] = SPLIT ? OP::load_t(Sls, BM, kk, 64 * wt + 16 * j, lane) : sfh[j];
