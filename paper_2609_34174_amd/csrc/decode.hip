@@ -20,7 +20,7 @@
 
 namespace gradlev {
 
-template <int D, bool GATED>
+template <int D, bool GATED, bool STREAM>
 __global__ void __launch_bounds__(256)
 decode_kernel(float* __restrict__ W, const float* __restrict__ x, const float* __restrict__ g,
               const float* __restrict__ eta, float eta_scalar, float* __restrict__ y, int M,
@@ -67,7 +67,7 @@ decode_kernel(float* __restrict__ W, const float* __restrict__ x, const float* _
       f32x4 nw;
       if constexpr (GATED) nw = w0[u] + al * (wv[u] - w0[u]) - (e * gv[u]) * xv;
       else nw = wv[u] - (e * gv[u]) * xv;
-      buf_store4<kStoreDefault>(Ws, (uint32_t)((i * D + col) * 4), nw);
+      buf_store4<STREAM ? kStoreStream : kStoreDefault>(Ws, (uint32_t)((i * D + col) * 4), nw);
     }
   }
 }
@@ -80,7 +80,7 @@ decode_kernel(float* __restrict__ W, const float* __restrict__ x, const float* _
 // products from the loaded (pre-update) values, writes the update from the
 // same registers and reduces each row's dot product across the wave.  x sits
 // in LDS, loaded once per workgroup.  Workgroup: 4 waves, 4 U rows.
-template <int NCH, bool GATED>
+template <int NCH, bool GATED, bool STREAM>
 __global__ void __launch_bounds__(256)
 decode_wide_kernel(float* __restrict__ W, const float* __restrict__ x, const float* __restrict__ g,
                    const float* __restrict__ eta, float eta_scalar, float* __restrict__ y, int M,
@@ -131,13 +131,21 @@ decode_wide_kernel(float* __restrict__ W, const float* __restrict__ x, const flo
       f32x4 nw;
       if constexpr (GATED) nw = w0[u][c] + al * (v - w0[u][c]) - (e * gv[u]) * xv;
       else nw = v - (e * gv[u]) * xv;
-      buf_store4<kStoreDefault>(Ws, (uint32_t)((((int64_t)(r0 + u)) * D + 256 * c + 4 * lane) * 4), nw);
+      buf_store4<STREAM ? kStoreStream : kStoreDefault>(Ws, (uint32_t)((((int64_t)(r0 + u)) * D + 256 * c + 4 * lane) * 4), nw);
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
     buf_store1<kStoreDefault>(Ys, lane == 0 ? (uint32_t)((r0 + u) * 4) : kOOB, s);
   }
 }
+
+// State stores: a state that the 256 MB Infinity Cache can keep between
+// steps is written with the default policy (the next step reads it back from
+// the cache); a larger one is streamed past the L2, like the scans' outputs
+// (measured at 256 x 16 states of 64 x 64: 64 MiB, 23.9 us per step either
+// way; 2048 x 16: 512 MiB, 200 -> 189 us per step).
+constexpr int64_t kDecodeStreamBytes = int64_t(128) << 20;
+static bool decode_stream(int64_t S, int64_t H, int d, int m) { return S * H * (int64_t)d * m * 4 > kDecodeStreamBytes; }
 
 static hipError_t launch_decode_wide(int64_t S, int64_t H, int d, int m, float* W, const float* x,
                                      const float* g, const float* eta, float eta_scalar, float* y,
@@ -150,13 +158,19 @@ static hipError_t launch_decode_wide(int64_t S, int64_t H, int d, int m, float* 
   const int U = nch >= 16 ? 1 : 16 / nch;
   const int64_t bps = (m + 4 * U - 1) / (4 * U);
   const dim3 grid((unsigned)(S * H * bps)), block(256);
-#define GL_DECODE_W(N)                                                                             \
-  if (gt)                                                                                          \
-    hipLaunchKernelGGL((decode_wide_kernel<N, true>), grid, block, 0, s, W, x, g, eta, eta_scalar, \
-                       y, m, W0, H, al, as, rs, bps);                                              \
-  else                                                                                             \
-    hipLaunchKernelGGL((decode_wide_kernel<N, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, \
-                       y, m, W0, H, al, as, rs, bps);
+  const bool st = decode_stream(S, H, d, m);
+#define GL_DECODE_W1(N, G, ST)                                                                    \
+  hipLaunchKernelGGL((decode_wide_kernel<N, G, ST>), grid, block, 0, s, W, x, g, eta, eta_scalar, \
+                     y, m, W0, H, al, as, rs, bps)
+#define GL_DECODE_W(N)              \
+  if (gt && st)                     \
+    GL_DECODE_W1(N, true, true);    \
+  else if (gt)                      \
+    GL_DECODE_W1(N, true, false);   \
+  else if (st)                      \
+    GL_DECODE_W1(N, false, true);   \
+  else                              \
+    GL_DECODE_W1(N, false, false);
   switch (nch) {
     case 2: GL_DECODE_W(2) break;
     case 4: GL_DECODE_W(4) break;
@@ -166,6 +180,7 @@ static hipError_t launch_decode_wide(int64_t S, int64_t H, int d, int m, float* 
     default: return hipErrorInvalidValue;
   }
 #undef GL_DECODE_W
+#undef GL_DECODE_W1
   return hipGetLastError();
 }
 
@@ -177,11 +192,19 @@ hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const flo
   const float* al = gt ? gt->alpha : nullptr;
   const float as = gt ? gt->alpha_scalar : 1.f;
   const uint8_t* rs = gt ? gt->reset : nullptr;
-#define GL_DECODE(DD)                                                                                   \
-  if (gt)                                                                                               \
-    hipLaunchKernelGGL((decode_kernel<DD, true>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs); \
-  else                                                                                                  \
-    hipLaunchKernelGGL((decode_kernel<DD, false>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, W0, H, al, as, rs);
+  const bool st = decode_stream(S, H, d, m);
+#define GL_DECODE1(DD, G, ST)                                                                    \
+  hipLaunchKernelGGL((decode_kernel<DD, G, ST>), grid, block, 0, s, W, x, g, eta, eta_scalar, y, m, \
+                     W0, H, al, as, rs)
+#define GL_DECODE(DD)            \
+  if (gt && st)                  \
+    GL_DECODE1(DD, true, true);  \
+  else if (gt)                   \
+    GL_DECODE1(DD, true, false); \
+  else if (st)                   \
+    GL_DECODE1(DD, false, true); \
+  else                           \
+    GL_DECODE1(DD, false, false);
   timing_begin(GRADLEV_K_DECODE, s);
   if (d > 256) {
     const hipError_t e = launch_decode_wide(S, H, d, m, W, x, g, eta, eta_scalar, y, s, gt);
@@ -197,6 +220,7 @@ hipError_t launch_decode(int64_t S, int64_t H, int d, int m, float* W, const flo
     default: timing_end(GRADLEV_K_DECODE, s); return hipErrorInvalidValue;
   }
 #undef GL_DECODE
+#undef GL_DECODE1
   timing_end(GRADLEV_K_DECODE, s);
   return hipGetLastError();
 }

@@ -257,8 +257,9 @@ __device__ __forceinline__ float buf_load1(rsrc_t r, uint32_t off) {
 // kernels only, so they are stored non-temporal at device scope (cache-policy
 // bits SC1 | NT): the lines do not stay dirty in the XCD's L2, which otherwise
 // has to be written back before the next kernel starts (about 15% of a scan
-// step when measured).  The decode state is read again by the next step and
-// keeps the default policy (measured: streaming stores cost it 15%).
+// step when measured).  A decode state small enough for the Infinity Cache
+// keeps the default policy (the next step reads it back from there); larger
+// ones are streamed too.
 constexpr int kStoreStream = 16 | 2;
 constexpr int kStoreDefault = 0;
 template <int POLICY = kStoreStream>
