@@ -23,10 +23,10 @@ struct KArgs {
   float* wend;   // fwd, or null: [BH][nsave][m][d] fast weights after each save_len-token block
   int64_t save_len, nsave;
   // Document resets (unit retention): reset [B][T] uint8, 1 where a document
-  // starts.  cstate [BH][ceil(T/C)][m][d]: the forward stores the state at the
-  // start of every chunk holding a reset there.  aggF [BH][nseg][d][m]: the
-  // backward's full dY x^T per segment (for dW0; aggB then holds the part
-  // before the segment's first reset).
+  // starts.  cstate [BH][ceil(T/C)][d][m]: the forward stores the state at the
+  // start of every chunk holding a reset there, transposed.  aggF
+  // [BH][nseg][d][m]: the backward's full dY x^T per segment (for dW0; aggB
+  // then holds the part before the segment's first reset).
   const uint8_t* reset;
   float* cstate;
   float* aggF;
