@@ -138,6 +138,7 @@ bwd_main_kernel(const BArgs a) {
   RstReg<RST> ra, rb;
   const rsrc_t Et = eta_rsrc(a.eta, bh, T);
   const rsrc_t Rrow = reset_rsrc(RST ? a.reset : nullptr, bh / a.H, T);
+  const float* W0h = a.W0 + (bh % a.H) * M * D;  // this head's W_0 (rows after a reset read it)
   typedef Tile4<OP, C, D, NT> TX;
   typedef Tile4<OP, C, M, NT> TM;
   auto fetch = [&](TX& xr, TM& gr, TM& dr, EtaReg<ETAV>& er, RstReg<RST>& rr, int64_t n) {
@@ -413,7 +414,7 @@ bwd_main_kernel(const BArgs a) {
       }
       if constexpr (HAS) {
         {
-          const float* w0 = a.W0 + (bh % a.H) * M * D;
+          const float* w0 = W0h;
 #pragma unroll
           for (int kb = 0; kb < M / 32; ++kb) {
             F wh[NWB], wl[NWB];

@@ -129,6 +129,13 @@ fwd_main_kernel(const KArgs a) {
   if constexpr (!RS)
     for (int i = tid; i < C * C; i += NT) Pl[i] = (E)0.f;
 
+  // Saved-state block of the chunk ends: index and end of the current block
+  // (save_len is a whole number of chunks and so divides t_begin).
+  int64_t save_idx = 0, save_next = -1;
+  if (a.wend) {
+    save_idx = t_begin / a.save_len;
+    save_next = (save_idx + 1) * a.save_len;
+  }
   auto chunk = [&](Tile4<OP, C, D, NT>& xr, Tile4<OP, C, M, NT>& gr, EtaReg<ETAV>& er, RstReg<RST>& rr,
                    int64_t t0) {
     // A step past the segment end (the second of a pair) sees zero tiles,
@@ -311,12 +318,17 @@ fwd_main_kernel(const KArgs a) {
       }
       // Saved for a backward: the fast weights after the last write of each
       // save_len-token block (and of the sequence), row-major [m][d]; lane
-      // (c, q) holds W[16w + c][16jb + 4q .. +3].
+      // (c, q) holds W[16w + c][16jb + 4q .. +3].  The blocks are whole
+      // chunks, so the next boundary is tracked instead of divided for.
       const int64_t te = t0 + C < t_end ? t0 + C : t_end;
-      if (a.wend && live && (te % a.save_len == 0 || te == T)) {
-        float* o = a.wend + (bh * a.nsave + (te - 1) / a.save_len) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
+      if (a.wend && live && (te == save_next || te == T)) {
+        float* o = a.wend + (bh * a.nsave + save_idx) * M * D + (int64_t)(16 * w + c) * D + 4 * q;
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) *reinterpret_cast<f32x4*>(o + 16 * jb) = Ws[jb];
+      }
+      if (live && te == save_next) {
+        save_next += a.save_len;
+        ++save_idx;
       }
     }
       };
