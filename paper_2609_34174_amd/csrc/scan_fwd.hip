@@ -65,7 +65,6 @@ fwd_main_kernel(const KArgs a) {
   const rsrc_t X = make_rsrc(static_cast<const E*>(a.X) + bh * T * D, (uint32_t)(T * D * sizeof(E)));
   const rsrc_t G = make_rsrc(static_cast<const E*>(a.G) + bh * T * M, (uint32_t)(T * M * sizeof(E)));
   const rsrc_t Y = make_rsrc(a.out0 + bh * T * M, (uint32_t)(T * M * 4));
-  const rsrc_t none = make_rsrc(nullptr, 0u);  // every access out of range
   // With resets: this sequence's chunk-start states (under 2 GiB, checked by the host).
   const int64_t nchs = (T + C - 1) / C;
   const rsrc_t Cst = make_rsrc(RST && a.cstate ? a.cstate + bh * nchs * M * D : nullptr,
@@ -142,7 +141,6 @@ fwd_main_kernel(const KArgs a) {
     // leaves the state unchanged and stores nothing.
     const bool live = t0 < t_end;
     const int nvalid = live ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
-    const rsrc_t Yc = live ? Y : none;
     __syncthreads();
     er.stage(et, C, a.eta_scalar, nvalid, -1.f, tid);
     xr.store(Xs, tid);
@@ -271,7 +269,9 @@ fwd_main_kernel(const KArgs a) {
       for (int tb = 0; tb < TB; ++tb) {
         // acc[tb][r] = y_t[i] with i = 16w + 4q + r, t = 16tb + c (rows past T are dropped).
         const int t = 16 * tb + c;
-        buf_store4(Yc, (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4), acc[tb]);
+        // A dead step's stores go past the resource's end (selecting the
+        // resource itself instead made the compiler loop over its values).
+        buf_store4(Y, live ? (uint32_t)(((t0 + t) * M + 16 * w + 4 * q) * 4) : kOOB, acc[tb]);
       }
     }
     // The eta-scaled V tiles were written by every wave; with register scores
