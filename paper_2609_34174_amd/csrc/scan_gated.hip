@@ -110,42 +110,110 @@ struct GateReg {
   }
 };
 
+// Cross-lane moves by DPP (a VALU operand modifier, no LDS round trip):
+// lane i reads lane i - N (SHR) or i + N (SHL) of its 16-lane row, or of the
+// whole wave (WAVE, N = 1); lanes without a source get `fill`.
+enum DppMove { kRowShr = 0x110, kRowShl = 0x100, kWaveShr1 = 0x138, kWaveShl1 = 0x130 };
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float src, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, src), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float lane_value(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Inclusive product scans inside each 16-lane row: upward (lane i: product
+// of lanes <= i of its row) or downward (lanes >= i).
+template <bool DOWN>
+__device__ __forceinline__ float row_scan_mul(float x) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) {
+    float t;
+    if (o == 1) t = dpp_move<(DOWN ? kRowShl : kRowShr) + 1>(x, 1.f);
+    else if (o == 2) t = dpp_move<(DOWN ? kRowShl : kRowShr) + 2>(x, 1.f);
+    else if (o == 4) t = dpp_move<(DOWN ? kRowShl : kRowShr) + 4>(x, 1.f);
+    else t = dpp_move<(DOWN ? kRowShl : kRowShr) + 8>(x, 1.f);
+    x *= t;
+  }
+  return x;
+}
+// The same over the whole wave: rows first, then each row times the totals
+// of the rows before it (after it, downward), read back from lanes 15, 31,
+// 47 (0, 16, 32, 48 downward) and multiplied in row order.
+template <bool DOWN>
+__device__ __forceinline__ float wave_scan_mul(float x, int lane) {
+  x = row_scan_mul<DOWN>(x);
+  const int row = lane >> 4;
+  if constexpr (!DOWN) {
+    const float r0 = lane_value(x, 15), r1 = lane_value(x, 31), r2 = lane_value(x, 47);
+    const float m1 = r0, m2 = r0 * r1, m3 = m2 * r2;
+    return x * (row == 0 ? 1.f : row == 1 ? m1 : row == 2 ? m2 : m3);
+  } else {
+    const float r1 = lane_value(x, 16), r2 = lane_value(x, 32), r3 = lane_value(x, 48);
+    const float m2 = r3, m1 = r2 * r3, m0 = r1 * m1;
+    return x * (row == 3 ? 1.f : row == 2 ? m2 : row == 1 ? m1 : m0);
+  }
+}
+
+// Inclusive scan of affine maps z -> A z + B over the wave: lane i ends with
+// its own map after those of the lanes below it (upward) or above it
+// (downward).  Rows by DPP, then each row after the composed maps of the
+// rows before it, read back from their end lanes.
+template <int O, bool DOWN>
+__device__ __forceinline__ void affine_step(float& A, float& B) {
+  const float pa = dpp_move<(DOWN ? kRowShl : kRowShr) + O>(A, 1.f);
+  const float pb = dpp_move<(DOWN ? kRowShl : kRowShr) + O>(B, 0.f);
+  B = A * pb + B;
+  A = A * pa;
+}
+template <bool DOWN>
+__device__ __forceinline__ void affine_scan(float& A, float& B, int lane) {
+  affine_step<1, DOWN>(A, B);
+  affine_step<2, DOWN>(A, B);
+  affine_step<4, DOWN>(A, B);
+  affine_step<8, DOWN>(A, B);
+  const int row = lane >> 4;
+  float ca, cb;  // composed map of the rows before (after) this one
+  if constexpr (!DOWN) {
+    const float a0 = lane_value(A, 15), b0 = lane_value(B, 15), a1 = lane_value(A, 31), b1 = lane_value(B, 31),
+                a2 = lane_value(A, 47), b2 = lane_value(B, 47);
+    const float c1a = a1 * a0, c1b = a1 * b0 + b1;
+    const float c2a = a2 * c1a, c2b = a2 * c1b + b2;
+    ca = row == 1 ? a0 : row == 2 ? c1a : c2a;
+    cb = row == 1 ? b0 : row == 2 ? c1b : c2b;
+    if (row == 0) return;
+  } else {
+    const float a3 = lane_value(A, 48), b3 = lane_value(B, 48), a2 = lane_value(A, 32), b2 = lane_value(B, 32),
+                a1 = lane_value(A, 16), b1 = lane_value(B, 16);
+    const float d2a = a2 * a3, d2b = a2 * b3 + b2;
+    const float d1a = a1 * d2a, d1b = a1 * d2b + b1;
+    ca = row == 2 ? a3 : row == 1 ? d2a : d1a;
+    cb = row == 2 ? b3 : row == 1 ? d2b : d1b;
+    if (row == 3) return;
+  }
+  B = A * cb + B;
+  A = A * ca;
+}
+
 // Decay products of a chunk (C <= 64), computed by one wave: lane t holds
-// alpha_t (1 for lanes >= C).  Log-step scans of products, whole chunk and
-// within 16-lane blocks.  Also vw[t] = vsign * eta_t * suf_t when vw != null.
+// alpha_t (1 for lanes >= C).  Product scans, whole chunk and within 16-lane
+// blocks.  Also vw[t] = vsign * eta_t * suf_t when vw != null.
 template <int C>
 __device__ __forceinline__ void gate_scan(const float* al, const float* et, float* pre, float* suf,
                                           float* pin, float* sinv, float* mid, float* tot,
                                           float* vw, float vsign, int lane) {
   constexpr int TB = C / 16;
   const float a = lane < C ? al[lane] : 1.f;
-  float p = a, s = a, pb = a, sb = a;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float u = __shfl_up(p, o);
-    if (lane >= o) p *= u;
-    const float v = __shfl_down(s, o);
-    if (lane + o < 64) s *= v;
-  }
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) {
-    const float u = __shfl_up(pb, o, 16);
-    if ((lane & 15) >= o) pb *= u;
-    const float v = __shfl_down(sb, o, 16);
-    if ((lane & 15) + o < 16) sb *= v;
-  }
-  float pex = __shfl_up(p, 1);
-  if (lane == 0) pex = 1.f;
-  float sex = __shfl_down(s, 1);
-  if (lane == 63) sex = 1.f;
-  float pbx = __shfl_up(pb, 1, 16);
-  if ((lane & 15) == 0) pbx = 1.f;
-  float sbx = __shfl_down(sb, 1, 16);
-  if ((lane & 15) == 15) sbx = 1.f;
+  const float pb = row_scan_mul<false>(a), sb = row_scan_mul<true>(a);
+  const float p = wave_scan_mul<false>(a, lane), s = wave_scan_mul<true>(a, lane);
+  const float pex = dpp_move<kWaveShr1>(p, 1.f);
+  const float sex = dpp_move<kWaveShl1>(s, 1.f);
+  const float pbx = dpp_move<kRowShr + 1>(pb, 1.f);
+  const float sbx = dpp_move<kRowShl + 1>(sb, 1.f);
   float blk[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) blk[k] = __shfl(pb, 16 * k + 15);
-  const float all = __shfl(p, 63);
+  for (int k = 0; k < 4; ++k) blk[k] = lane_value(pb, 16 * k + 15);
+  const float all = lane_value(p, 63);
   if (lane < C) {
     pre[lane] = pex;
     suf[lane] = sex;
@@ -918,24 +986,11 @@ bwd_gated_kernel(const GArgs a) {
       if (!in) c3 = c2 = 0.f;
       const float at = in ? al[tc] : 1.f;
       // z_t = alpha_{t-1} z_{t-1} + c2_{t-1}:  affine scan (A, B) upward.
-      float A = __shfl_up(at, 1), B = __shfl_up(c2, 1);
-      if (ln == 0) A = 0.f, B = 0.f;
+      float A = dpp_move<kWaveShr1>(at, 0.f), B = dpp_move<kWaveShr1>(c2, 0.f);
       // w_t = alpha_{t+1} w_{t+1} + c3_{t+1}: affine scan downward.
-      float A2 = __shfl_down(at, 1), B2 = __shfl_down(c3, 1);
-      if (ln == 63) A2 = 0.f, B2 = 0.f;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const float pa = __shfl_up(A, o), pb = __shfl_up(B, o);
-        if (ln >= o) {
-          B = A * pb + B;
-          A = A * pa;
-        }
-        const float qa = __shfl_down(A2, o), qb = __shfl_down(B2, o);
-        if (ln + o < 64) {
-          B2 = A2 * qb + B2;
-          A2 = A2 * qa;
-        }
-      }
+      float A2 = dpp_move<kWaveShl1>(at, 0.f), B2 = dpp_move<kWaveShl1>(c3, 0.f);
+      affine_scan<false>(A, B, ln);
+      affine_scan<true>(A2, B2, ln);
       if (in) {
         const float pt = pre[tc], st = suf[tc];
         const float dal = (pt * st * t1 + pt * B2 + st * B + da) * gm[tc];
