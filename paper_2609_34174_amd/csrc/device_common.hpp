@@ -253,6 +253,34 @@ __device__ __forceinline__ f32x4 buf_load4(rsrc_t r, uint32_t off, const float*)
 __device__ __forceinline__ float buf_load1(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
 }
+// Cross-lane moves by DPP (a VALU operand modifier, no LDS round trip):
+// lane i reads lane i - N (SHR) or i + N (SHL) of its 16-lane row, or of the
+// whole wave (WAVE, N = 1), or lane (i + N) mod 16 of its row (ROR); lanes
+// without a source get `fill`.
+enum DppMove { kRowShr = 0x110, kRowShl = 0x100, kRowRor = 0x120, kWaveShr1 = 0x138, kWaveShl1 = 0x130 };
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float src, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, src), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float lane_value(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Sum over each 16-lane row, in every lane of the row.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dpp_move<kRowRor + 8>(x, 0.f);
+  x += dpp_move<kRowRor + 4>(x, 0.f);
+  x += dpp_move<kRowRor + 2>(x, 0.f);
+  x += dpp_move<kRowRor + 1>(x, 0.f);
+  return x;
+}
+// Sum over the wave (the same value in every lane): the row sums added in
+// row order.
+__device__ __forceinline__ float wave_sum(float x) {
+  x = row_sum16(x);
+  return ((lane_value(x, 0) + lane_value(x, 16)) + lane_value(x, 32)) + lane_value(x, 48);
+}
+
 // Store cache policies.  Scan outputs are written once and read by later
 // kernels only, so they are stored non-temporal at device scope (cache-policy
 // bits SC1 | NT): the lines do not stay dirty in the XCD's L2, which otherwise

@@ -110,18 +110,6 @@ struct GateReg {
   }
 };
 
-// Cross-lane moves by DPP (a VALU operand modifier, no LDS round trip):
-// lane i reads lane i - N (SHR) or i + N (SHL) of its 16-lane row, or of the
-// whole wave (WAVE, N = 1); lanes without a source get `fill`.
-enum DppMove { kRowShr = 0x110, kRowShl = 0x100, kWaveShr1 = 0x138, kWaveShl1 = 0x130 };
-template <int CTRL>
-__device__ __forceinline__ float dpp_move(float src, float fill) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
-                                                               __builtin_bit_cast(int, src), CTRL, 0xf, 0xf, false));
-}
-__device__ __forceinline__ float lane_value(float v, int l) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
-}
 // Inclusive product scans inside each 16-lane row: upward (lane i: product
 // of lanes <= i of its row) or downward (lanes >= i).
 template <bool DOWN>
@@ -798,8 +786,7 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) t1 += Lam[ib][r] * dn[ib][r];
       }
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) t1 += __shfl_xor(t1, o);
+      t1 = wave_sum(t1);
       if (ln == 0) t1p[w] = t1;
     }
     __syncthreads();
