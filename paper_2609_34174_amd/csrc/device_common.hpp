@@ -84,6 +84,88 @@ __device__ __forceinline__ int lds_off(int r, int k, int K) {
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+// The lane-dependent part of the fragment addresses into a [rows][K] tile of
+// ES-byte elements.  For a row block starting at a multiple of 16 the swizzle
+// key of row row0 + (lane % 16) is the lane's own, and a 4-chunk step of the
+// column changes the XORed chunk index by a constant: so every address of the
+// fragment reads below is one of four per-lane byte offsets plus a
+// compile-time constant.
+//   n[j]: row lane%16, chunk (4j + q) ^ swz     (load_n halves, 4-element stores)
+//   t[j]: row 4q + c/4, chunk (4j + c%4) ^ swz  (load_t halves)
+// with q = lane / 16, c = lane % 16.  With PRE the offsets are computed once
+// and pass through an empty asm statement, so the compiler can neither
+// re-derive them per use from the lane nor hoist every derived address into
+// a register of its own (8 registers per tile width); without PRE every
+// address is formed from the lane where it is used.
+template <int K, int ES, bool PRE>
+struct LaneOff {
+  static constexpr int NJ = K >= 64 ? 4 : K / 16;
+  int n[PRE ? NJ : 1], t[PRE ? NJ : 1], lane;
+  // Byte offset of element (row0 + c, k + 4q); row0 and k multiples of 16.
+  __device__ __forceinline__ int nat(int row0, int k) const {
+    if constexpr (!PRE) return lds_off(row0 + (lane & 15), k + 4 * (lane >> 4), K) * ES;
+    const int kc = k >> 2;
+    return (row0 * K + 4 * (kc & ~15)) * ES + n[(kc >> 2) & 3];
+  }
+  // Byte offset of element (r0 + 4q + c/4, n0 + 4(c%4)); r0 and n0 multiples of 16.
+  __device__ __forceinline__ int tat(int r0, int n0) const {
+    if constexpr (!PRE) return lds_off(r0 + 4 * (lane >> 4) + ((lane & 15) >> 2), n0 + 4 * (lane & 3), K) * ES;
+    const int kc = n0 >> 2;
+    return (r0 * K + 4 * (kc & ~15)) * ES + t[(kc >> 2) & 3];
+  }
+  // The same for a column known only at run time (wave-uniform): with PRE
+  // the variant is picked by selects, once, and the result kept opaque.
+  __device__ __forceinline__ int nat_rt(int row0, int k) const {
+    if constexpr (!PRE) return nat(row0, k);
+    return pick(row0, k, n);
+  }
+  __device__ __forceinline__ int tat_rt(int r0, int n0) const {
+    if constexpr (!PRE) return tat(r0, n0);
+    return pick(r0, n0, t);
+  }
+
+ private:
+  template <int N>
+  __device__ __forceinline__ int pick(int r0, int col, const int (&v)[N]) const {
+    const int kc = col >> 2, j = (kc >> 2) & 3;
+    int x = v[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) x = j == i ? v[i] : x;
+    x += (r0 * K + 4 * (kc & ~15)) * ES;
+    asm volatile("" : "+v"(x));
+    return x;
+  }
+};
+template <int K, int ES, bool PRE>
+__device__ __forceinline__ LaneOff<K, ES, PRE> lane_off(int lane) {
+  LaneOff<K, ES, PRE> o;
+  o.lane = lane;
+  if constexpr (PRE) {
+    const int c = lane & 15, q = lane >> 4, sn = swz(c, K), st = swz(4 * q + (c >> 2), K);
+#pragma unroll
+    for (int j = 0; j < LaneOff<K, ES, PRE>::NJ; ++j) {
+      o.n[j] = (c * K + 4 * ((4 * j + q) ^ sn)) * ES;
+      o.t[j] = ((4 * q + (c >> 2)) * K + 4 * ((4 * j + (c & 3)) ^ st)) * ES;
+      asm volatile("" : "+v"(o.n[j]), "+v"(o.t[j]));
+    }
+  }
+  return o;
+}
+// The offsets of width K2 given those of width K1 (shared when equal).
+template <int K2, int K1, int ES, bool PRE>
+__device__ __forceinline__ LaneOff<K2, ES, PRE> lane_off_like(const LaneOff<K1, ES, PRE>& o) {
+  if constexpr (K1 == K2) return o;
+  else return lane_off<K2, ES, PRE>(o.lane);
+}
+template <class T>
+__device__ __forceinline__ const T& at_byte(const void* base, int off) {
+  return *reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+template <class T>
+__device__ __forceinline__ T* ptr_byte(void* base, int off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
 // ---------------------------------------------------------------------------
 // Operand policies.  load_n reads the fragment of row (row0 + c) of a tile
 // with k along the tile's columns; load_t reads it with k along the tile's
@@ -124,6 +206,36 @@ struct OpBF16 {
     const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + lds_off(r + 16, n, K)));
     const i16x8 v = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
     return __builtin_bit_cast(frag, v);
+  }
+  // The same reads from precomputed lane offsets (row0, k0, n0 multiples of
+  // 16); tcol is the offset of a transposed read's column block chosen at
+  // run time.
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_n(const elem* base, const LaneOff<K, 2, PRE>& L, int row0, int k0) {
+    const bf16x4 a = at_byte<bf16x4>(base, L.nat(row0, k0));
+    const bf16x4 b = at_byte<bf16x4>(base, L.nat(row0, k0 + 16));
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
+  __device__ static __forceinline__ frag tr_pair(const elem* base, int oa, int ob) {
+    const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)((const char*)base + oa));
+    const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)((const char*)base + ob));
+    const i16x8 v = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(frag, v);
+  }
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 2, PRE>& L, int k0, int n0) {
+    return tr_pair(base, L.tat(k0, n0), L.tat(k0 + 16, n0));
+  }
+  struct tcol {
+    int off;
+  };
+  template <int K, bool PRE>
+  __device__ static __forceinline__ tcol make_tcol(const LaneOff<K, 2, PRE>& L, int n0) {
+    return tcol{L.tat_rt(0, n0)};
+  }
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 2, PRE>&, int k0, tcol col) {
+    return tr_pair(base, k0 * K * 2 + col.off, (k0 + 16) * K * 2 + col.off);
   }
   __device__ static __forceinline__ f32x8 to_f32(frag f) {
     f32x8 v;
@@ -196,6 +308,26 @@ struct OpF32 {
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = base[lds_off(k0 + slot_k(e, q), n0 + c, K)];
     return v;
+  }
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_n(const elem* base, const LaneOff<K, 4, PRE>& L, int row0, int k0) {
+    return cat(at_byte<f32x4>(base, L.nat(row0, k0)), at_byte<f32x4>(base, L.nat(row0, k0 + 16)));
+  }
+  // fp32 transposed fragments are gathered element by element from the lane.
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 4, PRE>& L, int k0, int n0) {
+    return load_t(base, K, k0, n0, L.lane);
+  }
+  struct tcol {
+    int n0;
+  };
+  template <int K, bool PRE>
+  __device__ static __forceinline__ tcol make_tcol(const LaneOff<K, 4, PRE>&, int n0) {
+    return tcol{n0};
+  }
+  template <int K, bool PRE>
+  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 4, PRE>& L, int k0, tcol col) {
+    return load_t(base, K, k0, col.n0, L.lane);
   }
   __device__ static __forceinline__ f32x8 to_f32(frag f) { return f; }
   __device__ static __forceinline__ frag neg(frag f) { return -f; }

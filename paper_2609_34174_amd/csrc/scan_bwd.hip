@@ -227,6 +227,23 @@ bwd_main_kernel(const BArgs a) {
     int ln = lane, td = tid;
     asm volatile("" : "+v"(ln), "+v"(td));
     const int c = ln & 15, q = ln >> 4;
+    // Fragment address offsets of this lane for the tile widths in use, and
+    // those of the wave's own column blocks (known only at run time).
+    // Precomputed for square maps; with d != m the extra offset sets would
+    // cost more registers than they save.
+    constexpr bool PRE = D == M;
+    const LaneOff<D, sizeof(E), PRE> lD = lane_off<D, sizeof(E), PRE>(ln);
+    const LaneOff<M, sizeof(E), PRE> lM = lane_off_like<M>(lD);
+    const LaneOff<C, sizeof(E), PRE> lC = lane_off_like<C>(lM);
+    typename OP::tcol tD[NWB], tM[NWB];
+    int nM[NWB];
+#pragma unroll
+    for (int e = 0; e < NWB; ++e) {
+      tD[e] = OP::make_tcol(lD, 16 * blk(e));
+      if constexpr (D == M) tM[e] = tD[e];
+      else tM[e] = OP::make_tcol(lM, 16 * blk(e));
+      nM[e] = lM.nat_rt(0, 16 * blk(e));
+    }
     const int64_t t0 = t_begin + n * C;
     const bool live = n >= 0;
     const int nvalid = live ? (int)(t_end - t0 < C ? t_end - t0 : C) : 0;
@@ -272,7 +289,7 @@ bwd_main_kernel(const BArgs a) {
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb)
-        acc = OP::mma(acc, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+        acc = OP::mma(acc, OP::load_n(Gs, lM, 16 * sb, 32 * kb), OP::load_n(Ds, lM, 16 * tb, 32 * kb));
       const int t = 16 * tb + c;
       // eta of the four s of this lane, read unconditionally (a select, not a branch per element).
       const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
@@ -283,7 +300,7 @@ bwd_main_kernel(const BArgs a) {
         if constexpr (HAS) keep = keep && same_doc(dm, s, t);
         acc[r] = keep ? acc[r] * es[r] : 0.f;
       }
-      OP::store4(Es + lds_off(t, 16 * sb + 4 * q, C), acc);
+      OP::store4(ptr_byte<E>(Es, lC.nat(16 * tb, 16 * sb)), acc);
     }
     if constexpr (SSH) {
       // Score tiles st[r] = x_s . x_t for the same (s, t) pairs, masked alike.
@@ -296,7 +313,7 @@ bwd_main_kernel(const BArgs a) {
         f32x4 st = zero4();
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb)
-          st = OP::mma(st, OP::load_n(Xs, D, 16 * sb, 32 * kb, ln), OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
+          st = OP::mma(st, OP::load_n(Xs, lD, 16 * sb, 32 * kb), OP::load_n(Xs, lD, 16 * tb, 32 * kb));
         const int t = 16 * tb + c;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -305,15 +322,15 @@ bwd_main_kernel(const BArgs a) {
           if constexpr (HAS) keep = keep && same_doc(dm, s, t);
           if (!keep) st[r] = 0.f;
         }
-        const int o = lds_off(t, 16 * sb + 4 * q, C);
-        OP::store4_split(Sh + o, Sl + o, st);
+        const int o = lC.nat(16 * tb, 16 * sb);
+        OP::store4_split(ptr_byte<E>(Sh, o), ptr_byte<E>(Sl, o), st);
       }
     }
     if (FULL && w < JB) {
 #pragma unroll
       for (int ib = 0; ib < IB; ++ib) {
-        const int o = lds_off(16 * w + c, 16 * ib + 4 * q, M);
-        OP::store4_split(Rh + o, Rl + o, Rj[ib]);
+        const int o = lM.nat(16 * w, 16 * ib);
+        OP::store4_split(ptr_byte<E>(Rh, o), ptr_byte<E>(Rl, o), Rj[ib]);
       }
     }
     __syncthreads();
@@ -325,7 +342,7 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
       for (int e = 0; e < NWB; ++e)
 #pragma unroll
-        for (int kb = 0; kb < C / 32; ++kb) xt[e][kb] = OP::load_t(Xs, D, 32 * kb, 16 * blk(e), ln);
+        for (int kb = 0; kb < C / 32; ++kb) xt[e][kb] = OP::load_t(Xs, lD, 32 * kb, tD[e]);
     }
 
     // (2) Un-write this chunk: W_n = W_{n+1} + (eta G)^T X (a chunk holding a
@@ -336,9 +353,9 @@ bwd_main_kernel(const BArgs a) {
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
-            const F vh = OP::load_t(Vh, M, 32 * kb, 16 * ib, ln);
+            const F vh = OP::load_t(Vh, lM, 32 * kb, 16 * ib);
             F vl = vh;
-            if constexpr (SPLITV) vl = OP::load_t(Vl, M, 32 * kb, 16 * ib, ln);
+            if constexpr (SPLITV) vl = OP::load_t(Vl, lM, 32 * kb, 16 * ib);
 #pragma unroll
             for (int e = 0; e < NWB; ++e) Wj[e][ib] = mma_split_a<OP>(Wj[e][ib], vh, vl, xt[e][kb]);
           }
@@ -353,7 +370,7 @@ bwd_main_kernel(const BArgs a) {
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
-            const F gq = OP::load_t(Gs, M, 32 * kb, 16 * ib, ln);
+            const F gq = OP::load_t(Gs, lM, 32 * kb, 16 * ib);
 #pragma unroll
             for (int e = 0; e < NWB; ++e) dw[e][ib] = OP::mma(dw[e][ib], gq, xt[e][kb]);
           }
@@ -390,17 +407,17 @@ bwd_main_kernel(const BArgs a) {
         for (int e = 0; e < NWB; ++e) {
           OP::split(cat(Wj[e][2 * kb], Wj[e][2 * kb + 1]), wh[e], wl[e]);
           if (FULL) {
-            rh[e] = OP::load_n(Rh, M, 16 * blk(e), 32 * kb, ln);
+            rh[e] = OP::load_n(Rh, lM, 16 * blk(e), 32 * kb);
             rl[e] = rh[e];
-            if constexpr (OP::kSplit == 2) rl[e] = OP::load_n(Rl, M, 16 * blk(e), 32 * kb, ln);
+            if constexpr (OP::kSplit == 2) rl[e] = OP::load_n(Rl, lM, 16 * blk(e), 32 * kb);
           }
         }
 #pragma unroll
         for (int hh = 0; hh < TBW; ++hh) {
           const int tb = tok3(hh);
-          F dq = OP::load_n(Ds, M, 16 * tb, 32 * kb, ln);
+          F dq = OP::load_n(Ds, lM, 16 * tb, 32 * kb);
           F gq;
-          if (FULL) gq = OP::load_n(Gs, M, 16 * tb, 32 * kb, ln);
+          if (FULL) gq = OP::load_n(Gs, lM, 16 * tb, 32 * kb);
           if constexpr (HAS) {
             dq = keep_row<OP>(dq, 16 * tb + c < fr);  // rows after the first reset read W_0 (below)
             if (FULL) gq = keep_row<OP>(gq, 16 * tb + c >= lr);  // only the last document sees R_n
@@ -429,7 +446,7 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
             for (int hh = 0; hh < TBW; ++hh) {
               const int tb = tok3(hh);
-              const F dq = keep_row<OP>(OP::load_n(Ds, M, 16 * tb, 32 * kb, ln), 16 * tb + c >= fr);
+              const F dq = keep_row<OP>(OP::load_n(Ds, lM, 16 * tb, 32 * kb), 16 * tb + c >= fr);
 #pragma unroll
               for (int e = 0; e < NWB; ++e) ga[e][hh] = mma_split_a<OP>(ga[e][hh], wh[e], wl[e], dq);
             }
@@ -451,12 +468,12 @@ bwd_main_kernel(const BArgs a) {
         for (int hh = 0; hh < TBW; ++hh) {
           const int tb = tok3(hh);
           if (kb <= tb / 2) {
-            const F ef = OP::load_n(Es, C, 16 * tb, 32 * kb, ln);
+            const F ef = OP::load_n(Es, lC, 16 * tb, 32 * kb);
 #pragma unroll
             for (int e = 0; e < NWB; ++e) ga[e][hh] = OP::mma(ga[e][hh], OP::neg(xt[e][kb]), ef);
           }
           if (FULL && kb >= tb / 2) {
-            const F ef = OP::load_t(Es, C, 32 * kb, 16 * tb, ln);
+            const F ef = OP::load_t(Es, lC, 32 * kb, 16 * tb);
 #pragma unroll
             for (int e = 0; e < NWB; ++e) xa2[e][hh] = OP::mma(xa2[e][hh], xt[e][kb], ef);
           }
@@ -504,11 +521,11 @@ bwd_main_kernel(const BArgs a) {
 #pragma unroll
           for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-            for (int kb = 0; kb < D / 32; ++kb) xr[tb][kb] = OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
+            for (int kb = 0; kb < D / 32; ++kb) xr[tb][kb] = OP::load_n(Xs, lD, 16 * tb, 32 * kb);
         }
         auto xrow = [&](int tb, int kb) -> F {
           if constexpr (XCACHE) return xr[tb][kb];
-          else return OP::load_n(Xs, D, 16 * tb, 32 * kb, ln);
+          else return OP::load_n(Xs, lD, 16 * tb, 32 * kb);
         };
         // -U^T[i][s] = sum_j R[i][j] X[s][j] + sum_t dY[t][i] S[t][s]
 #pragma unroll
@@ -516,9 +533,9 @@ bwd_main_kernel(const BArgs a) {
           F rh[NWB], rl[NWB];
 #pragma unroll
           for (int e = 0; e < NWB; ++e) {
-            rh[e] = OP::load_t(Rh, M, 32 * kb, 16 * blk(e), ln);
+            rh[e] = OP::load_t(Rh, lM, 32 * kb, tM[e]);
             rl[e] = rh[e];
-            if constexpr (OP::kSplit == 2) rl[e] = OP::load_t(Rl, M, 32 * kb, 16 * blk(e), ln);
+            if constexpr (OP::kSplit == 2) rl[e] = OP::load_t(Rl, lM, 32 * kb, tM[e]);
           }
 #pragma unroll
           for (int hh = 0; hh < TBW; ++hh) {
@@ -535,14 +552,14 @@ bwd_main_kernel(const BArgs a) {
           for (int kb = 0; kb < C / 32; ++kb) {
             F dq[NWB];
 #pragma unroll
-            for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, M, 32 * kb, 16 * blk(e), ln);
+            for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, lM, 32 * kb, tM[e]);
 #pragma unroll
             for (int hh = 0; hh < TBW; ++hh) {
               const int sb = tok4(hh);
               if (sb > 2 * kb + 1) continue;
-              const F sh = OP::load_t(Sh, C, 32 * kb, 16 * sb, ln);
+              const F sh = OP::load_t(Sh, lC, 32 * kb, 16 * sb);
               F sl = sh;
-              if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, C, 32 * kb, 16 * sb, ln);
+              if constexpr (OP::kSplit == 2) sl = OP::load_t(Sl, lC, 32 * kb, 16 * sb);
 #pragma unroll
               for (int e = 0; e < NWB; ++e) ua[e][hh] = mma_split_b<OP>(ua[e][hh], dq[e], sh, sl);
             }
@@ -555,7 +572,7 @@ bwd_main_kernel(const BArgs a) {
         for (int kb = 0; kb < C / 32; ++kb) {
           F dq[NWB];
 #pragma unroll
-          for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, M, 32 * kb, 16 * blk(e), ln);
+          for (int e = 0; e < NWB; ++e) dq[e] = OP::load_t(Ds, lM, 32 * kb, tM[e]);
 #pragma unroll
           for (int hh = 0; hh < TBW; ++hh) {
             const int sb = tok4(hh);
@@ -613,7 +630,7 @@ bwd_main_kernel(const BArgs a) {
             float p = 0.f;
 #pragma unroll
             for (int e = 0; e < NWB; ++e) {
-              const vec4 gv = *reinterpret_cast<const vec4*>(Gs + lds_off(s, 16 * blk(e) + 4 * q, M));
+              const vec4 gv = at_byte<vec4>(Gs, 16 * sb * M * (int)sizeof(E) + nM[e]);
 #pragma unroll
               for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[e][hh][r];
             }
@@ -637,7 +654,7 @@ bwd_main_kernel(const BArgs a) {
         for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
           for (int ib = 0; ib < IB; ++ib) {
-            F dsf = OP::load_t(Ds, M, 32 * kb, 16 * ib, ln);
+            F dsf = OP::load_t(Ds, lM, 32 * kb, 16 * ib);
             if constexpr (HAS) dsf = mask_k<OP>(dsf, 32 * kb, q, 0, fr);
             Rj[ib] = OP::mma(Rj[ib], dsf, xt[PAIR ? H : 0][kb]);
           }
