@@ -105,34 +105,39 @@ struct LaneOff {
   __device__ __forceinline__ int nat(int row0, int k) const {
     if constexpr (!PRE) return lds_off(row0 + (lane & 15), k + 4 * (lane >> 4), K) * ES;
     const int kc = k >> 2;
-    return (row0 * K + 4 * (kc & ~15)) * ES + n[(kc >> 2) & 3];
+    return (row0 * K + 4 * (kc & ~15)) * ES + sel(n, (kc >> 2) & 3);
   }
   // Byte offset of element (r0 + 4q + c/4, n0 + 4(c%4)); r0 and n0 multiples of 16.
   __device__ __forceinline__ int tat(int r0, int n0) const {
     if constexpr (!PRE) return lds_off(r0 + 4 * (lane >> 4) + ((lane & 15) >> 2), n0 + 4 * (lane & 3), K) * ES;
     const int kc = n0 >> 2;
-    return (r0 * K + 4 * (kc & ~15)) * ES + t[(kc >> 2) & 3];
+    return (r0 * K + 4 * (kc & ~15)) * ES + sel(t, (kc >> 2) & 3);
   }
   // The same for a column known only at run time (wave-uniform): with PRE
-  // the variant is picked by selects, once, and the result kept opaque.
+  // the offset is formed once from the lane (no run-time index into the
+  // arrays above, which would move them to scratch memory) and kept opaque.
   __device__ __forceinline__ int nat_rt(int row0, int k) const {
     if constexpr (!PRE) return nat(row0, k);
-    return pick(row0, k, n);
+    const int kc = k >> 2, c = lane & 15, q = lane >> 4;
+    int x = (row0 * K + 4 * (kc & ~15) + c * K + 4 * ((kc & 12) + q ^ swz(c, K))) * ES;
+    asm volatile("" : "+v"(x));
+    return x;
   }
   __device__ __forceinline__ int tat_rt(int r0, int n0) const {
     if constexpr (!PRE) return tat(r0, n0);
-    return pick(r0, n0, t);
+    const int kc = n0 >> 2, c = lane & 15, q = lane >> 4;
+    int x = (r0 * K + 4 * (kc & ~15) + (4 * q + (c >> 2)) * K + 4 * ((kc & 12) + (c & 3) ^ swz(4 * q + (c >> 2), K))) * ES;
+    asm volatile("" : "+v"(x));
+    return x;
   }
 
  private:
+  // v[j] by selects (j a compile-time constant wherever these are used).
   template <int N>
-  __device__ __forceinline__ int pick(int r0, int col, const int (&v)[N]) const {
-    const int kc = col >> 2, j = (kc >> 2) & 3;
+  __device__ static __forceinline__ int sel(const int (&v)[N], int j) {
     int x = v[0];
 #pragma unroll
     for (int i = 1; i < N; ++i) x = j == i ? v[i] : x;
-    x += (r0 * K + 4 * (kc & ~15)) * ES;
-    asm volatile("" : "+v"(x));
     return x;
   }
 };
@@ -212,6 +217,7 @@ struct OpBF16 {
   // run time.
   template <int K, bool PRE>
   __device__ static __forceinline__ frag load_n(const elem* base, const LaneOff<K, 2, PRE>& L, int row0, int k0) {
+    if constexpr (!PRE) return load_n(base, K, row0, k0, L.lane);
     const bf16x4 a = at_byte<bf16x4>(base, L.nat(row0, k0));
     const bf16x4 b = at_byte<bf16x4>(base, L.nat(row0, k0 + 16));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -224,18 +230,23 @@ struct OpBF16 {
   }
   template <int K, bool PRE>
   __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 2, PRE>& L, int k0, int n0) {
+    if constexpr (!PRE) return load_t(base, K, k0, n0, L.lane);
     return tr_pair(base, L.tat(k0, n0), L.tat(k0 + 16, n0));
   }
   struct tcol {
     int off;
   };
+  // (Without precomputed offsets tcol keeps the column and the address is
+  // formed at the read.)
   template <int K, bool PRE>
   __device__ static __forceinline__ tcol make_tcol(const LaneOff<K, 2, PRE>& L, int n0) {
-    return tcol{L.tat_rt(0, n0)};
+    if constexpr (PRE) return tcol{L.tat_rt(0, n0)};
+    else return tcol{n0};
   }
   template <int K, bool PRE>
-  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 2, PRE>&, int k0, tcol col) {
-    return tr_pair(base, k0 * K * 2 + col.off, (k0 + 16) * K * 2 + col.off);
+  __device__ static __forceinline__ frag load_t(const elem* base, const LaneOff<K, 2, PRE>& L, int k0, tcol col) {
+    if constexpr (PRE) return tr_pair(base, k0 * K * 2 + col.off, (k0 + 16) * K * 2 + col.off);
+    else return load_t(base, L, k0, col.off);
   }
   __device__ static __forceinline__ f32x8 to_f32(frag f) {
     f32x8 v;
@@ -311,6 +322,7 @@ struct OpF32 {
   }
   template <int K, bool PRE>
   __device__ static __forceinline__ frag load_n(const elem* base, const LaneOff<K, 4, PRE>& L, int row0, int k0) {
+    if constexpr (!PRE) return load_n(base, K, row0, k0, L.lane);
     return cat(at_byte<f32x4>(base, L.nat(row0, k0)), at_byte<f32x4>(base, L.nat(row0, k0 + 16)));
   }
   // fp32 transposed fragments are gathered element by element from the lane.

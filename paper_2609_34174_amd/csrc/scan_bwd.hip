@@ -242,7 +242,7 @@ bwd_main_kernel(const BArgs a) {
       tD[e] = OP::make_tcol(lD, 16 * blk(e));
       if constexpr (D == M) tM[e] = tD[e];
       else tM[e] = OP::make_tcol(lM, 16 * blk(e));
-      nM[e] = lM.nat_rt(0, 16 * blk(e));
+      nM[e] = PRE ? lM.nat_rt(0, 16 * blk(e)) : 0;
     }
     const int64_t t0 = t_begin + n * C;
     const bool live = n >= 0;
@@ -630,7 +630,7 @@ bwd_main_kernel(const BArgs a) {
             float p = 0.f;
 #pragma unroll
             for (int e = 0; e < NWB; ++e) {
-              const vec4 gv = at_byte<vec4>(Gs, 16 * sb * M * (int)sizeof(E) + nM[e]);
+              const vec4 gv = at_byte<vec4>(Gs, PRE ? 16 * sb * M * (int)sizeof(E) + nM[e] : lM.nat(16 * sb, 16 * blk(e)));
 #pragma unroll
               for (int r = 0; r < 4; ++r) p -= (float)gv[r] * ua[e][hh][r];
             }

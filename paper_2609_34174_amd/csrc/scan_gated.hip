@@ -765,6 +765,32 @@ bwd_gated_kernel(const GArgs a) {
     int ln = lane, td = tid;
     asm volatile("" : "+v"(ln), "+v"(td));
     const int c = ln & 15, q = ln >> 4;
+    // Fragment address offsets of this lane (precomputed at 64 x 64),
+    // those of the wave's own column blocks, and the lane part of the
+    // transposed element reads of the F tile (rows 4q + r, column c).
+    constexpr bool PRE = D == 64 && M == 64;
+    const LaneOff<D, sizeof(E), PRE> lD = lane_off<D, sizeof(E), PRE>(ln);
+    const LaneOff<M, sizeof(E), PRE> lM = lane_off_like<M>(lD);
+    const LaneOff<C, sizeof(E), PRE> lC = lane_off_like<C>(lM);
+    const int rw = SPLITW ? w - JB : w;  // row block of u and dG
+    const typename OP::tcol tDw = OP::make_tcol(lD, 16 * w), tMr = OP::make_tcol(lM, 16 * rw);
+    const int nDw = PRE ? lD.nat_rt(0, 16 * w) : 0, nMr = PRE ? lM.nat_rt(0, 16 * rw) : 0;
+    // Element r of the 4-element chunk (row 16tb + c, column 16wb + 4q) of
+    // X or G, and element (16ub + 4q + r, 16tb + c) of the F tile.
+    auto x_el = [&](int tb, int r) -> float {
+      if constexpr (PRE) return (float)at_byte<E>(Xs, 16 * tb * D * (int)sizeof(E) + nDw + r * (int)sizeof(E));
+      else return (float)Xs[lds_off(16 * tb + c, 16 * w + 4 * q + r, D)];
+    };
+    auto g_el = [&](int tb, int r) -> float {
+      if constexpr (PRE) return (float)at_byte<E>(Gs, 16 * tb * M * (int)sizeof(E) + nMr + r * (int)sizeof(E));
+      else return (float)Gs[lds_off(16 * tb + c, 16 * rw + 4 * q + r, M)];
+    };
+    int fcol = 4 * q * C + 4 * ((c >> 2) ^ q) + (c & 3);
+    if constexpr (PRE) asm volatile("" : "+v"(fcol));
+    auto f_off = [&](int ub, int tb, int r) {
+      if constexpr (PRE) return (16 * ub + r) * C + 4 * ((4 * tb) ^ ((4 * r) & (C / 4 - 1))) + fcol;
+      else return lds_off(16 * ub + 4 * q + r, 16 * tb + c, C);
+    };
     const int64_t t0 = n * C;
     const int nvalid = (int)(t_end - t0 < C ? t_end - t0 : C);
     f32x4 dn[IB];
@@ -781,8 +807,8 @@ bwd_gated_kernel(const GArgs a) {
       float t1 = 0.f;
 #pragma unroll
       for (int ib = 0; ib < IB; ++ib) {
-        const int o = lds_off(16 * w + c, 16 * ib + 4 * q, M);
-        OP::store4_split(LTh + o, LTl + o, Lam[ib]);
+        const int o = lM.nat(16 * w, 16 * ib);
+        OP::store4_split(ptr_byte<E>(LTh, o), ptr_byte<E>(LTl, o), Lam[ib]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) t1 += Lam[ib][r] * dn[ib][r];
       }
@@ -804,22 +830,22 @@ bwd_gated_kernel(const GArgs a) {
       f32x4 gx = zero4(), ed = zero4();
 #pragma unroll
       for (int kb = 0; kb < D / 32; ++kb)
-        gx = OP::mma(gx, OP::load_n(Xs, D, 16 * sb, 32 * kb, ln), OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
+        gx = OP::mma(gx, OP::load_n(Xs, lD, 16 * sb, 32 * kb), OP::load_n(Xs, lD, 16 * tb, 32 * kb));
 #pragma unroll
       for (int kb = 0; kb < M / 32; ++kb)
-        ed = OP::mma(ed, OP::load_n(Gs, M, 16 * sb, 32 * kb, ln), OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+        ed = OP::mma(ed, OP::load_n(Gs, lM, 16 * sb, 32 * kb), OP::load_n(Ds, lM, 16 * tb, 32 * kb));
       const f32x4 f = decay4<TB>(al, pin, sinv, mid, sb, tb, q, c);
       const f32x4 es = *reinterpret_cast<const f32x4*>(et + 16 * sb + 4 * q);
       const int t = 16 * tb + c;
       f32x4 kk;
 #pragma unroll
       for (int r = 0; r < 4; ++r) kk[r] = (16 * sb + 4 * q + r < t) ? -es[r] * ed[r] * gx[r] : 0.f;
-      const int o = lds_off(t, 16 * sb + 4 * q, C);
-      OP::store4_split(Plh + o, Pll + o, f);
-      OP::store4_split(Peh + o, Pel + o, f * ed);
-      OP::store4_split(E1h + o, E1l + o, -es * f * ed);
-      OP::store4_split(Pgh + o, Pgl + o, f * gx);
-      OP::store4_split(Kh + o, Kl + o, kk);
+      const int o = lC.nat(16 * tb, 16 * sb);
+      OP::store4_split(ptr_byte<E>(Plh, o), ptr_byte<E>(Pll, o), f);
+      OP::store4_split(ptr_byte<E>(Peh, o), ptr_byte<E>(Pel, o), f * ed);
+      OP::store4_split(ptr_byte<E>(E1h, o), ptr_byte<E>(E1l, o), -es * f * ed);
+      OP::store4_split(ptr_byte<E>(Pgh, o), ptr_byte<E>(Pgl, o), f * gx);
+      OP::store4_split(ptr_byte<E>(Kh, o), ptr_byte<E>(Kl, o), kk);
     }
     const float tt = tot;
     fetch(n - 1);
@@ -828,7 +854,7 @@ bwd_gated_kernel(const GArgs a) {
     F xt[C / 32];
     if (w < JB) {
 #pragma unroll
-      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, D, 32 * kb, 16 * w, ln);
+      for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, lD, 32 * kb, tDw);
       // Read side: gtilde = W_0^T dY + pre Delta_n^T dY - (E1 X); write side of dX.
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
@@ -838,23 +864,23 @@ bwd_gated_kernel(const GArgs a) {
         for (int kb = 0; kb < M / 32; ++kb) {
           F dh, dl;
           OP::split(cat(dn[2 * kb], dn[2 * kb + 1]), dh, dl);
-          ad = mma_split_a<OP>(ad, dh, dl, OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+          ad = mma_split_a<OP>(ad, dh, dl, OP::load_n(Ds, lM, 16 * tb, 32 * kb));
         }
         // c3_t partial: x_t . (Delta_n^T dY_t) over this wave's j.
         float c3 = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) c3 += (float)Xs[lds_off(t, 16 * w + 4 * q + r, D)] * ad[r];
+        for (int r = 0; r < 4; ++r) c3 += x_el(tb, r) * ad[r];
         c3 = sum_q(c3);
         if (q == 0) c3p[w][t] = c3;
         f32x4 ag = ad * pre[t];
 #pragma unroll
         for (int kb = 0; kb < M / 32; ++kb)
-          ag = mma_split_a<OP>(ag, w0h[kb], w0l[kb], OP::load_n(Ds, M, 16 * tb, 32 * kb, ln));
+          ag = mma_split_a<OP>(ag, w0h[kb], w0l[kb], OP::load_n(Ds, lM, 16 * tb, 32 * kb));
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F eh = OP::load_n(E1h, C, 16 * tb, 32 * kb, ln);
+          const F eh = OP::load_n(E1h, lC, 16 * tb, 32 * kb);
           F el = eh;
-          if constexpr (SPL) el = OP::load_n(E1l, C, 16 * tb, 32 * kb, ln);
+          if constexpr (SPL) el = OP::load_n(E1l, lC, 16 * tb, 32 * kb);
           ag = mma_split_b<OP>(ag, xt[kb], eh, el);
         }
         const uint32_t off = (uint32_t)(((t0 + t) * D + 16 * w + 4 * q) * 4);
@@ -866,13 +892,13 @@ bwd_gated_kernel(const GArgs a) {
           for (int kb = 0; kb < M / 32; ++kb) {
             F lh, ll;
             OP::split(cat(Lam[2 * kb], Lam[2 * kb + 1]), lh, ll);
-            qs = mma_split_a<OP>(qs, lh, ll, OP::load_n(Gs, M, 16 * tb, 32 * kb, ln));
+            qs = mma_split_a<OP>(qs, lh, ll, OP::load_n(Gs, lM, 16 * tb, 32 * kb));
           }
 #pragma unroll
           for (int kb = 0; kb < C / 32; ++kb) {
-            const F ph = OP::load_t(Peh, C, 32 * kb, 16 * tb, ln);
+            const F ph = OP::load_t(Peh, lC, 32 * kb, 16 * tb);
             F pl = ph;
-            if constexpr (SPL) pl = OP::load_t(Pel, C, 32 * kb, 16 * tb, ln);
+            if constexpr (SPL) pl = OP::load_t(Pel, lC, 32 * kb, 16 * tb);
             qi = mma_split_b<OP>(qi, xt[kb], ph, pl);
           }
           const f32x4 dx = ag - et[t] * (suf[t] * qs + qi);
@@ -881,7 +907,6 @@ bwd_gated_kernel(const GArgs a) {
       }
     }
     if (SPLITW ? (w >= JB && w < JB + IB) : w < IB) {
-      const int rw = SPLITW ? w - JB : w;  // row block of u and dG
       // u_t = -(suf_t Lambda_e x_t + sum_{u>t} F[u][t] (x_u . x_t) dY_u).
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
@@ -889,23 +914,23 @@ bwd_gated_kernel(const GArgs a) {
         f32x4 us = zero4(), ui = zero4();
 #pragma unroll
         for (int kb = 0; kb < D / 32; ++kb) {
-          const F lh = OP::load_t(LTh, M, 32 * kb, 16 * rw, ln);
+          const F lh = OP::load_t(LTh, lM, 32 * kb, tMr);
           F ll = lh;
-          if constexpr (SPL) ll = OP::load_t(LTl, M, 32 * kb, 16 * rw, ln);
-          us = mma_split_a<OP>(us, lh, ll, OP::load_n(Xs, D, 16 * tb, 32 * kb, ln));
+          if constexpr (SPL) ll = OP::load_t(LTl, lM, 32 * kb, tMr);
+          us = mma_split_a<OP>(us, lh, ll, OP::load_n(Xs, lD, 16 * tb, 32 * kb));
         }
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
-          const F ph = OP::load_t(Pgh, C, 32 * kb, 16 * tb, ln);
+          const F ph = OP::load_t(Pgh, lC, 32 * kb, 16 * tb);
           F pl = ph;
-          if constexpr (SPL) pl = OP::load_t(Pgl, C, 32 * kb, 16 * tb, ln);
-          ui = mma_split_b<OP>(ui, OP::load_t(Ds, M, 32 * kb, 16 * rw, ln), ph, pl);
+          if constexpr (SPL) pl = OP::load_t(Pgl, lC, 32 * kb, 16 * tb);
+          ui = mma_split_b<OP>(ui, OP::load_t(Ds, lM, 32 * kb, tMr), ph, pl);
         }
         const f32x4 u = -(suf[t] * us + ui);
         float c2 = 0.f, de = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float gv = (float)Gs[lds_off(t, 16 * rw + 4 * q + r, M)];
+          const float gv = g_el(tb, r);
           c2 += gv * us[r];
           de += gv * u[r];
         }
@@ -930,12 +955,12 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
         for (int kb = 0; kb < C / 32; ++kb) {
           if (32 * kb > 16 * tb + 15) break;
-          const F kh = OP::load_n(Kh, C, 16 * ub, 32 * kb, ln);
-          const F fh = OP::load_n(Plh, C, 16 * tb, 32 * kb, ln);
+          const F kh = OP::load_n(Kh, lC, 16 * ub, 32 * kb);
+          const F fh = OP::load_n(Plh, lC, 16 * tb, 32 * kb);
           z = OP::mma(z, kh, fh);
           if constexpr (SPL) {
-            z = OP::mma(z, OP::load_n(Kl, C, 16 * ub, 32 * kb, ln), fh);
-            z = OP::mma(z, kh, OP::load_n(Pll, C, 16 * tb, 32 * kb, ln));
+            z = OP::mma(z, OP::load_n(Kl, lC, 16 * ub, 32 * kb), fh);
+            z = OP::mma(z, kh, OP::load_n(Pll, lC, 16 * tb, 32 * kb));
           }
         }
         // z[r] = Z[u = 16ub + 4q + r][t = 16tb + c]
@@ -943,7 +968,7 @@ bwd_gated_kernel(const GArgs a) {
         float s = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int o = lds_off(16 * ub + 4 * q + r, t, C);
+          const int o = f_off(ub, tb, r);
           float fv = (float)Plh[o];
           if constexpr (SPL) fv += (float)Pll[o];
           s += fv * z[r];
@@ -994,9 +1019,9 @@ bwd_gated_kernel(const GArgs a) {
       for (int kb = 0; kb < C / 32; ++kb) {
 #pragma unroll
         for (int ib = 0; ib < IB; ++ib) {
-          const F ph = OP::load_t(Dph, M, 32 * kb, 16 * ib, ln);
+          const F ph = OP::load_t(Dph, lM, 32 * kb, 16 * ib);
           F pl = ph;
-          if constexpr (SPL) pl = OP::load_t(Dpl, M, 32 * kb, 16 * ib, ln);
+          if constexpr (SPL) pl = OP::load_t(Dpl, lM, 32 * kb, 16 * ib);
           Lam[ib] = mma_split_a<OP>(Lam[ib], ph, pl, xt[kb]);
         }
       }
