@@ -119,14 +119,14 @@ struct LaneOff {
   __device__ __forceinline__ int nat_rt(int row0, int k) const {
     if constexpr (!PRE) return nat(row0, k);
     const int kc = k >> 2, c = lane & 15, q = lane >> 4;
-    int x = (row0 * K + 4 * (kc & ~15) + c * K + 4 * ((kc & 12) + q ^ swz(c, K))) * ES;
+    int x = (row0 * K + 4 * (kc & ~15) + c * K + 4 * (((kc & 12) + q) ^ swz(c, K))) * ES;
     asm volatile("" : "+v"(x));
     return x;
   }
   __device__ __forceinline__ int tat_rt(int r0, int n0) const {
     if constexpr (!PRE) return tat(r0, n0);
     const int kc = n0 >> 2, c = lane & 15, q = lane >> 4;
-    int x = (r0 * K + 4 * (kc & ~15) + (4 * q + (c >> 2)) * K + 4 * ((kc & 12) + (c & 3) ^ swz(4 * q + (c >> 2), K))) * ES;
+    int x = (r0 * K + 4 * (kc & ~15) + (4 * q + (c >> 2)) * K + 4 * (((kc & 12) + (c & 3)) ^ swz(4 * q + (c >> 2), K))) * ES;
     asm volatile("" : "+v"(x));
     return x;
   }
