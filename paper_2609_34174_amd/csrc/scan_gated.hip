@@ -856,6 +856,33 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
       for (int kb = 0; kb < C / 32; ++kb) xt[kb] = OP::load_t(Xs, lD, 32 * kb, tDw);
       // Read side: gtilde = W_0^T dY + pre Delta_n^T dY - (E1 X); write side of dX.
+      // The chunk's state and Lambda_e are split once for all token blocks
+      // at 64 x 64 (elsewhere per block: the held halves would spill).
+      constexpr bool HOIST = D == 64 && M == 64;
+      F dnh[HOIST ? M / 32 : 1], dnl[HOIST ? M / 32 : 1], lmh[HOIST ? M / 32 : 1], lml[HOIST ? M / 32 : 1];
+      if constexpr (HOIST) {
+#pragma unroll
+        for (int kb = 0; kb < M / 32; ++kb) {
+          OP::split(cat(dn[2 * kb], dn[2 * kb + 1]), dnh[kb], dnl[kb]);
+          OP::split(cat(Lam[2 * kb], Lam[2 * kb + 1]), lmh[kb], lml[kb]);
+        }
+      }
+      auto dn_split = [&](int kb, F& h, F& l) {
+        if constexpr (HOIST) {
+          h = dnh[kb];
+          l = dnl[kb];
+        } else {
+          OP::split(cat(dn[2 * kb], dn[2 * kb + 1]), h, l);
+        }
+      };
+      auto lam_split = [&](int kb, F& h, F& l) {
+        if constexpr (HOIST) {
+          h = lmh[kb];
+          l = lml[kb];
+        } else {
+          OP::split(cat(Lam[2 * kb], Lam[2 * kb + 1]), h, l);
+        }
+      };
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
         const int t = 16 * tb + c;
@@ -863,7 +890,7 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
         for (int kb = 0; kb < M / 32; ++kb) {
           F dh, dl;
-          OP::split(cat(dn[2 * kb], dn[2 * kb + 1]), dh, dl);
+          dn_split(kb, dh, dl);
           ad = mma_split_a<OP>(ad, dh, dl, OP::load_n(Ds, lM, 16 * tb, 32 * kb));
         }
         // c3_t partial: x_t . (Delta_n^T dY_t) over this wave's j.
@@ -891,7 +918,7 @@ bwd_gated_kernel(const GArgs a) {
 #pragma unroll
           for (int kb = 0; kb < M / 32; ++kb) {
             F lh, ll;
-            OP::split(cat(Lam[2 * kb], Lam[2 * kb + 1]), lh, ll);
+            lam_split(kb, lh, ll);
             qs = mma_split_a<OP>(qs, lh, ll, OP::load_n(Gs, lM, 16 * tb, 32 * kb));
           }
 #pragma unroll
