@@ -972,9 +972,11 @@ bwd_gated_kernel(const GArgs a) {
     }
     if (a.dalpha) {
       // Z[u][t] = sum_s K[u][s] F[t][s]; column sums of F[u][t] Z[u][t] over u > t.
+      // With split roles the tiles are dealt from the u/dG waves first: the
+      // gtilde/dX waves have the longer phase before this one.
 #pragma unroll
       for (int idx = 0; idx < TB * (TB + 1) / 2; ++idx) {
-        if (idx % NW != w) continue;
+        if ((SPLITW ? (idx + JB) % NW : idx % NW) != w) continue;
         int ub = 0;
         while ((ub + 1) * (ub + 2) / 2 <= idx) ++ub;
         const int tb = idx - ub * (ub + 1) / 2;
