@@ -150,11 +150,12 @@ int make_saved_plan(const gradlev_shape* s, Plan* out, size_t* saved_bytes) {
 // Saved: segment-end weights [BH][nseg_b][m][d], then the chunk-start states
 // [BH][ceil(T/64)][d][m], transposed (written only for chunks that hold a reset).
 // Workspace: forward aggregates [BH][nseg_f][m][d]; backward pre-reset and
-// full dY x^T aggregates [BH][nseg_b][d][m] each.
+// full dY x^T aggregates [BH][nseg_b][d][m] each; then one int per segment
+// (its last / first document start, recorded by the aggregate passes).
 struct ResetPlan {
   Plan p;
   size_t off_cstate, saved_bytes;
-  size_t off_aggF, ws;
+  size_t off_aggF, off_seg, ws;
 };
 
 int make_reset_plan(const gradlev_shape* s, ResetPlan* out) {
@@ -177,7 +178,9 @@ int make_reset_plan(const gradlev_shape* s, ResetPlan* out) {
   const size_t agg_f = out->p.fwd.nseg > 1 ? round_up((size_t)BH * out->p.fwd.nseg * md, 256) : 0;
   const size_t agg_b = round_up((size_t)BH * out->p.bwd.nseg * md, 256);
   out->off_aggF = agg_b;
-  out->ws = agg_f > 2 * agg_b ? agg_f : 2 * agg_b;
+  out->off_seg = agg_f > 2 * agg_b ? agg_f : 2 * agg_b;
+  const int64_t nseg = out->p.fwd.nseg > out->p.bwd.nseg ? out->p.fwd.nseg : out->p.bwd.nseg;
+  out->ws = out->off_seg + round_up((size_t)BH * nseg * sizeof(int), 256);
   return GRADLEV_OK;
 }
 
@@ -693,6 +696,7 @@ int gradlev_scan_fwd_reset_save(const gradlev_shape* s, const float* W0, const v
   f.reset = reset;
   f.cstate = reinterpret_cast<float*>(reinterpret_cast<char*>(saved) + r.off_cstate);
   f.resets = true;
+  f.segreset = reinterpret_cast<int*>(static_cast<char*>(workspace) + r.off_seg);
   const hipError_t e = launch_scan_fwd(r.p.fwd, f, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }
@@ -731,6 +735,7 @@ int gradlev_scan_bwd_reset_saved(const gradlev_shape* s, const float* W0, const 
   b.reset = reset;
   b.cstate = reinterpret_cast<const float*>(reinterpret_cast<const char*>(saved) + r.off_cstate);
   b.resets = true;
+  b.segreset = reinterpret_cast<int*>(ws + r.off_seg);
   const hipError_t e = launch_scan_bwd(r.p.bwd, b, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GRADLEV_OK : GRADLEV_ERR_HIP;
 }

@@ -30,6 +30,7 @@ struct FwdPtrs {
   const uint8_t* reset;     // [B][T] document starts (unit retention with resets), or nullptr
   float* cstate;            // with resets: [B*H][ceil(T/64)][d][m] chunk-start states of reset chunks, transposed
   bool resets;              // run the reset kernels (reset may still be nullptr: no document starts)
+  int* segreset;            // with resets: [B*H][nseg] workspace ints (each segment's last document start)
 };
 
 struct BwdPtrs {
@@ -52,6 +53,7 @@ struct BwdPtrs {
   const float* cstate;   // the forward's chunk-start states of reset chunks, with `resets`
   float* aggF;           // with resets: [B*H][nseg][d][m] full dY x^T per segment (for dW0)
   bool resets;
+  int* segreset;         // with resets: [B*H][nseg] workspace ints (each segment's first document start)
 };
 
 // Gated scans (retention and resets).  Workspace: segment aggregates

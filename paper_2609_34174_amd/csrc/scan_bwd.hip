@@ -43,6 +43,7 @@ struct BArgs {
   const float* wend;  // [BH][nseg][m][d]: the forward's segment-end weights, or null (then W_0 - sum A)
   const uint8_t* reset;  // [B][T] document starts (RST kernels)
   const float* cstate;   // [BH][ceil(T/C)][d][m]: chunk-start states of the chunks holding a reset, transposed
+  const int* segreset;   // RST, or null: each work item's first document start (-1: none), from the aggregate pass
 };
 
 // Output modes compiled separately so that no accumulator crosses a runtime
@@ -157,7 +158,17 @@ bwd_main_kernel(const BArgs a) {
   int64_t j_last = a.nseg - 1;
   bool no_sfx = false;
   if constexpr (RST) {
-    const int64_t fr = first_reset_in<NT>(Rrow, t_end, T, tid, red);
+    // The first document start after the segment: that of the nearest later
+    // segment holding one, as the aggregate pass found them.
+    int64_t fr = -1;
+    if (a.segreset) {
+      for (int64_t j = a.nseg - 1; j > seg; --j) {
+        const int v = a.segreset[bh * a.nseg + j];
+        if (v >= 0) fr = v;
+      }
+    } else {
+      fr = first_reset_in<NT>(Rrow, t_end, T, tid, red);
+    }
     if (fr == t_end) no_sfx = true;
     else if (fr > 0) j_last = fr / a.seg_len;
   }
@@ -1162,6 +1173,7 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
   k.aggB = f.aggB;
   k.reset = f.reset;
   k.aggF = f.aggF;
+  k.segreset = f.resets && !read_only ? f.segreset : nullptr;  // the pass that records them runs only then
   if (f.resets) {
     // Document resets at unit retention (the saved pair; exclusive 64 x 64
     // maps, 64-token chunks): pre-reset suffix aggregates and full per-segment
@@ -1194,6 +1206,7 @@ static hipError_t bwd_dispatch2(const ScanProblem& p, const BwdPtrs& f, hipStrea
       b.wend = f.wend;
       b.reset = f.reset;
       b.cstate = f.cstate;
+      b.segreset = k.segreset;
       timing_begin(GRADLEV_K_BWD_MAIN, s);
       if (read_only)
         hipLaunchKernelGGL((bwd_main_kernel<OP, D, M, C, false, ETAV, kOutRead, true>), dim3(grid), dim3(NT), 0, s, b);

@@ -30,6 +30,10 @@ struct KArgs {
   const uint8_t* reset;
   float* cstate;
   float* aggF;
+  // With resets, or null: per work item (bh * nseg + seg) the aggregate pass
+  // records the segment's last (forward) or first (backward) document start,
+  // -1 for none, so that the main kernel need not search the flags again.
+  int* segreset;
 };
 
 // ---------------------------------------------------------------------------
@@ -395,9 +399,11 @@ agg_kernel(const KArgs a, int64_t nagg) {
     if constexpr (WA) {
       const int64_t lr = last_reset_in<NT>(rrow, t_begin - 1, t_end - 1, threadIdx.x, red);
       if (lr >= 0) wlo = lr;
+      if (a.segreset && threadIdx.x == 0) a.segreset[bh * a.nseg + seg] = (int)lr;
     } else {
       const int64_t fr = first_reset_in<NT>(rrow, t_begin, t_end, threadIdx.x, red);
       if (fr >= 0) bhi = fr;
+      if (a.segreset && threadIdx.x == 0) a.segreset[bh * a.nseg + seg] = (int)fr;
     }
   }
 

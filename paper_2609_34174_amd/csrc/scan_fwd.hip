@@ -93,7 +93,18 @@ fwd_main_kernel(const KArgs a) {
   int64_t j_first = 0;
   bool from_w0 = false;
   if constexpr (RST) {
-    const int64_t lr = last_reset_in<NT>(Rrow, 0, t_begin, tid, red);
+    // The last document start at or before t_begin: the latest one the
+    // aggregate pass found in an earlier segment, or t_begin itself.
+    int64_t lr = -1;
+    if (a.segreset) {
+      for (int64_t j = 0; j < seg; ++j) {
+        const int v = a.segreset[bh * a.nseg + j];
+        if (v > lr) lr = v;
+      }
+      if (t_begin >= 1 && __builtin_amdgcn_raw_buffer_load_b8(Rrow, (int)t_begin, 0, 0) != 0) lr = t_begin;
+    } else {
+      lr = last_reset_in<NT>(Rrow, 0, t_begin, tid, red);
+    }
     if (lr == t_begin) from_w0 = true;
     else if (lr > 0) j_first = lr / a.seg_len;
   }
@@ -447,6 +458,7 @@ hipError_t launch_scan_fwd(const ScanProblem& p, const FwdPtrs& f, hipStream_t s
   k.nsave = f.nsave;
   k.reset = f.reset;
   k.cstate = f.cstate;
+  k.segreset = f.resets && p.nseg > 1 ? f.segreset : nullptr;  // written by the aggregate pass
   if (f.resets && p.chunk != 64) return hipErrorInvalidValue;
   if (p.bf16) {
     if (p.chunk == 128) return fwd_by_dims<OpBF16, 128>(p, k, f.resets, s);
