@@ -162,10 +162,10 @@ bwd_main_kernel(const BArgs a) {
     // segment holding one, as the aggregate pass found them.
     int64_t fr = -1;
     if (a.segreset) {
-      for (int64_t j = a.nseg - 1; j > seg; --j) {
-        const int v = a.segreset[bh * a.nseg + j];
-        if (v >= 0) fr = v;
-      }
+      // Lane j > seg reads segment j's record (one load each, in parallel).
+      const int v = lane > seg && lane < a.nseg ? a.segreset[bh * a.nseg + lane] : -1;
+      const uint64_t m = __ballot(v >= 0);
+      if (m) fr = __builtin_amdgcn_readlane(v, __builtin_ctzll(m));
     } else {
       fr = first_reset_in<NT>(Rrow, t_end, T, tid, red);
     }

@@ -97,10 +97,11 @@ fwd_main_kernel(const KArgs a) {
     // aggregate pass found in an earlier segment, or t_begin itself.
     int64_t lr = -1;
     if (a.segreset) {
-      for (int64_t j = 0; j < seg; ++j) {
-        const int v = a.segreset[bh * a.nseg + j];
-        if (v > lr) lr = v;
-      }
+      // Lane j < seg reads segment j's record (one load each, in parallel);
+      // the latest segment holding a document start has the latest one.
+      const int v = lane < seg ? a.segreset[bh * a.nseg + lane] : -1;
+      const uint64_t m = __ballot(v >= 0);
+      if (m) lr = __builtin_amdgcn_readlane(v, 63 - __builtin_clzll(m));
       if (t_begin >= 1 && __builtin_amdgcn_raw_buffer_load_b8(Rrow, (int)t_begin, 0, 0) != 0) lr = t_begin;
     } else {
       lr = last_reset_in<NT>(Rrow, 0, t_begin, tid, red);
