@@ -21,7 +21,8 @@
 // with no sequential dependency.  Kernels:
 //
 //   wide_gate_kernel   per sequence: c_t, and the zero count and log-sum
-//                      prefixes of the retentions that give F exactly;
+//                      prefixes of the retentions that give F exactly
+//                      (wide_prep_kernel: the same beside the bf16 W_0 split);
 //   wide_score_kernel  64 x 64 tiles of S (contraction over the query width),
 //                      scaled by F and c, masked to s < t, stored as bf16
 //                      hi + lo (fp32 for fp32 inputs);
@@ -72,8 +73,8 @@ __device__ __forceinline__ void gate_at(const WGateArgs& g, int64_t bh, int64_t 
 __device__ __forceinline__ int zc_step(int z, float a) { return a == 0.f ? z + 2 : (a < 0.f ? z ^ 1 : z); }
 __device__ __forceinline__ int zc_join(int l, int r) { return ((l & ~1) + (r & ~1)) | ((l ^ r) & 1); }
 
-static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g) {
-  const int64_t bh = blockIdx.x, b = bh / g.H;
+__device__ __forceinline__ void wide_gate_block(const WGateArgs& g, int64_t bh) {
+  const int64_t b = bh / g.H;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t per = (g.Tp + 255) / 256;
   const int64_t t0 = tid * per, t1 = t0 + per < g.Tp ? t0 + per : g.Tp;
@@ -128,6 +129,7 @@ static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g
     g.cw[bh * g.Tp + t] = -e;
   }
 }
+static __global__ void __launch_bounds__(256) wide_gate_kernel(const WGateArgs g) { wide_gate_block(g, blockIdx.x); }
 
 // ---------------------------------------------------------------------------
 // Staging of a ROWS x COLS tile of a row-major global matrix into a swizzled
@@ -707,10 +709,19 @@ static __global__ void __launch_bounds__(256) wide_dw0_kernel(const WDw0Args a) 
 
 // fp32 W_0 split once per call into bf16 hi and lo planes of the same
 // layout (the output tiles then stage bf16 directly; the split costs one
-// pass over W_0 instead of one per row tile).
-static __global__ void __launch_bounds__(256) wide_split_w0(const float* __restrict__ W0, bf16* __restrict__ hi,
-                                                            bf16* __restrict__ lo, int64_t n4) {
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
+// pass over W_0 instead of one per row tile).  The gate prefixes ride in
+// the same launch: blocks [0, nbh) take one sequence each (a sequential
+// span per thread, a few blocks only), the rest split W_0 beside them,
+// instead of the prefixes running alone ahead of the scores.
+static __global__ void __launch_bounds__(256) wide_prep_kernel(const WGateArgs g, int64_t nbh,
+                                                               const float* __restrict__ W0, bf16* __restrict__ hi,
+                                                               bf16* __restrict__ lo, int64_t n4) {
+  if ((int64_t)blockIdx.x < nbh) {
+    wide_gate_block(g, blockIdx.x);
+    return;
+  }
+  const int64_t nb = (int64_t)gridDim.x - nbh;
+  for (int64_t i = ((int64_t)blockIdx.x - nbh) * 256 + threadIdx.x; i < n4; i += nb * 256)
     OpBF16::store4_split(hi + 4 * i, lo + 4 * i, *reinterpret_cast<const f32x4*>(W0 + 4 * i));
 }
 
@@ -1076,12 +1087,17 @@ void wide_out(const WideProblem& p, const WidePtrs& f, const WideWs& ws, int mod
   else hipLaunchKernelGGL((wide_out_kernel<OP, false, 128, 0>), dim3(g), dim3(512), 0, s, oa);
 }
 
+// The gate prefixes and, for bf16 operands, the W_0 split in one launch.
 template <class OP>
-void wide_split(const WideProblem& p, const WidePtrs& f, const WideWs& ws, hipStream_t s) {
-  if (OP::kSplit != 2) return;
-  const int64_t n4 = p.H * (int64_t)p.m * p.d / 4;
-  const unsigned g = (unsigned)(n4 / 256 < 4096 ? (n4 + 255) / 256 : 4096);
-  hipLaunchKernelGGL(wide_split_w0, dim3(g), dim3(256), 0, s, f.W0, ws.Wh, ws.Wl, n4);
+void wide_prep(const WideProblem& p, const WidePtrs& f, const WideWs& ws, hipStream_t s) {
+  if (OP::kSplit != 2) {
+    wide_gates<OP>(p, f, ws, s);
+    return;
+  }
+  WGateArgs g{f.eta, f.eta_scalar, f.eta_mul, f.alpha, f.alpha_scalar, f.reset, p.H, p.T, p.Tp, ws.cw, ws.zc, ws.lc};
+  const int64_t n4 = p.H * (int64_t)p.m * p.d / 4, BH = p.B * p.H;
+  const int64_t gs = n4 / 256 < 4096 ? (n4 + 255) / 256 : 4096;
+  hipLaunchKernelGGL(wide_prep_kernel, dim3((unsigned)(BH + gs)), dim3(256), 0, s, g, BH, f.W0, ws.Wh, ws.Wl, n4);
 }
 
 // Forward (read = false: Q = K = X, V = G) or transpose read (read = true:
@@ -1090,10 +1106,9 @@ template <class OP>
 hipError_t wide_run(const WideProblem& p, const WidePtrs& f, bool read, float* out, hipStream_t s) {
   const WideWs ws = wide_ws(p, f.ws);
   timing_begin(GRADLEV_K_WIDE_SCORE, s);
-  wide_gates<OP>(p, f, ws, s);
+  wide_prep<OP>(p, f, ws, s);
   wide_scores<OP>(p, ws, read ? f.dY : f.X, read ? f.G : f.X, read ? p.m : p.d, s);
   timing_end(GRADLEV_K_WIDE_SCORE, s);
-  wide_split<OP>(p, f, ws, s);
   timing_begin(GRADLEV_K_WIDE_OUT, s);
   wide_out<OP>(p, f, ws, 0, read, read ? f.dY : f.X, read ? p.m : p.d, read ? f.X : f.G, read ? p.d : p.m, out,
                nullptr, s);
