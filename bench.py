@@ -738,7 +738,7 @@ def secondary_gated(gl, torch, W, device, steps=20, warmup=50, nsets=8, lag=2, s
     return res
 
 
-def secondary_mlp_lm(gl, torch, device, steps=5, warmup=2):
+def secondary_mlp_lm(gl, torch, device, steps=20, warmup=5):
     """The paper's adapted final MLP at its LM width (Appendix E: d = 1024,
     hidden = 4096, 1024-token context, two sequences per GPU, bf16 activations,
     tanh-approximate GELU, unit retention, document resets, per-token write
